@@ -1,0 +1,163 @@
+"""Benchmark: MoE layer forward + backward on one MI355X.
+
+One step = top-k gate -> capacity-bounded dispatch -> expert FFN grouped GEMMs
+-> weighted combine -> dX chain -> dW products, over one batch of seeded
+synthetic input already resident in HBM (the 8192-token, d_model 1024,
+d_ff 4096, 16-expert, top-2, bf16 layer by default).  Prints ONE JSON line.
+
+Per-call durations come from HIP events recorded around every C-ABI call on
+the stream the kernels run on, over the timed steps.  The roofline object
+reports the expert FFN forward (its two grouped bf16 MFMA GEMMs) against the
+dense bf16 MFMA peak.  The CPU baseline is the float64 oracle on a bounded
+sample of the same workload.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 2|3|4] [--no-cpu-baseline]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+MI355X_PEAK_BF16_TFLOPS = 2500.0   # dense bf16 MFMA
+MI355X_PEAK_HBM_GBPS = 8000.0
+METRIC = "MoE layer fwd+bwd tokens/s on 1 MI355X; expert GEMM MFMA util; dispatch GB/s"
+CALLS = ["gate", "dispatch", "expert_ffn_fwd", "combine", "bwd_dx", "bwd_dw"]
+
+
+def _args():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", type=int, default=2, choices=[2, 3, 4])
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-sample-tokens", type=int, default=1024)
+    return ap.parse_args()
+
+
+def cpu_baseline(spec, inp, n_tokens):
+    """The oracle, as it stands, on the first n_tokens tokens of the workload."""
+    from dataclasses import replace
+    from oracle import moe_oracle as O
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        threads = os.cpu_count() or 1
+    sub = {k: (v[:n_tokens] if k in ("x", "dy") else v) for k, v in inp.items()}
+    s = replace(spec, T=n_tokens)
+    t0 = time.perf_counter()
+    fw = O.layer_forward(s, sub)
+    O.layer_backward(s, sub, fw)
+    dt = time.perf_counter() - t0
+    return {"value": n_tokens / dt, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"float64 oracle layer forward+backward on the first {n_tokens} tokens of the same "
+                      f"workload (capacity recomputed for {n_tokens} tokens), {dt:.1f} s wall"}
+
+
+def main():
+    a = _args()
+    if a.gpus != 1:
+        print(f"bench.py measures one GPU's share of the MoE layer step; --gpus {a.gpus} is not supported "
+              f"(the all-to-all between GPUs is not part of this build).", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    from paper_2404_19429_amd import lancet_moe as L
+    from synth import layer_inputs, layer_spec
+
+    spec = layer_spec(a.config)
+    inp = layer_inputs(spec)
+    C = L.moe_capacity(spec.T, spec.E, spec.k, spec.cf_num, spec.cf_den)
+    cfg = L.make_cfg(spec.T, spec.d, spec.f, spec.E, spec.k, C, spec.G, spec.dtype, spec.act, spec.renorm)
+    dt = torch.bfloat16 if spec.dtype == "bf16" else torch.float32
+    dev = {n: torch.from_numpy(inp[n]).cuda().to(dt).contiguous() for n in ("x", "Wg", "W1", "W2", "dy")}
+    bias = None if inp["bias"] is None else torch.from_numpy(inp["bias"]).cuda()
+    b = L.alloc_layer(cfg)
+    stream = torch.cuda.current_stream()
+
+    def step(evs=None):
+        def mark(i):
+            if evs is not None:
+                evs[i].record(stream)
+        mark(0)
+        L.moe_gate_topk(cfg, dev["x"], dev["Wg"], bias, b.logits, b.idx, b.w)
+        mark(1)
+        L.moe_dispatch(cfg, dev["x"], b.idx, b.carry, b.fill, b.slot, b.send_buf, b.ws_dispatch)
+        mark(2)
+        L.moe_expert_ffn_fwd(cfg, b.send_buf, b.carry, b.fill, dev["W1"], dev["W2"], b.H, b.A, b.O)
+        mark(3)
+        L.moe_combine(cfg, b.O, b.idx, b.slot, b.w, b.y)
+        mark(4)
+        L.moe_bwd_dx(cfg, dev["Wg"], b.logits, b.idx, b.w, b.slot, b.carry, b.fill, b.H, b.O, dev["W1"],
+                     dev["W2"], dev["dy"], b.dO, b.dH, b.dXe, b.dlogits, b.dx, b.ws_dx)
+        mark(5)
+        L.moe_bwd_dw(cfg, dev["x"], b.dlogits, b.carry, b.fill, b.send_buf, b.A, b.dO, b.dH, b.dW1, b.dW2,
+                     b.dWg, b.ws_dw)
+        mark(6)
+
+    for _ in range(a.warmup):
+        step()
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(7)] for _ in range(a.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(a.steps):
+        step(evs[i])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    per_call = {c: 0.0 for c in CALLS}
+    for e in evs:
+        for j, c in enumerate(CALLS):
+            per_call[c] += e[j].elapsed_time(e[j + 1])
+    per_call = {c: v / a.steps for c, v in per_call.items()}       # ms per step
+    step_ms = sum(evs[i][0].elapsed_time(evs[i][6]) for i in range(a.steps)) / a.steps
+
+    fill = b.fill.cpu().numpy()
+    N = int(fill.sum())                                           # kept (token, expert) rows
+    d, f, T = spec.d, spec.f, spec.T
+    eb = 2 if spec.dtype == "bf16" else 4
+    gemm_fwd_flop = 4.0 * N * d * f
+    ffn_s = per_call["expert_ffn_fwd"] * 1e-3
+    achieved_tflops = gemm_fwd_flop / ffn_s / 1e12
+    expert_gemm_s = (per_call["expert_ffn_fwd"]) * 1e-3
+    disp_bytes = (T * d + N * d) * eb + T * spec.k * 4 * 2          # read x, write kept rows, idx + slot
+    dispatch_gbps = disp_bytes / (per_call["dispatch"] * 1e-3) / 1e9
+    tokens_per_s = T / (wall / a.steps)
+
+    out = {
+        "metric": METRIC,
+        "value": tokens_per_s,
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": a.steps,
+        "warmup": a.warmup,
+        "ms_per_step": wall / a.steps * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": spec.dtype,
+        "data": "synthetic (seeded Gaussian hidden states and weights; no dataset)",
+        "config": {"workload": spec.name, "T": T, "d_model": d, "d_ff": f, "E": spec.E, "k": spec.k,
+                   "C": C, "capacity_factor": f"{spec.cf_num}/{spec.cf_den}", "act": spec.act,
+                   "kept_rows": N, "parallelism": "single GPU (one GPU's share; all-to-all not run)"},
+        "roofline": {"kernel": "expert FFN forward: 2 grouped bf16 MFMA GEMMs (gemm_bf16_kernel FWD1 + FWD2)",
+                     "bound": "mfma", "achieved": achieved_tflops, "peak": MI355X_PEAK_BF16_TFLOPS,
+                     "unit": "TFLOP/s", "frac": achieved_tflops / MI355X_PEAK_BF16_TFLOPS, "traffic": None},
+        "expert_gemm_mfma_frac": achieved_tflops / MI355X_PEAK_BF16_TFLOPS,
+        "dispatch_GBps": dispatch_gbps,
+        "dispatch_hbm_frac": dispatch_gbps / MI355X_PEAK_HBM_GBPS,
+        "per_call_ms": per_call,
+        "event_ms_per_step": step_ms,
+    }
+    if not a.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(spec, inp, a.cpu_sample_tokens)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -46,6 +46,7 @@ __all__ = [
     "act", "act_grad", "expert_ffn", "combine",
     "combine_bwd", "expert_bwd_dx", "expert_bwd_dw", "dispatch_bwd", "gate_bwd",
     "layer_forward", "layer_backward", "expert_row_forward", "expert_row_backward",
+    "expert_rows", "expert_dw1_row", "expert_dw2_col",
 ]
 
 F64 = np.float64
@@ -368,3 +369,30 @@ def expert_row_backward(x_row, dO_row, W1e, W2e, kind: str):
     dH = dA * act_grad(h, kind)
     dX = np.asarray(W1e, F64).T @ dH
     return dH, dX
+
+
+def expert_rows(x, dy, idx, slot, w, e: int):
+    """The rows expert e holds, in buffer order: (X_e, dO_e) with dO = w * dy."""
+    T, k = idx.shape
+    pairs = sorted((int(slot[t, r]), t, r) for t in range(T) for r in range(k)
+                   if int(idx[t, r]) == e and slot[t, r] >= 0)
+    ts = [t for _, t, _ in pairs]
+    ws = np.array([w[t, r] for _, t, r in pairs], F64)
+    X = np.asarray(x, F64)[ts]
+    dO = ws[:, None] * np.asarray(dy, F64)[ts]
+    return X, dO
+
+
+def expert_dw1_row(X_rows, dO_rows, W1e, W2e, kind: str, i: int):
+    """Row i of dW1_e = sum over the expert's rows m of dH[m][i] X[m], with
+    dH[m][i] = <W2_e[:, i], dO[m]> * act'(<W1_e[i], X[m]>)."""
+    h_i = X_rows @ np.asarray(W1e[i], F64)
+    dH_i = (dO_rows @ np.asarray(W2e, F64)[:, i]) * act_grad(h_i, kind)
+    return dH_i @ X_rows
+
+
+def expert_dw2_col(X_rows, dO_rows, W1e, kind: str, c: int):
+    """Column c of dW2_e = sum over the expert's rows m of dO[m] A[m][c], with
+    A[m][c] = act(<W1_e[c], X[m]>)."""
+    a_c = act(X_rows @ np.asarray(W1e[c], F64), kind)
+    return dO_rows.T @ a_c

@@ -1,0 +1,217 @@
+// C ABI of the MoE-layer library: host-side validation, then kernel launches.
+// Validation needs no GPU, so every error path can be exercised on a host
+// without one; only a call that passes validation touches the HIP runtime.
+#include <cstdio>
+#include <cstdarg>
+#include <cstring>
+#include <string>
+
+#include "internal.h"
+
+namespace {
+
+thread_local std::string g_err;
+
+moe_status fail(moe_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return st;
+}
+
+moe_status ok() {
+  g_err.clear();
+  return MOE_OK;
+}
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+#define REQUIRE_PTR(p)                                                            \
+  do {                                                                            \
+    if ((p) == nullptr) return fail(MOE_EINVAL, "%s: " #p " is NULL", fn);        \
+    if (!aligned16(p)) return fail(MOE_EALIGN, "%s: " #p " is not 16-byte aligned", fn); \
+  } while (0)
+// Token-sized arrays (T rows) may be NULL when T == 0.
+#define REQUIRE_TPTR(p)                                                           \
+  do {                                                                            \
+    if (cfg->T > 0) REQUIRE_PTR(p); else OPTIONAL_PTR(p);                         \
+  } while (0)
+#define OPTIONAL_PTR(p)                                                           \
+  do {                                                                            \
+    if ((p) != nullptr && !aligned16(p))                                          \
+      return fail(MOE_EALIGN, "%s: " #p " is not 16-byte aligned", fn);           \
+  } while (0)
+
+moe_status check_cfg(const moe_cfg* c, const char* fn, bool need_gemm_shape) {
+  if (!c) return fail(MOE_EINVAL, "%s: cfg is NULL", fn);
+  if (c->dtype != MOE_F32 && c->dtype != MOE_BF16) return fail(MOE_EDTYPE, "%s: unknown dtype %d", fn, c->dtype);
+  if (c->act < MOE_ACT_IDENTITY || c->act > MOE_ACT_GELU_ERF) return fail(MOE_EINVAL, "%s: unknown act %d", fn, c->act);
+  if (c->renorm != 0 && c->renorm != 1) return fail(MOE_EINVAL, "%s: renorm must be 0 or 1", fn);
+  if (c->T < 0) return fail(MOE_EINVAL, "%s: T < 0", fn);
+  if (c->T > (int64_t)1 << 31) return fail(MOE_ESHAPE, "%s: T > 2^31 unsupported", fn);
+  if (c->E < 1 || c->E > lmoe::kMaxE) return fail(MOE_ESHAPE, "%s: E=%d outside 1..%d", fn, c->E, lmoe::kMaxE);
+  if (c->k < 1 || c->k > c->E || c->k > lmoe::kMaxK)
+    return fail(MOE_EINVAL, "%s: k=%d outside 1..min(E, %d)", fn, c->k, lmoe::kMaxK);
+  if (c->C < 1) return fail(MOE_EINVAL, "%s: C=%d < 1", fn, c->C);
+  if (c->G < 1 || c->E % c->G != 0) return fail(MOE_EINVAL, "%s: G=%d does not divide E=%d", fn, c->G, c->E);
+  if (c->d_model < 8 || c->d_model % 8 != 0) return fail(MOE_ESHAPE, "%s: d_model=%d not a positive multiple of 8", fn, c->d_model);
+  if (c->d_ff < 8 || c->d_ff % 8 != 0) return fail(MOE_ESHAPE, "%s: d_ff=%d not a positive multiple of 8", fn, c->d_ff);
+  if ((int64_t)c->C * c->E * (int64_t)(c->d_model > c->d_ff ? c->d_model : c->d_ff) > ((int64_t)1 << 40))
+    return fail(MOE_ESHAPE, "%s: E*C*max(d, f) too large", fn);
+  if (need_gemm_shape && c->dtype == MOE_BF16 && (c->d_model % 64 != 0 || c->d_ff % 64 != 0))
+    return fail(MOE_ESHAPE, "%s: bf16 expert GEMMs need d_model and d_ff multiples of 64", fn);
+  return MOE_OK;
+}
+
+// One gfx950 check per device, then cached.
+moe_status check_device(const char* fn) {
+  static thread_local int checked_dev = -1;
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess) return fail(MOE_EDEVICE, "%s: no HIP device", fn);
+  if (dev == checked_dev) return MOE_OK;
+  hipDeviceProp_t prop;
+  if (hipGetDeviceProperties(&prop, dev) != hipSuccess) return fail(MOE_EDEVICE, "%s: cannot query device %d", fn, dev);
+  if (std::strncmp(prop.gcnArchName, "gfx950", 6) != 0)
+    return fail(MOE_EDEVICE, "%s: device %d is %s, this library is built for gfx950", fn, dev, prop.gcnArchName);
+  checked_dev = dev;
+  return MOE_OK;
+}
+
+moe_status check_launch(const char* fn) {
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return fail(MOE_ELAUNCH, "%s: %s", fn, hipGetErrorString(e));
+  return ok();
+}
+
+#define CHECK(expr)                        \
+  do {                                     \
+    const moe_status _st = (expr);         \
+    if (_st != MOE_OK) return _st;         \
+  } while (0)
+
+}  // namespace
+
+extern "C" {
+
+int32_t moe_capacity(int64_t T, int32_t E, int32_t k, int32_t cf_num, int32_t cf_den) {
+  if (T < 0 || E < 1 || k < 1 || cf_num < 1 || cf_den < 1) return -1;
+  if (T == 0) return 0;
+  const __int128 num = (__int128)k * T * cf_num;
+  const __int128 den = (__int128)E * cf_den;
+  const __int128 c = (num + den - 1) / den;
+  if (c > INT32_MAX) return -1;
+  return (int32_t)c;
+}
+
+size_t moe_workspace_bytes(const moe_cfg* cfg, int32_t call) {
+  const char* fn = "moe_workspace_bytes";
+  if (check_cfg(cfg, fn, false) != MOE_OK) return 0;
+  switch (call) {
+    case MOE_CALL_DISPATCH: return lmoe::dispatch_ws_bytes(*cfg);
+    case MOE_CALL_BWD_DX: return lmoe::bwd_dx_ws_bytes(*cfg);
+    case MOE_CALL_BWD_DW: return lmoe::bwd_dw_ws_bytes(*cfg);
+    default: fail(MOE_EINVAL, "%s: unknown call %d", fn, call); return 0;
+  }
+}
+
+const char* moe_last_error(void) { return g_err.c_str(); }
+
+moe_status moe_gate_topk(const moe_cfg* cfg, const void* x, const void* Wg, const float* bias, float* logits,
+                         int32_t* idx, float* w, moe_stream_t stream) {
+  const char* fn = "moe_gate_topk";
+  CHECK(check_cfg(cfg, fn, false));
+  REQUIRE_TPTR(x); REQUIRE_PTR(Wg); OPTIONAL_PTR(bias);
+  REQUIRE_TPTR(logits); REQUIRE_TPTR(idx); REQUIRE_TPTR(w);
+  CHECK(check_device(fn));
+  lmoe::launch_gate(*cfg, x, Wg, bias, logits, idx, w, (hipStream_t)stream);
+  return check_launch(fn);
+}
+
+moe_status moe_dispatch(const moe_cfg* cfg, const void* x, const int32_t* idx, const int32_t* carry, int32_t* fill,
+                        int32_t* slot, void* send_buf, void* ws, size_t ws_bytes, moe_stream_t stream) {
+  const char* fn = "moe_dispatch";
+  CHECK(check_cfg(cfg, fn, false));
+  REQUIRE_TPTR(x); REQUIRE_TPTR(idx); OPTIONAL_PTR(carry); REQUIRE_PTR(fill);
+  REQUIRE_TPTR(slot); REQUIRE_PTR(send_buf);
+  if (carry != nullptr && (const void*)carry == (const void*)fill)
+    return fail(MOE_EINVAL, "%s: carry and fill may not alias", fn);
+  const size_t need = lmoe::dispatch_ws_bytes(*cfg);
+  if (need > 0) {
+    if (ws == nullptr || ws_bytes < need)
+      return fail(MOE_EWORKSPACE, "%s: workspace of %zu bytes needed, %zu given", fn, need, ws ? ws_bytes : 0);
+    REQUIRE_PTR(ws);
+  }
+  CHECK(check_device(fn));
+  lmoe::launch_dispatch(*cfg, x, idx, carry, fill, slot, send_buf, ws, (hipStream_t)stream);
+  return check_launch(fn);
+}
+
+moe_status moe_expert_ffn_fwd(const moe_cfg* cfg, const void* send_buf, const int32_t* row_begin,
+                              const int32_t* row_end, const void* W1, const void* W2, void* H, void* A,
+                              void* expert_out, moe_stream_t stream) {
+  const char* fn = "moe_expert_ffn_fwd";
+  CHECK(check_cfg(cfg, fn, true));
+  REQUIRE_PTR(send_buf); OPTIONAL_PTR(row_begin); REQUIRE_PTR(row_end);
+  REQUIRE_PTR(W1); REQUIRE_PTR(W2); REQUIRE_PTR(H); REQUIRE_PTR(A); REQUIRE_PTR(expert_out);
+  CHECK(check_device(fn));
+  lmoe::launch_expert_fwd(*cfg, send_buf, row_begin, row_end, W1, W2, H, A, expert_out, (hipStream_t)stream);
+  return check_launch(fn);
+}
+
+moe_status moe_combine(const moe_cfg* cfg, const void* expert_out, const int32_t* idx, const int32_t* slot,
+                       const float* w, void* y, moe_stream_t stream) {
+  const char* fn = "moe_combine";
+  CHECK(check_cfg(cfg, fn, false));
+  REQUIRE_PTR(expert_out); REQUIRE_TPTR(idx); REQUIRE_TPTR(slot); REQUIRE_TPTR(w); REQUIRE_TPTR(y);
+  CHECK(check_device(fn));
+  lmoe::launch_combine(*cfg, expert_out, idx, slot, w, y, (hipStream_t)stream);
+  return check_launch(fn);
+}
+
+moe_status moe_bwd_dx(const moe_cfg* cfg, const void* Wg, const float* logits, const int32_t* idx, const float* w,
+                      const int32_t* slot, const int32_t* row_begin, const int32_t* row_end, const void* H,
+                      const void* expert_out, const void* W1, const void* W2, const void* dy, void* dO, void* dH,
+                      void* dXe, float* dlogits, void* dx, void* ws, size_t ws_bytes, moe_stream_t stream) {
+  const char* fn = "moe_bwd_dx";
+  CHECK(check_cfg(cfg, fn, true));
+  REQUIRE_PTR(Wg); REQUIRE_TPTR(logits); REQUIRE_TPTR(idx); REQUIRE_TPTR(w); REQUIRE_TPTR(slot);
+  OPTIONAL_PTR(row_begin); REQUIRE_PTR(row_end); REQUIRE_PTR(H); REQUIRE_PTR(expert_out);
+  REQUIRE_PTR(W1); REQUIRE_PTR(W2); REQUIRE_TPTR(dy); REQUIRE_PTR(dO); REQUIRE_PTR(dH); REQUIRE_PTR(dXe);
+  REQUIRE_TPTR(dlogits); REQUIRE_TPTR(dx);
+  const size_t need = lmoe::bwd_dx_ws_bytes(*cfg);
+  if (need > 0 && (ws == nullptr || ws_bytes < need))
+    return fail(MOE_EWORKSPACE, "%s: workspace of %zu bytes needed", fn, need);
+  (void)ws;
+  CHECK(check_device(fn));
+  hipStream_t s = (hipStream_t)stream;
+  lmoe::launch_combine_bwd(*cfg, logits, idx, w, slot, expert_out, dy, dO, dlogits, s);
+  lmoe::launch_expert_bwd_dx(*cfg, dO, row_begin, row_end, H, W1, W2, dH, dXe, s);
+  lmoe::launch_dispatch_bwd(*cfg, Wg, dlogits, idx, slot, dXe, dx, s);
+  return check_launch(fn);
+}
+
+moe_status moe_bwd_dw(const moe_cfg* cfg, const void* x, const float* dlogits, const int32_t* row_begin,
+                      const int32_t* row_end, const void* send_buf, const void* A, const void* dO, const void* dH,
+                      void* dW1, void* dW2, float* dWg, void* ws, size_t ws_bytes, moe_stream_t stream) {
+  const char* fn = "moe_bwd_dw";
+  CHECK(check_cfg(cfg, fn, true));
+  REQUIRE_TPTR(dlogits); OPTIONAL_PTR(row_begin); REQUIRE_PTR(row_end); REQUIRE_PTR(send_buf);
+  REQUIRE_PTR(A); REQUIRE_PTR(dO); REQUIRE_PTR(dH); REQUIRE_PTR(dW1); REQUIRE_PTR(dW2); REQUIRE_PTR(dWg);
+  REQUIRE_TPTR(x);
+  const size_t need = lmoe::bwd_dw_ws_bytes(*cfg);
+  if (need > 0) {
+    if (ws == nullptr || ws_bytes < need)
+      return fail(MOE_EWORKSPACE, "%s: workspace of %zu bytes needed, %zu given", fn, need, ws ? ws_bytes : 0);
+    REQUIRE_PTR(ws);
+  }
+  CHECK(check_device(fn));
+  hipStream_t s = (hipStream_t)stream;
+  lmoe::launch_expert_bwd_dw(*cfg, send_buf, A, dO, dH, row_begin, row_end, dW1, dW2, s);
+  lmoe::launch_dwg(*cfg, x, dlogits, dWg, ws, s);
+  return check_launch(fn);
+}
+
+}  // extern "C"

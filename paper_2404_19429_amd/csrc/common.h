@@ -1,0 +1,112 @@
+// Internal device helpers shared by the MoE kernels (gfx950, wave64).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "lancet_moe.h"
+
+namespace lmoe {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+constexpr int kWave = 64;
+
+// ------------------------------------------------------------------ bf16 <-> f32
+__device__ __forceinline__ float bf16_bits_to_f32(uint32_t h) { return __uint_as_float(h << 16); }
+
+// Round to nearest, ties to even; NaN stays NaN.
+__device__ __forceinline__ uint32_t f32_to_bf16_bits(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (u >> 16) | 0x40u;
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return u >> 16;
+}
+
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  return f32_to_bf16_bits(lo) | (f32_to_bf16_bits(hi) << 16);
+}
+
+// A 16-byte vector of 8 bf16 or 4 f32 elements, unpacked to float.
+template <typename T> struct Vec;
+template <> struct Vec<uint16_t> {       // bf16 storage
+  static constexpr int N = 8;
+  __device__ static void load(const void* p, float* v) {
+    u32x4 r = *reinterpret_cast<const u32x4*>(p);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      v[2 * i] = __uint_as_float(r[i] << 16);
+      v[2 * i + 1] = __uint_as_float(r[i] & 0xffff0000u);
+    }
+  }
+  __device__ static void store(void* p, const float* v) {
+    u32x4 r;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) r[i] = pack_bf16x2(v[2 * i], v[2 * i + 1]);
+    *reinterpret_cast<u32x4*>(p) = r;
+  }
+};
+template <> struct Vec<float> {
+  static constexpr int N = 4;
+  __device__ static void load(const void* p, float* v) {
+    f32x4 r = *reinterpret_cast<const f32x4*>(p);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) v[i] = r[i];
+  }
+  __device__ static void store(void* p, const float* v) {
+    f32x4 r;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) r[i] = v[i];
+    *reinterpret_cast<f32x4*>(p) = r;
+  }
+};
+
+// ------------------------------------------------------------------- wave ops
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
+  return v;
+}
+
+__device__ __forceinline__ uint64_t wave_max_u64(uint64_t v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    uint64_t w = __shfl_xor(v, o, kWave);
+    v = w > v ? w : v;
+  }
+  return v;
+}
+
+// ------------------------------------------------------------------ activation
+__device__ __forceinline__ float act_fwd(float h, int act) {
+  switch (act) {
+    case MOE_ACT_RELU: return h > 0.f ? h : 0.f;
+    case MOE_ACT_GELU_TANH: {
+      const float c = 0.7978845608028654f;  // sqrt(2/pi)
+      return 0.5f * h * (1.f + tanhf(c * (h + 0.044715f * h * h * h)));
+    }
+    case MOE_ACT_GELU_ERF: return 0.5f * h * (1.f + erff(h * 0.7071067811865476f));
+    default: return h;
+  }
+}
+
+__device__ __forceinline__ float act_bwd(float h, int act) {
+  switch (act) {
+    case MOE_ACT_RELU: return h > 0.f ? 1.f : 0.f;
+    case MOE_ACT_GELU_TANH: {
+      const float c = 0.7978845608028654f;
+      float u = c * (h + 0.044715f * h * h * h);
+      float th = tanhf(u);
+      float du = c * (1.f + 3.f * 0.044715f * h * h);
+      return 0.5f * (1.f + th) + 0.5f * h * (1.f - th * th) * du;
+    }
+    case MOE_ACT_GELU_ERF:
+      return 0.5f * (1.f + erff(h * 0.7071067811865476f)) + h * expf(-0.5f * h * h) * 0.3989422804014327f;
+    default: return 1.f;
+  }
+}
+
+}  // namespace lmoe

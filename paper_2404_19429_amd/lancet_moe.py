@@ -1,0 +1,260 @@
+"""Python binding of liblancet_moe.so (ctypes).
+
+Argument marshalling only: every function here has the name of the C-ABI
+entry point it calls, checks that each tensor is a contiguous device tensor
+of the right dtype and at least the size the call will touch (the C ABI takes
+bare pointers and cannot check sizes), and passes pointers and the current
+HIP stream.  All computation happens in the HIP kernels.  There is no CPU
+fallback: if the library is missing, importing this module raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+from typing import Optional
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "liblancet_moe.so")
+
+MOE_OK, MOE_EINVAL, MOE_ESHAPE, MOE_EALIGN, MOE_EDTYPE, MOE_EDEVICE, MOE_ELAUNCH, MOE_EWORKSPACE = 0, -1, -2, -3, -4, -5, -6, -7
+MOE_F32, MOE_BF16 = 0, 1
+ACTS = {"identity": 0, "relu": 1, "gelu_tanh": 2, "gelu_erf": 3}
+MOE_CALL_DISPATCH, MOE_CALL_BWD_DX, MOE_CALL_BWD_DW = 0, 1, 2
+
+#: Every symbol include/lancet_moe.h declares.
+EXPORTS = ["moe_capacity", "moe_workspace_bytes", "moe_last_error", "moe_gate_topk", "moe_dispatch",
+           "moe_expert_ffn_fwd", "moe_combine", "moe_bwd_dx", "moe_bwd_dw"]
+
+
+class MoeError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"status {status}: {msg}")
+        self.status = status
+
+
+class moe_cfg(ctypes.Structure):
+    _fields_ = [("T", ctypes.c_int64), ("d_model", ctypes.c_int32), ("d_ff", ctypes.c_int32),
+                ("E", ctypes.c_int32), ("k", ctypes.c_int32), ("C", ctypes.c_int32), ("G", ctypes.c_int32),
+                ("dtype", ctypes.c_int32), ("act", ctypes.c_int32), ("renorm", ctypes.c_int32)]
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2404_19429_amd.build`")
+    lib = ctypes.CDLL(LIB_PATH)
+    P, I32, I64, SZ = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
+    CFG = ctypes.POINTER(moe_cfg)
+    sig = {
+        "moe_capacity": (I32, [I64, I32, I32, I32, I32]),
+        "moe_workspace_bytes": (SZ, [CFG, I32]),
+        "moe_last_error": (ctypes.c_char_p, []),
+        "moe_gate_topk": (I32, [CFG, P, P, P, P, P, P, P]),
+        "moe_dispatch": (I32, [CFG, P, P, P, P, P, P, P, SZ, P]),
+        "moe_expert_ffn_fwd": (I32, [CFG, P, P, P, P, P, P, P, P, P]),
+        "moe_combine": (I32, [CFG, P, P, P, P, P, P]),
+        "moe_bwd_dx": (I32, [CFG] + [P] * 18 + [SZ, P]),
+        "moe_bwd_dw": (I32, [CFG] + [P] * 12 + [SZ, P]),
+    }
+    for name, (res, args) in sig.items():
+        fn = getattr(lib, name)
+        fn.restype, fn.argtypes = res, args
+    return lib
+
+
+_lib = _load()
+
+
+# ----------------------------------------------------------------------- helpers
+def make_cfg(T, d_model, d_ff, E, k, C, G=1, dtype="bf16", act="gelu_tanh", renorm=1) -> moe_cfg:
+    dt = {"bf16": MOE_BF16, "f32": MOE_F32}[dtype] if isinstance(dtype, str) else int(dtype)
+    return moe_cfg(int(T), int(d_model), int(d_ff), int(E), int(k), int(C), int(G), dt,
+                   ACTS[act] if isinstance(act, str) else int(act), int(renorm))
+
+
+def torch_dtype(cfg: moe_cfg):
+    return torch.bfloat16 if cfg.dtype == MOE_BF16 else torch.float32
+
+
+def _stream(stream) -> int:
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, torch.cuda.Stream):
+        return stream.cuda_stream
+    return int(stream)
+
+
+def _ptr(t: Optional[torch.Tensor], name: str, dtype, numel: int, nullable: bool = False):
+    if t is None:
+        if nullable:
+            return None
+        raise ValueError(f"{name} is required")
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if t.numel() < numel:
+        raise ValueError(f"{name} has {t.numel()} elements, the call touches {numel}")
+    return t.data_ptr() if t.numel() else None
+
+
+def _check(st: int):
+    if st != MOE_OK:
+        raise MoeError(st, _lib.moe_last_error().decode())
+
+
+# ------------------------------------------------------------------- entry points
+def moe_capacity(T: int, E: int, k: int, cf_num: int, cf_den: int) -> int:
+    return int(_lib.moe_capacity(T, E, k, cf_num, cf_den))
+
+
+def moe_workspace_bytes(cfg: moe_cfg, call: int) -> int:
+    return int(_lib.moe_workspace_bytes(ctypes.byref(cfg), call))
+
+
+def moe_last_error() -> str:
+    return _lib.moe_last_error().decode()
+
+
+def moe_gate_topk(cfg, x, Wg, bias, logits, idx, w, stream=None):
+    dt = torch_dtype(cfg)
+    T, d, E, k = cfg.T, cfg.d_model, cfg.E, cfg.k
+    _check(_lib.moe_gate_topk(ctypes.byref(cfg), _ptr(x, "x", dt, T * d), _ptr(Wg, "Wg", dt, E * d),
+                              _ptr(bias, "bias", torch.float32, E, nullable=True),
+                              _ptr(logits, "logits", torch.float32, T * E), _ptr(idx, "idx", torch.int32, T * k),
+                              _ptr(w, "w", torch.float32, T * k), _stream(stream)))
+
+
+def moe_dispatch(cfg, x, idx, carry, fill, slot, send_buf, ws, stream=None):
+    dt = torch_dtype(cfg)
+    T, d, E, k, C = cfg.T, cfg.d_model, cfg.E, cfg.k, cfg.C
+    need = moe_workspace_bytes(cfg, MOE_CALL_DISPATCH)
+    _check(_lib.moe_dispatch(ctypes.byref(cfg), _ptr(x, "x", dt, T * d), _ptr(idx, "idx", torch.int32, T * k),
+                             _ptr(carry, "carry", torch.int32, E, nullable=True), _ptr(fill, "fill", torch.int32, E),
+                             _ptr(slot, "slot", torch.int32, T * k), _ptr(send_buf, "send_buf", dt, E * C * d),
+                             _ptr(ws, "ws", torch.uint8, need, nullable=need == 0),
+                             ws.numel() if ws is not None else 0, _stream(stream)))
+
+
+def moe_expert_ffn_fwd(cfg, send_buf, row_begin, row_end, W1, W2, H, A, expert_out, stream=None):
+    dt = torch_dtype(cfg)
+    d, f, E, C = cfg.d_model, cfg.d_ff, cfg.E, cfg.C
+    _check(_lib.moe_expert_ffn_fwd(ctypes.byref(cfg), _ptr(send_buf, "send_buf", dt, E * C * d),
+                                   _ptr(row_begin, "row_begin", torch.int32, E, nullable=True),
+                                   _ptr(row_end, "row_end", torch.int32, E), _ptr(W1, "W1", dt, E * f * d),
+                                   _ptr(W2, "W2", dt, E * d * f), _ptr(H, "H", dt, E * C * f),
+                                   _ptr(A, "A", dt, E * C * f), _ptr(expert_out, "expert_out", dt, E * C * d),
+                                   _stream(stream)))
+
+
+def moe_combine(cfg, expert_out, idx, slot, w, y, stream=None):
+    dt = torch_dtype(cfg)
+    T, d, E, k, C = cfg.T, cfg.d_model, cfg.E, cfg.k, cfg.C
+    _check(_lib.moe_combine(ctypes.byref(cfg), _ptr(expert_out, "expert_out", dt, E * C * d),
+                            _ptr(idx, "idx", torch.int32, T * k), _ptr(slot, "slot", torch.int32, T * k),
+                            _ptr(w, "w", torch.float32, T * k), _ptr(y, "y", dt, T * d), _stream(stream)))
+
+
+def moe_bwd_dx(cfg, Wg, logits, idx, w, slot, row_begin, row_end, H, expert_out, W1, W2, dy, dO, dH, dXe,
+               dlogits, dx, ws=None, stream=None):
+    dt = torch_dtype(cfg)
+    T, d, f, E, k, C = cfg.T, cfg.d_model, cfg.d_ff, cfg.E, cfg.k, cfg.C
+    need = moe_workspace_bytes(cfg, MOE_CALL_BWD_DX)
+    _check(_lib.moe_bwd_dx(ctypes.byref(cfg), _ptr(Wg, "Wg", dt, E * d), _ptr(logits, "logits", torch.float32, T * E),
+                           _ptr(idx, "idx", torch.int32, T * k), _ptr(w, "w", torch.float32, T * k),
+                           _ptr(slot, "slot", torch.int32, T * k),
+                           _ptr(row_begin, "row_begin", torch.int32, E, nullable=True),
+                           _ptr(row_end, "row_end", torch.int32, E), _ptr(H, "H", dt, E * C * f),
+                           _ptr(expert_out, "expert_out", dt, E * C * d), _ptr(W1, "W1", dt, E * f * d),
+                           _ptr(W2, "W2", dt, E * d * f), _ptr(dy, "dy", dt, T * d), _ptr(dO, "dO", dt, E * C * d),
+                           _ptr(dH, "dH", dt, E * C * f), _ptr(dXe, "dXe", dt, E * C * d),
+                           _ptr(dlogits, "dlogits", torch.float32, T * E), _ptr(dx, "dx", dt, T * d),
+                           _ptr(ws, "ws", torch.uint8, need, nullable=need == 0),
+                           ws.numel() if ws is not None else 0, _stream(stream)))
+
+
+def moe_bwd_dw(cfg, x, dlogits, row_begin, row_end, send_buf, A, dO, dH, dW1, dW2, dWg, ws, stream=None):
+    dt = torch_dtype(cfg)
+    T, d, f, E, C = cfg.T, cfg.d_model, cfg.d_ff, cfg.E, cfg.C
+    need = moe_workspace_bytes(cfg, MOE_CALL_BWD_DW)
+    _check(_lib.moe_bwd_dw(ctypes.byref(cfg), _ptr(x, "x", dt, T * d, nullable=T == 0),
+                           _ptr(dlogits, "dlogits", torch.float32, T * E),
+                           _ptr(row_begin, "row_begin", torch.int32, E, nullable=True),
+                           _ptr(row_end, "row_end", torch.int32, E), _ptr(send_buf, "send_buf", dt, E * C * d),
+                           _ptr(A, "A", dt, E * C * f), _ptr(dO, "dO", dt, E * C * d), _ptr(dH, "dH", dt, E * C * f),
+                           _ptr(dW1, "dW1", dt, E * f * d), _ptr(dW2, "dW2", dt, E * d * f),
+                           _ptr(dWg, "dWg", torch.float32, E * d),
+                           _ptr(ws, "ws", torch.uint8, need, nullable=need == 0),
+                           ws.numel() if ws is not None else 0, _stream(stream)))
+
+
+# ------------------------------------------------------------- layer step driver
+@dataclass
+class LayerBuffers:
+    """Device tensors of one MoE layer step (allocated once, reused every step)."""
+    cfg: moe_cfg
+    logits: torch.Tensor
+    idx: torch.Tensor
+    w: torch.Tensor
+    carry: torch.Tensor
+    fill: torch.Tensor
+    slot: torch.Tensor
+    send_buf: torch.Tensor
+    H: torch.Tensor
+    A: torch.Tensor
+    O: torch.Tensor
+    y: torch.Tensor
+    dO: torch.Tensor
+    dH: torch.Tensor
+    dXe: torch.Tensor
+    dlogits: torch.Tensor
+    dx: torch.Tensor
+    dW1: torch.Tensor
+    dW2: torch.Tensor
+    dWg: torch.Tensor
+    ws_dispatch: torch.Tensor
+    ws_dx: torch.Tensor
+    ws_dw: torch.Tensor
+
+
+def alloc_layer(cfg: moe_cfg, device="cuda") -> LayerBuffers:
+    dt = torch_dtype(cfg)
+    T, d, f, E, k, C = cfg.T, cfg.d_model, cfg.d_ff, cfg.E, cfg.k, cfg.C
+    e = lambda *s, dtype=dt: torch.empty(*s, dtype=dtype, device=device)
+    return LayerBuffers(
+        cfg=cfg, logits=e(T, E, dtype=torch.float32), idx=e(T, k, dtype=torch.int32), w=e(T, k, dtype=torch.float32),
+        carry=torch.zeros(E, dtype=torch.int32, device=device), fill=e(E, dtype=torch.int32),
+        slot=e(T, k, dtype=torch.int32), send_buf=e(E, C, d), H=e(E, C, f), A=e(E, C, f), O=e(E, C, d), y=e(T, d),
+        dO=e(E, C, d), dH=e(E, C, f), dXe=e(E, C, d), dlogits=e(T, E, dtype=torch.float32), dx=e(T, d),
+        dW1=e(E, f, d), dW2=e(E, d, f), dWg=e(E, d, dtype=torch.float32),
+        ws_dispatch=e(max(16, moe_workspace_bytes(cfg, MOE_CALL_DISPATCH)), dtype=torch.uint8),
+        ws_dx=e(max(16, moe_workspace_bytes(cfg, MOE_CALL_BWD_DX)), dtype=torch.uint8),
+        ws_dw=e(max(16, moe_workspace_bytes(cfg, MOE_CALL_BWD_DW)), dtype=torch.uint8),
+    )
+
+
+def layer_forward(b: LayerBuffers, x, Wg, bias, W1, W2, stream=None):
+    """gate -> dispatch -> experts -> combine, all on one stream."""
+    c = b.cfg
+    moe_gate_topk(c, x, Wg, bias, b.logits, b.idx, b.w, stream)
+    moe_dispatch(c, x, b.idx, b.carry, b.fill, b.slot, b.send_buf, b.ws_dispatch, stream)
+    moe_expert_ffn_fwd(c, b.send_buf, b.carry, b.fill, W1, W2, b.H, b.A, b.O, stream)
+    moe_combine(c, b.O, b.idx, b.slot, b.w, b.y, stream)
+
+
+def layer_backward(b: LayerBuffers, x, Wg, W1, W2, dy, stream=None, dw_stream=None):
+    """dX chain on `stream`; the dW products on `dw_stream` (default: same stream),
+    ordered after the dX chain by an event."""
+    c = b.cfg
+    moe_bwd_dx(c, Wg, b.logits, b.idx, b.w, b.slot, b.carry, b.fill, b.H, b.O, W1, W2, dy, b.dO, b.dH, b.dXe,
+               b.dlogits, b.dx, b.ws_dx, stream)
+    if dw_stream is not None:
+        ev = torch.cuda.Event()
+        ev.record(stream if isinstance(stream, torch.cuda.Stream) else torch.cuda.current_stream())
+        dw_stream.wait_event(ev)
+    moe_bwd_dw(c, x, b.dlogits, b.carry, b.fill, b.send_buf, b.A, b.dO, b.dH, b.dW1, b.dW2, b.dWg, b.ws_dw,
+               dw_stream if dw_stream is not None else stream)

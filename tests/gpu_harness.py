@@ -1,0 +1,86 @@
+"""Helpers for the GPU parity tests: upload seeded inputs, run the HIP layer
+through the C ABI, download results, and compare against the oracle.
+
+Float metric (per tensor): max|gpu - ref| / max|ref| <= tol, with tol 1e-5 for
+float32 workloads and 2e-2 for bf16 ones.  Integer results are compared
+bit-exactly.  Rows of [E][C][*] buffers past an expert's fill are never
+compared; the harness fills those buffers with NaN before the run so a kernel
+that read an unspecified row would poison its outputs and fail the test.
+"""
+from __future__ import annotations
+
+import sys
+
+import numpy as np
+import torch
+
+from oracle import moe_oracle as O
+
+TOL = {"f32": 1e-5, "bf16": 2e-2}
+
+
+def log(msg: str):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def normwise(gpu, ref) -> float:
+    gpu = np.asarray(gpu, np.float64)
+    ref = np.asarray(ref, np.float64)
+    assert gpu.shape == ref.shape, (gpu.shape, ref.shape)
+    if gpu.size == 0:
+        return 0.0
+    assert np.all(np.isfinite(gpu)), "non-finite values in GPU output"
+    scale = np.max(np.abs(ref))
+    err = np.max(np.abs(gpu - ref))
+    return float(err / scale) if scale > 0 else float(err)
+
+
+def assert_close(name, gpu, ref, tol):
+    e = normwise(gpu, ref)
+    assert e <= tol, f"{name}: normwise error {e:.3e} > {tol:.1e}"
+    return e
+
+
+def to_dev(a, dtype):
+    if a is None:
+        return None
+    return torch.from_numpy(np.ascontiguousarray(a, np.float32)).to("cuda").to(dtype).contiguous()
+
+
+def host(t):
+    return t.detach().float().cpu().numpy() if t.is_floating_point() else t.detach().cpu().numpy()
+
+
+def kept_rows(buf, fill, lo=None):
+    """Concatenate rows [lo_e, fill_e) of every expert block."""
+    E = buf.shape[0]
+    lo = np.zeros(E, np.int64) if lo is None else lo
+    return np.concatenate([buf[e, int(lo[e]):int(fill[e])] for e in range(E)], axis=0)
+
+
+def nan_fill(b):
+    for name in ("send_buf", "H", "A", "O", "dO", "dH", "dXe"):
+        getattr(b, name).fill_(float("nan"))
+
+
+def run_layer(L, spec, inp, C, backward=True, dw_stream=None, carry=None):
+    """Run gate -> dispatch -> experts -> combine (and the backward) on cuda:0."""
+    dt = torch.bfloat16 if spec.dtype == "bf16" else torch.float32
+    cfg = L.make_cfg(inp["x"].shape[0], spec.d, spec.f, spec.E, spec.k, C, spec.G, spec.dtype, spec.act,
+                     spec.renorm)
+    b = L.alloc_layer(cfg)
+    nan_fill(b)
+    if carry is not None:
+        b.carry.copy_(torch.as_tensor(np.asarray(carry), dtype=torch.int32))
+    dev = {n: to_dev(inp[n], dt) for n in ("x", "Wg", "W1", "W2", "dy")}
+    bias = None if inp.get("bias") is None else torch.as_tensor(inp["bias"], dtype=torch.float32).cuda()
+    L.layer_forward(b, dev["x"], dev["Wg"], bias, dev["W1"], dev["W2"])
+    if backward:
+        L.layer_backward(b, dev["x"], dev["Wg"], dev["W1"], dev["W2"], dev["dy"], dw_stream=dw_stream)
+    torch.cuda.synchronize()
+    return b, dev
+
+
+def spec_C(spec, T=None):
+    return O.capacity(spec.T if T is None else T, spec.E, spec.k, spec.cf_num, spec.cf_den)

@@ -1,0 +1,111 @@
+"""C-ABI tests that need no GPU: the library loads, exports every symbol the
+header declares, and rejects invalid arguments on the host before launching."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "lancet_moe.h")
+
+L = pytest.importorskip("paper_2404_19429_amd.lancet_moe", reason="library not built")
+
+
+def _declared():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(moe_[a-z_0-9]+)\s*\(", src)))
+
+
+def test_header_declares_and_library_exports_every_symbol():
+    names = _declared()
+    assert set(names) == set(L.EXPORTS), names
+    lib = ctypes.CDLL(L.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+@pytest.mark.parametrize("T,E,k,num,den,expect", [(8192, 16, 2, 5, 4, 1280), (16384, 8, 2, 5, 4, 5120),
+                                                  (32768, 64, 2, 2, 1, 2048), (256, 4, 1, 5, 4, 80),
+                                                  (0, 4, 1, 5, 4, 0), (10, 3, 1, 1, 1, 4)])
+def test_capacity(T, E, k, num, den, expect):
+    assert L.moe_capacity(T, E, k, num, den) == expect
+
+
+@pytest.mark.parametrize("args", [(-1, 4, 1, 1, 1), (10, 0, 1, 1, 1), (10, 4, 0, 1, 1), (10, 4, 1, 0, 1),
+                                  (10, 4, 1, 1, 0), (1 << 40, 1, 8, 8, 1)])
+def test_capacity_invalid(args):
+    assert L.moe_capacity(*args) == -1
+
+
+def _cfg(**kw):
+    base = dict(T=1024, d_model=256, d_ff=512, E=8, k=2, C=320, G=1, dtype="bf16", act="gelu_tanh", renorm=1)
+    base.update(kw)
+    return L.make_cfg(**base)
+
+
+GOOD = 4096  # a fake, 16-byte aligned address: validation never dereferences it
+
+
+def _gate(cfg, x=GOOD, Wg=GOOD, bias=None, logits=GOOD, idx=GOOD, w=GOOD):
+    return L._lib.moe_gate_topk(ctypes.byref(cfg) if cfg is not None else None, x, Wg, bias, logits, idx, w, None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(k=0), L.MOE_EINVAL), (dict(k=9, E=16), L.MOE_EINVAL), (dict(k=5, E=4), L.MOE_EINVAL),
+    (dict(E=0), L.MOE_ESHAPE), (dict(E=65), L.MOE_ESHAPE), (dict(C=0), L.MOE_EINVAL),
+    (dict(G=3), L.MOE_EINVAL), (dict(G=0), L.MOE_EINVAL), (dict(d_model=100), L.MOE_ESHAPE),
+    (dict(d_ff=4), L.MOE_ESHAPE), (dict(T=-1), L.MOE_EINVAL), (dict(act=7), L.MOE_EINVAL),
+    (dict(renorm=2), L.MOE_EINVAL), (dict(dtype=5), L.MOE_EDTYPE),
+])
+def test_invalid_cfg_rejected_before_launch(kw, status):
+    assert _gate(_cfg(**kw)) == status
+    assert L.moe_last_error()
+
+
+def test_null_and_misaligned_pointers():
+    c = _cfg()
+    assert L._lib.moe_gate_topk(None, GOOD, GOOD, None, GOOD, GOOD, GOOD, None) == L.MOE_EINVAL
+    assert _gate(c, x=None) == L.MOE_EINVAL and "x is NULL" in L.moe_last_error()
+    assert _gate(c, idx=None) == L.MOE_EINVAL
+    assert _gate(c, w=GOOD + 4) == L.MOE_EALIGN
+    assert _gate(c, bias=GOOD + 8) == L.MOE_EALIGN
+
+
+def test_valid_call_without_gpu_reports_device_error():
+    assert _gate(_cfg()) == L.MOE_EDEVICE
+    assert "device" in L.moe_last_error()
+
+
+def test_dispatch_workspace_and_alias_checks():
+    c = _cfg()
+    need = L.moe_workspace_bytes(c, L.MOE_CALL_DISPATCH)
+    assert need > 0
+    lib = L._lib
+    assert lib.moe_dispatch(ctypes.byref(c), GOOD, GOOD, None, GOOD, GOOD, GOOD, None, 0, None) == L.MOE_EWORKSPACE
+    assert lib.moe_dispatch(ctypes.byref(c), GOOD, GOOD, None, GOOD, GOOD, GOOD, GOOD, need - 1, None) == L.MOE_EWORKSPACE
+    assert lib.moe_dispatch(ctypes.byref(c), GOOD, GOOD, GOOD, GOOD, GOOD, GOOD, GOOD, need, None) == L.MOE_EINVAL
+    assert "alias" in L.moe_last_error()
+    assert lib.moe_dispatch(ctypes.byref(c), GOOD, GOOD, GOOD, GOOD * 2, GOOD, GOOD, GOOD, need, None) == L.MOE_EDEVICE
+
+
+def test_bf16_gemm_shape_rule():
+    c = _cfg(d_model=72)         # multiple of 8 (gate/dispatch fine) but not of 64
+    lib = L._lib
+    assert lib.moe_expert_ffn_fwd(ctypes.byref(c), *([GOOD] * 8), None) == L.MOE_ESHAPE
+    assert _gate(c) == L.MOE_EDEVICE
+    c32 = _cfg(d_model=72, dtype="f32")
+    assert lib.moe_expert_ffn_fwd(ctypes.byref(c32), *([GOOD] * 8), None) == L.MOE_EDEVICE
+
+
+def test_workspace_bytes_invalid_cfg_is_zero():
+    assert L.moe_workspace_bytes(_cfg(k=0), 0) == 0
+    assert L.moe_workspace_bytes(_cfg(), 9) == 0
+
+
+def test_binding_rejects_host_tensors_and_short_buffers():
+    import torch
+    c = _cfg(T=4, d_model=8, d_ff=8, E=2, k=1, C=4)
+    with pytest.raises(ValueError, match="device tensor"):
+        L.moe_gate_topk(c, torch.zeros(4, 8, dtype=torch.bfloat16), None, None, None, None, None, stream=0)

@@ -240,3 +240,21 @@ def test_gelu_tanh_closed_values():
     np.testing.assert_allclose(O.act_grad(hs, "gelu_tanh"), num, rtol=1e-7, atol=1e-9)
     ref = 0.5 * hs * (1 + np.array([math.erf(v / math.sqrt(2)) for v in hs]))
     np.testing.assert_allclose(O.act(hs, "gelu_erf"), ref, rtol=1e-13, atol=1e-15)
+
+
+def test_sampled_dw_forms_match_layer():
+    spec = _spec(T=60, E=3, k=2, act="gelu_tanh")
+    inp = _inputs(spec, seed=13, skew=1.0)
+    fw = O.layer_forward(spec, inp)
+    bw = O.layer_backward(spec, inp, fw)
+    for e in range(spec.E):
+        X, dO = O.expert_rows(inp["x"], inp["dy"], fw["idx"], fw["slot"], fw["w"], e)
+        n = int(fw["fill"][e])
+        np.testing.assert_allclose(X, fw["buf"][e, :n], rtol=0, atol=0)
+        np.testing.assert_allclose(dO, bw["dO"][e, :n], rtol=1e-15, atol=0)
+        for i in (0, spec.f - 1, 5):
+            np.testing.assert_allclose(O.expert_dw1_row(X, dO, inp["W1"][e], inp["W2"][e], spec.act, i),
+                                       bw["dW1"][e, i], rtol=1e-11, atol=1e-13)
+        for c in (0, spec.f - 1, 7):
+            np.testing.assert_allclose(O.expert_dw2_col(X, dO, inp["W1"][e], spec.act, c),
+                                       bw["dW2"][e, :, c], rtol=1e-11, atol=1e-13)
