@@ -49,10 +49,28 @@ def _compile(src: str, verbose: bool) -> str:
     return obj
 
 
+def _check_gemm_isa(verbose: bool) -> None:
+    """Refuse a build whose GEMM uses an inline-asm LDS read before its wait."""
+    from paper_2404_19429_amd.isa_check import check_text
+    out = os.path.join(BUILD, "gemm.s")
+    cmd = [_hipcc(), "-x", "hip", "-S", "--offload-device-only", os.path.join(CSRC, "gemm.hip"), "-o", out] + HIPCC_FLAGS
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError("hipcc -S failed on gemm.hip:\n" + r.stderr)
+    bad = check_text(open(out).read())
+    if bad:
+        detail = "\n".join(f"{k}: {v[:3]}" for k, v in bad.items())
+        raise RuntimeError("GEMM ISA check failed: asm LDS read results used before their wait\n" + detail)
+    if verbose:
+        print("GEMM ISA check passed", flush=True)
+
+
 def build(verbose: bool = False) -> str:
     os.makedirs(BUILD, exist_ok=True)
-    with cf.ThreadPoolExecutor(max_workers=min(8, len(SOURCES))) as ex:
+    with cf.ThreadPoolExecutor(max_workers=min(8, len(SOURCES) + 1)) as ex:
+        isa = ex.submit(_check_gemm_isa, verbose)
         objs = list(ex.map(lambda s: _compile(s, verbose), SOURCES))
+        isa.result()
     tmp = LIB + ".tmp"
     cmd = [_hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp] + objs
     if verbose:
@@ -65,4 +83,6 @@ def build(verbose: bool = False) -> str:
 
 
 if __name__ == "__main__":
+    if ROOT not in sys.path:
+        sys.path.insert(0, ROOT)
     print(build(verbose="-v" in sys.argv))

@@ -71,181 +71,379 @@ __device__ __forceinline__ void epilogue_store(const GemmParams& p, int64_t off,
 }
 
 // ----------------------------------------------------------------- bf16 MFMA
-// Tile loader for an operand whose K dimension is contiguous in memory:
-// ROWS (M or N) x BK tile, 16-byte vectors along K.
-template <int ROWS, int BK, int NT>
-struct LoadKContig {
-  static constexpr int KV = BK / 8;
-  static constexpr int NV = ROWS * KV / NT;
-  static_assert(NV >= 1 && ROWS * KV % NT == 0, "tile/threads mismatch");
-  u32x4 v[NV];
-  __device__ void load(const uint16_t* base, int64_t ld, int row0, int rowlim, int k0, int klim, int tid) {
+// Operand tiles (BK = 32, one MFMA K step) move global -> LDS with
+// global_load_lds_dwordx4 (each lane's 16 bytes land at LDS base + 16 * lane)
+// into a STAGES-deep ring.  A lane whose element lies outside the operand
+// reads a 16-byte zero page instead, so every wave issues the same number of
+// loads per tile and the vmcnt arithmetic below is exact.  Barriers inside the
+// K loop are plain s_barrier (with a compiler memory clobber) preceded by an
+// explicit s_waitcnt: a full __syncthreads() fence would also drain the loads
+// that are meant to stay in flight.
+//
+// Schedule of iteration kt: wait until tile kt+1 has landed, barrier, refill
+// the stage of tile kt (its fragments are already in registers) with tile
+// kt+STAGES, read the fragments of tile kt+1, and multiply tile kt.  Loads get
+// STAGES-1 iterations to land and fragment reads overlap the MFMAs.
+//
+// LDS layouts:
+//  * K-contiguous operand, ROWS x 32: fragment-linear.  The 16 x 32 MFMA
+//    fragment of rows 16f..16f+15 is 1 KB at offset 1 KB * f, lane L's 16
+//    bytes (row 16f + L%16, k = 8*(L/16) .. +7) at 16 * L: one DMA instruction
+//    fills one fragment and one ds_read_b128 reads it, both linear.
+//  * MN-contiguous operand, 32 x COLS (row = k, as in memory): 16-byte chunk c
+//    of row k stored at chunk c ^ hsw(k), hsw(k) = 2 * ((k & 3) | ((k >> 3) & 1) << 2).
+//    Fragments are read with ds_read_b64_tr_b16: within each 16-lane group,
+//    lane j addresses row k0 + j/4, columns n0 + 4*(j%4) .. +3, and receives
+//    column n0 + j of rows k0 .. k0+3 -- two such reads give the 8-element K
+//    run of the MFMA operand.
+constexpr int kBKb = 32;
+__device__ __forceinline__ int hsw(int k) { return 2 * ((k & 3) | (((k >> 3) & 1) << 2)); }
+
+__device__ __attribute__((aligned(16))) uint32_t g_zero16[4];  // zero-initialised, never written
+
+typedef __attribute__((address_space(3))) void lds_void;
+
+__device__ __forceinline__ void dma16(const void* src, uint16_t* lds_wave_base) {
+  __builtin_amdgcn_global_load_lds(src, (lds_void*)lds_wave_base, 16, 0, 0);
+}
+
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_barrier" ::: "memory"); }
+
+// Fragment reads are inline asm (ds_read_b128 and ds_read_b64_tr_b16) so that
+// the compiler, which cannot tell them apart from the in-flight LDS-DMA tile
+// loads, does not drain those loads before them (it does for the builtins).
+// Each asm block issues up to kReadChunk reads and ends with
+// s_waitcnt lgkmcnt(0): its outputs are complete when the block ends, so the
+// compiler may copy, spill or reuse them freely, and the LGKM counter never
+// holds more than kReadChunk of them.  Read latency still overlaps the MFMAs
+// issued before the block, which keep executing while the wave waits.
+constexpr int kReadChunk = 8;
+__device__ __forceinline__ uint32_t lds_addr(const uint16_t* p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) uint16_t*)p;
+}
+
+#define LMOE_R128(i) "ds_read_b128 %" #i ", %" #i "\n"
+template <int N> struct Rd128;
+template <> struct Rd128<8> {
+  __device__ static void run(u32x4* o, const uint32_t* a) {
+    asm volatile("ds_read_b128 %0, %8\n ds_read_b128 %1, %9\n ds_read_b128 %2, %10\n ds_read_b128 %3, %11\n"
+                 "ds_read_b128 %4, %12\n ds_read_b128 %5, %13\n ds_read_b128 %6, %14\n ds_read_b128 %7, %15\n"
+                 "s_waitcnt lgkmcnt(0)"
+                 : "=&v"(o[0]), "=&v"(o[1]), "=&v"(o[2]), "=&v"(o[3]), "=&v"(o[4]), "=&v"(o[5]), "=&v"(o[6]), "=&v"(o[7])
+                 : "v"(a[0]), "v"(a[1]), "v"(a[2]), "v"(a[3]), "v"(a[4]), "v"(a[5]), "v"(a[6]), "v"(a[7])
+                 : "memory");
+  }
+};
+template <> struct Rd128<4> {
+  __device__ static void run(u32x4* o, const uint32_t* a) {
+    asm volatile("ds_read_b128 %0, %4\n ds_read_b128 %1, %5\n ds_read_b128 %2, %6\n ds_read_b128 %3, %7\n"
+                 "s_waitcnt lgkmcnt(0)"
+                 : "=&v"(o[0]), "=&v"(o[1]), "=&v"(o[2]), "=&v"(o[3])
+                 : "v"(a[0]), "v"(a[1]), "v"(a[2]), "v"(a[3])
+                 : "memory");
+  }
+};
+template <int N> struct RdTr;
+template <> struct RdTr<8> {
+  __device__ static void run(u32x2* o, const uint32_t* a) {
+    asm volatile("ds_read_b64_tr_b16 %0, %8\n ds_read_b64_tr_b16 %1, %9\n ds_read_b64_tr_b16 %2, %10\n"
+                 "ds_read_b64_tr_b16 %3, %11\n ds_read_b64_tr_b16 %4, %12\n ds_read_b64_tr_b16 %5, %13\n"
+                 "ds_read_b64_tr_b16 %6, %14\n ds_read_b64_tr_b16 %7, %15\n"
+                 "s_waitcnt lgkmcnt(0)"
+                 : "=&v"(o[0]), "=&v"(o[1]), "=&v"(o[2]), "=&v"(o[3]), "=&v"(o[4]), "=&v"(o[5]), "=&v"(o[6]), "=&v"(o[7])
+                 : "v"(a[0]), "v"(a[1]), "v"(a[2]), "v"(a[3]), "v"(a[4]), "v"(a[5]), "v"(a[6]), "v"(a[7])
+                 : "memory");
+  }
+};
+#undef LMOE_R128
+
+// vmcnt(n) (gfx9 encoding; expcnt and lgkmcnt unrestricted).
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+
+// Wait until at most n * LPS vector-memory operations are pending (n <= NMAX, decided at run time).
+template <int LPS, int NMAX>
+__device__ __forceinline__ void wait_vm_tiles(int n) {
+  if constexpr (NMAX <= 0) {
+    wait_vm<0>();
+  } else {
+    if (n >= NMAX) wait_vm<NMAX * LPS>();
+    else wait_vm_tiles<LPS, NMAX - 1>(n);
+  }
+}
+
+// K-contiguous operand: ROWS x 32 tile, one wave instruction fills one fragment.
+template <int ROWS, int NW>
+struct TileK {
+  static constexpr int NI = ROWS / 16 / NW;     // loads per wave per tile
+  static_assert(NI >= 1 && ROWS % (16 * NW) == 0, "tile/waves mismatch");
+  __device__ static void issue(const uint16_t* base, int64_t ld, int row0, int rowlim, int k0, int klim,
+                               uint16_t* stage, int wid, int lane) {
 #pragma unroll
-    for (int i = 0; i < NV; ++i) {
-      const int q = tid + i * NT;
-      const int r = q / KV, kc = q % KV;
-      const int row = row0 + r, k = k0 + kc * 8;
-      if (row < rowlim && k < klim) v[i] = *reinterpret_cast<const u32x4*>(base + (int64_t)row * ld + k);
-      else v[i] = u32x4{0u, 0u, 0u, 0u};
+    for (int i = 0; i < NI; ++i) {
+      const int q = i * NW + wid;
+      const int row = row0 + 16 * q + (lane & 15), k = k0 + 8 * (lane >> 4);
+      const void* src = (row < rowlim && k < klim) ? (const void*)(base + (int64_t)row * ld + k) : (const void*)g_zero16;
+      dma16(src, stage + q * 512);
     }
   }
-  __device__ void store(uint16_t* lds, int ldk, int tid) const {
+  // Reads FN fragments (rows r0 + 16 j) of one stage, kReadChunk per asm block.
+  template <int NF>
+  __device__ static void read(u32x4 (&f)[NF], const uint16_t* stage, int r0, int lane) {
+    static_assert(NF % 4 == 0, "fragment count");
 #pragma unroll
-    for (int i = 0; i < NV; ++i) {
-      const int q = tid + i * NT;
-      const int r = q / KV, kc = q % KV;
-      *reinterpret_cast<u32x4*>(lds + r * ldk + kc * 8) = v[i];
+    for (int c = 0; c < NF; c += (NF >= 8 ? 8 : 4)) {
+      constexpr int N = NF >= 8 ? 8 : 4;
+      uint32_t a[N];
+#pragma unroll
+      for (int u = 0; u < N; ++u) a[u] = lds_addr(stage + ((r0 >> 4) + c + u) * 512 + lane * 8);
+      Rd128<N>::run(&f[c], a);
     }
   }
 };
 
-// Tile loader for an operand that is contiguous along M/N: memory row = k.
-// Each thread loads R consecutive k rows of 8 MN values and writes the
-// transposed 8 x R block as K runs.
-template <int COLS, int BK, int NT>
-struct LoadMNContig {
-  static constexpr int CB = COLS / 8;
-  static constexpr int R = ((BK / 8) * CB >= NT) ? 8 : 4;
-  static constexpr int NS = (BK / R) * CB / NT;
-  static_assert(NS >= 1 && (BK / R) * CB % NT == 0, "tile/threads mismatch");
-  u32x4 v[NS][R];
-  __device__ void load(const uint16_t* base, int64_t ld, int col0, int collim, int k0, int klim, int tid) {
+// MN-contiguous operand: 32 x COLS tile (row = k), one wave instruction fills 64 chunks.
+template <int COLS, int NW>
+struct TileMN {
+  static constexpr int CPR = COLS / 8;          // 16-byte chunks per row
+  static constexpr int NI = kBKb * CPR / 64 / NW;
+  static_assert(NI >= 1 && (kBKb * CPR) % (64 * NW) == 0 && CPR >= 16, "tile/waves mismatch");
+  __device__ static void issue(const uint16_t* base, int64_t ld, int col0, int collim, int k0, int klim,
+                               uint16_t* stage, int wid, int lane) {
 #pragma unroll
-    for (int i = 0; i < NS; ++i) {
-      const int q = tid + i * NT;
-      const int cb = q % CB, kb = q / CB;
-      const int col = col0 + cb * 8;
-#pragma unroll
-      for (int j = 0; j < R; ++j) {
-        const int k = k0 + kb * R + j;
-        if (col < collim && k < klim) v[i][j] = *reinterpret_cast<const u32x4*>(base + (int64_t)k * ld + col);
-        else v[i][j] = u32x4{0u, 0u, 0u, 0u};
-      }
+    for (int i = 0; i < NI; ++i) {
+      const int q = i * NW + wid;
+      const int L = q * 64 + lane;
+      const int k = L / CPR;
+      const int lc = (L % CPR) ^ hsw(k);
+      const int col = col0 + 8 * lc, kk = k0 + k;
+      const void* src = (col < collim && kk < klim) ? (const void*)(base + (int64_t)kk * ld + col) : (const void*)g_zero16;
+      dma16(src, stage + q * 512);
     }
   }
-  __device__ void store(uint16_t* lds, int ldk, int tid) const {
+  // Reads NF 16 (m or n) x 32 k fragments at columns c0 + 16 j: lane gets column
+  // c0 + 16 j + lane%16, k = 8*(lane/16) .. +7 (two transposed reads: k .. k+3, k+4 .. k+7).
+  template <int NF>
+  __device__ static void read(u32x4 (&f)[NF], const uint16_t* stage, int c0, int lane) {
+    static_assert(NF % 4 == 0, "fragment count");
+    const int j = lane & 15;
+    const int k = 8 * (lane >> 4) + (j >> 2);
+    const int h = hsw(k);                                 // hsw(k + 4) == hsw(k)
 #pragma unroll
-    for (int i = 0; i < NS; ++i) {
-      const int q = tid + i * NT;
-      const int cb = q % CB, kb = q / CB;
+    for (int c = 0; c < NF; c += 4) {
+      uint32_t a[8];
 #pragma unroll
-      for (int c = 0; c < 8; ++c) {
-        uint32_t o[R / 2];
-#pragma unroll
-        for (int qq = 0; qq < R / 2; ++qq) {
-          const uint32_t lo = v[i][2 * qq][c >> 1], hi = v[i][2 * qq + 1][c >> 1];
-          o[qq] = (c & 1) ? ((lo >> 16) | (hi & 0xffff0000u)) : ((lo & 0xffffu) | (hi << 16));
-        }
-        uint16_t* dst = lds + (cb * 8 + c) * ldk + kb * R;
-        if constexpr (R == 8) *reinterpret_cast<u32x4*>(dst) = u32x4{o[0], o[1], o[2], o[3]};
-        else *reinterpret_cast<u32x2*>(dst) = u32x2{o[0], o[1]};
+      for (int u = 0; u < 4; ++u) {
+        const int col = c0 + 16 * (c + u) + 4 * (j & 3);
+        const int off = k * COLS + (((col >> 3) ^ h) << 3) + (col & 7);
+        a[2 * u] = lds_addr(stage + off);
+        a[2 * u + 1] = lds_addr(stage + off + 4 * COLS);
       }
+      u32x2 o[8];
+      RdTr<8>::run(o, a);
+#pragma unroll
+      for (int u = 0; u < 4; ++u) f[c + u] = u32x4{o[2 * u][0], o[2 * u][1], o[2 * u + 1][0], o[2 * u + 1][1]};
     }
   }
 };
 
-template <int BM, int BN, int BK, int WGM, int WGN, bool B_K, bool RAGGED_K, int EPI, typename OutT>
-__global__ __launch_bounds__(WGM* WGN * 64) void gemm_bf16_kernel(GemmParams p) {
-  constexpr int NT = WGM * WGN * 64;
+// Persistent grouped GEMM: one block per CU walks the list of real tiles of
+// all groups.  Tiles are numbered group by group, m-tile by m-tile, n fastest;
+// the list is cut into 8 contiguous ranges, one per XCD (workgroups are
+// dealt to XCDs round-robin by block index), so the blocks sharing an XCD's
+// L2 work on neighbouring tiles that share A rows and B columns.
+template <int BM, int BN, int WGM, int WGN, int STAGES, int OCC, bool B_K, bool RAGGED_K, int EPI, int ACT>
+__global__ __attribute__((amdgpu_flat_work_group_size(WGM * WGN * 64, WGM * WGN * 64),
+                          amdgpu_waves_per_eu(OCC, OCC))) void
+gemm_bf16_kernel(GemmParams p, int tilesM, int tilesN, int groups) {
+  constexpr int NW = WGM * WGN;
   constexpr int WTM = BM / WGM, WTN = BN / WGN;
   constexpr int FM = WTM / 16, FN = WTN / 16;
-  constexpr int LDK = BK + 8;
-  static_assert(BK % 32 == 0, "BK must be a multiple of the MFMA K (32)");
-  __shared__ __attribute__((aligned(16))) uint16_t As[2][BM * LDK];
-  __shared__ __attribute__((aligned(16))) uint16_t Bs[2][BN * LDK];
+  constexpr int BK = kBKb;
+  constexpr int STAGE = (BM + BN) * BK;          // elements per pipeline stage
+  constexpr int EPI_LD = WTN + 4;                // fp32 staging row stride
+  constexpr int EPI_ROWS = (NW * 32 * EPI_LD * 4 <= STAGES * STAGE * 2) ? 32 : 16;  // rows staged at once
+  constexpr bool A_K = !RAGGED_K;
+  constexpr bool BK_C = B_K && !RAGGED_K;
+  using TA = typename std::conditional<A_K, TileK<BM, NW>, TileMN<BM, NW>>::type;
+  using TB = typename std::conditional<BK_C, TileK<BN, NW>, TileMN<BN, NW>>::type;
+  constexpr int LPS = TA::NI + TB::NI;           // loads per wave per stage
+  static_assert(STAGES >= 2 && LPS * (STAGES - 1) < 64, "vmcnt range");
+  static_assert(WTM % EPI_ROWS == 0, "wave tile rows must be a multiple of the staged slice");
+  static_assert(NW * EPI_ROWS * EPI_LD * 4 <= STAGES * STAGE * 2, "epilogue staging does not fit");
+  extern __shared__ __attribute__((aligned(16))) uint16_t lds[];
+  __shared__ int s_prefix[kMaxE + 1];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wid = tid >> 6;
   const int wm = wid / WGN, wn = wid % WGN;
-  const int g = blockIdx.z;
-  const int m0 = blockIdx.y * BM;
-  const int n0 = blockIdx.x * BN;
 
-  int lo, span;
-  group_rows(p, g, lo, span);
-  int Mlim, Klim;
-  if constexpr (RAGGED_K) {
-    Mlim = p.M;
-    Klim = span;
-  } else {
-    Mlim = span;
-    Klim = p.K;
-    if (m0 >= Mlim) return;
-  }
-
-  const uint16_t* Ab;
-  const uint16_t* Bb;
-  if constexpr (RAGGED_K) {
-    Ab = (const uint16_t*)p.A + g * p.sA + (int64_t)lo * p.lda;
-    Bb = (const uint16_t*)p.B + g * p.sB + (int64_t)lo * p.ldb;
-  } else {
-    Ab = (const uint16_t*)p.A + g * p.sA + (int64_t)lo * p.lda;
-    Bb = (const uint16_t*)p.B + g * p.sB;
-  }
-
-  using ALoader = typename std::conditional<RAGGED_K, LoadMNContig<BM, BK, NT>, LoadKContig<BM, BK, NT>>::type;
-  using BLoader = typename std::conditional<B_K && !RAGGED_K, LoadKContig<BN, BK, NT>, LoadMNContig<BN, BK, NT>>::type;
-  ALoader la;
-  BLoader lb;
-
-  f32x4 acc[FM][FN];
-#pragma unroll
-  for (int i = 0; i < FM; ++i)
-#pragma unroll
-    for (int j = 0; j < FN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-  const int nk = (Klim + BK - 1) / BK;
-  if (nk > 0) {
-    la.load(Ab, p.lda, m0, Mlim, 0, Klim, tid);
-    lb.load(Bb, p.ldb, n0, p.N, 0, Klim, tid);
-    la.store(As[0], LDK, tid);
-    lb.store(Bs[0], LDK, tid);
-    __syncthreads();
-  }
-  for (int kt = 0; kt < nk; ++kt) {
-    const int cur = kt & 1;
-    const bool more = kt + 1 < nk;
-    if (more) {
-      la.load(Ab, p.lda, m0, Mlim, (kt + 1) * BK, Klim, tid);
-      lb.load(Bb, p.ldb, n0, p.N, (kt + 1) * BK, Klim, tid);
-    }
-    const uint16_t* as = As[cur] + (wm * WTM + (lane & 15)) * LDK + (lane >> 4) * 8;
-    const uint16_t* bs = Bs[cur] + (wn * WTN + (lane & 15)) * LDK + (lane >> 4) * 8;
-#pragma unroll
-    for (int ks = 0; ks < BK / 32; ++ks) {
-      bf16x8 af[FM], bfr[FN];
-#pragma unroll
-      for (int i = 0; i < FM; ++i) af[i] = *reinterpret_cast<const bf16x8*>(as + i * 16 * LDK + ks * 32);
-#pragma unroll
-      for (int j = 0; j < FN; ++j) bfr[j] = *reinterpret_cast<const bf16x8*>(bs + j * 16 * LDK + ks * 32);
-#pragma unroll
-      for (int i = 0; i < FM; ++i)
-#pragma unroll
-        for (int j = 0; j < FN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
-    }
-    if (more) {
-      la.store(As[cur ^ 1], LDK, tid);
-      lb.store(Bs[cur ^ 1], LDK, tid);
-    }
-    __syncthreads();
-  }
-
-  // Lane holds C[4*(lane/16) + v][lane % 16] of each 16x16 block.
-  const int64_t cbase = (int64_t)g * p.sC + (RAGGED_K ? 0 : (int64_t)lo * p.ldc);
-#pragma unroll
-  for (int i = 0; i < FM; ++i) {
-#pragma unroll
-    for (int v = 0; v < 4; ++v) {
-      const int row = m0 + wm * WTM + i * 16 + 4 * (lane >> 4) + v;
-      if (row >= Mlim) continue;
-#pragma unroll
-      for (int j = 0; j < FN; ++j) {
-        const int col = n0 + wn * WTN + j * 16 + (lane & 15);
-        if (col < p.N) epilogue_store<EPI, OutT>(p, cbase + (int64_t)row * p.ldc + col, acc[i][j][v]);
+  // Tile counts per group -> exclusive prefix (one wave, groups <= 64).
+  if (wid == 0) {
+    int cnt = 0;
+    if (lane < groups) {
+      if constexpr (RAGGED_K) {
+        cnt = tilesM * tilesN;
+      } else {
+        int lo, span;
+        group_rows(p, lane, lo, span);
+        cnt = ((span + BM - 1) / BM) * tilesN;
       }
     }
+    int incl = cnt;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int u = __shfl_up(incl, o, 64);
+      if (lane >= o) incl += u;
+    }
+    if (lane < groups) s_prefix[lane + 1] = incl;
+    if (lane == 0) s_prefix[0] = 0;
+  }
+  __syncthreads();
+  const int total = s_prefix[groups];
+  const int nslot = gridDim.x / 8;
+  const int xcd = blockIdx.x % 8, slot = blockIdx.x / 8;
+  const int per = (total + 7) / 8;
+  const int t_begin = xcd * per + slot;
+  const int t_end = min(total, (xcd + 1) * per);
+
+  for (int t = t_begin; t < t_end; t += nslot) {
+    int g = 0;
+    while (g + 1 < groups && s_prefix[g + 1] <= t) ++g;
+    const int local = t - s_prefix[g];
+    const int m0 = (local / tilesN) * BM;
+    const int n0 = (local % tilesN) * BN;
+    int lo, span;
+    group_rows(p, g, lo, span);
+    const int Mlim = RAGGED_K ? p.M : span;
+    const int Klim = RAGGED_K ? span : p.K;
+    const uint16_t* Ab = (const uint16_t*)p.A + g * p.sA + (int64_t)lo * p.lda;
+    const uint16_t* Bb = (const uint16_t*)p.B + g * p.sB + (RAGGED_K ? (int64_t)lo * p.ldb : 0);
+
+    f32x4 acc[FM][FN];
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < FN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    const int nk = (Klim + BK - 1) / BK;
+    auto issue = [&](int kt) {
+      uint16_t* st = lds + (kt % STAGES) * STAGE;
+      TA::issue(Ab, p.lda, m0, Mlim, kt * BK, Klim, st, wid, lane);
+      TB::issue(Bb, p.ldb, n0, p.N, kt * BK, Klim, st + BM * BK, wid, lane);
+    };
+    // Fragment reads of one tile: the A fragments, then the B fragments, each in
+    // asm blocks of at most kReadChunk reads that complete before they return.
+    auto read_a = [&](int kt, u32x4 (&fa)[FM]) {
+      TA::template read<FM>(fa, lds + (kt % STAGES) * STAGE, wm * WTM, lane);
+    };
+    auto read_b = [&](int kt, u32x4 (&fb)[FN]) {
+      TB::template read<FN>(fb, lds + (kt % STAGES) * STAGE + BM * BK, wn * WTN, lane);
+    };
+    auto mfma_rows = [&](int i0, int i1, u32x4 (&ca)[FM], u32x4 (&cb)[FN]) {
+#pragma unroll
+      for (int i = 0; i < FM; ++i) {
+        if (i < i0 || i >= i1) continue;
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, ca[i]),
+                                                              __builtin_bit_cast(bf16x8, cb[j]), acc[i][j], 0, 0, 0);
+      }
+    };
+    // One K step: multiply tile kt (fragments in ca/cb) in two halves; the
+    // fragments of tile kt+1 are read into na/nb before each half, so the read
+    // latency overlaps the MFMAs already in the pipe.  Called with the two
+    // register sets in alternating roles (static indexing).
+    auto step = [&](int kt, u32x4 (&ca)[FM], u32x4 (&cb)[FN], u32x4 (&na)[FM], u32x4 (&nb)[FN]) {
+      const bool more = kt + 1 < nk;
+      if (more) {
+        // tile kt+1 has landed once only tiles kt+2 .. min(kt+STAGES-1, nk-1) are pending
+        wait_vm_tiles<LPS, STAGES - 2>(min(STAGES - 2, nk - 2 - kt));
+        lds_barrier();  // tile kt+1 is in LDS for every wave; no wave reads tile kt's stage any more
+        if (kt + STAGES < nk) issue(kt + STAGES);
+        read_a(kt + 1, na);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      mfma_rows(0, FM / 2, ca, cb);
+      __builtin_amdgcn_sched_barrier(0);
+      if (more) read_b(kt + 1, nb);
+      __builtin_amdgcn_sched_barrier(0);
+      mfma_rows(FM / 2, FM, ca, cb);
+      __builtin_amdgcn_sched_barrier(0);
+    };
+
+    u32x4 fa0[FM], fb0[FN], fa1[FM], fb1[FN];
+    if (nk > 0) {
+#pragma unroll
+      for (int s = 0; s < STAGES; ++s)
+        if (s < nk) issue(s);
+      wait_vm_tiles<LPS, STAGES - 1>(min(STAGES - 1, nk - 1));  // tile 0 has landed
+      lds_barrier();
+      read_a(0, fa0);
+      read_b(0, fb0);
+    }
+    for (int kt = 0; kt < nk; kt += 2) {
+      step(kt, fa0, fb0, fa1, fb1);
+      if (kt + 1 < nk) step(kt + 1, fa1, fb1, fa0, fb0);
+    }
+    wait_vm<0>();
+    lds_barrier();  // all waves are done reading the operand stages
+
+    // Epilogue: stage 32-row slices of the wave tile through LDS as float,
+    // then write 16-byte vectors (8 bf16) with the epilogue applied.
+    float* st = reinterpret_cast<float*>(lds) + wid * (EPI_ROWS * EPI_LD);
+    uint16_t* C = (uint16_t*)p.C + (int64_t)g * p.sC + (RAGGED_K ? 0 : (int64_t)lo * p.ldc);
+    uint16_t* C2 = EPI == EPI_FWD1 ? (uint16_t*)p.C2 + (int64_t)g * p.sC + (int64_t)lo * p.ldc : nullptr;
+    const uint16_t* Aux = EPI == EPI_DACT ? (const uint16_t*)p.Aux + (int64_t)g * p.sC + (int64_t)lo * p.ldc : nullptr;
+    const int g4 = lane >> 4;
+#pragma unroll
+    for (int pass = 0; pass < WTM / EPI_ROWS; ++pass) {
+#pragma unroll
+      for (int ii = 0; ii < EPI_ROWS / 16; ++ii) {
+        const int i = pass * (EPI_ROWS / 16) + ii;
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+#pragma unroll
+          for (int v = 0; v < 4; ++v) st[(ii * 16 + 4 * g4 + v) * EPI_LD + j * 16 + (lane & 15)] = acc[i][j][v];
+      }
+      // The staging slice is private to this wave and LDS executes a wave's
+      // accesses in order, so no barrier is needed between writes and reads.
+      constexpr int CPR = WTN / 8;          // 8-column chunks per row
+#pragma unroll
+      for (int q = lane; q < EPI_ROWS * CPR; q += 64) {
+        const int rr = q / CPR, cc = q % CPR;
+        const int row = m0 + wm * WTM + pass * EPI_ROWS + rr;
+        const int col = n0 + wn * WTN + cc * 8;
+        if (row < Mlim && col < p.N) {
+          float v[8];
+          const f32x4 a = *reinterpret_cast<const f32x4*>(st + rr * EPI_LD + cc * 8);
+          const f32x4 b = *reinterpret_cast<const f32x4*>(st + rr * EPI_LD + cc * 8 + 4);
+#pragma unroll
+          for (int u = 0; u < 4; ++u) { v[u] = a[u]; v[4 + u] = b[u]; }
+          const int64_t off = (int64_t)row * p.ldc + col;
+          if constexpr (EPI == EPI_FWD1) {
+            Vec<uint16_t>::store(C + off, v);
+#pragma unroll
+            for (int u = 0; u < 8; ++u) v[u] = act_fwd_t<ACT>(v[u]);
+            Vec<uint16_t>::store(C2 + off, v);
+          } else if constexpr (EPI == EPI_DACT) {
+            float h[8];
+            Vec<uint16_t>::load(Aux + off, h);
+#pragma unroll
+            for (int u = 0; u < 8; ++u) v[u] *= act_bwd_t<ACT>(h[u]);
+            Vec<uint16_t>::store(C + off, v);
+          } else {
+            Vec<uint16_t>::store(C + off, v);
+          }
+        }
+      }
+    }
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    lds_barrier();  // every wave is done with its staging slice before the next tile's loads land
   }
 }
 
@@ -327,15 +525,58 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmParams p) {
 }
 
 // --------------------------------------------------------------- launchers
-constexpr int kBM = 128, kBN = 128, kBK = 64, kWGM = 2, kWGN = 2;
+// Tile shape, LDS stages and resident blocks per CU (OCC) of the bf16 kernel.
+#ifndef LMOE_GEMM_TILE
+#define LMOE_GEMM_TILE 128, 128, 2, 2, 4, 2
+#endif
+template <int BM_, int BN_, int WGM_, int WGN_, int STAGES_, int OCC_> struct TileCfg {
+  static constexpr int BM = BM_, BN = BN_, WGM = WGM_, WGN = WGN_, STAGES = STAGES_, OCC = OCC_;
+};
+using Tile = TileCfg<LMOE_GEMM_TILE>;
+constexpr int kBM = Tile::BM, kBN = Tile::BN;
+
+static int num_cus() {
+  static int n = 0;
+  if (n == 0) {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
+      n = 256;
+  }
+  return n;
+}
+
+template <bool B_K, bool RAGGED_K, int EPI, int ACT>
+static void launch_bf16(const moe_cfg& c, const GemmParams& p, int tilesM, int tilesN, hipStream_t s) {
+  constexpr int NT = Tile::WGM * Tile::WGN * 64;
+  constexpr size_t shmem = Tile::STAGES * (size_t)(Tile::BM + Tile::BN) * kBKb * sizeof(uint16_t);
+  auto kern = gemm_bf16_kernel<Tile::BM, Tile::BN, Tile::WGM, Tile::WGN, Tile::STAGES, Tile::OCC, B_K, RAGGED_K, EPI, ACT>;
+  static bool attr_set = false;
+  if (!attr_set) {
+    (void)hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)shmem);
+    attr_set = true;
+  }
+  const int64_t max_tiles = (int64_t)tilesM * tilesN * c.E;
+  int blocks = num_cus() * Tile::OCC;
+  if (max_tiles < blocks) blocks = (int)((max_tiles + 7) / 8 * 8);
+  blocks = (blocks + 7) / 8 * 8;
+  hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(NT), shmem, s, p, tilesM, tilesN, c.E);
+}
 
 template <bool B_K, bool RAGGED_K, int EPI>
 static void run_gemm(const moe_cfg& c, const GemmParams& p, int tilesM, int tilesN, hipStream_t s) {
   if (tilesM <= 0 || tilesN <= 0 || c.E <= 0) return;
   if (c.dtype == MOE_BF16) {
-    dim3 grid((unsigned)tilesN, (unsigned)tilesM, (unsigned)c.E);
-    hipLaunchKernelGGL((gemm_bf16_kernel<kBM, kBN, kBK, kWGM, kWGN, B_K, RAGGED_K, EPI, uint16_t>), grid,
-                       dim3(kWGM * kWGN * 64), 0, s, p);
+    if constexpr (EPI == EPI_STORE) {
+      launch_bf16<B_K, RAGGED_K, EPI, MOE_ACT_IDENTITY>(c, p, tilesM, tilesN, s);
+    } else {
+      switch (c.act) {
+        case MOE_ACT_RELU: launch_bf16<B_K, RAGGED_K, EPI, MOE_ACT_RELU>(c, p, tilesM, tilesN, s); break;
+        case MOE_ACT_GELU_TANH: launch_bf16<B_K, RAGGED_K, EPI, MOE_ACT_GELU_TANH>(c, p, tilesM, tilesN, s); break;
+        case MOE_ACT_GELU_ERF: launch_bf16<B_K, RAGGED_K, EPI, MOE_ACT_GELU_ERF>(c, p, tilesM, tilesN, s); break;
+        default: launch_bf16<B_K, RAGGED_K, EPI, MOE_ACT_IDENTITY>(c, p, tilesM, tilesN, s); break;
+      }
+    }
   } else {
     dim3 grid((unsigned)tilesN, (unsigned)tilesM, (unsigned)c.E);
     hipLaunchKernelGGL((gemm_f32_kernel<B_K, RAGGED_K, EPI>), grid, dim3(256), 0, s, p);

@@ -17,7 +17,8 @@ from typing import Optional
 import torch
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "liblancet_moe.so")
+#: The in-tree build; LANCET_MOE_LIB may name another build of the same library.
+LIB_PATH = os.environ.get("LANCET_MOE_LIB") or os.path.join(_HERE, "liblancet_moe.so")
 
 MOE_OK, MOE_EINVAL, MOE_ESHAPE, MOE_EALIGN, MOE_EDTYPE, MOE_EDEVICE, MOE_ELAUNCH, MOE_EWORKSPACE = 0, -1, -2, -3, -4, -5, -6, -7
 MOE_F32, MOE_BF16 = 0, 1

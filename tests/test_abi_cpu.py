@@ -109,3 +109,18 @@ def test_binding_rejects_host_tensors_and_short_buffers():
     c = _cfg(T=4, d_model=8, d_ff=8, E=2, k=1, C=4)
     with pytest.raises(ValueError, match="device tensor"):
         L.moe_gate_topk(c, torch.zeros(4, 8, dtype=torch.bfloat16), None, None, None, None, None, stream=0)
+
+
+def test_isa_check_flags_use_before_wait():
+    from paper_2404_19429_amd.isa_check import check_text
+    clean = """_ZN4lmoe16gemm_bf16_kernelX:
+\t;;#ASMSTART
+\tds_read_b128 v[4:7], v1
+\ts_waitcnt lgkmcnt(0)
+\t;;#ASMEND
+\tv_mfma_f32_16x16x32_bf16 a[0:3], v[4:7], v[8:11], a[0:3]
+"""
+    bad = clean.replace("\ts_waitcnt lgkmcnt(0)\n", "").replace(";;#ASMEND\n", ";;#ASMEND\n\tv_mov_b32 v20, v5\n")
+    assert check_text(clean) == {}
+    hits = check_text(bad)
+    assert list(hits) == ["_ZN4lmoe16gemm_bf16_kernelX"] and any("v_mov_b32" in h for h in hits["_ZN4lmoe16gemm_bf16_kernelX"])
