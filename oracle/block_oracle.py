@@ -12,9 +12,16 @@ its exact gradient for L = sum <dy, out>.
 Readings: LayerNorm with eps 1e-5 and affine gain/bias; QKV projection
 Wqkv [3d][d] laid out as q, k, v blocks, head h using columns h*hd .. h*hd+hd-1
 of each; scores scaled by 1/sqrt(hd); no biases on the projections; the MoE
-layer is moe_oracle's (capacity of the unpartitioned token count).  The MoE
-input is rounded to the workload dtype (bf16) before the gate, as the layer's
-input is a tensor of that dtype.
+layer is moe_oracle's (capacity of the unpartitioned token count).
+
+Storage precision: in a bf16 block every activation that lives in memory
+between two operations is a bf16 tensor -- the LN1 output, q/k/v, the
+attention output, the residual stream h and the MoE input m.  With
+``round_acts`` (the default for a bf16 block) the oracle computes each
+operation in float64 from the rounded inputs and rounds its result once to
+bf16 (nearest, ties to even), so the top-k decision is taken on the same
+bf16 MoE input a bf16 implementation sees.  The block output and every
+gradient stay float64; the backward treats the rounding as the identity.
 """
 from __future__ import annotations
 
@@ -98,19 +105,25 @@ def attention_bwd(do, q, k, v, p, B, S, H):
     return _merge(dq), _merge(dk), _merge(dv)
 
 
-def block_forward(spec, inp, moe_round=True, exact_logits=False):
+def block_forward(spec, inp, round_acts=None, exact_logits=False):
     """spec: BlockSpec-like (B, S, d, heads, moe=LayerSpec-like).  inp: x, ln1_g, ln1_b, Wqkv,
-    Wo, ln2_g, ln2_b, Wg, W1, W2 (and dy for the backward).  ``exact_logits`` keeps the gate
+    Wo, ln2_g, ln2_b, Wg, W1, W2 (and dy for the backward).  ``round_acts`` (default: the
+    block is bf16) rounds the stored activations to bf16; ``exact_logits`` keeps the gate
     logits in float64 (for comparisons against float64 autograd)."""
     B, S, d, H = spec.B, spec.S, spec.d, spec.heads
+    if round_acts is None:
+        round_acts = spec.moe.dtype == "bf16"
+    rnd = round_bf16_f64 if round_acts else (lambda t: t)
     x = np.asarray(inp["x"], F64)
     a, a_hat, a_rstd = layernorm(x, inp["ln1_g"], inp["ln1_b"])
-    qkv = a @ np.asarray(inp["Wqkv"], F64).T
+    a = rnd(a)
+    qkv = rnd(a @ np.asarray(inp["Wqkv"], F64).T)
     q, k, v = qkv[:, :d], qkv[:, d:2 * d], qkv[:, 2 * d:]
     o, p = attention(q, k, v, B, S, H)
-    h = x + o @ np.asarray(inp["Wo"], F64).T
+    o = rnd(o)
+    h = rnd(x + o @ np.asarray(inp["Wo"], F64).T)
     m, m_hat, m_rstd = layernorm(h, inp["ln2_g"], inp["ln2_b"])
-    m_in = round_bf16_f64(m) if (moe_round and spec.moe.dtype == "bf16") else m
+    m_in = rnd(m)
     moe_inp = {"x": m_in, "Wg": inp["Wg"], "W1": inp["W1"], "W2": inp["W2"], "bias": None}
     mw = M.layer_forward(spec.moe, moe_inp, exact_logits=exact_logits)
     out = h + mw["y"]

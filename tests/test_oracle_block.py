@@ -139,3 +139,38 @@ def test_block_chunked_routing_equals_unchunked():
         np.testing.assert_array_equal(part["slot"], mw["slot"][sl])
         np.testing.assert_allclose(part["y"], mw["y"][sl], rtol=1e-13, atol=1e-14)
         carry = part["fill"]
+
+
+def _bf16_spec():
+    sp = _spec(B=2, S=16, d=32, H=2, E=4, k=2, f=48)
+    sp.moe.dtype = "bf16"
+    return sp
+
+
+def _is_bf16(a):
+    a = np.asarray(a, np.float64)
+    return np.array_equal(BO.round_bf16_f64(a), a)
+
+
+def test_bf16_block_stores_bf16_activations():
+    """A bf16 block's stored activations are bf16 values; the float32 block's are not."""
+    spec = _bf16_spec()
+    inp = {k: (BO.round_bf16_f64(v) if isinstance(v, np.ndarray) else v) for k, v in _inputs(spec, 13).items()}
+    fw = BO.block_forward(spec, inp)
+    for n in ("a", "q", "k", "v", "o", "h", "m_in"):
+        assert _is_bf16(fw[n]), n
+    raw = BO.block_forward(spec, inp, round_acts=False)
+    for n in ("a", "q", "o", "h"):
+        assert not _is_bf16(raw[n]), n
+
+
+def test_bf16_block_rounding_stays_within_bf16_error():
+    """Rounding the stored activations moves the block output by bf16-sized amounts only."""
+    spec = _bf16_spec()
+    inp = {k: (BO.round_bf16_f64(v) if isinstance(v, np.ndarray) else v) for k, v in _inputs(spec, 14).items()}
+    fw = BO.block_forward(spec, inp, exact_logits=True)
+    raw = BO.block_forward(spec, inp, round_acts=False, exact_logits=True)
+    np.testing.assert_array_equal(fw["moe"]["idx"], raw["moe"]["idx"])
+    for n in ("h", "m", "out"):
+        err = np.abs(fw[n] - raw[n]).max() / np.abs(raw[n]).max()
+        assert 0 < err < 2.0 ** -6, (n, err)
