@@ -145,7 +145,7 @@ moe_status moe_combine(const moe_cfg* cfg, const void* expert_out, const int32_t
                        const int32_t* slot, const float* w, void* y, moe_stream_t stream);
 
 /* Activation-gradient (dX) chain of the layer backward for L = sum <dy, y>
- * (Sec. 2.2 "Opportunity 1", Fig. "example_dw"):
+ * (Sec. 2.3 "Opportunity 1"; Fig. "example_dw" in Sec. 2.2):
  *   combine backward: dO[e][s] = w[t][r] dy[t], g[t][r] = <dy[t], expert_out[e][s]>;
  *   gate backward (gradient through the weights only, not the selection):
  *     renorm:  dlogits[t][e_r] = w_r (g_r - sum_s w_s g_s), 0 for unselected;
@@ -173,6 +173,121 @@ moe_status moe_bwd_dw(const moe_cfg* cfg, const void* x, const float* dlogits,
                       const int32_t* row_begin, const int32_t* row_end, const void* send_buf,
                       const void* A, const void* dO, const void* dH, void* dW1, void* dW2, float* dWg,
                       void* ws, size_t ws_bytes, moe_stream_t stream);
+
+/* ------------------------------------------------------------------ block */
+
+/* The pre-LN transformer block whose FFN is the MoE layer, with its
+ * non-MoE computation partitioned along the batch and pipelined against the
+ * MoE layer's data movement (Sec. 2.3 "Opportunity 2" and "Challenge 1",
+ * Fig. "part_all"; Sec. 5.3 "Pipeline Scheduling"):
+ *   a = LN1(x), [q k v] = a Wqkv^T, o = causal multi-head attention(q, k, v),
+ *   h = x + o Wo^T, m = LN2(h), out = h + MoE(m).
+ * LayerNorm: eps 1e-5, gain and bias.  Attention: head dim 128, scores
+ * scaled by 1/sqrt(128), softmax in float; head j uses columns
+ * 128 j .. 128 j + 127 of each of the q, k, v blocks of Wqkv [3d][d].  No
+ * projection biases.  bf16 only (moe.dtype = MOE_BF16). */
+typedef struct {
+  int32_t B;     /* sequences */
+  int32_t S;     /* tokens per sequence (any S >= 1) */
+  int32_t heads; /* d_model = 128 * heads, d_model <= 4096 */
+  moe_cfg moe;   /* the MoE layer: moe.T = B*S, moe.d_model = d_model, moe.C = the
+                    capacity of all B*S tokens (batch partitions share it) */
+} moe_block_cfg;
+
+typedef struct {           /* all bf16, caller-owned, read only */
+  const void* ln1_g;       /* [d] */
+  const void* ln1_b;       /* [d] */
+  const void* Wqkv;        /* [3d][d] */
+  const void* Wo;          /* [d][d] */
+  const void* ln2_g;       /* [d] */
+  const void* ln2_b;       /* [d] */
+  const void* Wg;          /* [E][d] */
+  const void* W1;          /* [E][f][d] */
+  const void* W2;          /* [E][d][f] */
+} moe_block_weights;
+
+typedef struct {           /* written by the backward (overwritten, not accumulated) */
+  float* dln1_g;           /* [d] float */
+  float* dln1_b;           /* [d] float */
+  void* dWqkv;             /* [3d][d] bf16 */
+  void* dWo;               /* [d][d] bf16 */
+  float* dln2_g;           /* [d] float */
+  float* dln2_b;           /* [d] float */
+  float* dWg;              /* [E][d] float */
+  void* dW1;               /* [E][f][d] bf16 */
+  void* dW2;               /* [E][d][f] bf16 */
+} moe_block_grads;
+
+/* Caller-owned activations: the forward writes the first group, the backward
+ * reads it and writes the second.  bf16 unless marked float/int32.
+ * T = B*S, Sp = S rounded up to a multiple of 64. */
+typedef struct {
+  void* a;                 /* [T][d] LN1(x) */
+  float* ln1_mean;         /* [T] float */
+  float* ln1_rstd;         /* [T] float, 1/sqrt(var + eps) */
+  void* qkv;               /* [T][3d] */
+  void* attn;              /* [T][d] attention output o, heads concatenated */
+  float* lse;              /* [B][heads][Sp] float, per-query log-sum-exp (base 2) */
+  void* h;                 /* [T][d] residual stream after attention */
+  float* ln2_mean;         /* [T] float */
+  float* ln2_rstd;         /* [T] float */
+  void* m;                 /* [T][d] LN2(h), the MoE layer's input */
+  float* logits;           /* [T][E] float */
+  int32_t* idx;            /* [T][k] int32 */
+  float* w;                /* [T][k] float */
+  int32_t* slot;           /* [T][k] int32 */
+  int32_t* fill;           /* [n_chunks][E] int32: fill after chunk i's dispatch; chunk i
+                              owns expert rows [fill[i-1], fill[i]) (fill[-1] = 0) */
+  void* send_buf;          /* [E][C][d] */
+  void* H;                 /* [E][C][f] */
+  void* A;                 /* [E][C][f] */
+  void* expert_out;        /* [E][C][d] */
+  /* backward */
+  void* dO;                /* [E][C][d] */
+  void* dH;                /* [E][C][f] */
+  void* dXe;               /* [E][C][d] */
+  float* dlogits;          /* [T][E] float */
+  void* dm;                /* [T][d] gradient at m */
+  void* dh;                /* [T][d] gradient at h */
+  void* dattn;             /* [T][d] gradient at o */
+  float* delta;            /* [B][heads][Sp] float, rowsum(dO * O) per query and head */
+  void* dqkv;              /* [T][3d] */
+  void* da;                /* [T][d] gradient at a */
+} moe_block_acts;
+
+typedef enum { MOE_BLOCK_FWD = 1, MOE_BLOCK_BWD = 2 } moe_block_pass;
+
+/* Workspace bytes moe_block_chunked needs (host only; 0 and a message on an
+ * invalid cfg or n_chunks). */
+size_t moe_block_workspace_bytes(const moe_block_cfg* cfg, int32_t n_chunks);
+
+/* One forward and/or backward pass of the block (passes = MOE_BLOCK_FWD,
+ * MOE_BLOCK_BWD or both).
+ *   Forward: the B sequences are split into n_chunks partitions of
+ *   B/n_chunks whole sequences.  streams[0] (compute) runs LN1, the QKV
+ *   projection, attention, the output projection with the residual, LN2 and
+ *   the gate of partition 0, 1, ...; then the experts of partition 0, 1, ...
+ *   streams[1] (data movement) runs partition i's dispatch as soon as its gate
+ *   is done -- starting from the capacity partition i-1 left, so routing,
+ *   slots and drops equal the unpartitioned layer -- and its combine (plus the
+ *   residual h) as soon as its experts are done.  Partition i's dispatch thus
+ *   overlaps partition i+1's attention, and its combine the next partition's
+ *   experts.  Every output is bitwise independent of n_chunks.
+ *   Backward (unpartitioned; L = sum <dy, out>): the dX chain runs on
+ *   streams[0]; every weight gradient (MoE dW1, dW2, dWg, dWo, dWqkv and the
+ *   LayerNorm gains and biases) is deferred to streams[2] as soon as its
+ *   inputs exist (Sec. 2.3 "Opportunity 1"; Sec. 4).
+ *   x [T][d], out [T][d], dy [T][d], dx [T][d], bf16.  The backward reads the
+ *   forward's acts (a forward with the same n_chunks must precede it).
+ *   streams: three hipStream_t (entries may repeat).  When the call returns,
+ *   all its work is ordered before any later work on streams[0].
+ *   ws: moe_block_workspace_bytes(cfg, n_chunks) bytes.
+ *   Errors: n_chunks must divide B (1 <= n_chunks <= 64); d_model = 128 heads
+ *   <= 4096; d_ff a multiple of 64; moe.T = B*S. */
+moe_status moe_block_chunked(const moe_block_cfg* cfg, const moe_block_weights* wts,
+                             const moe_block_grads* grads, const void* x, void* out, const void* dy,
+                             void* dx, const moe_block_acts* acts, int32_t passes, int32_t n_chunks,
+                             const moe_stream_t* streams, void* ws, size_t ws_bytes);
 
 #ifdef __cplusplus
 }

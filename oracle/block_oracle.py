@@ -35,7 +35,7 @@ F64 = np.float64
 LN_EPS = 1e-5
 
 __all__ = ["layernorm", "layernorm_bwd", "attention", "attention_bwd", "block_forward", "block_backward",
-           "round_bf16_f64"]
+           "block_forward_tokens", "round_bf16_f64"]
 
 
 def round_bf16_f64(a: np.ndarray) -> np.ndarray:
@@ -150,3 +150,37 @@ def block_backward(spec, inp, fw):
     dx = dh + dx_ln
     return dict(dx=dx, dh=dh, dm=dm, do=do, dq=dq, dk=dk, dv=dv, dqkv=dqkv, da=da, dWo=dWo, dWqkv=dWqkv,
                 dln1_g=dln1_g, dln1_b=dln1_b, dln2_g=dln2_g, dln2_b=dln2_b, moe=mb)
+
+
+def block_forward_tokens(spec, inp, seq, positions, round_acts=None):
+    """The block at selected positions of sequence ``seq`` only, from that
+    sequence's causal prefix (for sampled checks of large batches).
+
+    Causal attention makes a token's h depend only on its sequence's earlier
+    tokens, and the MoE output of a token none of whose choices is dropped
+    depends only on the token itself, so this equals block_forward on those
+    rows whenever the batch drops nothing (the caller checks that).  Returns
+    h, m_in, logits, idx, w and out for the positions, in the given order."""
+    S, d, H = spec.S, spec.d, spec.heads
+    lay = spec.moe
+    if round_acts is None:
+        round_acts = lay.dtype == "bf16"
+    rnd = round_bf16_f64 if round_acts else (lambda t: t)
+    pos = np.asarray(positions, np.int64)
+    P = int(pos.max()) + 1
+    x = np.asarray(inp["x"], F64)[seq * S: seq * S + P]
+    a = rnd(layernorm(x, inp["ln1_g"], inp["ln1_b"])[0])
+    qkv = rnd(a @ np.asarray(inp["Wqkv"], F64).T)
+    o, _ = attention(qkv[:, :d], qkv[:, d:2 * d], qkv[:, 2 * d:], 1, P, H)
+    o = rnd(o[pos])
+    h = rnd(x[pos] + o @ np.asarray(inp["Wo"], F64).T)
+    m_in = rnd(layernorm(h, inp["ln2_g"], inp["ln2_b"])[0])
+    logits = M.gate_logits(m_in, inp["Wg"], None)
+    idx = M.topk_route(logits, lay.k)
+    _, w = M.gate_weights(logits, idx, lay.renorm)
+    y = np.zeros_like(h)
+    for t in range(len(pos)):
+        for r in range(lay.k):
+            e = int(idx[t, r])
+            y[t] += w[t, r] * M.expert_row_forward(m_in[t], inp["W1"][e], inp["W2"][e], lay.act)[2]
+    return dict(h=h, m_in=m_in, logits=logits, idx=idx, w=w, out=h + y)

@@ -263,7 +263,7 @@ def expert_bwd_dx(dO, H, row_begin, row_end, W1, W2, kind: str):
 
 
 def expert_bwd_dw(dO, A, dH, buf, row_begin, row_end):
-    """Weight-gradient (dW) half, independent of the dX chain (Sec. 2.2
+    """Weight-gradient (dW) half, independent of the dX chain (Sec. 2.3
     "Opportunity 1"): dW2_e = dO_e^T A_e, dW1_e = dH_e^T X_e over the expert's
     rows; an expert with no rows gets exact zeros."""
     E, C, d = dO.shape

@@ -18,7 +18,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "liblancet_moe.so")
-SOURCES = ["api.cpp", "gate.hip", "route.hip", "gemm.hip"]
+SOURCES = ["api.cpp", "block.cpp", "gate.hip", "route.hip", "gemm.hip", "attn.hip", "norm.hip"]
 ARCH = "gfx950"
 
 HIPCC_FLAGS = [
@@ -49,28 +49,32 @@ def _compile(src: str, verbose: bool) -> str:
     return obj
 
 
-def _check_gemm_isa(verbose: bool) -> None:
-    """Refuse a build whose GEMM uses an inline-asm LDS read before its wait."""
+ASM_READ_SOURCES = ["gemm.hip", "attn.hip"]  # kernels that read LDS through inline asm
+
+
+def _check_isa(src: str, verbose: bool) -> None:
+    """Refuse a build whose kernels use an inline-asm LDS read before its wait."""
     from paper_2404_19429_amd.isa_check import check_text
-    out = os.path.join(BUILD, "gemm.s")
-    cmd = [_hipcc(), "-x", "hip", "-S", "--offload-device-only", os.path.join(CSRC, "gemm.hip"), "-o", out] + HIPCC_FLAGS
+    out = os.path.join(BUILD, os.path.splitext(src)[0] + ".s")
+    cmd = [_hipcc(), "-x", "hip", "-S", "--offload-device-only", os.path.join(CSRC, src), "-o", out] + HIPCC_FLAGS
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
-        raise RuntimeError("hipcc -S failed on gemm.hip:\n" + r.stderr)
-    bad = check_text(open(out).read())
+        raise RuntimeError(f"hipcc -S failed on {src}:\n" + r.stderr)
+    bad = check_text(open(out).read(), "_ZN4lmoe")
     if bad:
         detail = "\n".join(f"{k}: {v[:3]}" for k, v in bad.items())
-        raise RuntimeError("GEMM ISA check failed: asm LDS read results used before their wait\n" + detail)
+        raise RuntimeError(f"ISA check failed on {src}: asm LDS read results used before their wait\n" + detail)
     if verbose:
-        print("GEMM ISA check passed", flush=True)
+        print(f"ISA check passed: {src}", flush=True)
 
 
 def build(verbose: bool = False) -> str:
     os.makedirs(BUILD, exist_ok=True)
-    with cf.ThreadPoolExecutor(max_workers=min(8, len(SOURCES) + 1)) as ex:
-        isa = ex.submit(_check_gemm_isa, verbose)
+    with cf.ThreadPoolExecutor(max_workers=min(8, len(SOURCES) + len(ASM_READ_SOURCES))) as ex:
+        isa = [ex.submit(_check_isa, s, verbose) for s in ASM_READ_SOURCES]
         objs = list(ex.map(lambda s: _compile(s, verbose), SOURCES))
-        isa.result()
+        for f in isa:
+            f.result()
     tmp = LIB + ".tmp"
     cmd = [_hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp] + objs
     if verbose:

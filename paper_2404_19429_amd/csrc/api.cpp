@@ -214,4 +214,66 @@ moe_status moe_bwd_dw(const moe_cfg* cfg, const void* x, const float* dlogits, c
   return check_launch(fn);
 }
 
+// ------------------------------------------------------------------ block
+namespace {
+
+moe_status check_block(const moe_block_cfg* c, int32_t n_chunks, const char* fn) {
+  if (!c) return fail(MOE_EINVAL, "%s: cfg is NULL", fn);
+  CHECK(check_cfg(&c->moe, fn, true));
+  if (c->moe.dtype != MOE_BF16) return fail(MOE_EDTYPE, "%s: the block is bf16 only", fn);
+  if (c->B < 1 || c->S < 1 || c->heads < 1) return fail(MOE_ESHAPE, "%s: B, S and heads must be >= 1", fn);
+  if ((int64_t)c->heads * 128 != c->moe.d_model)
+    return fail(MOE_ESHAPE, "%s: d_model=%d is not 128 * heads (heads=%d)", fn, c->moe.d_model, c->heads);
+  if (c->moe.d_model > 4096) return fail(MOE_ESHAPE, "%s: d_model=%d > 4096", fn, c->moe.d_model);
+  if (c->moe.T != (int64_t)c->B * c->S) return fail(MOE_EINVAL, "%s: moe.T must equal B*S", fn);
+  if (n_chunks < 1 || n_chunks > 64 || c->B % n_chunks != 0)
+    return fail(MOE_EINVAL, "%s: n_chunks=%d must divide B=%d (1..64)", fn, n_chunks, c->B);
+  return MOE_OK;
+}
+
+}  // namespace
+
+size_t moe_block_workspace_bytes(const moe_block_cfg* cfg, int32_t n_chunks) {
+  if (check_block(cfg, n_chunks, "moe_block_workspace_bytes") != MOE_OK) return 0;
+  return lmoe::block_ws_bytes(*cfg, n_chunks);
+}
+
+moe_status moe_block_chunked(const moe_block_cfg* cfg, const moe_block_weights* wts, const moe_block_grads* grads,
+                             const void* x, void* out, const void* dy, void* dx, const moe_block_acts* acts,
+                             int32_t passes, int32_t n_chunks, const moe_stream_t* streams, void* ws,
+                             size_t ws_bytes) {
+  const char* fn = "moe_block_chunked";
+  CHECK(check_block(cfg, n_chunks, fn));
+  if (passes < 1 || passes > 3) return fail(MOE_EINVAL, "%s: passes=%d (1 forward, 2 backward, 3 both)", fn, passes);
+  if (!wts || !acts || !streams) return fail(MOE_EINVAL, "%s: weights, acts and streams are required", fn);
+  REQUIRE_PTR(x);
+  REQUIRE_PTR(wts->ln1_g); REQUIRE_PTR(wts->ln1_b); REQUIRE_PTR(wts->Wqkv); REQUIRE_PTR(wts->Wo);
+  REQUIRE_PTR(wts->ln2_g); REQUIRE_PTR(wts->ln2_b); REQUIRE_PTR(wts->Wg); REQUIRE_PTR(wts->W1); REQUIRE_PTR(wts->W2);
+  REQUIRE_PTR(acts->a); REQUIRE_PTR(acts->ln1_mean); REQUIRE_PTR(acts->ln1_rstd); REQUIRE_PTR(acts->qkv);
+  REQUIRE_PTR(acts->attn); REQUIRE_PTR(acts->lse); REQUIRE_PTR(acts->h); REQUIRE_PTR(acts->ln2_mean);
+  REQUIRE_PTR(acts->ln2_rstd); REQUIRE_PTR(acts->m); REQUIRE_PTR(acts->logits); REQUIRE_PTR(acts->idx);
+  REQUIRE_PTR(acts->w); REQUIRE_PTR(acts->slot); REQUIRE_PTR(acts->fill); REQUIRE_PTR(acts->send_buf);
+  REQUIRE_PTR(acts->H); REQUIRE_PTR(acts->A); REQUIRE_PTR(acts->expert_out);
+  if (passes & MOE_BLOCK_FWD) REQUIRE_PTR(out);
+  if (passes & MOE_BLOCK_BWD) {
+    REQUIRE_PTR(dy); REQUIRE_PTR(dx);
+    if (!grads) return fail(MOE_EINVAL, "%s: grads is NULL for a backward pass", fn);
+    REQUIRE_PTR(grads->dln1_g); REQUIRE_PTR(grads->dln1_b); REQUIRE_PTR(grads->dWqkv); REQUIRE_PTR(grads->dWo);
+    REQUIRE_PTR(grads->dln2_g); REQUIRE_PTR(grads->dln2_b); REQUIRE_PTR(grads->dWg); REQUIRE_PTR(grads->dW1);
+    REQUIRE_PTR(grads->dW2);
+    REQUIRE_PTR(acts->dO); REQUIRE_PTR(acts->dH); REQUIRE_PTR(acts->dXe); REQUIRE_PTR(acts->dlogits);
+    REQUIRE_PTR(acts->dm); REQUIRE_PTR(acts->dh); REQUIRE_PTR(acts->dattn); REQUIRE_PTR(acts->delta);
+    REQUIRE_PTR(acts->dqkv); REQUIRE_PTR(acts->da);
+  }
+  const size_t need = lmoe::block_ws_bytes(*cfg, n_chunks);
+  if (ws == nullptr || ws_bytes < need)
+    return fail(MOE_EWORKSPACE, "%s: workspace of %zu bytes needed, %zu given", fn, need, ws ? ws_bytes : 0);
+  REQUIRE_PTR(ws);
+  CHECK(check_device(fn));
+  const hipStream_t st[3] = {(hipStream_t)streams[0], (hipStream_t)streams[1], (hipStream_t)streams[2]};
+  const hipError_t e = lmoe::run_block(*cfg, *wts, grads, x, out, dy, dx, *acts, passes, n_chunks, st, ws);
+  if (e != hipSuccess) return fail(MOE_ELAUNCH, "%s: %s", fn, hipGetErrorString(e));
+  return ok();
+}
+
 }  // extern "C"

@@ -1,6 +1,6 @@
 // Grouped expert GEMMs over the [E][C][*] dispatch layout.
 //
-// One launch covers every expert (grid z = expert).  Two raggedness modes:
+// One launch covers every expert.  Two raggedness modes:
 //   ragged-M (forward and dX products): expert e owns buffer rows
 //     [rb_e, re_e); C(m, n) = sum_k A(rb_e + m, k) B(k, n) with A row-major
 //     (K contiguous).  Tiles past the expert's row count exit at once, so no
@@ -9,19 +9,19 @@
 //     [rb_e, re_e); both operands are row-major in the token dimension, i.e.
 //     MN contiguous.  An expert with no rows stores exact zeros.
 //
-// bf16 path: v_mfma_f32_16x16x32_bf16 with float accumulation.  Tiles are
-// staged global -> VGPR -> LDS with one barrier per K step (double buffer);
-// operands that are MN-contiguous in memory are transposed in registers
-// (8x8 or 4x8 blocks of 16-bit values) while being written to LDS, so every
-// LDS tile is K-contiguous and each lane reads its 8-element K run with one
-// 16-byte LDS read.  Epilogues: plain store, (H, act(H)) store, and
-// dA * act'(H) for the backward.
+// bf16 path: a persistent kernel with v_mfma_f32_16x16x32_bf16 and float
+// accumulation; operand tiles stream global -> LDS asynchronously through a
+// multi-stage ring (details below).  Epilogues: plain store, (H, act(H))
+// store, dA * act'(H) for the backward, and a residual add.
+// The same kernel serves dense products (one group, no row ranges): the
+// block's projections and their weight gradients.
 // f32 path: a plain LDS-tiled FMA GEMM with the same addressing.
 #include "internal.h"
+#include "lds_ops.h"
 
 namespace lmoe {
 
-enum { EPI_STORE = 0, EPI_FWD1 = 1, EPI_DACT = 2 };
+enum { EPI_STORE = 0, EPI_FWD1 = 1, EPI_DACT = 2, EPI_RES = 3 };
 
 struct GemmParams {
   const void* A;
@@ -31,18 +31,18 @@ struct GemmParams {
   void* C;
   int64_t ldc, sC;
   void* C2;         // EPI_FWD1: act(acc), same layout as C
-  const void* Aux;  // EPI_DACT: pre-activation H, same layout as C
+  const void* Aux;  // EPI_DACT: pre-activation H; EPI_RES: residual added to the product; same layout as C
   const int32_t* rb;
   const int32_t* re;
   int M, N, K;      // ragged-M: N, K used;  ragged-K: M, N used
   int act;
-  int cap;          // rows per expert block (C): row ranges are clamped to [0, cap]
+  int cap;          // rows per expert block (C): row ranges are clamped to [0, cap]; re == NULL means [0, cap)
 };
 
 // Row range of group g, clamped to the buffer so bad ranges cannot reach outside it.
 __device__ __forceinline__ void group_rows(const GemmParams& p, int g, int& lo, int& span) {
   int a = p.rb ? p.rb[g] : 0;
-  int b = p.re[g];
+  int b = p.re ? p.re[g] : p.cap;
   a = a < 0 ? 0 : (a > p.cap ? p.cap : a);
   b = b < a ? a : (b > p.cap ? p.cap : b);
   lo = a;
@@ -98,82 +98,6 @@ __device__ __forceinline__ void epilogue_store(const GemmParams& p, int64_t off,
 //    run of the MFMA operand.
 constexpr int kBKb = 32;
 __device__ __forceinline__ int hsw(int k) { return 2 * ((k & 3) | (((k >> 3) & 1) << 2)); }
-
-__device__ __attribute__((aligned(16))) uint32_t g_zero16[4];  // zero-initialised, never written
-
-typedef __attribute__((address_space(3))) void lds_void;
-
-__device__ __forceinline__ void dma16(const void* src, uint16_t* lds_wave_base) {
-  __builtin_amdgcn_global_load_lds(src, (lds_void*)lds_wave_base, 16, 0, 0);
-}
-
-__device__ __forceinline__ void lds_barrier() { asm volatile("s_barrier" ::: "memory"); }
-
-// Fragment reads are inline asm (ds_read_b128 and ds_read_b64_tr_b16) so that
-// the compiler, which cannot tell them apart from the in-flight LDS-DMA tile
-// loads, does not drain those loads before them (it does for the builtins).
-// Each asm block issues up to kReadChunk reads and ends with
-// s_waitcnt lgkmcnt(0): its outputs are complete when the block ends, so the
-// compiler may copy, spill or reuse them freely, and the LGKM counter never
-// holds more than kReadChunk of them.  Read latency still overlaps the MFMAs
-// issued before the block, which keep executing while the wave waits.
-constexpr int kReadChunk = 8;
-__device__ __forceinline__ uint32_t lds_addr(const uint16_t* p) {
-  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) uint16_t*)p;
-}
-
-#define LMOE_R128(i) "ds_read_b128 %" #i ", %" #i "\n"
-template <int N> struct Rd128;
-template <> struct Rd128<8> {
-  __device__ static void run(u32x4* o, const uint32_t* a) {
-    asm volatile("ds_read_b128 %0, %8\n ds_read_b128 %1, %9\n ds_read_b128 %2, %10\n ds_read_b128 %3, %11\n"
-                 "ds_read_b128 %4, %12\n ds_read_b128 %5, %13\n ds_read_b128 %6, %14\n ds_read_b128 %7, %15\n"
-                 "s_waitcnt lgkmcnt(0)"
-                 : "=&v"(o[0]), "=&v"(o[1]), "=&v"(o[2]), "=&v"(o[3]), "=&v"(o[4]), "=&v"(o[5]), "=&v"(o[6]), "=&v"(o[7])
-                 : "v"(a[0]), "v"(a[1]), "v"(a[2]), "v"(a[3]), "v"(a[4]), "v"(a[5]), "v"(a[6]), "v"(a[7])
-                 : "memory");
-  }
-};
-template <> struct Rd128<4> {
-  __device__ static void run(u32x4* o, const uint32_t* a) {
-    asm volatile("ds_read_b128 %0, %4\n ds_read_b128 %1, %5\n ds_read_b128 %2, %6\n ds_read_b128 %3, %7\n"
-                 "s_waitcnt lgkmcnt(0)"
-                 : "=&v"(o[0]), "=&v"(o[1]), "=&v"(o[2]), "=&v"(o[3])
-                 : "v"(a[0]), "v"(a[1]), "v"(a[2]), "v"(a[3])
-                 : "memory");
-  }
-};
-template <int N> struct RdTr;
-template <> struct RdTr<8> {
-  __device__ static void run(u32x2* o, const uint32_t* a) {
-    asm volatile("ds_read_b64_tr_b16 %0, %8\n ds_read_b64_tr_b16 %1, %9\n ds_read_b64_tr_b16 %2, %10\n"
-                 "ds_read_b64_tr_b16 %3, %11\n ds_read_b64_tr_b16 %4, %12\n ds_read_b64_tr_b16 %5, %13\n"
-                 "ds_read_b64_tr_b16 %6, %14\n ds_read_b64_tr_b16 %7, %15\n"
-                 "s_waitcnt lgkmcnt(0)"
-                 : "=&v"(o[0]), "=&v"(o[1]), "=&v"(o[2]), "=&v"(o[3]), "=&v"(o[4]), "=&v"(o[5]), "=&v"(o[6]), "=&v"(o[7])
-                 : "v"(a[0]), "v"(a[1]), "v"(a[2]), "v"(a[3]), "v"(a[4]), "v"(a[5]), "v"(a[6]), "v"(a[7])
-                 : "memory");
-  }
-};
-#undef LMOE_R128
-
-// vmcnt(n) (gfx9 encoding; expcnt and lgkmcnt unrestricted).
-template <int N>
-__device__ __forceinline__ void wait_vm() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
-}
-
-// Wait until at most n * LPS vector-memory operations are pending (n <= NMAX, decided at run time).
-template <int LPS, int NMAX>
-__device__ __forceinline__ void wait_vm_tiles(int n) {
-  if constexpr (NMAX <= 0) {
-    wait_vm<0>();
-  } else {
-    if (n >= NMAX) wait_vm<NMAX * LPS>();
-    else wait_vm_tiles<LPS, NMAX - 1>(n);
-  }
-}
 
 // K-contiguous operand: ROWS x 32 tile, one wave instruction fills one fragment.
 template <int ROWS, int NW>
@@ -398,7 +322,8 @@ gemm_bf16_kernel(GemmParams p, int tilesM, int tilesN, int groups) {
     float* st = reinterpret_cast<float*>(lds) + wid * (EPI_ROWS * EPI_LD);
     uint16_t* C = (uint16_t*)p.C + (int64_t)g * p.sC + (RAGGED_K ? 0 : (int64_t)lo * p.ldc);
     uint16_t* C2 = EPI == EPI_FWD1 ? (uint16_t*)p.C2 + (int64_t)g * p.sC + (int64_t)lo * p.ldc : nullptr;
-    const uint16_t* Aux = EPI == EPI_DACT ? (const uint16_t*)p.Aux + (int64_t)g * p.sC + (int64_t)lo * p.ldc : nullptr;
+    const uint16_t* Aux = (EPI == EPI_DACT || EPI == EPI_RES)
+                              ? (const uint16_t*)p.Aux + (int64_t)g * p.sC + (int64_t)lo * p.ldc : nullptr;
     const int g4 = lane >> 4;
 #pragma unroll
     for (int pass = 0; pass < WTM / EPI_ROWS; ++pass) {
@@ -435,6 +360,12 @@ gemm_bf16_kernel(GemmParams p, int tilesM, int tilesN, int groups) {
             Vec<uint16_t>::load(Aux + off, h);
 #pragma unroll
             for (int u = 0; u < 8; ++u) v[u] *= act_bwd_t<ACT>(h[u]);
+            Vec<uint16_t>::store(C + off, v);
+          } else if constexpr (EPI == EPI_RES) {
+            float r[8];
+            Vec<uint16_t>::load(Aux + off, r);
+#pragma unroll
+            for (int u = 0; u < 8; ++u) v[u] += r[u];
             Vec<uint16_t>::store(C + off, v);
           } else {
             Vec<uint16_t>::store(C + off, v);
@@ -547,7 +478,7 @@ static int num_cus() {
 }
 
 template <bool B_K, bool RAGGED_K, int EPI, int ACT>
-static void launch_bf16(const moe_cfg& c, const GemmParams& p, int tilesM, int tilesN, hipStream_t s) {
+static void launch_bf16(int groups, const GemmParams& p, int tilesM, int tilesN, hipStream_t s) {
   constexpr int NT = Tile::WGM * Tile::WGN * 64;
   constexpr size_t shmem = Tile::STAGES * (size_t)(Tile::BM + Tile::BN) * kBKb * sizeof(uint16_t);
   auto kern = gemm_bf16_kernel<Tile::BM, Tile::BN, Tile::WGM, Tile::WGN, Tile::STAGES, Tile::OCC, B_K, RAGGED_K, EPI, ACT>;
@@ -556,31 +487,39 @@ static void launch_bf16(const moe_cfg& c, const GemmParams& p, int tilesM, int t
     (void)hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)shmem);
     attr_set = true;
   }
-  const int64_t max_tiles = (int64_t)tilesM * tilesN * c.E;
+  const int64_t max_tiles = (int64_t)tilesM * tilesN * groups;
   int blocks = num_cus() * Tile::OCC;
   if (max_tiles < blocks) blocks = (int)((max_tiles + 7) / 8 * 8);
   blocks = (blocks + 7) / 8 * 8;
-  hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(NT), shmem, s, p, tilesM, tilesN, c.E);
+  hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(NT), shmem, s, p, tilesM, tilesN, groups);
+}
+
+// groups: experts (or 1 for a dense product); dtype/act as in moe_cfg.
+template <bool B_K, bool RAGGED_K, int EPI>
+static void run_gemm(int dtype, int act, int groups, const GemmParams& p, int tilesM, int tilesN, hipStream_t s) {
+  if (tilesM <= 0 || tilesN <= 0 || groups <= 0) return;
+  if (dtype == MOE_BF16) {
+    if constexpr (EPI == EPI_STORE || EPI == EPI_RES) {
+      launch_bf16<B_K, RAGGED_K, EPI, MOE_ACT_IDENTITY>(groups, p, tilesM, tilesN, s);
+    } else {
+      switch (act) {
+        case MOE_ACT_RELU: launch_bf16<B_K, RAGGED_K, EPI, MOE_ACT_RELU>(groups, p, tilesM, tilesN, s); break;
+        case MOE_ACT_GELU_TANH: launch_bf16<B_K, RAGGED_K, EPI, MOE_ACT_GELU_TANH>(groups, p, tilesM, tilesN, s); break;
+        case MOE_ACT_GELU_ERF: launch_bf16<B_K, RAGGED_K, EPI, MOE_ACT_GELU_ERF>(groups, p, tilesM, tilesN, s); break;
+        default: launch_bf16<B_K, RAGGED_K, EPI, MOE_ACT_IDENTITY>(groups, p, tilesM, tilesN, s); break;
+      }
+    }
+  } else {
+    if constexpr (EPI != EPI_RES) {
+      dim3 grid((unsigned)tilesN, (unsigned)tilesM, (unsigned)groups);
+      hipLaunchKernelGGL((gemm_f32_kernel<B_K, RAGGED_K, EPI>), grid, dim3(256), 0, s, p);
+    }
+  }
 }
 
 template <bool B_K, bool RAGGED_K, int EPI>
 static void run_gemm(const moe_cfg& c, const GemmParams& p, int tilesM, int tilesN, hipStream_t s) {
-  if (tilesM <= 0 || tilesN <= 0 || c.E <= 0) return;
-  if (c.dtype == MOE_BF16) {
-    if constexpr (EPI == EPI_STORE) {
-      launch_bf16<B_K, RAGGED_K, EPI, MOE_ACT_IDENTITY>(c, p, tilesM, tilesN, s);
-    } else {
-      switch (c.act) {
-        case MOE_ACT_RELU: launch_bf16<B_K, RAGGED_K, EPI, MOE_ACT_RELU>(c, p, tilesM, tilesN, s); break;
-        case MOE_ACT_GELU_TANH: launch_bf16<B_K, RAGGED_K, EPI, MOE_ACT_GELU_TANH>(c, p, tilesM, tilesN, s); break;
-        case MOE_ACT_GELU_ERF: launch_bf16<B_K, RAGGED_K, EPI, MOE_ACT_GELU_ERF>(c, p, tilesM, tilesN, s); break;
-        default: launch_bf16<B_K, RAGGED_K, EPI, MOE_ACT_IDENTITY>(c, p, tilesM, tilesN, s); break;
-      }
-    }
-  } else {
-    dim3 grid((unsigned)tilesN, (unsigned)tilesM, (unsigned)c.E);
-    hipLaunchKernelGGL((gemm_f32_kernel<B_K, RAGGED_K, EPI>), grid, dim3(256), 0, s, p);
-  }
+  run_gemm<B_K, RAGGED_K, EPI>(c.dtype, c.act, c.E, p, tilesM, tilesN, s);
 }
 
 static int tile_m(const moe_cfg& c) { return c.dtype == MOE_BF16 ? kBM : 64; }
@@ -616,6 +555,26 @@ void launch_expert_bwd_dw(const moe_cfg& c, const void* X, const void* A, const 
   // dW1_e [f][d] = dH_e^T X_e
   GemmParams p1{dH, f, C * f, X, d, C * d, dW1, d, f * d, nullptr, nullptr, rb, re, (int)f, (int)d, 0, c.act, (int)C};
   run_gemm<false, true, EPI_STORE>(c, p1, cdiv(f, tile_m(c)), cdiv(d, tile_n(c)), s);
+}
+
+// Dense bf16 products of the transformer block (one group, every row).
+void launch_dense(int64_t M, int N, int K, const void* A, int64_t lda, const void* B, int64_t ldb, bool b_nk,
+                  void* C, int64_t ldc, const void* resid, hipStream_t s) {
+  GemmParams p{A, lda, 0, B, ldb, 0, C, ldc, 0, nullptr, resid, nullptr, nullptr, 0, N, K, 0, (int)M};
+  const int tm = cdiv(M, kBM), tn = cdiv(N, kBN);
+  if (b_nk) {
+    if (resid) run_gemm<true, false, EPI_RES>(MOE_BF16, 0, 1, p, tm, tn, s);
+    else run_gemm<true, false, EPI_STORE>(MOE_BF16, 0, 1, p, tm, tn, s);
+  } else {
+    if (resid) run_gemm<false, false, EPI_RES>(MOE_BF16, 0, 1, p, tm, tn, s);
+    else run_gemm<false, false, EPI_STORE>(MOE_BF16, 0, 1, p, tm, tn, s);
+  }
+}
+
+void launch_dense_wgrad(int M, int N, int64_t K, const void* A, int64_t lda, const void* B, int64_t ldb, void* C,
+                        int64_t ldc, hipStream_t s) {
+  GemmParams p{A, lda, 0, B, ldb, 0, C, ldc, 0, nullptr, nullptr, nullptr, nullptr, M, N, 0, 0, (int)K};
+  run_gemm<false, true, EPI_STORE>(MOE_BF16, 0, 1, p, cdiv(M, kBM), cdiv(N, kBN), s);
 }
 
 }  // namespace lmoe

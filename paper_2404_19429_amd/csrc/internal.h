@@ -18,7 +18,7 @@ size_t dispatch_ws_bytes(const moe_cfg& c);
 void launch_dispatch(const moe_cfg& c, const void* x, const int32_t* idx, const int32_t* carry, int32_t* fill,
                      int32_t* slot, void* send_buf, void* ws, hipStream_t s);
 void launch_combine(const moe_cfg& c, const void* O, const int32_t* idx, const int32_t* slot, const float* w,
-                    void* y, hipStream_t s);
+                    void* y, hipStream_t s, const void* resid = nullptr);
 size_t bwd_dx_ws_bytes(const moe_cfg& c);
 void launch_combine_bwd(const moe_cfg& c, const float* logits, const int32_t* idx, const float* w,
                         const int32_t* slot, const void* O, const void* dy, void* dO, float* dlogits, hipStream_t s);
@@ -34,5 +34,37 @@ void launch_expert_bwd_dx(const moe_cfg& c, const void* dO, const int32_t* rb, c
                           const void* W1, const void* W2, void* dH, void* dXe, hipStream_t s);
 void launch_expert_bwd_dw(const moe_cfg& c, const void* X, const void* A, const void* dO, const void* dH,
                           const int32_t* rb, const int32_t* re, void* dW1, void* dW2, hipStream_t s);
+
+// Dense bf16 products (gemm.hip).  launch_dense: C[M][N] = A[M][K] op(B)
+// (+ resid, same layout as C), B is [N][K] if b_nk else [K][N].
+// launch_dense_wgrad: C[M][N] = A^T B with A [K][M], B [K][N] (sum over K rows).
+void launch_dense(int64_t M, int N, int K, const void* A, int64_t lda, const void* B, int64_t ldb, bool b_nk,
+                  void* C, int64_t ldc, const void* resid, hipStream_t s);
+void launch_dense_wgrad(int M, int N, int64_t K, const void* A, int64_t lda, const void* B, int64_t ldb, void* C,
+                        int64_t ldc, hipStream_t s);
+
+// attn.hip: causal attention of the block (head dim 128).  Pointers are at
+// the first token of nseq whole sequences of S tokens; lse and delta rows have
+// stride attn_stat_stride(S).
+inline int attn_stat_stride(int S) { return (S + 63) / 64 * 64; }
+void launch_attn_fwd(const void* qkv, void* o, float* lse, int nseq, int S, int H, hipStream_t s);
+void launch_attn_bwd(const void* qkv, const void* o, const void* dout, const float* lse, float* delta, void* dqkv,
+                     int nseq, int S, int H, hipStream_t s);
+
+// norm.hip: LayerNorm (eps 1e-5) of bf16 rows of width d (multiple of 8, <= 4096).
+// The backward writes ln_bwd_blocks(T) x 2 x d float partials, reduced by
+// launch_ln_gain_reduce into the gain and bias gradients.
+int ln_bwd_blocks(int64_t T);
+void launch_ln_fwd(const void* x, const void* g, const void* b, void* y, float* mean, float* rstd, int64_t T, int d,
+                   hipStream_t s);
+void launch_ln_bwd(const void* dyl, const void* x, const float* mean, const float* rstd, const void* g,
+                   const void* dres, void* dx, float* part, int64_t T, int d, hipStream_t s);
+void launch_ln_gain_reduce(const float* part, int64_t T, int d, float* dg, float* db, hipStream_t s);
+
+// block.cpp: the partitioned block (arguments validated by the C ABI layer).
+size_t block_ws_bytes(const moe_block_cfg& c, int n_chunks);
+hipError_t run_block(const moe_block_cfg& c, const moe_block_weights& W, const moe_block_grads* G, const void* x,
+                     void* out, const void* dy, void* dx, const moe_block_acts& A, int passes, int n,
+                     const hipStream_t st[3], void* ws);
 
 }  // namespace lmoe

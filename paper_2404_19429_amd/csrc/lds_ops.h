@@ -1,0 +1,86 @@
+// LDS helpers shared by the MFMA kernels: asynchronous global -> LDS loads
+// (global_load_lds_dwordx4), barriers that leave those loads in flight, and
+// fragment reads as inline asm.
+//
+// The compiler cannot tell an LDS read from the in-flight LDS-DMA loads it
+// might alias, and waits for every pending vector-memory operation before a
+// builtin LDS read.  The fragment reads are therefore inline asm; each asm
+// block issues up to 8 reads and ends with s_waitcnt lgkmcnt(0), so its
+// outputs are complete when the block ends and the compiler may copy, spill
+// or reuse them freely.  Read latency still overlaps the MFMAs issued before
+// the block.  The build checks the assembly for any use of an asm read's
+// result before its wait.
+#pragma once
+
+#include "common.h"
+
+namespace lmoe {
+
+static __device__ __attribute__((aligned(16))) uint32_t g_zero16[4];  // zero-initialised, never written
+
+typedef __attribute__((address_space(3))) void lds_void;
+
+__device__ __forceinline__ void dma16(const void* src, uint16_t* lds_wave_base) {
+  __builtin_amdgcn_global_load_lds(src, (lds_void*)lds_wave_base, 16, 0, 0);
+}
+
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_barrier" ::: "memory"); }
+
+// Reads per asm block (the LGKM counter never holds more than this many).
+constexpr int kReadChunk = 8;
+__device__ __forceinline__ uint32_t lds_addr(const uint16_t* p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) uint16_t*)p;
+}
+
+template <int N> struct Rd128;
+template <> struct Rd128<8> {
+  __device__ static void run(u32x4* o, const uint32_t* a) {
+    asm volatile("ds_read_b128 %0, %8\n ds_read_b128 %1, %9\n ds_read_b128 %2, %10\n ds_read_b128 %3, %11\n"
+                 "ds_read_b128 %4, %12\n ds_read_b128 %5, %13\n ds_read_b128 %6, %14\n ds_read_b128 %7, %15\n"
+                 "s_waitcnt lgkmcnt(0)"
+                 : "=&v"(o[0]), "=&v"(o[1]), "=&v"(o[2]), "=&v"(o[3]), "=&v"(o[4]), "=&v"(o[5]), "=&v"(o[6]), "=&v"(o[7])
+                 : "v"(a[0]), "v"(a[1]), "v"(a[2]), "v"(a[3]), "v"(a[4]), "v"(a[5]), "v"(a[6]), "v"(a[7])
+                 : "memory");
+  }
+};
+template <> struct Rd128<4> {
+  __device__ static void run(u32x4* o, const uint32_t* a) {
+    asm volatile("ds_read_b128 %0, %4\n ds_read_b128 %1, %5\n ds_read_b128 %2, %6\n ds_read_b128 %3, %7\n"
+                 "s_waitcnt lgkmcnt(0)"
+                 : "=&v"(o[0]), "=&v"(o[1]), "=&v"(o[2]), "=&v"(o[3])
+                 : "v"(a[0]), "v"(a[1]), "v"(a[2]), "v"(a[3])
+                 : "memory");
+  }
+};
+template <int N> struct RdTr;
+template <> struct RdTr<8> {
+  __device__ static void run(u32x2* o, const uint32_t* a) {
+    asm volatile("ds_read_b64_tr_b16 %0, %8\n ds_read_b64_tr_b16 %1, %9\n ds_read_b64_tr_b16 %2, %10\n"
+                 "ds_read_b64_tr_b16 %3, %11\n ds_read_b64_tr_b16 %4, %12\n ds_read_b64_tr_b16 %5, %13\n"
+                 "ds_read_b64_tr_b16 %6, %14\n ds_read_b64_tr_b16 %7, %15\n"
+                 "s_waitcnt lgkmcnt(0)"
+                 : "=&v"(o[0]), "=&v"(o[1]), "=&v"(o[2]), "=&v"(o[3]), "=&v"(o[4]), "=&v"(o[5]), "=&v"(o[6]), "=&v"(o[7])
+                 : "v"(a[0]), "v"(a[1]), "v"(a[2]), "v"(a[3]), "v"(a[4]), "v"(a[5]), "v"(a[6]), "v"(a[7])
+                 : "memory");
+  }
+};
+
+// vmcnt(n) (gfx9 encoding; expcnt and lgkmcnt unrestricted).
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+
+// Wait until at most n * LPS vector-memory operations are pending (n <= NMAX, decided at run time).
+template <int LPS, int NMAX>
+__device__ __forceinline__ void wait_vm_tiles(int n) {
+  if constexpr (NMAX <= 0) {
+    wait_vm<0>();
+  } else {
+    if (n >= NMAX) wait_vm<NMAX * LPS>();
+    else wait_vm_tiles<LPS, NMAX - 1>(n);
+  }
+}
+
+}  // namespace lmoe

@@ -161,11 +161,13 @@ void launch_dispatch(const moe_cfg& c, const void* x, const int32_t* idx, const 
 }
 
 // -------------------------------------------------------------------- combine
-// y[t][:] = sum_r kept w[t][r] * O[e][s][:], in rank order, float accumulation.
+// y[t][:] = resid[t][:] + sum_r kept w[t][r] * O[e][s][:], in rank order, float
+// accumulation (resid NULL = 0; the block passes its residual stream).
 template <typename T>
 __global__ __launch_bounds__(256) void combine_kernel(const T* __restrict__ O, const int32_t* __restrict__ idx,
                                                       const int32_t* __restrict__ slot, const float* __restrict__ w,
-                                                      T* __restrict__ y, int64_t T_tokens, int d, int E, int k, int C) {
+                                                      const T* __restrict__ resid, T* __restrict__ y, int64_t T_tokens,
+                                                      int d, int E, int k, int C) {
   constexpr int V = Vec<T>::N;
   const int nc = d / V;
   const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -173,8 +175,12 @@ __global__ __launch_bounds__(256) void combine_kernel(const T* __restrict__ O, c
   const int c = (int)(gid - t * nc);
   if (t >= T_tokens) return;
   float acc[V];
+  if (resid) {
+    Vec<T>::load(resid + t * d + (int64_t)c * V, acc);
+  } else {
 #pragma unroll
-  for (int i = 0; i < V; ++i) acc[i] = 0.f;
+    for (int i = 0; i < V; ++i) acc[i] = 0.f;
+  }
   for (int r = 0; r < k; ++r) {
     const int s = slot[t * k + r];
     const int e = idx[t * k + r];
@@ -190,16 +196,17 @@ __global__ __launch_bounds__(256) void combine_kernel(const T* __restrict__ O, c
 }
 
 void launch_combine(const moe_cfg& c, const void* O, const int32_t* idx, const int32_t* slot, const float* w,
-                    void* y, hipStream_t s) {
+                    void* y, hipStream_t s, const void* resid) {
   if (c.T == 0) return;
   if (c.dtype == MOE_BF16) {
     const int64_t n = c.T * (c.d_model / 8);
     hipLaunchKernelGGL(combine_kernel<uint16_t>, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s,
-                       (const uint16_t*)O, idx, slot, w, (uint16_t*)y, c.T, c.d_model, c.E, c.k, c.C);
+                       (const uint16_t*)O, idx, slot, w, (const uint16_t*)resid, (uint16_t*)y, c.T, c.d_model, c.E,
+                       c.k, c.C);
   } else {
     const int64_t n = c.T * (c.d_model / 4);
     hipLaunchKernelGGL(combine_kernel<float>, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s,
-                       (const float*)O, idx, slot, w, (float*)y, c.T, c.d_model, c.E, c.k, c.C);
+                       (const float*)O, idx, slot, w, (const float*)resid, (float*)y, c.T, c.d_model, c.E, c.k, c.C);
   }
 }
 

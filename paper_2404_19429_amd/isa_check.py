@@ -1,10 +1,11 @@
-"""Build-time check of the compiled bf16 GEMM (gfx950 assembly of this build).
+"""Build-time check of the compiled MFMA kernels (gfx950 assembly of this build).
 
-The GEMM reads LDS fragments with inline-asm blocks that must end with
-``s_waitcnt lgkmcnt(0)``.  This check scans the assembly of every
-gemm_bf16_kernel instantiation and fails if any register written by an asm
-LDS read is touched before an ``s_waitcnt lgkmcnt(0)`` has retired it --
-i.e. if an asm block lost its wait or the compiler used a result early.
+The GEMM and attention kernels read LDS fragments with inline-asm blocks that
+must end with ``s_waitcnt lgkmcnt(0)``.  This check scans the assembly of
+every kernel whose name starts with the given prefix and fails if any
+register written by an asm LDS read is touched before an
+``s_waitcnt lgkmcnt(0)`` has retired it -- i.e. if an asm block lost its wait
+or the compiler used a result early.
 """
 from __future__ import annotations
 

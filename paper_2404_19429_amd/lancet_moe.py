@@ -27,7 +27,9 @@ MOE_CALL_DISPATCH, MOE_CALL_BWD_DX, MOE_CALL_BWD_DW = 0, 1, 2
 
 #: Every symbol include/lancet_moe.h declares.
 EXPORTS = ["moe_capacity", "moe_workspace_bytes", "moe_last_error", "moe_gate_topk", "moe_dispatch",
-           "moe_expert_ffn_fwd", "moe_combine", "moe_bwd_dx", "moe_bwd_dw"]
+           "moe_expert_ffn_fwd", "moe_combine", "moe_bwd_dx", "moe_bwd_dw", "moe_block_workspace_bytes",
+           "moe_block_chunked"]
+MOE_BLOCK_FWD, MOE_BLOCK_BWD = 1, 2
 
 
 class MoeError(RuntimeError):
@@ -40,6 +42,29 @@ class moe_cfg(ctypes.Structure):
     _fields_ = [("T", ctypes.c_int64), ("d_model", ctypes.c_int32), ("d_ff", ctypes.c_int32),
                 ("E", ctypes.c_int32), ("k", ctypes.c_int32), ("C", ctypes.c_int32), ("G", ctypes.c_int32),
                 ("dtype", ctypes.c_int32), ("act", ctypes.c_int32), ("renorm", ctypes.c_int32)]
+
+
+class moe_block_cfg(ctypes.Structure):
+    _fields_ = [("B", ctypes.c_int32), ("S", ctypes.c_int32), ("heads", ctypes.c_int32), ("moe", moe_cfg)]
+
+
+BLOCK_WEIGHTS = ["ln1_g", "ln1_b", "Wqkv", "Wo", "ln2_g", "ln2_b", "Wg", "W1", "W2"]
+BLOCK_GRADS = ["dln1_g", "dln1_b", "dWqkv", "dWo", "dln2_g", "dln2_b", "dWg", "dW1", "dW2"]
+BLOCK_ACTS_FWD = ["a", "ln1_mean", "ln1_rstd", "qkv", "attn", "lse", "h", "ln2_mean", "ln2_rstd", "m", "logits",
+                  "idx", "w", "slot", "fill", "send_buf", "H", "A", "expert_out"]
+BLOCK_ACTS_BWD = ["dO", "dH", "dXe", "dlogits", "dm", "dh", "dattn", "delta", "dqkv", "da"]
+
+
+class moe_block_weights(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in BLOCK_WEIGHTS]
+
+
+class moe_block_grads(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in BLOCK_GRADS]
+
+
+class moe_block_acts(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in BLOCK_ACTS_FWD + BLOCK_ACTS_BWD]
 
 
 def _load():
@@ -58,6 +83,10 @@ def _load():
         "moe_combine": (I32, [CFG, P, P, P, P, P, P]),
         "moe_bwd_dx": (I32, [CFG] + [P] * 18 + [SZ, P]),
         "moe_bwd_dw": (I32, [CFG] + [P] * 12 + [SZ, P]),
+        "moe_block_workspace_bytes": (SZ, [ctypes.POINTER(moe_block_cfg), I32]),
+        "moe_block_chunked": (I32, [ctypes.POINTER(moe_block_cfg), ctypes.POINTER(moe_block_weights),
+                                    ctypes.POINTER(moe_block_grads), P, P, P, P, ctypes.POINTER(moe_block_acts),
+                                    I32, I32, ctypes.POINTER(P), P, SZ]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -259,3 +288,73 @@ def layer_backward(b: LayerBuffers, x, Wg, W1, W2, dy, stream=None, dw_stream=No
         dw_stream.wait_event(ev)
     moe_bwd_dw(c, x, b.dlogits, b.carry, b.fill, b.send_buf, b.A, b.dO, b.dH, b.dW1, b.dW2, b.dWg, b.ws_dw,
                dw_stream if dw_stream is not None else stream)
+
+
+# ------------------------------------------------------------------------ block
+def make_block_cfg(B, S, heads, d_ff, E, k, C, G=1, act="gelu_tanh", renorm=1) -> moe_block_cfg:
+    d = 128 * heads
+    return moe_block_cfg(int(B), int(S), int(heads), make_cfg(B * S, d, d_ff, E, k, C, G, "bf16", act, renorm))
+
+
+def block_shapes(cfg: moe_block_cfg, n_chunks: int):
+    """{name: (numel, dtype)} of every weight, gradient and activation of the block."""
+    m = cfg.moe
+    T, d, f, E, k, C = m.T, m.d_model, m.d_ff, m.E, m.k, m.C
+    Sp = (cfg.S + 63) // 64 * 64
+    st = cfg.B * cfg.heads * Sp
+    bf, f32, i32 = torch.bfloat16, torch.float32, torch.int32
+    return {
+        "ln1_g": (d, bf), "ln1_b": (d, bf), "Wqkv": (3 * d * d, bf), "Wo": (d * d, bf), "ln2_g": (d, bf),
+        "ln2_b": (d, bf), "Wg": (E * d, bf), "W1": (E * f * d, bf), "W2": (E * d * f, bf),
+        "dln1_g": (d, f32), "dln1_b": (d, f32), "dWqkv": (3 * d * d, bf), "dWo": (d * d, bf), "dln2_g": (d, f32),
+        "dln2_b": (d, f32), "dWg": (E * d, f32), "dW1": (E * f * d, bf), "dW2": (E * d * f, bf),
+        "a": (T * d, bf), "ln1_mean": (T, f32), "ln1_rstd": (T, f32), "qkv": (T * 3 * d, bf), "attn": (T * d, bf),
+        "lse": (st, f32), "h": (T * d, bf), "ln2_mean": (T, f32), "ln2_rstd": (T, f32), "m": (T * d, bf),
+        "logits": (T * E, f32), "idx": (T * k, i32), "w": (T * k, f32), "slot": (T * k, i32),
+        "fill": (n_chunks * E, i32), "send_buf": (E * C * d, bf), "H": (E * C * f, bf), "A": (E * C * f, bf),
+        "expert_out": (E * C * d, bf), "dO": (E * C * d, bf), "dH": (E * C * f, bf), "dXe": (E * C * d, bf),
+        "dlogits": (T * E, f32), "dm": (T * d, bf), "dh": (T * d, bf), "dattn": (T * d, bf), "delta": (st, f32),
+        "dqkv": (T * 3 * d, bf), "da": (T * d, bf),
+    }
+
+
+def moe_block_workspace_bytes(cfg: moe_block_cfg, n_chunks: int) -> int:
+    return int(_lib.moe_block_workspace_bytes(ctypes.byref(cfg), n_chunks))
+
+
+def moe_block_chunked(cfg: moe_block_cfg, weights: dict, grads: Optional[dict], x, out, dy, dx, acts: dict,
+                      passes: int, n_chunks: int, streams, ws):
+    """streams: three torch.cuda.Stream (or raw handles) -- compute, data movement, weight gradients."""
+    shp = block_shapes(cfg, n_chunks)
+    T, d = cfg.moe.T, cfg.moe.d_model
+    bwd = bool(passes & MOE_BLOCK_BWD)
+    fwd = bool(passes & MOE_BLOCK_FWD)
+    w = moe_block_weights(*[_ptr(weights[n], n, shp[n][1], shp[n][0]) for n in BLOCK_WEIGHTS])
+    g = None
+    if bwd:
+        g = moe_block_grads(*[_ptr(grads[n], n, shp[n][1], shp[n][0]) for n in BLOCK_GRADS])
+    names = BLOCK_ACTS_FWD + (BLOCK_ACTS_BWD if bwd else [])
+    a = moe_block_acts(*[_ptr(acts[n], n, shp[n][1], shp[n][0]) if n in names else None
+                         for n in BLOCK_ACTS_FWD + BLOCK_ACTS_BWD])
+    need = moe_block_workspace_bytes(cfg, n_chunks)
+    st = (ctypes.c_void_p * 3)(*[_stream(s) for s in streams])
+    _check(_lib.moe_block_chunked(ctypes.byref(cfg), ctypes.byref(w), ctypes.byref(g) if g is not None else None,
+                                  _ptr(x, "x", torch.bfloat16, T * d),
+                                  _ptr(out, "out", torch.bfloat16, T * d) if fwd else None,
+                                  _ptr(dy, "dy", torch.bfloat16, T * d) if bwd else None,
+                                  _ptr(dx, "dx", torch.bfloat16, T * d) if bwd else None,
+                                  ctypes.byref(a), int(passes), int(n_chunks), st,
+                                  _ptr(ws, "ws", torch.uint8, need), ws.numel(), ))
+
+
+def alloc_block(cfg: moe_block_cfg, n_chunks: int, device="cuda", names=None) -> dict:
+    """Empty device tensors for the block's gradients and activations (and its
+    workspace under "ws"); weights are the caller's."""
+    shp = block_shapes(cfg, n_chunks)
+    out = {}
+    for n in BLOCK_GRADS + BLOCK_ACTS_FWD + BLOCK_ACTS_BWD:
+        if names is None or n in names:
+            numel, dt = shp[n]
+            out[n] = torch.empty(numel, dtype=dt, device=device)
+    out["ws"] = torch.empty(max(16, moe_block_workspace_bytes(cfg, n_chunks)), dtype=torch.uint8, device=device)
+    return out

@@ -124,3 +124,56 @@ def test_isa_check_flags_use_before_wait():
     assert check_text(clean) == {}
     hits = check_text(bad)
     assert list(hits) == ["_ZN4lmoe16gemm_bf16_kernelX"] and any("v_mov_b32" in h for h in hits["_ZN4lmoe16gemm_bf16_kernelX"])
+
+
+def _block_call(cfg, n_chunks=2, passes=3, grads=True, ws_bytes=None, **acts_over):
+    w = L.moe_block_weights(*([GOOD] * len(L.BLOCK_WEIGHTS)))
+    g = L.moe_block_grads(*([GOOD] * len(L.BLOCK_GRADS))) if grads else None
+    names = L.BLOCK_ACTS_FWD + L.BLOCK_ACTS_BWD
+    a = L.moe_block_acts(*[acts_over.get(n, GOOD) for n in names])
+    st = (ctypes.c_void_p * 3)(None, None, None)
+    need = L.moe_block_workspace_bytes(cfg, n_chunks)
+    ws = need if ws_bytes is None else ws_bytes
+    return L._lib.moe_block_chunked(ctypes.byref(cfg), ctypes.byref(w), ctypes.byref(g) if g else None, GOOD,
+                                    GOOD, GOOD, GOOD, ctypes.byref(a), passes, n_chunks, st, GOOD, ws)
+
+
+def _bcfg(**kw):
+    base = dict(B=8, S=2048, heads=16, d_ff=8192, E=16, k=2, C=2560)
+    base.update(kw)
+    return L.make_block_cfg(**base)
+
+
+def test_block_workspace_bytes():
+    assert L.moe_block_workspace_bytes(_bcfg(), 4) > 0
+    assert L.moe_block_workspace_bytes(_bcfg(), 3) == 0 and "n_chunks" in L.moe_last_error()
+
+
+def test_block_valid_call_without_gpu_reports_device_error():
+    assert _block_call(_bcfg(), 4) == L.MOE_EDEVICE
+
+
+@pytest.mark.parametrize("mutate,status", [
+    (lambda c: setattr(c, "heads", 15), L.MOE_ESHAPE),              # d_model != 128 * heads
+    (lambda c: setattr(c.moe, "T", 100), L.MOE_EINVAL),             # T != B * S
+    (lambda c: setattr(c.moe, "dtype", L.MOE_F32), L.MOE_EDTYPE),   # bf16 only
+    (lambda c: setattr(c.moe, "d_ff", 8200), L.MOE_ESHAPE),         # d_ff not a multiple of 64
+    (lambda c: setattr(c, "B", 0), L.MOE_ESHAPE),
+])
+def test_block_invalid_cfg(mutate, status):
+    c = _bcfg()
+    mutate(c)
+    assert _block_call(c, 4) == status
+    assert L.moe_last_error()
+
+
+def test_block_invalid_arguments():
+    c = _bcfg()
+    assert _block_call(c, 3) == L.MOE_EINVAL                         # 3 does not divide B = 8
+    assert _block_call(c, 4, passes=0) == L.MOE_EINVAL
+    assert _block_call(c, 4, grads=False) == L.MOE_EINVAL             # backward without gradients
+    assert _block_call(c, 4, passes=L.MOE_BLOCK_FWD, grads=False) == L.MOE_EDEVICE
+    assert _block_call(c, 4, ws_bytes=16) == L.MOE_EWORKSPACE
+    assert _block_call(c, 4, qkv=None) == L.MOE_EINVAL and "qkv" in L.moe_last_error()
+    assert _block_call(c, 4, lse=GOOD + 4) == L.MOE_EALIGN
+    assert _block_call(c, 4, passes=L.MOE_BLOCK_FWD, dqkv=None) == L.MOE_EDEVICE   # backward buffers unused

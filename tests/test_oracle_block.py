@@ -174,3 +174,19 @@ def test_bf16_block_rounding_stays_within_bf16_error():
     for n in ("h", "m", "out"):
         err = np.abs(fw[n] - raw[n]).max() / np.abs(raw[n]).max()
         assert 0 < err < 2.0 ** -6, (n, err)
+
+
+def test_block_forward_tokens_matches_block_forward():
+    """The sampled-token form equals the whole-batch block on rows whose choices are all kept."""
+    spec = _bf16_spec()
+    spec.moe.cf_num, spec.moe.cf_den = 4, 1          # capacity large enough that nothing drops
+    inp = {k: (BO.round_bf16_f64(v) if isinstance(v, np.ndarray) else v) for k, v in _inputs(spec, 15).items()}
+    fw = BO.block_forward(spec, inp)
+    assert (fw["moe"]["slot"] >= 0).all()
+    pos = [0, 5, 15, 9]
+    got = BO.block_forward_tokens(spec, inp, 1, pos)
+    rows = [spec.S + p for p in pos]
+    for n in ("h", "m_in", "out"):
+        np.testing.assert_allclose(got[n], fw[n][rows], rtol=1e-12, atol=1e-12, err_msg=n)
+    np.testing.assert_array_equal(got["idx"], fw["moe"]["idx"][rows])
+    np.testing.assert_array_equal(got["logits"], fw["moe"]["logits"][rows])
