@@ -11,7 +11,15 @@ reports the expert FFN forward (its two grouped bf16 MFMA GEMMs) against the
 dense bf16 MFMA peak.  The CPU baseline is the float64 oracle on a bounded
 sample of the same workload.
 
-Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 2|3|4] [--no-cpu-baseline]
+With --workload block: one step = forward + backward of the pre-LN MoE block
+(8 sequences x 2048 tokens, d_model 2048, 16 heads, 16 experts, d_ff 8192,
+top-2) through moe_block_chunked with 4 batch partitions on three streams;
+the line also reports forward and backward times with 1 partition and with
+all work on a single stream, which isolate the pipelining and the deferred
+weight gradients.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 2|3|4] [--workload layer|block]
+                       [--no-cpu-baseline]
 """
 from __future__ import annotations
 
@@ -37,6 +45,7 @@ def _args():
     ap.add_argument("--config", type=int, default=2, choices=[2, 3, 4])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-tokens", type=int, default=8192)
+    ap.add_argument("--workload", default="layer", choices=["layer", "block"])
     return ap.parse_args()
 
 
@@ -60,12 +69,130 @@ def cpu_baseline(spec, inp, n_tokens):
                       f"workload (capacity recomputed for {n_tokens} tokens), {dt:.1f} s wall"}
 
 
+def block_cpu_baseline(spec, inp, S_sample):
+    """The block oracle, as it stands, on the first S_sample tokens of sequence 0."""
+    from dataclasses import replace
+    from oracle import block_oracle as BO
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        threads = os.cpu_count() or 1
+    sub = dict(inp)
+    sub["x"], sub["dy"] = inp["x"][:S_sample], inp["dy"][:S_sample]
+    s = replace(spec, B=1, S=S_sample, moe=replace(spec.moe, T=S_sample))
+    t0 = time.perf_counter()
+    fw = BO.block_forward(s, sub)
+    BO.block_backward(s, sub, fw)
+    dt = time.perf_counter() - t0
+    return {"value": S_sample / dt, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"float64 oracle block forward+backward on the first {S_sample} tokens of sequence 0 "
+                      f"(one sequence of {S_sample}; capacity recomputed), {dt:.1f} s wall"}
+
+
+def block_flops(spec, kept):
+    """Algorithmic MFMA flops of one block step: projections, causal attention, experts."""
+    T, d, f, S, B = spec.B * spec.S, spec.d, spec.moe.f, spec.S, spec.B
+    proj = 2.0 * T * d * (3 * d) + 2.0 * T * d * d                  # QKV + output projection
+    attn_fwd = 2 * 2.0 * B * S * (S + 1) / 2 * d                   # QK^T and PV over the causal half
+    experts = 4.0 * kept * d * f
+    fwd = proj + attn_fwd + experts
+    bwd = 2 * proj + 2 * attn_fwd + 2 * experts                    # dX + dW; attention dQ, dK, dV, dP
+    return fwd, bwd
+
+
+def main_block(a):
+    import torch
+    from paper_2404_19429_amd import lancet_moe as L
+    from synth import BLOCK5, block_inputs
+
+    spec = BLOCK5
+    inp = block_inputs(spec)
+    m = spec.moe
+    T = spec.B * spec.S
+    C = L.moe_capacity(T, m.E, m.k, m.cf_num, m.cf_den)
+    cfg = L.make_block_cfg(spec.B, spec.S, spec.heads, m.f, m.E, m.k, C, m.G, m.act, m.renorm)
+    bf = torch.bfloat16
+    w = {n: torch.from_numpy(inp[n]).cuda().to(bf).reshape(-1) for n in L.BLOCK_WEIGHTS}
+    x = torch.from_numpy(inp["x"]).cuda().to(bf).reshape(-1)
+    dy = torch.from_numpy(inp["dy"]).cuda().to(bf).reshape(-1)
+    out, dx = torch.empty_like(x), torch.empty_like(x)
+    n = spec.n_chunks
+    bufs = {nc: L.alloc_block(cfg, nc) for nc in (n, 1)}
+    main = torch.cuda.current_stream()
+    three = [main, torch.cuda.Stream(), torch.cuda.Stream()]
+    one = [main] * 3
+
+    def run(passes, nc, streams):
+        b = bufs[nc]
+        L.moe_block_chunked(cfg, w, b, x, out, dy, dx, b, passes, nc, streams, b["ws"])
+
+    def timed(passes, nc, streams, steps, warm):
+        if passes == L.MOE_BLOCK_BWD:
+            run(L.MOE_BLOCK_FWD, nc, streams)            # activations for the backward
+        for _ in range(warm):
+            run(passes, nc, streams)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(main)
+        for _ in range(steps):
+            run(passes, nc, streams)
+        e1.record(main)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / steps
+
+    FB = L.MOE_BLOCK_FWD | L.MOE_BLOCK_BWD
+    for _ in range(a.warmup):
+        run(FB, n, three)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(a.steps):
+        run(FB, n, three)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    step_s = wall / a.steps
+    k = max(3, a.steps // 2)
+    variants = {
+        "fwd_4part_3streams": timed(L.MOE_BLOCK_FWD, n, three, k, 2),
+        "fwd_4part_1stream": timed(L.MOE_BLOCK_FWD, n, one, k, 2),
+        "fwd_1part_3streams": timed(L.MOE_BLOCK_FWD, 1, three, k, 2),
+        "bwd_3streams": timed(L.MOE_BLOCK_BWD, n, three, k, 2),
+        "bwd_1stream": timed(L.MOE_BLOCK_BWD, n, one, k, 2),
+    }
+    kept = int(bufs[n]["fill"].view(n, m.E)[-1].sum().item())
+    fwd_fl, bwd_fl = block_flops(spec, kept)
+    achieved = (fwd_fl + bwd_fl) / step_s / 1e12
+    res = {
+        "metric": "MoE block fwd+bwd tokens/s on 1 MI355X (batch-partitioned, 3 HIP streams)",
+        "value": T / step_s,
+        "unit": "tokens/s",
+        "n_gpus": 1, "steps": a.steps, "warmup": a.warmup, "ms_per_step": step_s * 1e3,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (seeded Gaussian hidden states and weights; no dataset)",
+        "config": {"workload": spec.name, "B": spec.B, "S": spec.S, "d_model": spec.d, "heads": spec.heads,
+                   "E": m.E, "k": m.k, "d_ff": m.f, "C": C, "n_chunks": n, "kept_rows": kept,
+                   "parallelism": "single GPU (one GPU's share; all-to-all not run)"},
+        "roofline": {"kernel": "whole block step (all MFMA work: projections, attention, experts)",
+                     "bound": "mfma", "achieved": achieved, "peak": MI355X_PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                     "frac": achieved / MI355X_PEAK_BF16_TFLOPS, "traffic": None},
+        "step_tflop": (fwd_fl + bwd_fl) / 1e12,
+        "variant_ms": variants,
+        "pipelining_gain_fwd_ms": variants["fwd_4part_1stream"] - variants["fwd_4part_3streams"],
+        "deferred_dw_gain_bwd_ms": variants["bwd_1stream"] - variants["bwd_3streams"],
+    }
+    if not a.no_cpu_baseline:
+        res["cpu_baseline"] = block_cpu_baseline(spec, inp, 512)
+    print(json.dumps(res), flush=True)
+
+
 def main():
     a = _args()
     if a.gpus != 1:
         print(f"bench.py measures one GPU's share of the MoE layer step; --gpus {a.gpus} is not supported "
               f"(the all-to-all between GPUs is not part of this build).", file=sys.stderr)
         sys.exit(2)
+    if a.workload == "block":
+        return main_block(a)
     import torch
     from paper_2404_19429_amd import lancet_moe as L
     from synth import layer_inputs, layer_spec
