@@ -1,6 +1,6 @@
 """Benchmark: MoE layer forward + backward on one MI355X.
 
-One step = top-k gate -> capacity-bounded dispatch -> expert FFN grouped GEMMs
+One step = expert-weight packing -> top-k gate -> capacity-bounded dispatch -> expert FFN grouped GEMMs
 -> weighted combine -> dX chain -> dW products, over one batch of seeded
 synthetic input already resident in HBM (the 8192-token, d_model 1024,
 d_ff 4096, 16-expert, top-2, bf16 layer by default).  Prints ONE JSON line.
@@ -34,7 +34,7 @@ import numpy as np
 MI355X_PEAK_BF16_TFLOPS = 2500.0   # dense bf16 MFMA
 MI355X_PEAK_HBM_GBPS = 8000.0
 METRIC = "MoE layer fwd+bwd tokens/s on 1 MI355X; expert GEMM MFMA util; dispatch GB/s"
-CALLS = ["gate", "dispatch", "expert_ffn_fwd", "combine", "bwd_dx", "bwd_dw"]
+CALLS = ["pack_weights", "gate", "dispatch", "expert_ffn_fwd", "combine", "bwd_dx", "bwd_dw"]
 
 
 def _args():
@@ -212,25 +212,27 @@ def main():
             if evs is not None:
                 evs[i].record(stream)
         mark(0)
-        L.moe_gate_topk(cfg, dev["x"], dev["Wg"], bias, b.logits, b.idx, b.w)
+        L.moe_pack_weights(cfg, dev["W1"], dev["W2"], b.W1p, b.W2p)
         mark(1)
-        L.moe_dispatch(cfg, dev["x"], b.idx, b.carry, b.fill, b.slot, b.send_buf, b.ws_dispatch)
+        L.moe_gate_topk(cfg, dev["x"], dev["Wg"], bias, b.logits, b.idx, b.w)
         mark(2)
-        L.moe_expert_ffn_fwd(cfg, b.send_buf, b.carry, b.fill, dev["W1"], dev["W2"], b.H, b.A, b.O)
+        L.moe_dispatch(cfg, dev["x"], b.idx, b.carry, b.fill, b.slot, b.send_buf, b.ws_dispatch)
         mark(3)
-        L.moe_combine(cfg, b.O, b.idx, b.slot, b.w, b.y)
+        L.moe_expert_ffn_fwd(cfg, b.send_buf, b.carry, b.fill, b.W1p, b.W2p, b.H, b.A, b.O)
         mark(4)
-        L.moe_bwd_dx(cfg, dev["Wg"], b.logits, b.idx, b.w, b.slot, b.carry, b.fill, b.H, b.O, dev["W1"],
-                     dev["W2"], dev["dy"], b.dO, b.dH, b.dXe, b.dlogits, b.dx, b.ws_dx)
+        L.moe_combine(cfg, b.O, b.idx, b.slot, b.w, b.y)
         mark(5)
+        L.moe_bwd_dx(cfg, dev["Wg"], b.logits, b.idx, b.w, b.slot, b.carry, b.fill, b.H, b.O, b.W1p,
+                     b.W2p, dev["dy"], b.dO, b.dH, b.dXe, b.dlogits, b.dx, b.ws_dx)
+        mark(6)
         L.moe_bwd_dw(cfg, dev["x"], b.dlogits, b.carry, b.fill, b.send_buf, b.A, b.dO, b.dH, b.dW1, b.dW2,
                      b.dWg, b.ws_dw)
-        mark(6)
+        mark(7)
 
     for _ in range(a.warmup):
         step()
     torch.cuda.synchronize()
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(7)] for _ in range(a.steps)]
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(len(CALLS) + 1)] for _ in range(a.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(a.steps):
@@ -242,7 +244,7 @@ def main():
         for j, c in enumerate(CALLS):
             per_call[c] += e[j].elapsed_time(e[j + 1])
     per_call = {c: v / a.steps for c, v in per_call.items()}       # ms per step
-    step_ms = sum(evs[i][0].elapsed_time(evs[i][6]) for i in range(a.steps)) / a.steps
+    step_ms = sum(evs[i][0].elapsed_time(evs[i][len(CALLS)]) for i in range(a.steps)) / a.steps
 
     fill = b.fill.cpu().numpy()
     N = int(fill.sum())                                           # kept (token, expert) rows

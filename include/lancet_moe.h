@@ -31,10 +31,18 @@
  *     moe_last_error() describes the problem.  T == 0 is valid.
  *   - Rows of an [E][C][*] buffer past an expert's filled range are
  *     unspecified: never read and never written by these calls.
+ *   - Expert buffers [E][C][X] (send_buf, H, A, expert_out, dO, dH, dXe) and
+ *     packed weights: for MOE_BF16 each expert's [C][X] matrix is stored in
+ *     16-row x 32-column blocks of 1 KiB, rows padded to Cp = C rounded up to
+ *     16: element (e, r, c) is at e*Cp*X + ((r/16)*(X/32) + c/32)*512 +
+ *     (r%16)*32 + c%32, so a buffer holds E*Cp*X elements.  (Each block is
+ *     one MFMA operand fragment; the GEMMs load it as one contiguous 1 KiB
+ *     run.)  For MOE_F32 they are plain row-major with Cp = C.
  *   - A device other than gfx950 gives MOE_EDEVICE; a failed launch
  *     MOE_ELAUNCH.
  *
- * Layouts (nn.Linear [out][in]): Wg [E][d], W1 [E][f][d], W2 [E][d][f].
+ * Layouts (nn.Linear [out][in]): Wg [E][d], W1 [E][f][d], W2 [E][d][f]
+ * (row-major; the expert GEMMs take copies made by moe_pack_weights).
  * Symbols: T tokens, d = d_model, f = d_ff, E experts, k top-k, C capacity,
  * G destination slices of E/G experts each.
  */
@@ -126,15 +134,23 @@ moe_status moe_dispatch(const moe_cfg* cfg, const void* x, const int32_t* idx, c
                         int32_t* fill, int32_t* slot, void* send_buf, void* ws, size_t ws_bytes,
                         moe_stream_t stream);
 
+/* Expert weights in the layout the expert GEMMs read, written once per
+ * weight update and used by moe_expert_ffn_fwd and moe_bwd_dx:
+ *   W1 [E][f][d], W2 [E][d][f] row-major dtype -> W1p [E][f][d], W2p [E][d][f]
+ *   in the expert-buffer layout above (bf16: blocks; float: a plain copy). */
+moe_status moe_pack_weights(const moe_cfg* cfg, const void* W1, const void* W2, void* W1p, void* W2p,
+                            moe_stream_t stream);
+
 /* Expert FFNs forward (Background, "Mixture of Experts"): for every expert e
  * and buffer row i in [row_begin_e, row_end_e):
  *   H[e][i] = W1_e x_i, A[e][i] = act(H[e][i]), expert_out[e][i] = W2_e A[e][i].
  *   send_buf [E][C][d], H and A [E][C][f], expert_out [E][C][d], all dtype;
- *   row_begin/row_end [E] int32 device arrays (row_begin NULL = zeros), the
- *   carry-in and fill of the dispatch that wrote these rows.  H and A are
- *   saved for the backward.  bf16 inputs use MFMA with float accumulation. */
+ *   W1p, W2p from moe_pack_weights; row_begin/row_end [E] int32 device arrays
+ *   (row_begin NULL = zeros), the carry-in and fill of the dispatch that
+ *   wrote these rows.  H and A are saved for the backward.  bf16 inputs use
+ *   MFMA with float accumulation. */
 moe_status moe_expert_ffn_fwd(const moe_cfg* cfg, const void* send_buf, const int32_t* row_begin,
-                              const int32_t* row_end, const void* W1, const void* W2, void* H, void* A,
+                              const int32_t* row_end, const void* W1p, const void* W2p, void* H, void* A,
                               void* expert_out, moe_stream_t stream);
 
 /* Weighted gather back to token order (Fig. "moe_and_sharding", Gather):
@@ -153,12 +169,13 @@ moe_status moe_combine(const moe_cfg* cfg, const void* expert_out, const int32_t
  *   experts: dH = (dO W2_e) * act'(H), dXe = dH W1_e on rows [row_begin_e, row_end_e);
  *   dispatch backward: dx[t] = sum over kept r of dXe[e_r][s_r] + sum_j dlogits[t][j] Wg_j.
  *   dO, dXe [E][C][d] and dH [E][C][f] dtype (dO and dH are kept for
- *   moe_bwd_dw), dlogits [T][E] float, dx [T][d] dtype.
+ *   moe_bwd_dw), dlogits [T][E] float, dx [T][d] dtype; W1p, W2p from
+ *   moe_pack_weights.
  *   ws: moe_workspace_bytes(cfg, MOE_CALL_BWD_DX) bytes. */
 moe_status moe_bwd_dx(const moe_cfg* cfg, const void* Wg, const float* logits, const int32_t* idx,
                       const float* w, const int32_t* slot, const int32_t* row_begin,
-                      const int32_t* row_end, const void* H, const void* expert_out, const void* W1,
-                      const void* W2, const void* dy, void* dO, void* dH, void* dXe, float* dlogits,
+                      const int32_t* row_end, const void* H, const void* expert_out, const void* W1p,
+                      const void* W2p, const void* dy, void* dO, void* dH, void* dXe, float* dlogits,
                       void* dx, void* ws, size_t ws_bytes, moe_stream_t stream);
 
 /* Weight-gradient (dW) products, schedulable on any stream after moe_bwd_dx
@@ -238,10 +255,12 @@ typedef struct {
   int32_t* slot;           /* [T][k] int32 */
   int32_t* fill;           /* [n_chunks][E] int32: fill after chunk i's dispatch; chunk i
                               owns expert rows [fill[i-1], fill[i]) (fill[-1] = 0) */
-  void* send_buf;          /* [E][C][d] */
+  void* send_buf;          /* [E][C][d] (expert buffers in the blocked layout, E*Cp*X elements) */
   void* H;                 /* [E][C][f] */
   void* A;                 /* [E][C][f] */
   void* expert_out;        /* [E][C][d] */
+  void* W1p;               /* [E][f][d] packed copy of W1 (moe_pack_weights), written by the forward */
+  void* W2p;               /* [E][d][f] packed copy of W2 */
   /* backward */
   void* dO;                /* [E][C][d] */
   void* dH;                /* [E][C][f] */

@@ -149,15 +149,26 @@ moe_status moe_dispatch(const moe_cfg* cfg, const void* x, const int32_t* idx, c
   return check_launch(fn);
 }
 
+moe_status moe_pack_weights(const moe_cfg* cfg, const void* W1, const void* W2, void* W1p, void* W2p,
+                            moe_stream_t stream) {
+  const char* fn = "moe_pack_weights";
+  CHECK(check_cfg(cfg, fn, true));
+  REQUIRE_PTR(W1); REQUIRE_PTR(W2); REQUIRE_PTR(W1p); REQUIRE_PTR(W2p);
+  if (W1 == W1p || W2 == W2p || W1p == W2p) return fail(MOE_EINVAL, "%s: packed and source weights may not alias", fn);
+  CHECK(check_device(fn));
+  lmoe::launch_pack_weights(*cfg, W1, W2, W1p, W2p, (hipStream_t)stream);
+  return check_launch(fn);
+}
+
 moe_status moe_expert_ffn_fwd(const moe_cfg* cfg, const void* send_buf, const int32_t* row_begin,
-                              const int32_t* row_end, const void* W1, const void* W2, void* H, void* A,
+                              const int32_t* row_end, const void* W1p, const void* W2p, void* H, void* A,
                               void* expert_out, moe_stream_t stream) {
   const char* fn = "moe_expert_ffn_fwd";
   CHECK(check_cfg(cfg, fn, true));
   REQUIRE_PTR(send_buf); OPTIONAL_PTR(row_begin); REQUIRE_PTR(row_end);
-  REQUIRE_PTR(W1); REQUIRE_PTR(W2); REQUIRE_PTR(H); REQUIRE_PTR(A); REQUIRE_PTR(expert_out);
+  REQUIRE_PTR(W1p); REQUIRE_PTR(W2p); REQUIRE_PTR(H); REQUIRE_PTR(A); REQUIRE_PTR(expert_out);
   CHECK(check_device(fn));
-  lmoe::launch_expert_fwd(*cfg, send_buf, row_begin, row_end, W1, W2, H, A, expert_out, (hipStream_t)stream);
+  lmoe::launch_expert_fwd(*cfg, send_buf, row_begin, row_end, W1p, W2p, H, A, expert_out, (hipStream_t)stream);
   return check_launch(fn);
 }
 
@@ -173,13 +184,13 @@ moe_status moe_combine(const moe_cfg* cfg, const void* expert_out, const int32_t
 
 moe_status moe_bwd_dx(const moe_cfg* cfg, const void* Wg, const float* logits, const int32_t* idx, const float* w,
                       const int32_t* slot, const int32_t* row_begin, const int32_t* row_end, const void* H,
-                      const void* expert_out, const void* W1, const void* W2, const void* dy, void* dO, void* dH,
+                      const void* expert_out, const void* W1p, const void* W2p, const void* dy, void* dO, void* dH,
                       void* dXe, float* dlogits, void* dx, void* ws, size_t ws_bytes, moe_stream_t stream) {
   const char* fn = "moe_bwd_dx";
   CHECK(check_cfg(cfg, fn, true));
   REQUIRE_PTR(Wg); REQUIRE_TPTR(logits); REQUIRE_TPTR(idx); REQUIRE_TPTR(w); REQUIRE_TPTR(slot);
   OPTIONAL_PTR(row_begin); REQUIRE_PTR(row_end); REQUIRE_PTR(H); REQUIRE_PTR(expert_out);
-  REQUIRE_PTR(W1); REQUIRE_PTR(W2); REQUIRE_TPTR(dy); REQUIRE_PTR(dO); REQUIRE_PTR(dH); REQUIRE_PTR(dXe);
+  REQUIRE_PTR(W1p); REQUIRE_PTR(W2p); REQUIRE_TPTR(dy); REQUIRE_PTR(dO); REQUIRE_PTR(dH); REQUIRE_PTR(dXe);
   REQUIRE_TPTR(dlogits); REQUIRE_TPTR(dx);
   const size_t need = lmoe::bwd_dx_ws_bytes(*cfg);
   if (need > 0 && (ws == nullptr || ws_bytes < need))
@@ -188,7 +199,7 @@ moe_status moe_bwd_dx(const moe_cfg* cfg, const void* Wg, const float* logits, c
   CHECK(check_device(fn));
   hipStream_t s = (hipStream_t)stream;
   lmoe::launch_combine_bwd(*cfg, logits, idx, w, slot, expert_out, dy, dO, dlogits, s);
-  lmoe::launch_expert_bwd_dx(*cfg, dO, row_begin, row_end, H, W1, W2, dH, dXe, s);
+  lmoe::launch_expert_bwd_dx(*cfg, dO, row_begin, row_end, H, W1p, W2p, dH, dXe, s);
   lmoe::launch_dispatch_bwd(*cfg, Wg, dlogits, idx, slot, dXe, dx, s);
   return check_launch(fn);
 }
@@ -253,7 +264,8 @@ moe_status moe_block_chunked(const moe_block_cfg* cfg, const moe_block_weights* 
   REQUIRE_PTR(acts->attn); REQUIRE_PTR(acts->lse); REQUIRE_PTR(acts->h); REQUIRE_PTR(acts->ln2_mean);
   REQUIRE_PTR(acts->ln2_rstd); REQUIRE_PTR(acts->m); REQUIRE_PTR(acts->logits); REQUIRE_PTR(acts->idx);
   REQUIRE_PTR(acts->w); REQUIRE_PTR(acts->slot); REQUIRE_PTR(acts->fill); REQUIRE_PTR(acts->send_buf);
-  REQUIRE_PTR(acts->H); REQUIRE_PTR(acts->A); REQUIRE_PTR(acts->expert_out);
+  REQUIRE_PTR(acts->H); REQUIRE_PTR(acts->A); REQUIRE_PTR(acts->expert_out); REQUIRE_PTR(acts->W1p);
+  REQUIRE_PTR(acts->W2p);
   if (passes & MOE_BLOCK_FWD) REQUIRE_PTR(out);
   if (passes & MOE_BLOCK_BWD) {
     REQUIRE_PTR(dy); REQUIRE_PTR(dx);

@@ -114,6 +114,7 @@ hipError_t run_block(const moe_block_cfg& c, const moe_block_weights& W, const m
     moe_cfg pc = mc;
     pc.T = Tc;
     HIP_TRY(order(Sc, Sx));  // the data-movement stream starts after the caller's earlier work
+    launch_pack_weights(mc, W.W1, W.W2, A.W1p, A.W2p, Sc);  // expert weights as the GEMMs read them
     std::vector<hipEvent_t> ev_disp(n);
     for (int i = 0; i < n; ++i) {  // pre-MoE stage, partitions in order
       const int64_t t0 = Tc * i;
@@ -135,7 +136,7 @@ hipError_t run_block(const moe_block_cfg& c, const moe_block_weights& W, const m
       const int64_t t0 = Tc * i;
       HIP_TRY(hipStreamWaitEvent(Sc, ev_disp[i], 0));
       const int32_t* rb = i == 0 ? nullptr : A.fill + (int64_t)(i - 1) * E;
-      launch_expert_fwd(mc, A.send_buf, rb, A.fill + (int64_t)i * E, W.W1, W.W2, A.H, A.A, A.expert_out, Sc);
+      launch_expert_fwd(mc, A.send_buf, rb, A.fill + (int64_t)i * E, A.W1p, A.W2p, A.H, A.A, A.expert_out, Sc);
       HIP_TRY(hipGetLastError());
       HIP_TRY(order(Sc, Sx));
       launch_combine(pc, A.expert_out, A.idx + t0 * k, A.slot + t0 * k, A.w + t0 * k, bfm(out, t0 * d), Sx,
@@ -150,7 +151,7 @@ hipError_t run_block(const moe_block_cfg& c, const moe_block_weights& W, const m
     HIP_TRY(order(Sc, Sw));  // the weight stream starts after the caller's earlier work
     // MoE layer: combine/gate backward, expert dX, dispatch backward -> dm
     launch_combine_bwd(mc, A.logits, A.idx, A.w, A.slot, A.expert_out, dy, A.dO, A.dlogits, Sc);
-    launch_expert_bwd_dx(mc, A.dO, nullptr, fill_end, A.H, W.W1, W.W2, A.dH, A.dXe, Sc);
+    launch_expert_bwd_dx(mc, A.dO, nullptr, fill_end, A.H, A.W1p, A.W2p, A.dH, A.dXe, Sc);
     launch_dispatch_bwd(mc, W.Wg, A.dlogits, A.idx, A.slot, A.dXe, A.dm, Sc);
     HIP_TRY(hipGetLastError());
     HIP_TRY(order(Sc, Sw));

@@ -64,6 +64,28 @@ template <> struct Vec<float> {
   }
 };
 
+// ------------------------------------------------------------ blocked layout
+// bf16 [E][C][X] buffers of the expert path (X a multiple of 32) are stored in
+// 16 x 32 blocks of 1 KiB: within expert e (Cp = C rounded up to 16 rows),
+// element (r, c) sits at e * Cp * X + blk_off(r, c, X).  A 16-row x 32-column
+// MFMA operand fragment is then one contiguous 1 KiB run, which the loads
+// into LDS move several times faster than 16 separate 64-byte row pieces.
+// The same blocks serve both GEMM orientations (rows x K and K x columns).
+// float buffers stay row-major (Cp = C).
+__host__ __device__ __forceinline__ int64_t blk_off(int64_t r, int64_t c, int64_t X) {
+  return ((r >> 4) * (X >> 5) + (c >> 5)) * 512 + (r & 15) * 32 + (c & 31);
+}
+__host__ __device__ __forceinline__ int64_t pad16(int64_t n) { return (n + 15) & ~(int64_t)15; }
+
+// Offset of (row, col) in one expert's [C][X] buffer for storage type T.
+template <typename T> __host__ __device__ __forceinline__ int64_t ebuf_off(int64_t r, int64_t c, int64_t X);
+template <> __host__ __device__ __forceinline__ int64_t ebuf_off<uint16_t>(int64_t r, int64_t c, int64_t X) {
+  return blk_off(r, c, X);
+}
+template <> __host__ __device__ __forceinline__ int64_t ebuf_off<float>(int64_t r, int64_t c, int64_t X) {
+  return r * X + c;
+}
+
 // ------------------------------------------------------------------- wave ops
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll

@@ -100,7 +100,8 @@ constexpr int kBKb = 32;
 __device__ __forceinline__ int hsw(int k) { return 2 * ((k & 3) | (((k >> 3) & 1) << 2)); }
 
 // K-contiguous operand: ROWS x 32 tile, one wave instruction fills one fragment.
-template <int ROWS, int NW>
+// BLK: the operand is stored in 16 x 32 blocks; a fragment is one block.
+template <int ROWS, int NW, bool BLK>
 struct TileK {
   static constexpr int NI = ROWS / 16 / NW;     // loads per wave per tile
   static_assert(NI >= 1 && ROWS % (16 * NW) == 0, "tile/waves mismatch");
@@ -111,6 +112,23 @@ struct TileK {
       const int q = i * NW + wid;
       const int row = row0 + 16 * q + (lane & 15), k = k0 + 8 * (lane >> 4);
       const void* src = (row < rowlim && k < klim) ? (const void*)(base + (int64_t)row * ld + k) : (const void*)g_zero16;
+      dma16(src, stage + q * 512);
+    }
+  }
+  // Blocked source: row0 (a multiple of 16) is the fragment's first row in
+  // the operand, rows at or past rowlim read zeros.  Lane l takes (row l%16,
+  // k chunk l/16) of the block, which is its fragment-linear LDS position.
+  __device__ static void issue_blk(const uint16_t* base, int64_t ld, int row0, int rowlim, int k0, int klim,
+                                   uint16_t* stage, int wid, int lane) {
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+      const int q = i * NW + wid;
+      const int rb = (row0 >> 4) + q;
+      const int row = 16 * rb + (lane & 15);
+      const void* src = (row < rowlim && k0 < klim)
+                            ? (const void*)(base + ((int64_t)rb * (ld >> 5) + (k0 >> 5)) * 512 + (lane & 15) * 32 +
+                                            (lane >> 4) * 8)
+                            : (const void*)g_zero16;
       dma16(src, stage + q * 512);
     }
   }
@@ -127,11 +145,28 @@ struct TileK {
       Rd128<N>::run(&f[c], a);
     }
   }
+  // Split form (NF = 4 or 8): start the reads, later complete them in place.
+  template <int NF>
+  __device__ static void read_issue(u32x4 (&f)[NF], u32x2 (&)[8], const uint16_t* stage, int r0, int lane) {
+    static_assert(NF == 4 || NF == 8, "split reads: 4 or 8 fragments");
+    uint32_t a[NF];
+#pragma unroll
+    for (int u = 0; u < NF; ++u) a[u] = lds_addr(stage + ((r0 >> 4) + u) * 512 + lane * 8);
+    Rd128Issue<NF>::run(f, a);
+  }
+  template <int NF>
+  __device__ static void read_finish(u32x4 (&f)[NF], u32x2 (&)[8]) { lds_wait(f); }
 };
 
 // MN-contiguous operand: 32 x COLS tile (row = k), one wave instruction fills 64 chunks.
-template <int COLS, int NW>
+// BLK: the operand is stored in 16 x 32 blocks and the stage keeps them as
+// [2][COLS/32] blocks of 16 rows x 4 chunks, chunk c of block row r at c ^ bsw(r):
+// the 16 lanes of a transposed read cover rows r..r+3 and the next lane group
+// rows r+8..r+11, and this swizzle puts those 8 x 32 bytes on distinct banks.
+__device__ __forceinline__ int bsw(int r) { return 2 * (((r >> 1) ^ (r >> 3)) & 1); }
+template <int COLS, int NW, bool BLK>
 struct TileMN {
+  static constexpr int CB = COLS / 32;          // column blocks per stage
   static constexpr int CPR = COLS / 8;          // 16-byte chunks per row
   static constexpr int NI = kBKb * CPR / 64 / NW;
   static_assert(NI >= 1 && (kBKb * CPR) % (64 * NW) == 0 && CPR >= 16, "tile/waves mismatch");
@@ -148,6 +183,34 @@ struct TileMN {
       dma16(src, stage + q * 512);
     }
   }
+  // Blocked source: k0 (a multiple of 16) is the stage's first row in the
+  // operand; rows outside [klo, khi) and column blocks at or past collim read zeros.
+  __device__ static void issue_blk(const uint16_t* base, int64_t ld, int col0, int collim, int k0, int klo, int khi,
+                                   uint16_t* stage, int wid, int lane) {
+    const int r = lane >> 2;
+    const int c = (lane & 3) ^ bsw(r);
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+      const int b = i * NW + wid;
+      const int kb = b / CB, cb = b % CB;
+      const int krow = k0 + 16 * kb + r;
+      const int col = col0 + 32 * cb;
+      const void* src = (krow >= klo && krow < khi && col < collim)
+                            ? (const void*)(base + ((int64_t)((k0 >> 4) + kb) * (ld >> 5) + (col >> 5)) * 512 +
+                                            r * 32 + c * 8)
+                            : (const void*)g_zero16;
+      dma16(src, stage + b * 512);
+    }
+  }
+  // LDS element offset of (k, col) in a stage.
+  __device__ static int lds_off(int k, int col) {
+    if constexpr (BLK) {
+      const int r = k & 15;
+      return ((k >> 4) * CB + (col >> 5)) * 512 + r * 32 + ((((col & 31) >> 3) ^ bsw(r)) << 3) + (col & 7);
+    } else {
+      return k * COLS + (((col >> 3) ^ hsw(k)) << 3) + (col & 7);
+    }
+  }
   // Reads NF 16 (m or n) x 32 k fragments at columns c0 + 16 j: lane gets column
   // c0 + 16 j + lane%16, k = 8*(lane/16) .. +7 (two transposed reads: k .. k+3, k+4 .. k+7).
   template <int NF>
@@ -155,16 +218,14 @@ struct TileMN {
     static_assert(NF % 4 == 0, "fragment count");
     const int j = lane & 15;
     const int k = 8 * (lane >> 4) + (j >> 2);
-    const int h = hsw(k);                                 // hsw(k + 4) == hsw(k)
 #pragma unroll
     for (int c = 0; c < NF; c += 4) {
       uint32_t a[8];
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
         const int col = c0 + 16 * (c + u) + 4 * (j & 3);
-        const int off = k * COLS + (((col >> 3) ^ h) << 3) + (col & 7);
-        a[2 * u] = lds_addr(stage + off);
-        a[2 * u + 1] = lds_addr(stage + off + 4 * COLS);
+        a[2 * u] = lds_addr(stage + lds_off(k, col));
+        a[2 * u + 1] = lds_addr(stage + lds_off(k + 4, col));
       }
       u32x2 o[8];
       RdTr<8>::run(o, a);
@@ -172,14 +233,49 @@ struct TileMN {
       for (int u = 0; u < 4; ++u) f[c + u] = u32x4{o[2 * u][0], o[2 * u][1], o[2 * u + 1][0], o[2 * u + 1][1]};
     }
   }
+  // Split form (NF = 4): the 8 transposed reads land in p; read_finish waits and assembles.
+  template <int NF>
+  __device__ static void read_issue(u32x4 (&)[NF], u32x2 (&p)[8], const uint16_t* stage, int c0, int lane) {
+    static_assert(NF == 4, "split transposed reads: 4 fragments");
+    const int j = lane & 15;
+    const int k = 8 * (lane >> 4) + (j >> 2);
+    uint32_t a[8];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int col = c0 + 16 * u + 4 * (j & 3);
+      a[2 * u] = lds_addr(stage + lds_off(k, col));
+      a[2 * u + 1] = lds_addr(stage + lds_off(k + 4, col));
+    }
+    RdTrIssue8::run(p, a);
+  }
+  template <int NF>
+  __device__ static void read_finish(u32x4 (&f)[NF], u32x2 (&p)[8]) {
+    lds_wait(p);
+#pragma unroll
+    for (int u = 0; u < 4; ++u) f[u] = u32x4{p[2 * u][0], p[2 * u][1], p[2 * u + 1][0], p[2 * u + 1][1]};
+  }
 };
 
-// Persistent grouped GEMM: one block per CU walks the list of real tiles of
-// all groups.  Tiles are numbered group by group, m-tile by m-tile, n fastest;
-// the list is cut into 8 contiguous ranges, one per XCD (workgroups are
-// dealt to XCDs round-robin by block index), so the blocks sharing an XCD's
-// L2 work on neighbouring tiles that share A rows and B columns.
-template <int BM, int BN, int WGM, int WGN, int STAGES, int OCC, bool B_K, bool RAGGED_K, int EPI, int ACT>
+// Persistent grouped GEMM: resident blocks walk the list of real tiles of all
+// groups.  Within a group, tiles are numbered panel by panel (kPanelN tile
+// columns wide), m-tile by m-tile inside a panel, n fastest.  The list is cut
+// into 8 contiguous ranges, one per XCD (workgroups are dealt to XCDs
+// round-robin by block index), so the ~64 tiles an XCD has in flight form an
+// 8 x 8 patch: each A row-slice and B column-slice it streams is shared by 8
+// tiles through that XCD's L2, instead of one A slice shared by a whole row of
+// tiles while every B slice of the row is fetched afresh.
+#ifndef LMOE_SPLIT_READS
+#define LMOE_SPLIT_READS 1
+#endif
+#ifndef LMOE_PANEL_N
+#define LMOE_PANEL_N 8
+#endif
+constexpr int kPanelN = LMOE_PANEL_N;
+// BLK: both operands in 16 x 32 blocks (expert buffers and packed weights),
+// ragged row ranges start at the block row containing row_begin; CBLK: the
+// output (and the epilogue's auxiliary input) too.  Otherwise row-major.
+template <int BM, int BN, int WGM, int WGN, int STAGES, int OCC, bool B_K, bool RAGGED_K, int EPI, int ACT, bool BLK,
+          bool CBLK>
 __global__ __attribute__((amdgpu_flat_work_group_size(WGM * WGN * 64, WGM * WGN * 64),
                           amdgpu_waves_per_eu(OCC, OCC))) void
 gemm_bf16_kernel(GemmParams p, int tilesM, int tilesN, int groups) {
@@ -192,8 +288,8 @@ gemm_bf16_kernel(GemmParams p, int tilesM, int tilesN, int groups) {
   constexpr int EPI_ROWS = (NW * 32 * EPI_LD * 4 <= STAGES * STAGE * 2) ? 32 : 16;  // rows staged at once
   constexpr bool A_K = !RAGGED_K;
   constexpr bool BK_C = B_K && !RAGGED_K;
-  using TA = typename std::conditional<A_K, TileK<BM, NW>, TileMN<BM, NW>>::type;
-  using TB = typename std::conditional<BK_C, TileK<BN, NW>, TileMN<BN, NW>>::type;
+  using TA = typename std::conditional<A_K, TileK<BM, NW, BLK>, TileMN<BM, NW, BLK>>::type;
+  using TB = typename std::conditional<BK_C, TileK<BN, NW, BLK>, TileMN<BN, NW, BLK>>::type;
   constexpr int LPS = TA::NI + TB::NI;           // loads per wave per stage
   static_assert(STAGES >= 2 && LPS * (STAGES - 1) < 64, "vmcnt range");
   static_assert(WTM % EPI_ROWS == 0, "wave tile rows must be a multiple of the staged slice");
@@ -215,6 +311,7 @@ gemm_bf16_kernel(GemmParams p, int tilesM, int tilesN, int groups) {
       } else {
         int lo, span;
         group_rows(p, lane, lo, span);
+        if (BLK && span > 0) span += lo & 15;  // tiles start at the block row holding row_begin
         cnt = ((span + BM - 1) / BM) * tilesN;
       }
     }
@@ -239,14 +336,23 @@ gemm_bf16_kernel(GemmParams p, int tilesM, int tilesN, int groups) {
     int g = 0;
     while (g + 1 < groups && s_prefix[g + 1] <= t) ++g;
     const int local = t - s_prefix[g];
-    const int m0 = (local / tilesN) * BM;
-    const int n0 = (local % tilesN) * BN;
     int lo, span;
     group_rows(p, g, lo, span);
+    const int hi = lo + span;
+    const int lo_al = BLK ? (lo & ~15) : lo;   // row (or K) origin of this group's tiles
+    if (BLK && span > 0) span += lo - lo_al;
+    // Panel order: n-panels of kPanelN tile columns, m-tiles within a panel,
+    // n fastest, so the tiles in flight on one XCD form a square-ish patch.
+    const int tmg = RAGGED_K ? tilesM : (span + BM - 1) / BM;
+    const int pnl = local / (tmg * kPanelN);
+    const int rem = local - pnl * tmg * kPanelN;
+    const int pw = min(kPanelN, tilesN - pnl * kPanelN);
+    const int m0 = (rem / pw) * BM;
+    const int n0 = (pnl * kPanelN + rem % pw) * BN;
     const int Mlim = RAGGED_K ? p.M : span;
     const int Klim = RAGGED_K ? span : p.K;
-    const uint16_t* Ab = (const uint16_t*)p.A + g * p.sA + (int64_t)lo * p.lda;
-    const uint16_t* Bb = (const uint16_t*)p.B + g * p.sB + (RAGGED_K ? (int64_t)lo * p.ldb : 0);
+    const uint16_t* Ab = (const uint16_t*)p.A + g * p.sA + (BLK ? 0 : (int64_t)lo * p.lda);
+    const uint16_t* Bb = (const uint16_t*)p.B + g * p.sB + (RAGGED_K && !BLK ? (int64_t)lo * p.ldb : 0);
 
     f32x4 acc[FM][FN];
 #pragma unroll
@@ -257,8 +363,16 @@ gemm_bf16_kernel(GemmParams p, int tilesM, int tilesN, int groups) {
     const int nk = (Klim + BK - 1) / BK;
     auto issue = [&](int kt) {
       uint16_t* st = lds + (kt % STAGES) * STAGE;
-      TA::issue(Ab, p.lda, m0, Mlim, kt * BK, Klim, st, wid, lane);
-      TB::issue(Bb, p.ldb, n0, p.N, kt * BK, Klim, st + BM * BK, wid, lane);
+      if constexpr (!BLK) {
+        TA::issue(Ab, p.lda, m0, Mlim, kt * BK, Klim, st, wid, lane);
+        TB::issue(Bb, p.ldb, n0, p.N, kt * BK, Klim, st + BM * BK, wid, lane);
+      } else {
+        if constexpr (A_K) TA::issue_blk(Ab, p.lda, lo_al + m0, (int)pad16(p.cap), kt * BK, Klim, st, wid, lane);
+        else TA::issue_blk(Ab, p.lda, m0, p.M, lo_al + kt * BK, lo, hi, st, wid, lane);
+        if constexpr (BK_C) TB::issue_blk(Bb, p.ldb, n0, p.N, kt * BK, Klim, st + BM * BK, wid, lane);
+        else if constexpr (RAGGED_K) TB::issue_blk(Bb, p.ldb, n0, p.N, lo_al + kt * BK, lo, hi, st + BM * BK, wid, lane);
+        else TB::issue_blk(Bb, p.ldb, n0, p.N, kt * BK, 0, p.K, st + BM * BK, wid, lane);
+      }
     };
     // Fragment reads of one tile: the A fragments, then the B fragments, each in
     // asm blocks of at most kReadChunk reads that complete before they return.
@@ -282,22 +396,42 @@ gemm_bf16_kernel(GemmParams p, int tilesM, int tilesN, int groups) {
     // fragments of tile kt+1 are read into na/nb before each half, so the read
     // latency overlaps the MFMAs already in the pipe.  Called with the two
     // register sets in alternating roles (static indexing).
+    // With split reads the fragment reads of tile kt+1 are started before a
+    // half of tile kt's MFMAs and completed after it, so their latency hides
+    // under those MFMAs.
+    constexpr bool kSplit = LMOE_SPLIT_READS && (A_K ? (FM == 4 || FM == 8) : FM == 4) &&
+                            (BK_C ? (FN == 4 || FN == 8) : FN == 4);
+    u32x2 pa[8], pb[8];
     auto step = [&](int kt, u32x4 (&ca)[FM], u32x4 (&cb)[FN], u32x4 (&na)[FM], u32x4 (&nb)[FN]) {
       const bool more = kt + 1 < nk;
+      const uint16_t* st = lds + ((kt + 1) % STAGES) * STAGE;
       if (more) {
         // tile kt+1 has landed once only tiles kt+2 .. min(kt+STAGES-1, nk-1) are pending
         wait_vm_tiles<LPS, STAGES - 2>(min(STAGES - 2, nk - 2 - kt));
         lds_barrier();  // tile kt+1 is in LDS for every wave; no wave reads tile kt's stage any more
         if (kt + STAGES < nk) issue(kt + STAGES);
-        read_a(kt + 1, na);
       }
+      // Split reads are unconditional (branch-free, so the pending registers
+      // are never copied): after the last tile they read a stale stage that
+      // no load is writing, and the values are discarded.
+      if constexpr (kSplit) TA::template read_issue<FM>(na, pa, st, wm * WTM, lane);
+      else if (more) read_a(kt + 1, na);
       __builtin_amdgcn_sched_barrier(0);
       mfma_rows(0, FM / 2, ca, cb);
       __builtin_amdgcn_sched_barrier(0);
-      if (more) read_b(kt + 1, nb);
+      if constexpr (kSplit) {
+        TA::template read_finish<FM>(na, pa);
+        TB::template read_issue<FN>(nb, pb, st + BM * BK, wn * WTN, lane);
+      } else if (more) {
+        read_b(kt + 1, nb);
+      }
       __builtin_amdgcn_sched_barrier(0);
       mfma_rows(FM / 2, FM, ca, cb);
       __builtin_amdgcn_sched_barrier(0);
+      if constexpr (kSplit) {
+        TB::template read_finish<FN>(nb, pb);
+        __builtin_amdgcn_sched_barrier(0);
+      }
     };
 
     u32x4 fa0[FM], fb0[FN], fa1[FM], fb1[FN];
@@ -320,10 +454,11 @@ gemm_bf16_kernel(GemmParams p, int tilesM, int tilesN, int groups) {
     // Epilogue: stage 32-row slices of the wave tile through LDS as float,
     // then write 16-byte vectors (8 bf16) with the epilogue applied.
     float* st = reinterpret_cast<float*>(lds) + wid * (EPI_ROWS * EPI_LD);
-    uint16_t* C = (uint16_t*)p.C + (int64_t)g * p.sC + (RAGGED_K ? 0 : (int64_t)lo * p.ldc);
-    uint16_t* C2 = EPI == EPI_FWD1 ? (uint16_t*)p.C2 + (int64_t)g * p.sC + (int64_t)lo * p.ldc : nullptr;
-    const uint16_t* Aux = (EPI == EPI_DACT || EPI == EPI_RES)
-                              ? (const uint16_t*)p.Aux + (int64_t)g * p.sC + (int64_t)lo * p.ldc : nullptr;
+    // Output rows are relative to lo_al; a row-major output starts at row lo_al.
+    const int64_t cofs = (int64_t)g * p.sC + (RAGGED_K || CBLK ? 0 : (int64_t)lo_al * p.ldc);
+    uint16_t* C = (uint16_t*)p.C + cofs;
+    uint16_t* C2 = EPI == EPI_FWD1 ? (uint16_t*)p.C2 + cofs : nullptr;
+    const uint16_t* Aux = (EPI == EPI_DACT || EPI == EPI_RES) ? (const uint16_t*)p.Aux + cofs : nullptr;
     const int g4 = lane >> 4;
 #pragma unroll
     for (int pass = 0; pass < WTM / EPI_ROWS; ++pass) {
@@ -343,13 +478,13 @@ gemm_bf16_kernel(GemmParams p, int tilesM, int tilesN, int groups) {
         const int rr = q / CPR, cc = q % CPR;
         const int row = m0 + wm * WTM + pass * EPI_ROWS + rr;
         const int col = n0 + wn * WTN + cc * 8;
-        if (row < Mlim && col < p.N) {
+        if (row < Mlim && col < p.N && (RAGGED_K || lo_al + row >= lo)) {
           float v[8];
           const f32x4 a = *reinterpret_cast<const f32x4*>(st + rr * EPI_LD + cc * 8);
           const f32x4 b = *reinterpret_cast<const f32x4*>(st + rr * EPI_LD + cc * 8 + 4);
 #pragma unroll
           for (int u = 0; u < 4; ++u) { v[u] = a[u]; v[4 + u] = b[u]; }
-          const int64_t off = (int64_t)row * p.ldc + col;
+          const int64_t off = CBLK ? blk_off(lo_al + row, col, p.ldc) : (int64_t)row * p.ldc + col;
           if constexpr (EPI == EPI_FWD1) {
             Vec<uint16_t>::store(C + off, v);
 #pragma unroll
@@ -477,11 +612,12 @@ static int num_cus() {
   return n;
 }
 
-template <bool B_K, bool RAGGED_K, int EPI, int ACT>
+template <bool B_K, bool RAGGED_K, int EPI, int ACT, bool BLK, bool CBLK>
 static void launch_bf16(int groups, const GemmParams& p, int tilesM, int tilesN, hipStream_t s) {
   constexpr int NT = Tile::WGM * Tile::WGN * 64;
   constexpr size_t shmem = Tile::STAGES * (size_t)(Tile::BM + Tile::BN) * kBKb * sizeof(uint16_t);
-  auto kern = gemm_bf16_kernel<Tile::BM, Tile::BN, Tile::WGM, Tile::WGN, Tile::STAGES, Tile::OCC, B_K, RAGGED_K, EPI, ACT>;
+  auto kern = gemm_bf16_kernel<Tile::BM, Tile::BN, Tile::WGM, Tile::WGN, Tile::STAGES, Tile::OCC, B_K, RAGGED_K, EPI,
+                               ACT, BLK, CBLK>;
   static bool attr_set = false;
   if (!attr_set) {
     (void)hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)shmem);
@@ -494,19 +630,24 @@ static void launch_bf16(int groups, const GemmParams& p, int tilesM, int tilesN,
   hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(NT), shmem, s, p, tilesM, tilesN, groups);
 }
 
-// groups: experts (or 1 for a dense product); dtype/act as in moe_cfg.
-template <bool B_K, bool RAGGED_K, int EPI>
+// groups: experts (or 1 for a dense product); dtype/act as in moe_cfg.  BLK,
+// CBLK (bf16 only): operands / output in the blocked layout.
+template <bool B_K, bool RAGGED_K, int EPI, bool BLK = false, bool CBLK = false>
 static void run_gemm(int dtype, int act, int groups, const GemmParams& p, int tilesM, int tilesN, hipStream_t s) {
   if (tilesM <= 0 || tilesN <= 0 || groups <= 0) return;
   if (dtype == MOE_BF16) {
     if constexpr (EPI == EPI_STORE || EPI == EPI_RES) {
-      launch_bf16<B_K, RAGGED_K, EPI, MOE_ACT_IDENTITY>(groups, p, tilesM, tilesN, s);
+      launch_bf16<B_K, RAGGED_K, EPI, MOE_ACT_IDENTITY, BLK, CBLK>(groups, p, tilesM, tilesN, s);
     } else {
       switch (act) {
-        case MOE_ACT_RELU: launch_bf16<B_K, RAGGED_K, EPI, MOE_ACT_RELU>(groups, p, tilesM, tilesN, s); break;
-        case MOE_ACT_GELU_TANH: launch_bf16<B_K, RAGGED_K, EPI, MOE_ACT_GELU_TANH>(groups, p, tilesM, tilesN, s); break;
-        case MOE_ACT_GELU_ERF: launch_bf16<B_K, RAGGED_K, EPI, MOE_ACT_GELU_ERF>(groups, p, tilesM, tilesN, s); break;
-        default: launch_bf16<B_K, RAGGED_K, EPI, MOE_ACT_IDENTITY>(groups, p, tilesM, tilesN, s); break;
+        case MOE_ACT_RELU: launch_bf16<B_K, RAGGED_K, EPI, MOE_ACT_RELU, BLK, CBLK>(groups, p, tilesM, tilesN, s); break;
+        case MOE_ACT_GELU_TANH:
+          launch_bf16<B_K, RAGGED_K, EPI, MOE_ACT_GELU_TANH, BLK, CBLK>(groups, p, tilesM, tilesN, s);
+          break;
+        case MOE_ACT_GELU_ERF:
+          launch_bf16<B_K, RAGGED_K, EPI, MOE_ACT_GELU_ERF, BLK, CBLK>(groups, p, tilesM, tilesN, s);
+          break;
+        default: launch_bf16<B_K, RAGGED_K, EPI, MOE_ACT_IDENTITY, BLK, CBLK>(groups, p, tilesM, tilesN, s); break;
       }
     }
   } else {
@@ -517,47 +658,53 @@ static void run_gemm(int dtype, int act, int groups, const GemmParams& p, int ti
   }
 }
 
-template <bool B_K, bool RAGGED_K, int EPI>
-static void run_gemm(const moe_cfg& c, const GemmParams& p, int tilesM, int tilesN, hipStream_t s) {
-  run_gemm<B_K, RAGGED_K, EPI>(c.dtype, c.act, c.E, p, tilesM, tilesN, s);
+// Expert products: bf16 operands and outputs in the blocked layout (dW outputs
+// row-major), float ones row-major.
+template <bool B_K, bool RAGGED_K, int EPI, bool CBLK>
+static void run_expert(const moe_cfg& c, const GemmParams& p, int tilesM, int tilesN, hipStream_t s) {
+  run_gemm<B_K, RAGGED_K, EPI, true, CBLK>(c.dtype, c.act, c.E, p, tilesM, tilesN, s);
 }
 
 static int tile_m(const moe_cfg& c) { return c.dtype == MOE_BF16 ? kBM : 64; }
 static int tile_n(const moe_cfg& c) { return c.dtype == MOE_BF16 ? kBN : 64; }
 static int cdiv(int64_t a, int b) { return (int)((a + b - 1) / b); }
+// Rows per expert block of an [E][C][*] buffer (C rounded up to 16 for bf16).
+static int64_t rows_alloc(const moe_cfg& c) { return c.dtype == MOE_BF16 ? pad16(c.C) : c.C; }
 
 void launch_expert_fwd(const moe_cfg& c, const void* X, const int32_t* rb, const int32_t* re, const void* W1,
                        const void* W2, void* H, void* A, void* O, hipStream_t s) {
-  const int64_t d = c.d_model, f = c.d_ff, C = c.C;
-  GemmParams p1{X, d, C * d, W1, d, f * d, H, f, C * f, A, nullptr, rb, re, 0, (int)f, (int)d, c.act, (int)C};
-  run_gemm<true, false, EPI_FWD1>(c, p1, cdiv(C, tile_m(c)), cdiv(f, tile_n(c)), s);
-  GemmParams p2{A, f, C * f, W2, f, d * f, O, d, C * d, nullptr, nullptr, rb, re, 0, (int)d, (int)f, c.act, (int)C};
-  run_gemm<true, false, EPI_STORE>(c, p2, cdiv(C, tile_m(c)), cdiv(d, tile_n(c)), s);
+  const int64_t d = c.d_model, f = c.d_ff, C = c.C, Cp = rows_alloc(c);
+  const int tm = cdiv(C + 15, tile_m(c));
+  GemmParams p1{X, d, Cp * d, W1, d, f * d, H, f, Cp * f, A, nullptr, rb, re, 0, (int)f, (int)d, c.act, (int)C};
+  run_expert<true, false, EPI_FWD1, true>(c, p1, tm, cdiv(f, tile_n(c)), s);
+  GemmParams p2{A, f, Cp * f, W2, f, d * f, O, d, Cp * d, nullptr, nullptr, rb, re, 0, (int)d, (int)f, c.act, (int)C};
+  run_expert<true, false, EPI_STORE, true>(c, p2, tm, cdiv(d, tile_n(c)), s);
 }
 
 void launch_expert_bwd_dx(const moe_cfg& c, const void* dO, const int32_t* rb, const int32_t* re, const void* H,
                           const void* W1, const void* W2, void* dH, void* dXe, hipStream_t s) {
-  const int64_t d = c.d_model, f = c.d_ff, C = c.C;
+  const int64_t d = c.d_model, f = c.d_ff, C = c.C, Cp = rows_alloc(c);
+  const int tm = cdiv(C + 15, tile_m(c));
   // dA = dO W2_e  (B(k=i, n=j) = W2[e][i][j], N contiguous), epilogue dH = dA * act'(H)
-  GemmParams p1{dO, d, C * d, W2, f, d * f, dH, f, C * f, nullptr, H, rb, re, 0, (int)f, (int)d, c.act, (int)C};
-  run_gemm<false, false, EPI_DACT>(c, p1, cdiv(C, tile_m(c)), cdiv(f, tile_n(c)), s);
+  GemmParams p1{dO, d, Cp * d, W2, f, d * f, dH, f, Cp * f, nullptr, H, rb, re, 0, (int)f, (int)d, c.act, (int)C};
+  run_expert<false, false, EPI_DACT, true>(c, p1, tm, cdiv(f, tile_n(c)), s);
   // dXe = dH W1_e  (B(k=i, n=j) = W1[e][i][j])
-  GemmParams p2{dH, f, C * f, W1, d, f * d, dXe, d, C * d, nullptr, nullptr, rb, re, 0, (int)d, (int)f, c.act, (int)C};
-  run_gemm<false, false, EPI_STORE>(c, p2, cdiv(C, tile_m(c)), cdiv(d, tile_n(c)), s);
+  GemmParams p2{dH, f, Cp * f, W1, d, f * d, dXe, d, Cp * d, nullptr, nullptr, rb, re, 0, (int)d, (int)f, c.act, (int)C};
+  run_expert<false, false, EPI_STORE, true>(c, p2, tm, cdiv(d, tile_n(c)), s);
 }
 
 void launch_expert_bwd_dw(const moe_cfg& c, const void* X, const void* A, const void* dO, const void* dH,
                           const int32_t* rb, const int32_t* re, void* dW1, void* dW2, hipStream_t s) {
-  const int64_t d = c.d_model, f = c.d_ff, C = c.C;
+  const int64_t d = c.d_model, f = c.d_ff, C = c.C, Cp = rows_alloc(c);
   // dW2_e [d][f] = dO_e^T A_e : A-operand(m, k) = dO[e][k][m], B(k, n) = A[e][k][n]
-  GemmParams p2{dO, d, C * d, A, f, C * f, dW2, f, d * f, nullptr, nullptr, rb, re, (int)d, (int)f, 0, c.act, (int)C};
-  run_gemm<false, true, EPI_STORE>(c, p2, cdiv(d, tile_m(c)), cdiv(f, tile_n(c)), s);
+  GemmParams p2{dO, d, Cp * d, A, f, Cp * f, dW2, f, d * f, nullptr, nullptr, rb, re, (int)d, (int)f, 0, c.act, (int)C};
+  run_expert<false, true, EPI_STORE, false>(c, p2, cdiv(d, tile_m(c)), cdiv(f, tile_n(c)), s);
   // dW1_e [f][d] = dH_e^T X_e
-  GemmParams p1{dH, f, C * f, X, d, C * d, dW1, d, f * d, nullptr, nullptr, rb, re, (int)f, (int)d, 0, c.act, (int)C};
-  run_gemm<false, true, EPI_STORE>(c, p1, cdiv(f, tile_m(c)), cdiv(d, tile_n(c)), s);
+  GemmParams p1{dH, f, Cp * f, X, d, Cp * d, dW1, d, f * d, nullptr, nullptr, rb, re, (int)f, (int)d, 0, c.act, (int)C};
+  run_expert<false, true, EPI_STORE, false>(c, p1, cdiv(f, tile_m(c)), cdiv(d, tile_n(c)), s);
 }
 
-// Dense bf16 products of the transformer block (one group, every row).
+// Dense bf16 products of the transformer block (one group, every row, row-major).
 void launch_dense(int64_t M, int N, int K, const void* A, int64_t lda, const void* B, int64_t ldb, bool b_nk,
                   void* C, int64_t ldc, const void* resid, hipStream_t s) {
   GemmParams p{A, lda, 0, B, ldb, 0, C, ldc, 0, nullptr, resid, nullptr, nullptr, 0, N, K, 0, (int)M};

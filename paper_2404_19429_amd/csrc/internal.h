@@ -27,6 +27,9 @@ void launch_dispatch_bwd(const moe_cfg& c, const void* Wg, const float* dlogits,
 size_t bwd_dw_ws_bytes(const moe_cfg& c);
 void launch_dwg(const moe_cfg& c, const void* x, const float* dlogits, float* dWg, void* ws, hipStream_t s);
 
+// Expert weights into the layout the expert GEMMs read (blocked for bf16, a copy for float).
+void launch_pack_weights(const moe_cfg& c, const void* W1, const void* W2, void* W1p, void* W2p, hipStream_t s);
+
 // gemm.hip: expert GEMMs over [E][C][*] buffers with per-expert row ranges.
 void launch_expert_fwd(const moe_cfg& c, const void* X, const int32_t* rb, const int32_t* re, const void* W1,
                        const void* W2, void* H, void* A, void* O, hipStream_t s);

@@ -65,6 +65,53 @@ template <> struct RdTr<8> {
   }
 };
 
+// Split reads: the *Issue blocks start up to 8 reads and return at once; the
+// outputs are pending until a following lds_wait(...) names them.  In between,
+// the caller may only issue independent work (the MFMAs of the previous
+// fragments); the build's ISA check rejects any compiled use of a pending
+// register before the wait.
+template <int N> struct Rd128Issue;
+template <> struct Rd128Issue<4> {
+  __device__ static void run(u32x4* o, const uint32_t* a) {
+    asm volatile("ds_read_b128 %0, %4\n ds_read_b128 %1, %5\n ds_read_b128 %2, %6\n ds_read_b128 %3, %7"
+                 : "=&v"(o[0]), "=&v"(o[1]), "=&v"(o[2]), "=&v"(o[3])
+                 : "v"(a[0]), "v"(a[1]), "v"(a[2]), "v"(a[3])
+                 : "memory");
+  }
+};
+template <> struct Rd128Issue<8> {
+  __device__ static void run(u32x4* o, const uint32_t* a) {
+    asm volatile("ds_read_b128 %0, %8\n ds_read_b128 %1, %9\n ds_read_b128 %2, %10\n ds_read_b128 %3, %11\n"
+                 "ds_read_b128 %4, %12\n ds_read_b128 %5, %13\n ds_read_b128 %6, %14\n ds_read_b128 %7, %15"
+                 : "=&v"(o[0]), "=&v"(o[1]), "=&v"(o[2]), "=&v"(o[3]), "=&v"(o[4]), "=&v"(o[5]), "=&v"(o[6]), "=&v"(o[7])
+                 : "v"(a[0]), "v"(a[1]), "v"(a[2]), "v"(a[3]), "v"(a[4]), "v"(a[5]), "v"(a[6]), "v"(a[7])
+                 : "memory");
+  }
+};
+struct RdTrIssue8 {
+  __device__ static void run(u32x2* o, const uint32_t* a) {
+    asm volatile("ds_read_b64_tr_b16 %0, %8\n ds_read_b64_tr_b16 %1, %9\n ds_read_b64_tr_b16 %2, %10\n"
+                 "ds_read_b64_tr_b16 %3, %11\n ds_read_b64_tr_b16 %4, %12\n ds_read_b64_tr_b16 %5, %13\n"
+                 "ds_read_b64_tr_b16 %6, %14\n ds_read_b64_tr_b16 %7, %15"
+                 : "=&v"(o[0]), "=&v"(o[1]), "=&v"(o[2]), "=&v"(o[3]), "=&v"(o[4]), "=&v"(o[5]), "=&v"(o[6]), "=&v"(o[7])
+                 : "v"(a[0]), "v"(a[1]), "v"(a[2]), "v"(a[3]), "v"(a[4]), "v"(a[5]), "v"(a[6]), "v"(a[7])
+                 : "memory");
+  }
+};
+__device__ __forceinline__ void lds_wait(u32x4 (&o)[4]) {
+  asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(o[0]), "+v"(o[1]), "+v"(o[2]), "+v"(o[3]) :: "memory");
+}
+__device__ __forceinline__ void lds_wait(u32x4 (&o)[8]) {
+  asm volatile("s_waitcnt lgkmcnt(0)"
+               : "+v"(o[0]), "+v"(o[1]), "+v"(o[2]), "+v"(o[3]), "+v"(o[4]), "+v"(o[5]), "+v"(o[6]), "+v"(o[7])
+               :: "memory");
+}
+__device__ __forceinline__ void lds_wait(u32x2 (&o)[8]) {
+  asm volatile("s_waitcnt lgkmcnt(0)"
+               : "+v"(o[0]), "+v"(o[1]), "+v"(o[2]), "+v"(o[3]), "+v"(o[4]), "+v"(o[5]), "+v"(o[6]), "+v"(o[7])
+               :: "memory");
+}
+
 // vmcnt(n) (gfx9 encoding; expcnt and lgkmcnt unrestricted).
 template <int N>
 __device__ __forceinline__ void wait_vm() {

@@ -12,6 +12,14 @@
 
 namespace lmoe {
 
+// Element offset of (expert e, row s, column col) in an [E][C][d] buffer:
+// blocked for bf16 (rows padded to 16), row-major for float.
+template <typename T>
+__device__ __forceinline__ int64_t eoff(int e, int s, int col, int d, int C) {
+  const int64_t rows = sizeof(T) == 2 ? pad16(C) : C;
+  return (int64_t)e * rows * d + ebuf_off<T>(s, col, d);
+}
+
 // ------------------------------------------------------------ slot assignment
 // counts[chunk][E]: assignments of each expert inside one chunk of tokens.
 __global__ __launch_bounds__(kRouteChunk) void route_count_kernel(const int32_t* __restrict__ idx,
@@ -128,7 +136,7 @@ __global__ __launch_bounds__(256) void dispatch_copy_kernel(const T* __restrict_
     const int s = slot[t * k + r];
     const int e = idx[t * k + r];
     if (s >= 0 && s < C && e >= 0 && e < E) {
-      *reinterpret_cast<u32x4*>(send + ((int64_t)e * C + s) * d + (int64_t)c * V) = v;
+      *reinterpret_cast<u32x4*>(send + eoff<T>(e, s, c * V, d, C)) = v;
     }
   }
 }
@@ -187,7 +195,7 @@ __global__ __launch_bounds__(256) void combine_kernel(const T* __restrict__ O, c
     if (s >= 0 && s < C && e >= 0 && e < E) {
       const float wr = w[t * k + r];
       float v[V];
-      Vec<T>::load(O + ((int64_t)e * C + s) * d + (int64_t)c * V, v);
+      Vec<T>::load(O + eoff<T>(e, s, c * V, d, C), v);
 #pragma unroll
       for (int i = 0; i < V; ++i) acc[i] = fmaf(wr, v[i], acc[i]);
     }
@@ -241,7 +249,7 @@ __global__ __launch_bounds__(256) void combine_bwd_kernel(const float* __restric
 #pragma unroll
     for (int r = 0; r < kMaxK; ++r) {
       if (sr[r] >= 0) {
-        const int64_t off = ((int64_t)er[r] * C + sr[r]) * d + (int64_t)c * V;
+        const int64_t off = eoff<T>(er[r], sr[r], c * V, d, C);
         float o[V], out[V];
         Vec<T>::load(O + off, o);
 #pragma unroll
@@ -320,7 +328,7 @@ __global__ __launch_bounds__(256) void dispatch_bwd_kernel(const T* __restrict__
     const int e = idx[t * k + r];
     if (s >= 0 && s < C && e >= 0 && e < E) {
       float v[V];
-      Vec<T>::load(dXe + ((int64_t)e * C + s) * d + (int64_t)c * V, v);
+      Vec<T>::load(dXe + eoff<T>(e, s, c * V, d, C), v);
 #pragma unroll
       for (int i = 0; i < V; ++i) acc[i] += v[i];
     }
@@ -446,6 +454,42 @@ void launch_dwg(const moe_cfg& c, const void* x, const float* dlogits, float* dW
   }
   hipLaunchKernelGGL(dwg_reduce_kernel, dim3((unsigned)((ed + 255) / 256)), dim3(256), 0, s, part, dWg, (int)nch,
                      c.E, c.d_model);
+}
+
+}  // namespace lmoe
+
+namespace lmoe {
+
+// ------------------------------------------------------------- weight packing
+// Row-major [R][X] matrices -> blocked layout (bf16), one thread per 16-byte
+// chunk: reads are coalesced along rows, writes land as 64-byte block rows.
+__global__ __launch_bounds__(256) void pack_blocked_kernel(const uint16_t* __restrict__ src, uint16_t* __restrict__ dst,
+                                                           int64_t nmat, int R, int X) {
+  const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int cpr = X / 8;
+  const int64_t per = (int64_t)R * cpr;
+  if (gid >= nmat * per) return;
+  const int64_t m = gid / per;
+  const int64_t rem = gid - m * per;
+  const int r = (int)(rem / cpr), c = (int)(rem % cpr) * 8;
+  const int64_t base = m * (int64_t)R * X;
+  *reinterpret_cast<u32x4*>(dst + base + blk_off(r, c, X)) =
+      *reinterpret_cast<const u32x4*>(src + base + (int64_t)r * X + c);
+}
+
+void launch_pack_weights(const moe_cfg& c, const void* W1, const void* W2, void* W1p, void* W2p, hipStream_t s) {
+  const int64_t E = c.E, d = c.d_model, f = c.d_ff;
+  if (c.dtype == MOE_BF16) {
+    const int64_t n = E * f * d / 8;
+    hipLaunchKernelGGL(pack_blocked_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s,
+                       (const uint16_t*)W1, (uint16_t*)W1p, E, (int)f, (int)d);
+    hipLaunchKernelGGL(pack_blocked_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s,
+                       (const uint16_t*)W2, (uint16_t*)W2p, E, (int)d, (int)f);
+  } else {
+    const size_t bytes = (size_t)E * f * d * sizeof(float);
+    (void)hipMemcpyAsync(W1p, W1, bytes, hipMemcpyDeviceToDevice, s);
+    (void)hipMemcpyAsync(W2p, W2, bytes, hipMemcpyDeviceToDevice, s);
+  }
 }
 
 }  // namespace lmoe

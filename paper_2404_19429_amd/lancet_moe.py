@@ -27,8 +27,8 @@ MOE_CALL_DISPATCH, MOE_CALL_BWD_DX, MOE_CALL_BWD_DW = 0, 1, 2
 
 #: Every symbol include/lancet_moe.h declares.
 EXPORTS = ["moe_capacity", "moe_workspace_bytes", "moe_last_error", "moe_gate_topk", "moe_dispatch",
-           "moe_expert_ffn_fwd", "moe_combine", "moe_bwd_dx", "moe_bwd_dw", "moe_block_workspace_bytes",
-           "moe_block_chunked"]
+           "moe_pack_weights", "moe_expert_ffn_fwd", "moe_combine", "moe_bwd_dx", "moe_bwd_dw",
+           "moe_block_workspace_bytes", "moe_block_chunked"]
 MOE_BLOCK_FWD, MOE_BLOCK_BWD = 1, 2
 
 
@@ -51,7 +51,7 @@ class moe_block_cfg(ctypes.Structure):
 BLOCK_WEIGHTS = ["ln1_g", "ln1_b", "Wqkv", "Wo", "ln2_g", "ln2_b", "Wg", "W1", "W2"]
 BLOCK_GRADS = ["dln1_g", "dln1_b", "dWqkv", "dWo", "dln2_g", "dln2_b", "dWg", "dW1", "dW2"]
 BLOCK_ACTS_FWD = ["a", "ln1_mean", "ln1_rstd", "qkv", "attn", "lse", "h", "ln2_mean", "ln2_rstd", "m", "logits",
-                  "idx", "w", "slot", "fill", "send_buf", "H", "A", "expert_out"]
+                  "idx", "w", "slot", "fill", "send_buf", "H", "A", "expert_out", "W1p", "W2p"]
 BLOCK_ACTS_BWD = ["dO", "dH", "dXe", "dlogits", "dm", "dh", "dattn", "delta", "dqkv", "da"]
 
 
@@ -79,6 +79,7 @@ def _load():
         "moe_last_error": (ctypes.c_char_p, []),
         "moe_gate_topk": (I32, [CFG, P, P, P, P, P, P, P]),
         "moe_dispatch": (I32, [CFG, P, P, P, P, P, P, P, SZ, P]),
+        "moe_pack_weights": (I32, [CFG, P, P, P, P, P]),
         "moe_expert_ffn_fwd": (I32, [CFG, P, P, P, P, P, P, P, P, P]),
         "moe_combine": (I32, [CFG, P, P, P, P, P, P]),
         "moe_bwd_dx": (I32, [CFG] + [P] * 18 + [SZ, P]),
@@ -106,6 +107,16 @@ def make_cfg(T, d_model, d_ff, E, k, C, G=1, dtype="bf16", act="gelu_tanh", reno
 
 def torch_dtype(cfg: moe_cfg):
     return torch.bfloat16 if cfg.dtype == MOE_BF16 else torch.float32
+
+
+def rows_alloc(cfg: moe_cfg) -> int:
+    """Rows per expert of an [E][C][X] buffer: C rounded up to 16 for bf16 (blocked layout), C for float."""
+    return (cfg.C + 15) // 16 * 16 if cfg.dtype == MOE_BF16 else cfg.C
+
+
+def expert_numel(cfg: moe_cfg, X: int) -> int:
+    """Elements of an [E][C][X] expert buffer (see the layout note in include/lancet_moe.h)."""
+    return cfg.E * rows_alloc(cfg) * X
 
 
 def _stream(stream) -> int:
@@ -161,47 +172,55 @@ def moe_gate_topk(cfg, x, Wg, bias, logits, idx, w, stream=None):
 
 def moe_dispatch(cfg, x, idx, carry, fill, slot, send_buf, ws, stream=None):
     dt = torch_dtype(cfg)
-    T, d, E, k, C = cfg.T, cfg.d_model, cfg.E, cfg.k, cfg.C
+    T, d, E, k = cfg.T, cfg.d_model, cfg.E, cfg.k
     need = moe_workspace_bytes(cfg, MOE_CALL_DISPATCH)
     _check(_lib.moe_dispatch(ctypes.byref(cfg), _ptr(x, "x", dt, T * d), _ptr(idx, "idx", torch.int32, T * k),
                              _ptr(carry, "carry", torch.int32, E, nullable=True), _ptr(fill, "fill", torch.int32, E),
-                             _ptr(slot, "slot", torch.int32, T * k), _ptr(send_buf, "send_buf", dt, E * C * d),
+                             _ptr(slot, "slot", torch.int32, T * k), _ptr(send_buf, "send_buf", dt, expert_numel(cfg, d)),
                              _ptr(ws, "ws", torch.uint8, need, nullable=need == 0),
                              ws.numel() if ws is not None else 0, _stream(stream)))
 
 
-def moe_expert_ffn_fwd(cfg, send_buf, row_begin, row_end, W1, W2, H, A, expert_out, stream=None):
+def moe_pack_weights(cfg, W1, W2, W1p, W2p, stream=None):
     dt = torch_dtype(cfg)
-    d, f, E, C = cfg.d_model, cfg.d_ff, cfg.E, cfg.C
-    _check(_lib.moe_expert_ffn_fwd(ctypes.byref(cfg), _ptr(send_buf, "send_buf", dt, E * C * d),
+    n = cfg.E * cfg.d_ff * cfg.d_model
+    _check(_lib.moe_pack_weights(ctypes.byref(cfg), _ptr(W1, "W1", dt, n), _ptr(W2, "W2", dt, n),
+                                 _ptr(W1p, "W1p", dt, n), _ptr(W2p, "W2p", dt, n), _stream(stream)))
+
+
+def moe_expert_ffn_fwd(cfg, send_buf, row_begin, row_end, W1p, W2p, H, A, expert_out, stream=None):
+    dt = torch_dtype(cfg)
+    d, f, E = cfg.d_model, cfg.d_ff, cfg.E
+    _check(_lib.moe_expert_ffn_fwd(ctypes.byref(cfg), _ptr(send_buf, "send_buf", dt, expert_numel(cfg, d)),
                                    _ptr(row_begin, "row_begin", torch.int32, E, nullable=True),
-                                   _ptr(row_end, "row_end", torch.int32, E), _ptr(W1, "W1", dt, E * f * d),
-                                   _ptr(W2, "W2", dt, E * d * f), _ptr(H, "H", dt, E * C * f),
-                                   _ptr(A, "A", dt, E * C * f), _ptr(expert_out, "expert_out", dt, E * C * d),
-                                   _stream(stream)))
+                                   _ptr(row_end, "row_end", torch.int32, E), _ptr(W1p, "W1p", dt, E * f * d),
+                                   _ptr(W2p, "W2p", dt, E * d * f), _ptr(H, "H", dt, expert_numel(cfg, f)),
+                                   _ptr(A, "A", dt, expert_numel(cfg, f)),
+                                   _ptr(expert_out, "expert_out", dt, expert_numel(cfg, d)), _stream(stream)))
 
 
 def moe_combine(cfg, expert_out, idx, slot, w, y, stream=None):
     dt = torch_dtype(cfg)
-    T, d, E, k, C = cfg.T, cfg.d_model, cfg.E, cfg.k, cfg.C
-    _check(_lib.moe_combine(ctypes.byref(cfg), _ptr(expert_out, "expert_out", dt, E * C * d),
+    T, d, k = cfg.T, cfg.d_model, cfg.k
+    _check(_lib.moe_combine(ctypes.byref(cfg), _ptr(expert_out, "expert_out", dt, expert_numel(cfg, d)),
                             _ptr(idx, "idx", torch.int32, T * k), _ptr(slot, "slot", torch.int32, T * k),
                             _ptr(w, "w", torch.float32, T * k), _ptr(y, "y", dt, T * d), _stream(stream)))
 
 
-def moe_bwd_dx(cfg, Wg, logits, idx, w, slot, row_begin, row_end, H, expert_out, W1, W2, dy, dO, dH, dXe,
+def moe_bwd_dx(cfg, Wg, logits, idx, w, slot, row_begin, row_end, H, expert_out, W1p, W2p, dy, dO, dH, dXe,
                dlogits, dx, ws=None, stream=None):
     dt = torch_dtype(cfg)
-    T, d, f, E, k, C = cfg.T, cfg.d_model, cfg.d_ff, cfg.E, cfg.k, cfg.C
+    T, d, f, E, k = cfg.T, cfg.d_model, cfg.d_ff, cfg.E, cfg.k
+    nd, nf = expert_numel(cfg, d), expert_numel(cfg, f)
     need = moe_workspace_bytes(cfg, MOE_CALL_BWD_DX)
     _check(_lib.moe_bwd_dx(ctypes.byref(cfg), _ptr(Wg, "Wg", dt, E * d), _ptr(logits, "logits", torch.float32, T * E),
                            _ptr(idx, "idx", torch.int32, T * k), _ptr(w, "w", torch.float32, T * k),
                            _ptr(slot, "slot", torch.int32, T * k),
                            _ptr(row_begin, "row_begin", torch.int32, E, nullable=True),
-                           _ptr(row_end, "row_end", torch.int32, E), _ptr(H, "H", dt, E * C * f),
-                           _ptr(expert_out, "expert_out", dt, E * C * d), _ptr(W1, "W1", dt, E * f * d),
-                           _ptr(W2, "W2", dt, E * d * f), _ptr(dy, "dy", dt, T * d), _ptr(dO, "dO", dt, E * C * d),
-                           _ptr(dH, "dH", dt, E * C * f), _ptr(dXe, "dXe", dt, E * C * d),
+                           _ptr(row_end, "row_end", torch.int32, E), _ptr(H, "H", dt, nf),
+                           _ptr(expert_out, "expert_out", dt, nd), _ptr(W1p, "W1p", dt, E * f * d),
+                           _ptr(W2p, "W2p", dt, E * d * f), _ptr(dy, "dy", dt, T * d), _ptr(dO, "dO", dt, nd),
+                           _ptr(dH, "dH", dt, nf), _ptr(dXe, "dXe", dt, nd),
                            _ptr(dlogits, "dlogits", torch.float32, T * E), _ptr(dx, "dx", dt, T * d),
                            _ptr(ws, "ws", torch.uint8, need, nullable=need == 0),
                            ws.numel() if ws is not None else 0, _stream(stream)))
@@ -209,13 +228,14 @@ def moe_bwd_dx(cfg, Wg, logits, idx, w, slot, row_begin, row_end, H, expert_out,
 
 def moe_bwd_dw(cfg, x, dlogits, row_begin, row_end, send_buf, A, dO, dH, dW1, dW2, dWg, ws, stream=None):
     dt = torch_dtype(cfg)
-    T, d, f, E, C = cfg.T, cfg.d_model, cfg.d_ff, cfg.E, cfg.C
+    T, d, f, E = cfg.T, cfg.d_model, cfg.d_ff, cfg.E
+    nd, nf = expert_numel(cfg, d), expert_numel(cfg, f)
     need = moe_workspace_bytes(cfg, MOE_CALL_BWD_DW)
     _check(_lib.moe_bwd_dw(ctypes.byref(cfg), _ptr(x, "x", dt, T * d, nullable=T == 0),
                            _ptr(dlogits, "dlogits", torch.float32, T * E),
                            _ptr(row_begin, "row_begin", torch.int32, E, nullable=True),
-                           _ptr(row_end, "row_end", torch.int32, E), _ptr(send_buf, "send_buf", dt, E * C * d),
-                           _ptr(A, "A", dt, E * C * f), _ptr(dO, "dO", dt, E * C * d), _ptr(dH, "dH", dt, E * C * f),
+                           _ptr(row_end, "row_end", torch.int32, E), _ptr(send_buf, "send_buf", dt, nd),
+                           _ptr(A, "A", dt, nf), _ptr(dO, "dO", dt, nd), _ptr(dH, "dH", dt, nf),
                            _ptr(dW1, "dW1", dt, E * f * d), _ptr(dW2, "dW2", dt, E * d * f),
                            _ptr(dWg, "dWg", torch.float32, E * d),
                            _ptr(ws, "ws", torch.uint8, need, nullable=need == 0),
@@ -246,6 +266,8 @@ class LayerBuffers:
     dW1: torch.Tensor
     dW2: torch.Tensor
     dWg: torch.Tensor
+    W1p: torch.Tensor
+    W2p: torch.Tensor
     ws_dispatch: torch.Tensor
     ws_dx: torch.Tensor
     ws_dw: torch.Tensor
@@ -255,12 +277,13 @@ def alloc_layer(cfg: moe_cfg, device="cuda") -> LayerBuffers:
     dt = torch_dtype(cfg)
     T, d, f, E, k, C = cfg.T, cfg.d_model, cfg.d_ff, cfg.E, cfg.k, cfg.C
     e = lambda *s, dtype=dt: torch.empty(*s, dtype=dtype, device=device)
+    nd, nf = expert_numel(cfg, d), expert_numel(cfg, f)
     return LayerBuffers(
         cfg=cfg, logits=e(T, E, dtype=torch.float32), idx=e(T, k, dtype=torch.int32), w=e(T, k, dtype=torch.float32),
         carry=torch.zeros(E, dtype=torch.int32, device=device), fill=e(E, dtype=torch.int32),
-        slot=e(T, k, dtype=torch.int32), send_buf=e(E, C, d), H=e(E, C, f), A=e(E, C, f), O=e(E, C, d), y=e(T, d),
-        dO=e(E, C, d), dH=e(E, C, f), dXe=e(E, C, d), dlogits=e(T, E, dtype=torch.float32), dx=e(T, d),
-        dW1=e(E, f, d), dW2=e(E, d, f), dWg=e(E, d, dtype=torch.float32),
+        slot=e(T, k, dtype=torch.int32), send_buf=e(nd), H=e(nf), A=e(nf), O=e(nd), y=e(T, d),
+        dO=e(nd), dH=e(nf), dXe=e(nd), dlogits=e(T, E, dtype=torch.float32), dx=e(T, d),
+        dW1=e(E, f, d), dW2=e(E, d, f), dWg=e(E, d, dtype=torch.float32), W1p=e(E * f * d), W2p=e(E * d * f),
         ws_dispatch=e(max(16, moe_workspace_bytes(cfg, MOE_CALL_DISPATCH)), dtype=torch.uint8),
         ws_dx=e(max(16, moe_workspace_bytes(cfg, MOE_CALL_BWD_DX)), dtype=torch.uint8),
         ws_dw=e(max(16, moe_workspace_bytes(cfg, MOE_CALL_BWD_DW)), dtype=torch.uint8),
@@ -268,19 +291,20 @@ def alloc_layer(cfg: moe_cfg, device="cuda") -> LayerBuffers:
 
 
 def layer_forward(b: LayerBuffers, x, Wg, bias, W1, W2, stream=None):
-    """gate -> dispatch -> experts -> combine, all on one stream."""
+    """weight packing -> gate -> dispatch -> experts -> combine, all on one stream."""
     c = b.cfg
+    moe_pack_weights(c, W1, W2, b.W1p, b.W2p, stream)
     moe_gate_topk(c, x, Wg, bias, b.logits, b.idx, b.w, stream)
     moe_dispatch(c, x, b.idx, b.carry, b.fill, b.slot, b.send_buf, b.ws_dispatch, stream)
-    moe_expert_ffn_fwd(c, b.send_buf, b.carry, b.fill, W1, W2, b.H, b.A, b.O, stream)
+    moe_expert_ffn_fwd(c, b.send_buf, b.carry, b.fill, b.W1p, b.W2p, b.H, b.A, b.O, stream)
     moe_combine(c, b.O, b.idx, b.slot, b.w, b.y, stream)
 
 
-def layer_backward(b: LayerBuffers, x, Wg, W1, W2, dy, stream=None, dw_stream=None):
-    """dX chain on `stream`; the dW products on `dw_stream` (default: same stream),
-    ordered after the dX chain by an event."""
+def layer_backward(b: LayerBuffers, x, Wg, dy, stream=None, dw_stream=None):
+    """dX chain on `stream` (with the weights packed by layer_forward); the dW
+    products on `dw_stream` (default: same stream), ordered after the dX chain by an event."""
     c = b.cfg
-    moe_bwd_dx(c, Wg, b.logits, b.idx, b.w, b.slot, b.carry, b.fill, b.H, b.O, W1, W2, dy, b.dO, b.dH, b.dXe,
+    moe_bwd_dx(c, Wg, b.logits, b.idx, b.w, b.slot, b.carry, b.fill, b.H, b.O, b.W1p, b.W2p, dy, b.dO, b.dH, b.dXe,
                b.dlogits, b.dx, b.ws_dx, stream)
     if dw_stream is not None:
         ev = torch.cuda.Event()
@@ -299,7 +323,8 @@ def make_block_cfg(B, S, heads, d_ff, E, k, C, G=1, act="gelu_tanh", renorm=1) -
 def block_shapes(cfg: moe_block_cfg, n_chunks: int):
     """{name: (numel, dtype)} of every weight, gradient and activation of the block."""
     m = cfg.moe
-    T, d, f, E, k, C = m.T, m.d_model, m.d_ff, m.E, m.k, m.C
+    T, d, f, E, k = m.T, m.d_model, m.d_ff, m.E, m.k
+    nd, nf = expert_numel(m, d), expert_numel(m, f)
     Sp = (cfg.S + 63) // 64 * 64
     st = cfg.B * cfg.heads * Sp
     bf, f32, i32 = torch.bfloat16, torch.float32, torch.int32
@@ -311,8 +336,9 @@ def block_shapes(cfg: moe_block_cfg, n_chunks: int):
         "a": (T * d, bf), "ln1_mean": (T, f32), "ln1_rstd": (T, f32), "qkv": (T * 3 * d, bf), "attn": (T * d, bf),
         "lse": (st, f32), "h": (T * d, bf), "ln2_mean": (T, f32), "ln2_rstd": (T, f32), "m": (T * d, bf),
         "logits": (T * E, f32), "idx": (T * k, i32), "w": (T * k, f32), "slot": (T * k, i32),
-        "fill": (n_chunks * E, i32), "send_buf": (E * C * d, bf), "H": (E * C * f, bf), "A": (E * C * f, bf),
-        "expert_out": (E * C * d, bf), "dO": (E * C * d, bf), "dH": (E * C * f, bf), "dXe": (E * C * d, bf),
+        "fill": (n_chunks * E, i32), "send_buf": (nd, bf), "H": (nf, bf), "A": (nf, bf),
+        "expert_out": (nd, bf), "W1p": (E * f * d, bf), "W2p": (E * d * f, bf), "dO": (nd, bf), "dH": (nf, bf),
+        "dXe": (nd, bf),
         "dlogits": (T * E, f32), "dm": (T * d, bf), "dh": (T * d, bf), "dattn": (T * d, bf), "delta": (st, f32),
         "dqkv": (T * 3 * d, bf), "da": (T * d, bf),
     }

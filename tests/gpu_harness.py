@@ -52,6 +52,27 @@ def host(t):
     return t.detach().float().cpu().numpy() if t.is_floating_point() else t.detach().cpu().numpy()
 
 
+EXPERT_X = {"send_buf": "d", "H": "f", "A": "f", "O": "d", "expert_out": "d", "dO": "d", "dH": "f", "dXe": "d"}
+
+
+def expert_host(t, cfg, X):
+    """An [E][C][X] expert buffer as a row-major numpy array (bf16 buffers are
+    stored in 16 x 32 blocks with C padded to a multiple of 16)."""
+    a = host(t)
+    E, C = cfg.E, cfg.C
+    if cfg.dtype == 1:  # bf16
+        Cp = (C + 15) // 16 * 16
+        return a.reshape(E, Cp // 16, X // 32, 16, 32).transpose(0, 1, 3, 2, 4).reshape(E, Cp, X)[:, :C]
+    return a.reshape(E, C, X)
+
+
+def ebuf(b, name):
+    """Expert buffer `name` of LayerBuffers b, row-major [E][C][X]."""
+    c = b.cfg
+    X = c.d_model if EXPERT_X[name] == "d" else c.d_ff
+    return expert_host(getattr(b, name), c, X)
+
+
 def kept_rows(buf, fill, lo=None):
     """Concatenate rows [lo_e, fill_e) of every expert block."""
     E = buf.shape[0]
@@ -77,7 +98,7 @@ def run_layer(L, spec, inp, C, backward=True, dw_stream=None, carry=None):
     bias = None if inp.get("bias") is None else torch.as_tensor(inp["bias"], dtype=torch.float32).cuda()
     L.layer_forward(b, dev["x"], dev["Wg"], bias, dev["W1"], dev["W2"])
     if backward:
-        L.layer_backward(b, dev["x"], dev["Wg"], dev["W1"], dev["W2"], dev["dy"], dw_stream=dw_stream)
+        L.layer_backward(b, dev["x"], dev["Wg"], dev["dy"], dw_stream=dw_stream)
     torch.cuda.synchronize()
     return b, dev
 

@@ -177,3 +177,18 @@ def test_block_invalid_arguments():
     assert _block_call(c, 4, qkv=None) == L.MOE_EINVAL and "qkv" in L.moe_last_error()
     assert _block_call(c, 4, lse=GOOD + 4) == L.MOE_EALIGN
     assert _block_call(c, 4, passes=L.MOE_BLOCK_FWD, dqkv=None) == L.MOE_EDEVICE   # backward buffers unused
+
+
+def test_pack_weights_validation():
+    c = _cfg()
+    lib = L._lib
+    assert lib.moe_pack_weights(ctypes.byref(c), GOOD, GOOD * 2, GOOD * 3, GOOD * 4, None) == L.MOE_EDEVICE
+    assert lib.moe_pack_weights(ctypes.byref(c), GOOD, GOOD * 2, GOOD, GOOD * 4, None) == L.MOE_EINVAL
+    assert lib.moe_pack_weights(ctypes.byref(c), GOOD, GOOD * 2, None, GOOD * 4, None) == L.MOE_EINVAL
+    assert lib.moe_pack_weights(ctypes.byref(_cfg(d_model=72)), GOOD, GOOD * 2, GOOD * 3, GOOD * 4, None) == L.MOE_ESHAPE
+
+
+def test_expert_buffer_sizes_pad_bf16_rows_to_16():
+    assert L.rows_alloc(_cfg(C=320)) == 320 and L.rows_alloc(_cfg(C=321)) == 336
+    assert L.rows_alloc(_cfg(C=321, dtype="f32")) == 321
+    assert L.expert_numel(_cfg(C=100, E=3), 64) == 3 * 112 * 64

@@ -10,7 +10,7 @@ import pytest
 
 from oracle import moe_oracle as O
 from synth import LayerSpec, layer_inputs, layer_spec
-from tests.gpu_harness import (TOL, assert_close, host, kept_rows, log, nan_fill, run_layer, spec_C,
+from tests.gpu_harness import (TOL, assert_close, ebuf, host, kept_rows, log, nan_fill, run_layer, spec_C,
                                to_dev)
 
 pytestmark = pytest.mark.gpu
@@ -61,13 +61,13 @@ def _check_layer(L, spec):
     np.testing.assert_array_equal(host(b.slot), fw["slot"])
     np.testing.assert_array_equal(host(b.fill), fill)
     assert_close("w", host(b.w), fw["w"], 1e-5)
-    np.testing.assert_array_equal(kept_rows(host(b.send_buf), fill), kept_rows(fw["buf"], fill))
+    np.testing.assert_array_equal(kept_rows(ebuf(b, "send_buf"), fill), kept_rows(fw["buf"], fill))
     for name in ("H", "A", "O"):
-        assert_close(name, kept_rows(host(getattr(b, name)), fill), kept_rows(fw[name], fill), tol)
+        assert_close(name, kept_rows(ebuf(b, name), fill), kept_rows(fw[name], fill), tol)
     assert_close("y", host(b.y), fw["y"], tol)
     for name in ("dO", "dH"):
-        assert_close(name, kept_rows(host(getattr(b, name)), fill), kept_rows(bw[name], fill), tol)
-    assert_close("dXe", kept_rows(host(b.dXe), fill), kept_rows(bw["dX"], fill), tol)
+        assert_close(name, kept_rows(ebuf(b, name), fill), kept_rows(bw[name], fill), tol)
+    assert_close("dXe", kept_rows(ebuf(b, "dXe"), fill), kept_rows(bw["dX"], fill), tol)
     assert_close("dlogits", host(b.dlogits), bw["dlogits"], tol)
     assert_close("dx", host(b.dx), bw["dx"], tol)
     assert_close("dW1", host(b.dW1), bw["dW1"], tol)
@@ -92,8 +92,8 @@ def test_layer_is_deterministic_and_dw_stream_independent(L):
     for name in ("logits", "idx", "w", "slot", "fill", "y", "dlogits", "dx", "dW1", "dW2", "dWg"):
         np.testing.assert_array_equal(host(getattr(b1, name)), host(getattr(b2, name)), err_msg=name)
     for name in ("send_buf", "H", "A", "O", "dO", "dH", "dXe"):
-        np.testing.assert_array_equal(kept_rows(host(getattr(b1, name)), fill),
-                                      kept_rows(host(getattr(b2, name)), fill), err_msg=name)
+        np.testing.assert_array_equal(kept_rows(ebuf(b1, name), fill),
+                                      kept_rows(ebuf(b2, name), fill), err_msg=name)
 
 
 def test_batch_partitions_with_capacity_carry_equal_unpartitioned(L):
@@ -114,21 +114,22 @@ def test_batch_partitions_with_capacity_carry_equal_unpartitioned(L):
     bias = torch.as_tensor(inp["bias"], dtype=torch.float32).cuda()
     fills = [torch.zeros(spec.E, dtype=torch.int32, device="cuda")]
     ws = torch.empty(max(16, L.moe_workspace_bytes(cfg, L.MOE_CALL_DISPATCH)), dtype=torch.uint8, device="cuda")
+    L.moe_pack_weights(cfg, dev["W1"], dev["W2"], b.W1p, b.W2p)
     for i in range(n):
         sl = slice(i * Tc, (i + 1) * Tc)
         xi = dev["x"][sl]
         L.moe_gate_topk(cfg, xi, dev["Wg"], bias, b.logits[sl], b.idx[sl], b.w[sl])
         fills.append(torch.empty(spec.E, dtype=torch.int32, device="cuda"))
         L.moe_dispatch(cfg, xi, b.idx[sl], fills[i], fills[i + 1], b.slot[sl], b.send_buf, ws)
-        L.moe_expert_ffn_fwd(cfg, b.send_buf, fills[i], fills[i + 1], dev["W1"], dev["W2"], b.H, b.A, b.O)
+        L.moe_expert_ffn_fwd(cfg, b.send_buf, fills[i], fills[i + 1], b.W1p, b.W2p, b.H, b.A, b.O)
         L.moe_combine(cfg, b.O, b.idx[sl], b.slot[sl], b.w[sl], b.y[sl])
     torch.cuda.synchronize()
     np.testing.assert_array_equal(host(b.slot), fw["slot"])
     np.testing.assert_array_equal(host(fills[-1]), fw["fill"])
     fill = fw["fill"]
     for name in ("send_buf", "H", "A", "O"):
-        np.testing.assert_array_equal(kept_rows(host(getattr(b, name)), fill),
-                                      kept_rows(host(getattr(full, name)), fill), err_msg=name)
+        np.testing.assert_array_equal(kept_rows(ebuf(b, name), fill),
+                                      kept_rows(ebuf(full, name), fill), err_msg=name)
     np.testing.assert_array_equal(host(b.y), host(full.y))
     # carries are the per-partition fills; every partition filled a contiguous, disjoint row range
     f = np.stack([host(t) for t in fills])
@@ -148,7 +149,8 @@ def test_zero_tokens(L):
     L.moe_gate_topk(cfg, x, torch.zeros(4, 64, dtype=torch.bfloat16, device="cuda"), None, b.logits, b.idx, b.w)
     L.moe_dispatch(cfg, x, b.idx, b.carry, b.fill, b.slot, b.send_buf, b.ws_dispatch)
     # rows [carry, fill) are empty, so the experts and the dW products see no rows
-    L.moe_expert_ffn_fwd(cfg, b.send_buf, b.carry, b.fill, W, W, b.H, b.A, b.O)
+    L.moe_pack_weights(cfg, W, W.clone(), b.W1p, b.W2p)
+    L.moe_expert_ffn_fwd(cfg, b.send_buf, b.carry, b.fill, b.W1p, b.W2p, b.H, b.A, b.O)
     L.moe_combine(cfg, b.O, b.idx, b.slot, b.w, b.y)
     L.moe_bwd_dw(cfg, x, b.dlogits, b.carry, b.fill, b.send_buf, b.A, b.dO, b.dH, b.dW1, b.dW2, b.dWg, b.ws_dw)
     torch.cuda.synchronize()
@@ -179,7 +181,7 @@ def _sampled_full(L, n, n_tok=40, seed=0):
     assert_close("w", host(b.w), w, 1e-5)
 
     # dispatch: every kept row bitwise equals its token's row, in slot order
-    send = host(b.send_buf)
+    send = ebuf(b, "send_buf")
     for e in range(spec.E):
         ts = [t for s_, t in sorted((int(slot[t, r]), t) for t in range(spec.T) for r in range(spec.k)
                                      if idx[t, r] == e and slot[t, r] >= 0)]
