@@ -33,6 +33,34 @@ import numpy as np
 
 MI355X_PEAK_BF16_TFLOPS = 2500.0   # dense bf16 MFMA
 MI355X_PEAK_HBM_GBPS = 8000.0
+ROOT = os.path.dirname(os.path.abspath(__file__))
+#: HBM bytes per expert-FFN-forward call from PMC counters, valid for the GEMM source it names.
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemm_expert_ffn_bf16_T8192_d1024_f4096_E16_pmc_traffic.md")
+GEMM_SOURCES = ["paper_2404_19429_amd/csrc/gemm.hip", "paper_2404_19429_amd/csrc/lds_ops.h",
+                "paper_2404_19429_amd/csrc/common.h"]
+
+
+def gemm_source_hash() -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for rel in GEMM_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(workload: str):
+    """Bytes per call recorded in the committed PMC summary, or None if it was
+    taken on another workload or on different GEMM sources."""
+    try:
+        text = open(TRAFFIC_FILE).read()
+    except OSError:
+        return None
+    kv = dict(line.split(":", 1) for line in text.splitlines() if line.startswith(("traffic_", "gemm_", "workload")))
+    kv = {k.strip(): v.strip() for k, v in kv.items()}
+    if kv.get("workload") != workload or kv.get("gemm_source_hash") != gemm_source_hash():
+        return None
+    return float(kv["traffic_bytes_per_call"])
 METRIC = "MoE layer fwd+bwd tokens/s on 1 MI355X; expert GEMM MFMA util; dispatch GB/s"
 CALLS = ["pack_weights", "gate", "dispatch", "expert_ffn_fwd", "combine", "bwd_dx", "bwd_dw"]
 
@@ -44,6 +72,8 @@ def _args():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", type=int, default=2, choices=[2, 3, 4])
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe-mib", type=int, default=0,
+                    help="run one plain device copy of this many MiB first (calibrates HBM byte counters)")
     ap.add_argument("--cpu-sample-tokens", type=int, default=8192)
     ap.add_argument("--workload", default="layer", choices=["layer", "block"])
     return ap.parse_args()
@@ -229,6 +259,13 @@ def main():
                      b.dWg, b.ws_dw)
         mark(7)
 
+    if a.copy_probe_mib > 0:   # a plain copy of known size: the counter scale for HBM bytes
+        src = torch.empty(a.copy_probe_mib * (1 << 20) // 2, dtype=torch.bfloat16, device="cuda").fill_(1.0)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     for _ in range(a.warmup):
         step()
     torch.cuda.synchronize()
@@ -276,7 +313,8 @@ def main():
                    "kept_rows": N, "parallelism": "single GPU (one GPU's share; all-to-all not run)"},
         "roofline": {"kernel": "expert FFN forward: 2 grouped bf16 MFMA GEMMs (gemm_bf16_kernel FWD1 + FWD2)",
                      "bound": "mfma", "achieved": achieved_tflops, "peak": MI355X_PEAK_BF16_TFLOPS,
-                     "unit": "TFLOP/s", "frac": achieved_tflops / MI355X_PEAK_BF16_TFLOPS, "traffic": None},
+                     "unit": "TFLOP/s", "frac": achieved_tflops / MI355X_PEAK_BF16_TFLOPS,
+                     "traffic": measured_traffic(spec.name)},
         "expert_gemm_mfma_frac": achieved_tflops / MI355X_PEAK_BF16_TFLOPS,
         "dispatch_GBps": dispatch_gbps,
         "dispatch_hbm_frac": dispatch_gbps / MI355X_PEAK_HBM_GBPS,
