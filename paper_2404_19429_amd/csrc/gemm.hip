@@ -513,6 +513,524 @@ gemm_bf16_kernel(GemmParams p, int tilesM, int tilesN, int groups) {
   }
 }
 
+// ------------------------------------------------------ wide bf16 MFMA tiles
+// The expert products at full size.  256 x 256 block tiles, one block per CU,
+// eight waves in a 2 x 4 grid, each owning a 128 x 64 tile (32 accumulator
+// fragments) -- two waves per SIMD, so one wave's MFMAs issue while the other
+// waits on memory (a four-wave 128 x 128 variant is kept for comparison).
+// Against 128 x 128 block tiles this halves the operand bytes a CU moves
+// global -> LDS per flop; the per-CU load path is what limits the smaller
+// tile.
+//
+// Operands reach LDS through raw buffer loads with the LDS flag: a scalar
+// buffer descriptor covers the operand's group from the current K-step on, so
+// a K-step only moves the descriptor, and an out-of-range lane sets bit 31 of
+// its offset, which the buffer range check turns into zeros.  Each K-step's
+// fragment reads for the next step and the loads refilling the stage just
+// consumed are interleaved one instruction at a time between the step's
+// MFMAs, so the wave keeps issuing MFMAs while memory operations queue.
+//
+// The K loop runs continuously over every tile a block owns: the load cursor
+// runs STAGES K-steps ahead of the compute cursor and crosses into the block's
+// next tile while the current one finishes, so that tile's first stages land
+// while the epilogue stores.  After an epilogue the first wait is a full
+// vmcnt(0): stores and loads share the counter, and the order in which they
+// complete is not relied on.
+//
+// The accumulators live in AGPRs through inline-asm MFMAs ("+a"), which keeps
+// every fragment in one register quad for the whole tile.  The compiler does
+// not see those MFMAs, so the hazards it would otherwise cover are fenced by
+// hand: s_nop after VALU writes of fragment registers an MFMA reads next, and
+// after the last MFMA of a tile before the accumulators are read.
+//
+// The product is computed transposed (MFMA A operand = a B fragment, B operand
+// = an A fragment), so each lane's four accumulator values are four
+// consecutive output columns of one row: the epilogue converts them with
+// v_cvt_pk_bf16_f32 and stores 8-byte vectors straight from registers.
+#ifndef LMOE_WIDE_STAGES
+#define LMOE_WIDE_STAGES 4
+#endif
+constexpr int kWB = 256;       // block tile (rows and columns)
+
+// Compile-time loop: f(std::integral_constant<int, I>) for I in [B, E).
+template <int B, int E, typename Fn>
+__device__ __forceinline__ void static_for(Fn&& f) {
+  if constexpr (B < E) {
+    f(std::integral_constant<int, B>{});
+    static_for<B + 1, E>(f);
+  }
+}
+
+struct WGeo {
+  int g;        // group (expert)
+  int m0, n0;   // tile origin (rows relative to lo_al for ragged-M products)
+  int lo, hi;   // the group's row range in its [C][*] block
+  int lo_al;    // lo rounded down to the 16-row block: origin of the tile rows (ragged-M) or of K (ragged-K)
+  int Mlim, Klim, nk;
+};
+
+__device__ __forceinline__ uint32_t cvt_pk_bf16(float lo, float hi) {
+  typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+  typedef float f32x2_t __attribute__((ext_vector_type(2)));
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t{lo, hi}), bf16x2_t));
+}
+__device__ __forceinline__ u32x2 pack4_bf16(const float (&v)[4]) {
+  return u32x2{cvt_pk_bf16(v[0], v[1]), cvt_pk_bf16(v[2], v[3])};
+}
+
+__device__ __forceinline__ void mfma_acc(f32x4& acc, const u32x4& a, const u32x4& b) {
+  asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %0" : "+a"(acc) : "v"(a), "v"(b));
+}
+// Wait states between VALU writes of fragment registers and the MFMAs that read them.
+__device__ __forceinline__ void valu_to_mfma_fence(u32x4 (&f)[8]) {
+  asm volatile("s_nop 4" : "+v"(f[0]), "+v"(f[1]), "+v"(f[2]), "+v"(f[3]), "+v"(f[4]), "+v"(f[5]), "+v"(f[6]),
+               "+v"(f[7]));
+}
+__device__ __forceinline__ void valu_to_mfma_fence(u32x4 (&f)[4]) {
+  asm volatile("s_nop 4" : "+v"(f[0]), "+v"(f[1]), "+v"(f[2]), "+v"(f[3]));
+}
+// Pins a row of accumulators in AGPRs at this point of the instruction stream.
+__device__ __forceinline__ void acc_pin(f32x4 (&a)[8]) {
+  asm volatile("" : "+a"(a[0]), "+a"(a[1]), "+a"(a[2]), "+a"(a[3]), "+a"(a[4]), "+a"(a[5]), "+a"(a[6]), "+a"(a[7]));
+}
+__device__ __forceinline__ void acc_pin(f32x4 (&a)[4]) {
+  asm volatile("" : "+a"(a[0]), "+a"(a[1]), "+a"(a[2]), "+a"(a[3]));
+}
+
+// One operand's loads for the K-steps of a tile (256 rows or columns x 32 K
+// per stage, blocked source), as raw buffer loads into LDS.  The buffer
+// descriptor spans the operand's group (expert) from the current K-step on, so
+// a K-step only moves the descriptor (scalar adds), and a lane whose chunk is
+// out of range carries bit 31 in its offset, which the buffer range check
+// turns into zeros.  K-contiguous (KC): the chunk of fragment q is a whole
+// 16 x 32 block, rows past `lim` read zeros.  MN-contiguous: 32 K rows x 256
+// columns as 2 x 8 blocks, each lane's chunk placed at its swizzled position;
+// columns past `lim` and, with KCHK, K rows outside [klo, khi) read zeros.
+constexpr int kBufCfg = 0x00020000;   // buffer descriptor word 3: raw 32-bit data, gfx9 family
+constexpr uint32_t kOob = 0x80000000u;
+template <bool KC, bool KCHK, int NW>
+struct WOp {
+  static constexpr int kWNI = 16 / NW;   // loads per wave per stage (16 blocks of 1 KB)
+  const char* base;      // the group's operand (uniform)
+  uint32_t bytes;        // its extent in bytes (uniform)
+  uint32_t stride;       // bytes per K-step (uniform)
+  uint32_t voff[kWNI];   // byte offset of the lane's chunk at K-step 0, | kOob if out of range
+  int kr[kWNI];          // KCHK: K row of the lane's chunk at K-step 0
+  int klo, khi;
+
+  // KC: row0 = first row of the tile (multiple of 16), lim = row limit.
+  // MN: row0 = first column of the tile, lim = column limit, korg = K origin (multiple of 16).
+  __device__ __forceinline__ void plan(const uint16_t* b, int64_t extent, int64_t ld, int row0, int lim, int korg,
+                                       int lo, int hi, int wid, int lane) {
+    base = (const char*)b;
+    bytes = (uint32_t)(extent * 2);
+    klo = lo;
+    khi = hi;
+    if constexpr (KC) {
+      stride = 1024;
+#pragma unroll
+      for (int i = 0; i < kWNI; ++i) {
+        const int rb = (row0 >> 4) + i * NW + wid;
+        const uint32_t off = (uint32_t)(rb * (int)(ld >> 5) * 512 + (lane & 15) * 32 + (lane >> 4) * 8) * 2u;
+        voff[i] = (16 * rb + (lane & 15) < lim) ? off : (off | kOob);
+        kr[i] = 0;
+      }
+    } else {
+      const int nb = (int)(ld >> 5);
+      stride = (uint32_t)nb * 2048u;
+      const int r = lane >> 2;
+      const int c = (lane & 3) ^ bsw(r);
+#pragma unroll
+      for (int i = 0; i < kWNI; ++i) {
+        const int b2 = i * NW + wid;
+        const int kb = b2 / 8, cb = b2 % 8;
+        const int col = row0 + 32 * cb;
+        const uint32_t off = (uint32_t)((((korg >> 4) + kb) * nb + (col >> 5)) * 512 + r * 32 + c * 8) * 2u;
+        voff[i] = col < lim ? off : (off | kOob);
+        kr[i] = korg + 16 * kb + r;
+      }
+    }
+  }
+  // Load i (0 .. kWNI-1) of K-step kk into its place in the stage.
+  __device__ __forceinline__ void issue(int i, int kk, uint16_t* stage, int wid) const {
+    const uint32_t adv = (uint32_t)kk * stride;
+    const __amdgpu_buffer_rsrc_t r =
+        __builtin_amdgcn_make_buffer_rsrc((void*)(base + adv), (short)0, (int)(bytes - adv), kBufCfg);
+    uint32_t vo = voff[i];
+    if constexpr (KCHK) {
+      const int k = kr[i] + 32 * kk;
+      if (k < klo || k >= khi) vo |= kOob;
+    }
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void*)(stage + (i * NW + wid) * 512), 16, vo, 0, 0, 0);
+  }
+};
+
+// NW = 4: waves 2 x 2, wave tile 128 x 128, one wave per SIMD.
+// NW = 8: waves 2 x 4, wave tile 128 x 64, two waves per SIMD, which lets the
+// SIMD issue one wave's MFMAs while the other waits on memory.
+template <int NW, int STAGES, bool B_K, bool RAGGED_K, int EPI, int ACT, bool CBLK>
+__global__ __attribute__((amdgpu_flat_work_group_size(NW * 64, NW * 64), amdgpu_waves_per_eu(NW / 4, NW / 4))) void
+gemm_wide_kernel(GemmParams p, int tilesM, int tilesN, int groups) {
+  constexpr int BK = kBKb;
+  constexpr int WGN = NW / 2;                   // wave grid 2 x WGN
+  constexpr int WTM = 128, WTN = kWB / WGN;     // wave tile
+  constexpr int FM = WTM / 16, FN = WTN / 16;   // fragments per wave tile side
+  constexpr int kWNI = 16 / NW;
+  constexpr int STAGE = (kWB + kWB) * BK;       // elements per pipeline stage
+  constexpr bool A_K = !RAGGED_K;
+  constexpr bool BK_C = B_K && !RAGGED_K;
+  using TA = typename std::conditional<A_K, TileK<kWB, NW, true>, TileMN<kWB, NW, true>>::type;
+  using TB = typename std::conditional<BK_C, TileK<kWB, NW, true>, TileMN<kWB, NW, true>>::type;
+  static_assert(TA::NI == kWNI && TB::NI == kWNI, "load plan");
+  constexpr int LPS = 2 * kWNI;                  // loads per wave per stage
+  static_assert(STAGES >= 2 && LPS * (STAGES - 1) < 64, "vmcnt range");
+  extern __shared__ __attribute__((aligned(16))) uint16_t lds[];
+
+  const int lane = threadIdx.x & 63;
+  const int wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int wm = wid / WGN, wn = wid % WGN;
+
+  // Tile counts per group and their inclusive prefix, one lane per group
+  // (groups <= 64); every wave computes the same values.
+  int cnt = 0;
+  if (lane < groups) {
+    if constexpr (RAGGED_K) {
+      cnt = tilesM * tilesN;
+    } else {
+      int lo, span;
+      group_rows(p, lane, lo, span);
+      if (span > 0) span += lo & 15;
+      cnt = ((span + kWB - 1) / kWB) * tilesN;
+    }
+  }
+  int incl = cnt;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int u = __shfl_up(incl, o, 64);
+    if (lane >= o) incl += u;
+  }
+  const int excl = incl - cnt;
+  const int total = __builtin_amdgcn_readfirstlane(__shfl(incl, groups - 1, 64));
+  const int nslot = gridDim.x / 8;
+  const int xcd = blockIdx.x % 8, slot = blockIdx.x / 8;
+  const int per = (total + 7) / 8;
+  const int t_begin = xcd * per + slot;
+  const int t_end = min(total, (xcd + 1) * per);
+  if (t_begin >= t_end) return;
+
+  auto geo = [&](int t) __attribute__((always_inline)) {
+    WGeo G;
+    G.g = __builtin_amdgcn_readfirstlane(__popcll(__ballot(lane < groups && incl <= t)));
+    const int local = t - __builtin_amdgcn_readfirstlane(__shfl(excl, G.g, 64));
+    int lo, span;
+    group_rows(p, G.g, lo, span);
+    G.lo = lo;
+    G.hi = lo + span;
+    G.lo_al = lo & ~15;
+    if (span > 0) span += lo - G.lo_al;
+    const int tmg = RAGGED_K ? tilesM : (span + kWB - 1) / kWB;
+    const int pnl = local / (tmg * kPanelN);
+    const int rem = local - pnl * tmg * kPanelN;
+    const int pw = min(kPanelN, tilesN - pnl * kPanelN);
+    G.m0 = (rem / pw) * kWB;
+    G.n0 = (pnl * kPanelN + rem % pw) * kWB;
+    G.Mlim = RAGGED_K ? p.M : span;
+    G.Klim = RAGGED_K ? span : p.K;
+    G.nk = max(1, (G.Klim + BK - 1) / BK);   // an empty ragged-K group runs one all-zero step
+    return G;
+  };
+
+  // Load cursor: tile lt, K-step lk of lnk; ls = stages issued so far.
+  WOp<A_K, RAGGED_K, NW> opA;
+  WOp<BK_C, RAGGED_K, NW> opB;
+  int lt = t_begin, lk = 0, lnk = 0, ls = 0;
+  auto plan = [&](int t) __attribute__((always_inline)) {
+    const WGeo G = geo(t);
+    const uint16_t* Ab = (const uint16_t*)p.A + G.g * p.sA;
+    const uint16_t* Bb = (const uint16_t*)p.B + G.g * p.sB;
+    if constexpr (A_K) opA.plan(Ab, p.sA, p.lda, G.lo_al + G.m0, (int)pad16(p.cap), 0, 0, 0, wid, lane);
+    else opA.plan(Ab, p.sA, p.lda, G.m0, p.M, G.lo_al, G.lo, G.hi, wid, lane);
+    if constexpr (BK_C) opB.plan(Bb, p.sB, p.ldb, G.n0, p.N, 0, 0, 0, wid, lane);
+    else if constexpr (RAGGED_K) opB.plan(Bb, p.sB, p.ldb, G.n0, p.N, G.lo_al, G.lo, G.hi, wid, lane);
+    else opB.plan(Bb, p.sB, p.ldb, G.n0, p.N, 0, 0, p.K, wid, lane);
+    lnk = G.nk;
+  };
+  plan(lt);
+  // Load q (0 .. 2 kWNI - 1; even: A, odd: B) of the next stage.
+  auto issue_load = [&](int q) __attribute__((always_inline)) {
+    if (lt >= t_end) return;
+    uint16_t* st = lds + (ls % STAGES) * STAGE;
+    if (q & 1) opB.issue(q >> 1, lk, st + kWB * BK, wid);
+    else opA.issue(q >> 1, lk, st, wid);
+  };
+  // Moves the load cursor past the stage just issued.
+  auto advance = [&]() __attribute__((always_inline)) {
+    if (lt >= t_end) return;
+    ++ls;
+    if (++lk == lnk) {
+      lk = 0;
+      lt += nslot;
+      if (lt < t_end) plan(lt);
+    }
+  };
+
+  // Fragment reads.  K-contiguous operands: 8 ds_read_b128 (one per
+  // fragment).  MN-contiguous: 16 ds_read_b64_tr_b16, two per fragment.
+  using Pend = u32x2[8];
+  auto read_issue = [&](auto tile, auto& f, Pend& p0, Pend& p1, const uint16_t* st, int c0)
+                        __attribute__((always_inline)) {
+    using T = decltype(tile);
+    constexpr int NF = sizeof(f) / sizeof(u32x4);
+    if constexpr (std::is_same<T, TileK<kWB, NW, true>>::value) {
+      T::template read_issue<NF>(f, p0, st, c0, lane);
+    } else {
+      const int j = lane & 15;
+      const int k = 8 * (lane >> 4) + (j >> 2);
+      uint32_t a0[8], a1[8];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int col0 = c0 + 16 * u + 4 * (j & 3), col1 = col0 + 64;
+        a0[2 * u] = lds_addr(st + T::lds_off(k, col0));
+        a0[2 * u + 1] = lds_addr(st + T::lds_off(k + 4, col0));
+        a1[2 * u] = lds_addr(st + T::lds_off(k, col1));
+        a1[2 * u + 1] = lds_addr(st + T::lds_off(k + 4, col1));
+      }
+      RdTrIssue8::run(p0, a0);
+      if constexpr (NF == 8) RdTrIssue8::run(p1, a1);
+    }
+  };
+  auto read_finish = [&](auto tile, auto& f, Pend& p0, Pend& p1) __attribute__((always_inline)) {
+    using T = decltype(tile);
+    constexpr int NF = sizeof(f) / sizeof(u32x4);
+    if constexpr (std::is_same<T, TileK<kWB, NW, true>>::value) {
+      lds_wait(f);
+    } else {
+      lds_wait(p0);
+      if constexpr (NF == 8) lds_retired(p1);
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        f[u] = u32x4{p0[2 * u][0], p0[2 * u][1], p0[2 * u + 1][0], p0[2 * u + 1][1]};
+        if constexpr (NF == 8) f[4 + u] = u32x4{p1[2 * u][0], p1[2 * u][1], p1[2 * u + 1][0], p1[2 * u + 1][1]};
+      }
+      valu_to_mfma_fence(f);
+    }
+  };
+
+  f32x4 acc[FM][FN];
+  auto zero_acc = [&]() __attribute__((always_inline)) {
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < FN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    asm volatile("s_nop 4" ::: "memory");
+#pragma unroll
+    for (int i = 0; i < FM; ++i) acc_pin(acc[i]);
+  };
+  // acc[i][j] holds the transposed 16 x 16 product: lane l has output row
+  // 16 i + l % 16, columns 16 j + 4 (l / 16) .. +3 of the wave tile.
+  auto mfma_rows = [&](int i0, int i1, u32x4 (&ca)[FM], u32x4 (&cb)[FN]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+      if (i < i0 || i >= i1) continue;
+#pragma unroll
+      for (int j = 0; j < FN; ++j) mfma_acc(acc[i][j], cb[j], ca[i]);
+    }
+  };
+
+  auto epilogue = [&](const WGeo& G) __attribute__((always_inline)) {
+    // Wait states between the last MFMA and the first read of its accumulator.
+    asm volatile("s_nop 15\n s_nop 15" ::: "memory");
+#pragma unroll
+    for (int i = 0; i < FM; ++i) acc_pin(acc[i]);
+    const int64_t cofs = (int64_t)G.g * p.sC + (RAGGED_K || CBLK ? 0 : (int64_t)G.lo_al * p.ldc);
+    uint16_t* C = (uint16_t*)p.C + cofs;
+    uint16_t* C2 = EPI == EPI_FWD1 ? (uint16_t*)p.C2 + cofs : nullptr;
+    const uint16_t* Aux = EPI == EPI_DACT ? (const uint16_t*)p.Aux + cofs : nullptr;
+    const int rl = lane & 15, cq = 4 * (lane >> 4);
+    auto offset = [&](int row, int col) __attribute__((always_inline)) -> int64_t {
+      return CBLK ? blk_off(G.lo_al + row, col, p.ldc) : (int64_t)row * p.ldc + col;
+    };
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {          // two halves of four fragment rows
+      u32x2 aux[4][FN];
+      if constexpr (EPI == EPI_DACT) {     // all loads of the half first, then the math
+#pragma unroll
+        for (int ii = 0; ii < 4; ++ii) {
+          const int row = G.m0 + wm * WTM + 16 * (4 * h + ii) + rl;
+          const bool rok = row < G.Mlim && (RAGGED_K || G.lo_al + row >= G.lo);
+#pragma unroll
+          for (int j = 0; j < FN; ++j) {
+            const int col = G.n0 + wn * WTN + 16 * j + cq;
+            aux[ii][j] = (rok && col < p.N) ? *reinterpret_cast<const u32x2*>(Aux + offset(row, col)) : u32x2{0u, 0u};
+          }
+        }
+      }
+#pragma unroll
+      for (int ii = 0; ii < 4; ++ii) {
+        const int i = 4 * h + ii;
+        const int row = G.m0 + wm * WTM + 16 * i + rl;
+        const bool rok = row < G.Mlim && (RAGGED_K || G.lo_al + row >= G.lo);
+#pragma unroll
+        for (int j = 0; j < FN; ++j) {
+          const int col = G.n0 + wn * WTN + 16 * j + cq;
+          if (!(rok && col < p.N)) continue;
+          const int64_t off = offset(row, col);
+          float v[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
+          if constexpr (EPI == EPI_FWD1) {
+            *reinterpret_cast<u32x2*>(C + off) = pack4_bf16(v);
+#pragma unroll
+            for (int u = 0; u < 4; ++u) v[u] = act_fwd_t<ACT>(v[u]);
+            *reinterpret_cast<u32x2*>(C2 + off) = pack4_bf16(v);
+          } else if constexpr (EPI == EPI_DACT) {
+            const u32x2 hv = aux[ii][j];
+            const float hh[4] = {__uint_as_float(hv[0] << 16), __uint_as_float(hv[0] & 0xffff0000u),
+                                 __uint_as_float(hv[1] << 16), __uint_as_float(hv[1] & 0xffff0000u)};
+#pragma unroll
+            for (int u = 0; u < 4; ++u) v[u] *= act_bwd_t<ACT>(hh[u]);
+            *reinterpret_cast<u32x2*>(C + off) = pack4_bf16(v);
+          } else {
+            *reinterpret_cast<u32x2*>(C + off) = pack4_bf16(v);
+          }
+        }
+      }
+    }
+  };
+
+  // Prologue: fill the ring, wait for the first stage, read its fragments.
+#pragma unroll
+  for (int s = 0; s < STAGES; ++s) {
+#pragma unroll
+    for (int q = 0; q < 2 * kWNI; ++q) issue_load(q);
+    advance();
+  }
+  wait_vm_tiles<LPS, STAGES - 1>(ls - 1);
+  lds_barrier();
+  u32x4 fa0[FM], fb0[FN], fa1[FM], fb1[FN];
+  Pend pa0, pa1, pb0, pb1;
+  read_issue(TA{}, fa0, pa0, pa1, lds, wm * WTM);
+  read_finish(TA{}, fa0, pa0, pa1);
+  read_issue(TB{}, fb0, pb0, pb1, lds + kWB * BK, wn * WTN);
+  read_finish(TB{}, fb0, pb0, pb1);
+  zero_acc();
+
+  int cs = 0;                // compute steps done (over all of the block's tiles)
+  bool stores_pending = false;
+  // One K-step: multiply the fragments in (ca, cb) while the next stage's
+  // loads are issued and its fragments read into (na, nb).
+  // Fragment read plan of the next stage: NRA reads for A, NRB for B (one
+  // ds_read_b128 per K-contiguous fragment, two ds_read_b64_tr_b16 per
+  // MN-contiguous one), each landing in its fragment or in a half-fragment
+  // pending register.
+  constexpr bool AK = std::is_same<TA, TileK<kWB, NW, true>>::value;
+  constexpr bool BKK = std::is_same<TB, TileK<kWB, NW, true>>::value;
+  constexpr int NRA = AK ? FM : 2 * FM, NRB = BKK ? FN : 2 * FN, NRD = NRA + NRB;
+  constexpr int NMF = FM * FN, NDMA = 2 * kWNI;
+  constexpr int RSPAN = NMF * 3 / 4;          // all reads issued within the first 3/4 of the MFMAs
+  u32x2 qa[2 * FM], qb[2 * FN];               // pending halves of MN-contiguous fragments
+  // LDS byte address of read r of an operand (fragment r, or half r % 2 of fragment r / 2).
+  auto read_addr = [&](auto tile, const uint16_t* st, int c0, int r) __attribute__((always_inline)) -> uint32_t {
+    using T = decltype(tile);
+    if constexpr (std::is_same<T, TileK<kWB, NW, true>>::value) {
+      return lds_addr(st + ((c0 >> 4) + r) * 512 + lane * 8);
+    } else {
+      const int j = lane & 15;
+      const int k = 8 * (lane >> 4) + (j >> 2) + 4 * (r & 1);
+      return lds_addr(st + T::lds_off(k, c0 + 16 * (r >> 1) + 4 * (j & 3)));
+    }
+  };
+  // One K-step: the MFMAs of (ca, cb), with the next stage's fragment reads
+  // into (na, nb) and the refill of this step's stage interleaved between
+  // them one instruction at a time, so the wave keeps issuing MFMAs while the
+  // memory operations queue.
+  auto step = [&](u32x4 (&ca)[FM], u32x4 (&cb)[FN], u32x4 (&na)[FM], u32x4 (&nb)[FN]) __attribute__((always_inline)) {
+    const uint16_t* st = lds + ((cs + 1) % STAGES) * STAGE;
+    const bool more = cs + 1 < ls;
+    if (more) {
+      if (stores_pending) {
+        wait_vm<0>();
+        stores_pending = false;
+      } else {
+        wait_vm_tiles<LPS, STAGES - 2>(ls - cs - 2);   // stage cs+1 has landed
+      }
+      lds_barrier();   // stage cs+1 is in LDS for every wave; no wave reads stage cs any more
+    }
+    // The reads are unconditional (branch-free, so pending registers are never
+    // copied); after the last step they read a stage no load is writing.
+    uint32_t ra[NRA], rb[NRB];
+#pragma unroll
+    for (int r = 0; r < NRA; ++r) ra[r] = read_addr(TA{}, st, wm * WTM, r);
+#pragma unroll
+    for (int r = 0; r < NRB; ++r) rb[r] = read_addr(TB{}, st + kWB * BK, wn * WTN, r);
+    __builtin_amdgcn_sched_barrier(0);
+    static_for<0, NMF>([&](auto mc) __attribute__((always_inline)) {
+      constexpr int m = decltype(mc)::value;
+      mfma_acc(acc[m / FN][m % FN], cb[m % FN], ca[m / FN]);
+      static_for<0, NRD>([&](auto rc) __attribute__((always_inline)) {
+        constexpr int r = decltype(rc)::value;
+        if constexpr ((r * RSPAN) / NRD == m) {
+          if constexpr (r < NRA) {
+            if constexpr (AK) rd128_issue(na[r], ra[r]);
+            else rdtr_issue(qa[r], ra[r]);
+          } else {
+            if constexpr (BKK) rd128_issue(nb[r - NRA], rb[r - NRA]);
+            else rdtr_issue(qb[r - NRA], rb[r - NRA]);
+          }
+          if constexpr (r % 8 == 7 && r + 1 < NRD) lds_wait_le<7>();
+        }
+      });
+      static_for<0, NDMA>([&](auto dc) __attribute__((always_inline)) {
+        constexpr int d = decltype(dc)::value;
+        if constexpr ((d * NMF) / NDMA + 1 == m) {
+          __builtin_amdgcn_sched_barrier(0);
+          issue_load(d);
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      });
+    });
+    lds_wait_all();
+    if constexpr (AK) {
+      lds_mark(na);
+    } else {
+      lds_mark(qa);
+#pragma unroll
+      for (int u = 0; u < FM; ++u) na[u] = u32x4{qa[2 * u][0], qa[2 * u][1], qa[2 * u + 1][0], qa[2 * u + 1][1]};
+      valu_to_mfma_fence(na);
+    }
+    if constexpr (BKK) {
+      lds_mark(nb);
+    } else {
+      lds_mark(qb);
+#pragma unroll
+      for (int u = 0; u < FN; ++u) nb[u] = u32x4{qb[2 * u][0], qb[2 * u][1], qb[2 * u + 1][0], qb[2 * u + 1][1]};
+      valu_to_mfma_fence(nb);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    if (more) advance();
+    ++cs;
+  };
+  for (int ct = t_begin; ct < t_end; ct += nslot) {
+    const WGeo Cg = geo(ct);
+    int kk = 0;
+    for (; kk + 2 <= Cg.nk; kk += 2) {
+      step(fa0, fb0, fa1, fb1);
+      step(fa1, fb1, fa0, fb0);
+    }
+    if (kk < Cg.nk) {   // odd step count: the next tile's fragments are in set 1
+      step(fa0, fb0, fa1, fb1);
+#pragma unroll
+      for (int u = 0; u < FM; ++u) fa0[u] = fa1[u];
+#pragma unroll
+      for (int u = 0; u < FN; ++u) fb0[u] = fb1[u];
+      valu_to_mfma_fence(fa0);
+      valu_to_mfma_fence(fb0);
+    }
+    epilogue(Cg);
+    zero_acc();
+    stores_pending = true;
+  }
+  wait_vm<0>();
+}
+
 // ------------------------------------------------------------------ f32 path
 template <bool B_K, bool RAGGED_K, int EPI>
 __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmParams p) {
@@ -658,15 +1176,51 @@ static void run_gemm(int dtype, int act, int groups, const GemmParams& p, int ti
   }
 }
 
-// Expert products: bf16 operands and outputs in the blocked layout (dW outputs
-// row-major), float ones row-major.
-template <bool B_K, bool RAGGED_K, int EPI, bool CBLK>
-static void run_expert(const moe_cfg& c, const GemmParams& p, int tilesM, int tilesN, hipStream_t s) {
-  run_gemm<B_K, RAGGED_K, EPI, true, CBLK>(c.dtype, c.act, c.E, p, tilesM, tilesN, s);
+#ifndef LMOE_WIDE_WAVES
+#define LMOE_WIDE_WAVES 8
+#endif
+template <bool B_K, bool RAGGED_K, int EPI, int ACT, bool CBLK>
+static void launch_wide(int groups, const GemmParams& p, int tilesM, int tilesN, hipStream_t s) {
+  constexpr int S = LMOE_WIDE_STAGES, NW = LMOE_WIDE_WAVES;
+  constexpr size_t shmem = S * (size_t)(2 * kWB) * kBKb * sizeof(uint16_t);
+  auto kern = gemm_wide_kernel<NW, S, B_K, RAGGED_K, EPI, ACT, CBLK>;
+  static bool attr_set = false;
+  if (!attr_set) {
+    (void)hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)shmem);
+    attr_set = true;
+  }
+  const int64_t max_tiles = (int64_t)tilesM * tilesN * groups;
+  int blocks = num_cus();
+  if (max_tiles < blocks) blocks = (int)max_tiles;
+  blocks = (blocks + 7) / 8 * 8;
+  hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(NW * 64), shmem, s, p, tilesM, tilesN, groups);
 }
 
-static int tile_m(const moe_cfg& c) { return c.dtype == MOE_BF16 ? kBM : 64; }
-static int tile_n(const moe_cfg& c) { return c.dtype == MOE_BF16 ? kBN : 64; }
+// Expert products.  bf16: blocked operands, wide tiles; outputs blocked
+// (CBLK) or row-major (the dW products).  float: the FMA kernel, row-major.
+// rows: rows of the output per group (ragged-M: the capacity C, with up to 15
+// alignment rows; ragged-K: M); cols: N.
+template <bool B_K, bool RAGGED_K, int EPI, bool CBLK>
+static void run_expert(const moe_cfg& c, const GemmParams& p, int64_t rows, int cols, hipStream_t s) {
+  if (rows <= 0 || cols <= 0 || c.E <= 0) return;
+  if (c.dtype != MOE_BF16) {
+    dim3 grid((unsigned)((cols + 63) / 64), (unsigned)((rows + 63) / 64), (unsigned)c.E);
+    if constexpr (EPI != EPI_RES) hipLaunchKernelGGL((gemm_f32_kernel<B_K, RAGGED_K, EPI>), grid, dim3(256), 0, s, p);
+    return;
+  }
+  const int tm = (int)((rows + (RAGGED_K ? 0 : 15) + kWB - 1) / kWB), tn = (cols + kWB - 1) / kWB;
+  if constexpr (EPI == EPI_STORE) {
+    launch_wide<B_K, RAGGED_K, EPI, MOE_ACT_IDENTITY, CBLK>(c.E, p, tm, tn, s);
+  } else {
+    switch (c.act) {
+      case MOE_ACT_RELU: launch_wide<B_K, RAGGED_K, EPI, MOE_ACT_RELU, CBLK>(c.E, p, tm, tn, s); break;
+      case MOE_ACT_GELU_TANH: launch_wide<B_K, RAGGED_K, EPI, MOE_ACT_GELU_TANH, CBLK>(c.E, p, tm, tn, s); break;
+      case MOE_ACT_GELU_ERF: launch_wide<B_K, RAGGED_K, EPI, MOE_ACT_GELU_ERF, CBLK>(c.E, p, tm, tn, s); break;
+      default: launch_wide<B_K, RAGGED_K, EPI, MOE_ACT_IDENTITY, CBLK>(c.E, p, tm, tn, s); break;
+    }
+  }
+}
+
 static int cdiv(int64_t a, int b) { return (int)((a + b - 1) / b); }
 // Rows per expert block of an [E][C][*] buffer (C rounded up to 16 for bf16).
 static int64_t rows_alloc(const moe_cfg& c) { return c.dtype == MOE_BF16 ? pad16(c.C) : c.C; }
@@ -674,23 +1228,21 @@ static int64_t rows_alloc(const moe_cfg& c) { return c.dtype == MOE_BF16 ? pad16
 void launch_expert_fwd(const moe_cfg& c, const void* X, const int32_t* rb, const int32_t* re, const void* W1,
                        const void* W2, void* H, void* A, void* O, hipStream_t s) {
   const int64_t d = c.d_model, f = c.d_ff, C = c.C, Cp = rows_alloc(c);
-  const int tm = cdiv(C + 15, tile_m(c));
   GemmParams p1{X, d, Cp * d, W1, d, f * d, H, f, Cp * f, A, nullptr, rb, re, 0, (int)f, (int)d, c.act, (int)C};
-  run_expert<true, false, EPI_FWD1, true>(c, p1, tm, cdiv(f, tile_n(c)), s);
+  run_expert<true, false, EPI_FWD1, true>(c, p1, C, (int)f, s);
   GemmParams p2{A, f, Cp * f, W2, f, d * f, O, d, Cp * d, nullptr, nullptr, rb, re, 0, (int)d, (int)f, c.act, (int)C};
-  run_expert<true, false, EPI_STORE, true>(c, p2, tm, cdiv(d, tile_n(c)), s);
+  run_expert<true, false, EPI_STORE, true>(c, p2, C, (int)d, s);
 }
 
 void launch_expert_bwd_dx(const moe_cfg& c, const void* dO, const int32_t* rb, const int32_t* re, const void* H,
                           const void* W1, const void* W2, void* dH, void* dXe, hipStream_t s) {
   const int64_t d = c.d_model, f = c.d_ff, C = c.C, Cp = rows_alloc(c);
-  const int tm = cdiv(C + 15, tile_m(c));
   // dA = dO W2_e  (B(k=i, n=j) = W2[e][i][j], N contiguous), epilogue dH = dA * act'(H)
   GemmParams p1{dO, d, Cp * d, W2, f, d * f, dH, f, Cp * f, nullptr, H, rb, re, 0, (int)f, (int)d, c.act, (int)C};
-  run_expert<false, false, EPI_DACT, true>(c, p1, tm, cdiv(f, tile_n(c)), s);
+  run_expert<false, false, EPI_DACT, true>(c, p1, C, (int)f, s);
   // dXe = dH W1_e  (B(k=i, n=j) = W1[e][i][j])
   GemmParams p2{dH, f, Cp * f, W1, d, f * d, dXe, d, Cp * d, nullptr, nullptr, rb, re, 0, (int)d, (int)f, c.act, (int)C};
-  run_expert<false, false, EPI_STORE, true>(c, p2, tm, cdiv(d, tile_n(c)), s);
+  run_expert<false, false, EPI_STORE, true>(c, p2, C, (int)d, s);
 }
 
 void launch_expert_bwd_dw(const moe_cfg& c, const void* X, const void* A, const void* dO, const void* dH,
@@ -698,10 +1250,10 @@ void launch_expert_bwd_dw(const moe_cfg& c, const void* X, const void* A, const 
   const int64_t d = c.d_model, f = c.d_ff, C = c.C, Cp = rows_alloc(c);
   // dW2_e [d][f] = dO_e^T A_e : A-operand(m, k) = dO[e][k][m], B(k, n) = A[e][k][n]
   GemmParams p2{dO, d, Cp * d, A, f, Cp * f, dW2, f, d * f, nullptr, nullptr, rb, re, (int)d, (int)f, 0, c.act, (int)C};
-  run_expert<false, true, EPI_STORE, false>(c, p2, cdiv(d, tile_m(c)), cdiv(f, tile_n(c)), s);
+  run_expert<false, true, EPI_STORE, false>(c, p2, d, (int)f, s);
   // dW1_e [f][d] = dH_e^T X_e
   GemmParams p1{dH, f, Cp * f, X, d, Cp * d, dW1, d, f * d, nullptr, nullptr, rb, re, (int)f, (int)d, 0, c.act, (int)C};
-  run_expert<false, true, EPI_STORE, false>(c, p1, cdiv(f, tile_m(c)), cdiv(d, tile_n(c)), s);
+  run_expert<false, true, EPI_STORE, false>(c, p1, f, (int)d, s);
 }
 
 // Dense bf16 products of the transformer block (one group, every row, row-major).

@@ -111,6 +111,44 @@ __device__ __forceinline__ void lds_wait(u32x2 (&o)[8]) {
                : "+v"(o[0]), "+v"(o[1]), "+v"(o[2]), "+v"(o[3]), "+v"(o[4]), "+v"(o[5]), "+v"(o[6]), "+v"(o[7])
                :: "memory");
 }
+// Marks registers of reads that an earlier lds_wait in the same sequence has
+// already retired (no instruction; keeps the compiler from touching them early).
+__device__ __forceinline__ void lds_retired(u32x2 (&o)[8]) {
+  asm volatile(""
+               : "+v"(o[0]), "+v"(o[1]), "+v"(o[2]), "+v"(o[3]), "+v"(o[4]), "+v"(o[5]), "+v"(o[6]), "+v"(o[7])
+               :: "memory");
+}
+
+// Single fragment reads for hand-interleaved schedules: the output is pending
+// until a later s_waitcnt lgkmcnt(0) followed by lds_mark on it.
+__device__ __forceinline__ void rd128_issue(u32x4& o, uint32_t a) {
+  asm volatile("ds_read_b128 %0, %1" : "=v"(o) : "v"(a) : "memory");
+}
+__device__ __forceinline__ void rdtr_issue(u32x2& o, uint32_t a) {
+  asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(o) : "v"(a) : "memory");
+}
+__device__ __forceinline__ void lds_wait_all() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+// At most n LDS operations outstanding (keeps the 4-bit counter from overflowing).
+template <int N>
+__device__ __forceinline__ void lds_wait_le() {
+  static_assert(N >= 0 && N < 16, "lgkmcnt range");
+  asm volatile("s_waitcnt lgkmcnt(%0)" ::"n"(N) : "memory");
+}
+// Marks registers of reads retired by an earlier lds_wait_all (no instruction).
+template <int N>
+__device__ __forceinline__ void lds_mark(u32x4 (&o)[N]) {
+#pragma unroll
+  for (int i = 0; i < N; i += 4)
+    asm volatile("" : "+v"(o[i]), "+v"(o[i + 1]), "+v"(o[i + 2]), "+v"(o[i + 3])::"memory");
+}
+template <int N>
+__device__ __forceinline__ void lds_mark(u32x2 (&o)[N]) {
+#pragma unroll
+  for (int i = 0; i < N; i += 8)
+    asm volatile(""
+                 : "+v"(o[i]), "+v"(o[i + 1]), "+v"(o[i + 2]), "+v"(o[i + 3]), "+v"(o[i + 4]), "+v"(o[i + 5]),
+                   "+v"(o[i + 6]), "+v"(o[i + 7])::"memory");
+}
 
 // vmcnt(n) (gfx9 encoding; expcnt and lgkmcnt unrestricted).
 template <int N>
