@@ -363,97 +363,161 @@ void launch_dispatch_bwd(const moe_cfg& c, const void* Wg, const float* dlogits,
 }
 
 // -------------------------------------------------------------------- dWg
-// dWg[e][:] = sum_t dlogits[t][e] x[t][:].  Stage 1: per token chunk partial
-// sums (one thread per column, float accumulators per expert); stage 2: sum
-// of the partials in chunk order.  Deterministic.
-constexpr int kDwgCols = 256;
+// dWg[e][:] = sum_t dlogits[t][e] x[t][:].  Stage 1: a block owns a slab of
+// 512 columns (each lane 8 consecutive columns, one 16-byte load per token),
+// a chunk of tokens and a group of up to 16 experts; its four waves take
+// every fourth token of the chunk, and their sums meet in LDS in wave order.
+// Stage 2 adds the chunk partials in chunk order.  Deterministic.
+constexpr int kDwgSlab = 512;     // columns per block
+constexpr int kDwgEG = 16;        // experts per block
 
-static int64_t dwg_chunk_tokens(int64_t T) {
-  int64_t tch = (T + 127) / 128;
-  return tch < 64 ? 64 : tch;
+struct DwgPlan {
+  int64_t tch, nch;
+  int slabs, egroups;
+};
+static DwgPlan dwg_plan(const moe_cfg& c) {
+  DwgPlan q;
+  q.slabs = (c.d_model + kDwgSlab - 1) / kDwgSlab;
+  q.egroups = (c.E + kDwgEG - 1) / kDwgEG;
+  // about 256 blocks over the chunks, at least 64 tokens per chunk
+  int64_t want = 256 / (q.slabs * q.egroups);
+  if (want < 1) want = 1;
+  int64_t tch = (c.T + want - 1) / want;
+  if (tch < 64) tch = 64;
+  q.tch = tch;
+  q.nch = (c.T + tch - 1) / tch;
+  return q;
 }
 
-template <typename T, int EMAX>
-__global__ __launch_bounds__(kDwgCols) void dwg_partial_kernel(const T* __restrict__ x, const float* __restrict__ dl,
-                                                               float* __restrict__ part, int64_t T_tokens, int d,
-                                                               int E, int64_t tch) {
-  __shared__ float sdl[64][EMAX];
+template <typename T> __device__ __forceinline__ void load8(const T* p, float (&v)[8]);
+template <> __device__ __forceinline__ void load8<uint16_t>(const uint16_t* p, float (&v)[8]) { Vec<uint16_t>::load(p, v); }
+template <> __device__ __forceinline__ void load8<float>(const float* p, float (&v)[8]) {
+  float a[4], b[4];
+  Vec<float>::load(p, a);
+  Vec<float>::load(p + 4, b);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    v[i] = a[i];
+    v[4 + i] = b[i];
+  }
+}
+
+template <typename T, int EG>
+__global__ __launch_bounds__(256) void dwg_partial_kernel(const T* __restrict__ x, const float* __restrict__ dl,
+                                                          float* __restrict__ part, int64_t T_tokens, int d, int E,
+                                                          int64_t tch) {
+  __shared__ float red[3][EG][kDwgSlab];
+  const int lane = threadIdx.x & 63;
+  const int wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int col = blockIdx.x * kDwgSlab + 8 * lane;
+  const int e0 = blockIdx.z * kDwgEG;
   const int64_t ch = blockIdx.y;
-  const int col = blockIdx.x * kDwgCols + threadIdx.x;
-  float acc[EMAX];
-#pragma unroll
-  for (int e = 0; e < EMAX; ++e) acc[e] = 0.f;
   const int64_t t_begin = ch * tch;
-  const int64_t t_end = (t_begin + tch < T_tokens) ? t_begin + tch : T_tokens;
-  for (int64_t tb = t_begin; tb < t_end; tb += 64) {
-    __syncthreads();
-    for (int i = threadIdx.x; i < 64 * EMAX; i += kDwgCols) {
-      const int tt = i / EMAX, e = i % EMAX;
-      sdl[tt][e] = (tb + tt < t_end && e < E) ? dl[(tb + tt) * E + e] : 0.f;
-    }
-    __syncthreads();
-    if (col < d) {
-      const int64_t n = (t_end - tb) < 64 ? (t_end - tb) : 64;
-      for (int tt = 0; tt < n; ++tt) {
-        float xv;
-        if constexpr (sizeof(T) == 2) xv = bf16_bits_to_f32(x[(tb + tt) * d + col]);
-        else xv = x[(tb + tt) * d + col];
+  const int64_t t_end = min(t_begin + tch, T_tokens);
+  float acc[EG][8];
 #pragma unroll
-        for (int e = 0; e < EMAX; ++e) acc[e] = fmaf(sdl[tt][e], xv, acc[e]);
+  for (int e = 0; e < EG; ++e)
+#pragma unroll
+    for (int j = 0; j < 8; ++j) acc[e][j] = 0.f;
+  const bool colok = col < d;
+  constexpr int U = 4;   // tokens in flight per wave
+  for (int64_t t0 = t_begin + wid; t0 < t_end; t0 += 4 * U) {
+    float xv[U][8];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int64_t t = t0 + 4 * u;
+      if (colok && t < t_end) load8<T>(x + t * d + col, xv[u]);
+      else
+#pragma unroll
+        for (int j = 0; j < 8; ++j) xv[u][j] = 0.f;
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int64_t t = t0 + 4 * u;
+      const bool tok = t < t_end;
+      const float* dr = dl + (tok ? t : t_begin) * E + e0;
+#pragma unroll
+      for (int e = 0; e < EG; ++e) {
+        const float g = (tok && e0 + e < E) ? dr[e] : 0.f;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) acc[e][j] = fmaf(g, xv[u][j], acc[e][j]);
       }
     }
   }
-  if (col < d) {
+  // Block sum in wave order: waves 1..3 hand their sums to wave 0 through LDS.
+  if (wid > 0) {
 #pragma unroll
-    for (int e = 0; e < EMAX; ++e)
-      if (e < E) part[(ch * E + e) * d + col] = acc[e];
+    for (int e = 0; e < EG; ++e)
+#pragma unroll
+      for (int j = 0; j < 8; ++j) red[wid - 1][e][8 * lane + j] = acc[e][j];
+  }
+  __syncthreads();
+  if (wid == 0 && colok) {
+    float* out = part + (ch * E + e0) * (int64_t)d + col;
+#pragma unroll
+    for (int e = 0; e < EG; ++e) {
+      if (e0 + e >= E) continue;
+      float v[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) v[j] = ((acc[e][j] + red[0][e][8 * lane + j]) + red[1][e][8 * lane + j]) + red[2][e][8 * lane + j];
+      Vec<float>::store(out + (int64_t)e * d, v);
+      Vec<float>::store(out + (int64_t)e * d + 4, v + 4);
+    }
   }
 }
 
+// dWg[i] = sum over chunks of part[c][i], in chunk order; 4 consecutive outputs per thread.
 __global__ __launch_bounds__(256) void dwg_reduce_kernel(const float* __restrict__ part, float* __restrict__ dWg,
-                                                         int nch, int E, int d) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= (int64_t)E * d) return;
-  float s = 0.f;
-  for (int c = 0; c < nch; ++c) s += part[(int64_t)c * E * d + i];
-  dWg[i] = s;
+                                                         int nch, int64_t ed) {
+  const int64_t i = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * 4;
+  if (i >= ed) return;
+  float s[4] = {0.f, 0.f, 0.f, 0.f};
+  int c = 0;
+  for (; c + 4 <= nch; c += 4) {
+    float v[4][4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) Vec<float>::load(part + (int64_t)(c + u) * ed + i, v[u]);
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) s[j] += v[u][j];
+  }
+  for (; c < nch; ++c) {
+    float v[4];
+    Vec<float>::load(part + (int64_t)c * ed + i, v);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) s[j] += v[j];
+  }
+  Vec<float>::store(dWg + i, s);
 }
 
 size_t bwd_dw_ws_bytes(const moe_cfg& c) {
-  const int64_t tch = dwg_chunk_tokens(c.T);
-  const int64_t nch = (c.T + tch - 1) / tch;
-  return (size_t)(nch * c.E * (int64_t)c.d_model) * sizeof(float);
-}
-
-template <typename T, int EMAX>
-static void launch_dwg_e(const moe_cfg& c, const void* x, const float* dl, float* part, int64_t tch, int64_t nch,
-                         hipStream_t s) {
-  dim3 grid((unsigned)((c.d_model + kDwgCols - 1) / kDwgCols), (unsigned)nch);
-  hipLaunchKernelGGL((dwg_partial_kernel<T, EMAX>), grid, dim3(kDwgCols), 0, s, (const T*)x, dl, part, c.T,
-                     c.d_model, c.E, tch);
+  const DwgPlan q = dwg_plan(c);
+  return (size_t)(q.nch * c.E * (int64_t)c.d_model) * sizeof(float);
 }
 
 template <typename T>
-static void launch_dwg_t(const moe_cfg& c, const void* x, const float* dl, float* part, int64_t tch, int64_t nch,
+static void launch_dwg_t(const moe_cfg& c, const void* x, const float* dl, float* part, const DwgPlan& q,
                          hipStream_t s) {
-  if (c.E <= 4) launch_dwg_e<T, 4>(c, x, dl, part, tch, nch, s);
-  else if (c.E <= 8) launch_dwg_e<T, 8>(c, x, dl, part, tch, nch, s);
-  else if (c.E <= 16) launch_dwg_e<T, 16>(c, x, dl, part, tch, nch, s);
-  else if (c.E <= 32) launch_dwg_e<T, 32>(c, x, dl, part, tch, nch, s);
-  else launch_dwg_e<T, 64>(c, x, dl, part, tch, nch, s);
+  dim3 grid((unsigned)q.slabs, (unsigned)q.nch, (unsigned)q.egroups);
+  if (c.E <= 4)
+    hipLaunchKernelGGL((dwg_partial_kernel<T, 4>), grid, dim3(256), 0, s, (const T*)x, dl, part, c.T, c.d_model, c.E, q.tch);
+  else if (c.E <= 8)
+    hipLaunchKernelGGL((dwg_partial_kernel<T, 8>), grid, dim3(256), 0, s, (const T*)x, dl, part, c.T, c.d_model, c.E, q.tch);
+  else
+    hipLaunchKernelGGL((dwg_partial_kernel<T, 16>), grid, dim3(256), 0, s, (const T*)x, dl, part, c.T, c.d_model, c.E, q.tch);
 }
 
 void launch_dwg(const moe_cfg& c, const void* x, const float* dlogits, float* dWg, void* ws, hipStream_t s) {
-  const int64_t ed = (int64_t)c.E * c.d_model;
-  const int64_t tch = dwg_chunk_tokens(c.T);
-  const int64_t nch = (c.T + tch - 1) / tch;   // 0 when T == 0: the reduce then writes zeros
+  const int64_t ed = (int64_t)c.E * c.d_model;   // a multiple of 8
+  const DwgPlan q = dwg_plan(c);                 // nch = 0 when T == 0: the reduce then writes zeros
   float* part = (float*)ws;
-  if (nch > 0) {
-    if (c.dtype == MOE_BF16) launch_dwg_t<uint16_t>(c, x, dlogits, part, tch, nch, s);
-    else launch_dwg_t<float>(c, x, dlogits, part, tch, nch, s);
+  if (q.nch > 0) {
+    if (c.dtype == MOE_BF16) launch_dwg_t<uint16_t>(c, x, dlogits, part, q, s);
+    else launch_dwg_t<float>(c, x, dlogits, part, q, s);
   }
-  hipLaunchKernelGGL(dwg_reduce_kernel, dim3((unsigned)((ed + 255) / 256)), dim3(256), 0, s, part, dWg, (int)nch,
-                     c.E, c.d_model);
+  hipLaunchKernelGGL(dwg_reduce_kernel, dim3((unsigned)((ed / 4 + 255) / 256)), dim3(256), 0, s, part, dWg,
+                     (int)q.nch, ed);
 }
 
 }  // namespace lmoe
