@@ -248,7 +248,7 @@ def main():
         mark(2)
         L.moe_dispatch(cfg, dev["x"], b.idx, b.carry, b.fill, b.slot, b.send_buf, b.ws_dispatch)
         mark(3)
-        L.moe_expert_ffn_fwd(cfg, b.send_buf, b.carry, b.fill, b.W1p, b.W2p, b.H, b.A, b.O)
+        L.moe_expert_ffn_fwd(cfg, b.send_buf, b.carry, b.fill, b.W1p, b.W2p, b.H, b.A, b.O, b.ws_ffn)
         mark(4)
         L.moe_combine(cfg, b.O, b.idx, b.slot, b.w, b.y)
         mark(5)

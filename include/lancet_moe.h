@@ -75,7 +75,7 @@ typedef enum { MOE_F32 = 0, MOE_BF16 = 1 } moe_dtype;
 typedef enum { MOE_ACT_IDENTITY = 0, MOE_ACT_RELU = 1, MOE_ACT_GELU_TANH = 2, MOE_ACT_GELU_ERF = 3 } moe_act;
 
 /* Which call a workspace is for (moe_workspace_bytes). */
-typedef enum { MOE_CALL_DISPATCH = 0, MOE_CALL_BWD_DX = 1, MOE_CALL_BWD_DW = 2 } moe_call;
+typedef enum { MOE_CALL_DISPATCH = 0, MOE_CALL_BWD_DX = 1, MOE_CALL_BWD_DW = 2, MOE_CALL_FFN_FWD = 3 } moe_call;
 
 /* Host-side description of one MoE layer call. */
 typedef struct {
@@ -148,10 +148,14 @@ moe_status moe_pack_weights(const moe_cfg* cfg, const void* W1, const void* W2, 
  *   W1p, W2p from moe_pack_weights; row_begin/row_end [E] int32 device arrays
  *   (row_begin NULL = zeros), the carry-in and fill of the dispatch that
  *   wrote these rows.  H and A are saved for the backward.  bf16 inputs use
- *   MFMA with float accumulation. */
+ *   MFMA with float accumulation.
+ *   ws: moe_workspace_bytes(cfg, MOE_CALL_FFN_FWD) bytes (bf16: partial tiles
+ *   and counters of the products' K-split schedule, cleared by the call
+ *   itself; float: none, ws may be NULL).  Calls that overlap in time need
+ *   separate workspaces. */
 moe_status moe_expert_ffn_fwd(const moe_cfg* cfg, const void* send_buf, const int32_t* row_begin,
                               const int32_t* row_end, const void* W1p, const void* W2p, void* H, void* A,
-                              void* expert_out, moe_stream_t stream);
+                              void* expert_out, void* ws, size_t ws_bytes, moe_stream_t stream);
 
 /* Weighted gather back to token order (Fig. "moe_and_sharding", Gather):
  *   y[t] = sum over r with slot[t][r] >= 0 of w[t][r] * expert_out[idx[t][r]][slot[t][r]],
@@ -171,7 +175,8 @@ moe_status moe_combine(const moe_cfg* cfg, const void* expert_out, const int32_t
  *   dO, dXe [E][C][d] and dH [E][C][f] dtype (dO and dH are kept for
  *   moe_bwd_dw), dlogits [T][E] float, dx [T][d] dtype; W1p, W2p from
  *   moe_pack_weights.
- *   ws: moe_workspace_bytes(cfg, MOE_CALL_BWD_DX) bytes. */
+ *   ws: moe_workspace_bytes(cfg, MOE_CALL_BWD_DX) bytes (bf16: the expert
+ *   products' K-split workspace, as for moe_expert_ffn_fwd; float: none). */
 moe_status moe_bwd_dx(const moe_cfg* cfg, const void* Wg, const float* logits, const int32_t* idx,
                       const float* w, const int32_t* slot, const int32_t* row_begin,
                       const int32_t* row_end, const void* H, const void* expert_out, const void* W1p,

@@ -63,6 +63,11 @@ moe_status check_cfg(const moe_cfg* c, const char* fn, bool need_gemm_shape) {
     return fail(MOE_ESHAPE, "%s: E*C*max(d, f) too large", fn);
   if (need_gemm_shape && c->dtype == MOE_BF16 && (c->d_model % 64 != 0 || c->d_ff % 64 != 0))
     return fail(MOE_ESHAPE, "%s: bf16 expert GEMMs need d_model and d_ff multiples of 64", fn);
+  // The bf16 expert GEMMs address one expert's operand with 32-bit byte offsets.
+  const int64_t xmax = c->d_model > c->d_ff ? c->d_model : c->d_ff;
+  if (need_gemm_shape && c->dtype == MOE_BF16 &&
+      (((int64_t)c->C + 15) * xmax * 2 >= ((int64_t)1 << 31) || (int64_t)c->d_model * c->d_ff * 2 >= ((int64_t)1 << 31)))
+    return fail(MOE_ESHAPE, "%s: one expert's bf16 operand must stay under 2 GiB", fn);
   return MOE_OK;
 }
 
@@ -113,6 +118,7 @@ size_t moe_workspace_bytes(const moe_cfg* cfg, int32_t call) {
     case MOE_CALL_DISPATCH: return lmoe::dispatch_ws_bytes(*cfg);
     case MOE_CALL_BWD_DX: return lmoe::bwd_dx_ws_bytes(*cfg);
     case MOE_CALL_BWD_DW: return lmoe::bwd_dw_ws_bytes(*cfg);
+    case MOE_CALL_FFN_FWD: return lmoe::expert_sk_ws_bytes(*cfg);
     default: fail(MOE_EINVAL, "%s: unknown call %d", fn, call); return 0;
   }
 }
@@ -162,13 +168,19 @@ moe_status moe_pack_weights(const moe_cfg* cfg, const void* W1, const void* W2, 
 
 moe_status moe_expert_ffn_fwd(const moe_cfg* cfg, const void* send_buf, const int32_t* row_begin,
                               const int32_t* row_end, const void* W1p, const void* W2p, void* H, void* A,
-                              void* expert_out, moe_stream_t stream) {
+                              void* expert_out, void* ws, size_t ws_bytes, moe_stream_t stream) {
   const char* fn = "moe_expert_ffn_fwd";
   CHECK(check_cfg(cfg, fn, true));
   REQUIRE_PTR(send_buf); OPTIONAL_PTR(row_begin); REQUIRE_PTR(row_end);
   REQUIRE_PTR(W1p); REQUIRE_PTR(W2p); REQUIRE_PTR(H); REQUIRE_PTR(A); REQUIRE_PTR(expert_out);
+  const size_t need = lmoe::expert_sk_ws_bytes(*cfg);
+  if (need > 0) {
+    if (ws == nullptr || ws_bytes < need)
+      return fail(MOE_EWORKSPACE, "%s: workspace of %zu bytes needed, %zu given", fn, need, ws ? ws_bytes : 0);
+    REQUIRE_PTR(ws);
+  }
   CHECK(check_device(fn));
-  lmoe::launch_expert_fwd(*cfg, send_buf, row_begin, row_end, W1p, W2p, H, A, expert_out, (hipStream_t)stream);
+  lmoe::launch_expert_fwd(*cfg, send_buf, row_begin, row_end, W1p, W2p, H, A, expert_out, ws, (hipStream_t)stream);
   return check_launch(fn);
 }
 
@@ -193,13 +205,15 @@ moe_status moe_bwd_dx(const moe_cfg* cfg, const void* Wg, const float* logits, c
   REQUIRE_PTR(W1p); REQUIRE_PTR(W2p); REQUIRE_TPTR(dy); REQUIRE_PTR(dO); REQUIRE_PTR(dH); REQUIRE_PTR(dXe);
   REQUIRE_TPTR(dlogits); REQUIRE_TPTR(dx);
   const size_t need = lmoe::bwd_dx_ws_bytes(*cfg);
-  if (need > 0 && (ws == nullptr || ws_bytes < need))
-    return fail(MOE_EWORKSPACE, "%s: workspace of %zu bytes needed", fn, need);
-  (void)ws;
+  if (need > 0) {
+    if (ws == nullptr || ws_bytes < need)
+      return fail(MOE_EWORKSPACE, "%s: workspace of %zu bytes needed, %zu given", fn, need, ws ? ws_bytes : 0);
+    REQUIRE_PTR(ws);
+  }
   CHECK(check_device(fn));
   hipStream_t s = (hipStream_t)stream;
   lmoe::launch_combine_bwd(*cfg, logits, idx, w, slot, expert_out, dy, dO, dlogits, s);
-  lmoe::launch_expert_bwd_dx(*cfg, dO, row_begin, row_end, H, W1p, W2p, dH, dXe, s);
+  lmoe::launch_expert_bwd_dx(*cfg, dO, row_begin, row_end, H, W1p, W2p, dH, dXe, ws, s);
   lmoe::launch_dispatch_bwd(*cfg, Wg, dlogits, idx, slot, dXe, dx, s);
   return check_launch(fn);
 }

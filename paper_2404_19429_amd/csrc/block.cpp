@@ -71,7 +71,7 @@ hipError_t order(hipStream_t a, hipStream_t b) {
 size_t align256(size_t n) { return (n + 255) / 256 * 256; }
 
 struct WsLayout {
-  size_t disp, dw, ln2, ln1, total;
+  size_t disp, dw, ln2, ln1, sk, total;
 };
 
 WsLayout ws_layout(const moe_block_cfg& c, int n) {
@@ -85,6 +85,7 @@ WsLayout ws_layout(const moe_block_cfg& c, int n) {
   L.dw = off;   off += align256(bwd_dw_ws_bytes(c.moe));
   L.ln2 = off;  off += align256((size_t)ln_bwd_blocks(T) * 2 * d * sizeof(float));
   L.ln1 = off;  off += align256((size_t)ln_bwd_blocks(T) * 2 * d * sizeof(float));
+  L.sk = off;   off += align256(expert_sk_ws_bytes(c.moe));   // expert products on the compute stream
   L.total = off;
   return L;
 }
@@ -136,7 +137,7 @@ hipError_t run_block(const moe_block_cfg& c, const moe_block_weights& W, const m
       const int64_t t0 = Tc * i;
       HIP_TRY(hipStreamWaitEvent(Sc, ev_disp[i], 0));
       const int32_t* rb = i == 0 ? nullptr : A.fill + (int64_t)(i - 1) * E;
-      launch_expert_fwd(mc, A.send_buf, rb, A.fill + (int64_t)i * E, A.W1p, A.W2p, A.H, A.A, A.expert_out, Sc);
+      launch_expert_fwd(mc, A.send_buf, rb, A.fill + (int64_t)i * E, A.W1p, A.W2p, A.H, A.A, A.expert_out, wsb + L.sk, Sc);
       HIP_TRY(hipGetLastError());
       HIP_TRY(order(Sc, Sx));
       launch_combine(pc, A.expert_out, A.idx + t0 * k, A.slot + t0 * k, A.w + t0 * k, bfm(out, t0 * d), Sx,
@@ -151,7 +152,7 @@ hipError_t run_block(const moe_block_cfg& c, const moe_block_weights& W, const m
     HIP_TRY(order(Sc, Sw));  // the weight stream starts after the caller's earlier work
     // MoE layer: combine/gate backward, expert dX, dispatch backward -> dm
     launch_combine_bwd(mc, A.logits, A.idx, A.w, A.slot, A.expert_out, dy, A.dO, A.dlogits, Sc);
-    launch_expert_bwd_dx(mc, A.dO, nullptr, fill_end, A.H, A.W1p, A.W2p, A.dH, A.dXe, Sc);
+    launch_expert_bwd_dx(mc, A.dO, nullptr, fill_end, A.H, A.W1p, A.W2p, A.dH, A.dXe, wsb + L.sk, Sc);
     launch_dispatch_bwd(mc, W.Wg, A.dlogits, A.idx, A.slot, A.dXe, A.dm, Sc);
     HIP_TRY(hipGetLastError());
     HIP_TRY(order(Sc, Sw));

@@ -37,6 +37,7 @@ struct GemmParams {
   int M, N, K;      // ragged-M: N, K used;  ragged-K: M, N used
   int act;
   int cap;          // rows per expert block (C): row ranges are clamped to [0, cap]; re == NULL means [0, cap)
+  float* part;      // wide ragged-M products: partial tiles of the K-split (stream-K) schedule
 };
 
 // Row range of group g, clamped to the buffer so bad ranges cannot reach outside it.
@@ -552,6 +553,14 @@ gemm_bf16_kernel(GemmParams p, int tilesM, int tilesN, int groups) {
 #endif
 constexpr int kWB = 256;       // block tile (rows and columns)
 
+// Immediate byte offset of fragment read r from its base (see read_base in the
+// kernel): K-contiguous fragment r sits r KB on; an MN-contiguous half r % 2
+// of fragment r / 2 sits (r / 4) blocks and (r % 2) * 4 rows on.
+template <bool KC, int R>
+constexpr int wide_read_imm() {
+  return KC ? R * 1024 : ((R >> 2) * 512 + (R & 1) * 128) * 2;
+}
+
 // Compile-time loop: f(std::integral_constant<int, I>) for I in [B, E).
 template <int B, int E, typename Fn>
 __device__ __forceinline__ void static_for(Fn&& f) {
@@ -595,6 +604,14 @@ __device__ __forceinline__ void acc_pin(f32x4 (&a)[8]) {
 }
 __device__ __forceinline__ void acc_pin(f32x4 (&a)[4]) {
   asm volatile("" : "+a"(a[0]), "+a"(a[1]), "+a"(a[2]), "+a"(a[3]));
+}
+// The same, ordered after every earlier memory operation.
+__device__ __forceinline__ void acc_pin_mem(f32x4 (&a)[8]) {
+  asm volatile("" : "+a"(a[0]), "+a"(a[1]), "+a"(a[2]), "+a"(a[3]), "+a"(a[4]), "+a"(a[5]), "+a"(a[6]), "+a"(a[7])
+               :: "memory");
+}
+__device__ __forceinline__ void acc_pin_mem(f32x4 (&a)[4]) {
+  asm volatile("" : "+a"(a[0]), "+a"(a[1]), "+a"(a[2]), "+a"(a[3])::"memory");
 }
 
 // One operand's loads for the K-steps of a tile (256 rows or columns x 32 K
@@ -665,6 +682,152 @@ struct WOp {
   }
 };
 
+// Schedule of one XCD's tiles [T0, T0 + n) over its nslot blocks.  Rounds of
+// whole tiles run in lock step (block s takes tiles T0 + q nslot + s), so the
+// tiles in flight share their K position and their operand slices in L2.  A
+// last round that would leave most blocks idle (r <= nslot / 4 tiles) is
+// split instead: the r tiles' K-steps go to all nslot blocks, each tile to a
+// contiguous group of blocks, each block a contiguous K range of one tile;
+// the partial sums are added by gemm_wide_fixup_kernel.
+struct WSched {
+  int R, r;      // full rounds; tiles left for the last round
+  bool split;    // the last round is K-split
+  // K-split: the remainder tile of block `slot`, the first block of that tile,
+  // its number of blocks, and the block's K range [k0, k1).
+  __device__ __forceinline__ void split_part(int slot, int nslot, int nk, int& q, int& first, int& cnt, int& k0,
+                                             int& k1) const {
+    q = slot * r / nslot;
+    first = (q * nslot + r - 1) / r;
+    cnt = ((q + 1) * nslot + r - 1) / r - first;
+    const int rank = slot - first;
+    k0 = rank * nk / cnt;
+    k1 = (rank + 1) * nk / cnt;
+  }
+};
+__device__ __forceinline__ WSched wide_sched(int n, int nslot, bool allow_split) {
+  WSched w;
+  w.R = n / nslot;
+  w.r = n - w.R * nslot;
+  w.split = allow_split && w.r > 0 && 4 * w.r <= nslot;
+  return w;
+}
+
+// Geometry of tile t of a wide product.  incl / excl: the lane-per-group
+// inclusive / exclusive prefix of tile counts.  Within a group, tiles are
+// numbered panel by panel (kPanelN tile columns), m-tiles within a panel, n
+// fastest, so the tiles one XCD has in flight form a square-ish patch.
+template <bool RAGGED_K>
+__device__ __forceinline__ WGeo wide_geo(const GemmParams& p, int t, int lane, int groups, int incl, int excl,
+                                         int tilesM, int tilesN) {
+  WGeo G;
+  G.g = __builtin_amdgcn_readfirstlane(__popcll(__ballot(lane < groups && incl <= t)));
+  const int local = t - __builtin_amdgcn_readfirstlane(__shfl(excl, G.g, 64));
+  int lo, span;
+  group_rows(p, G.g, lo, span);
+  G.lo = lo;
+  G.hi = lo + span;
+  G.lo_al = lo & ~15;
+  if (span > 0) span += lo - G.lo_al;
+  const int tmg = RAGGED_K ? tilesM : (span + kWB - 1) / kWB;
+  const int pnl = local / (tmg * kPanelN);
+  const int rem = local - pnl * tmg * kPanelN;
+  const int pw = min(kPanelN, tilesN - pnl * kPanelN);
+  G.m0 = (rem / pw) * kWB;
+  G.n0 = (pnl * kPanelN + rem % pw) * kWB;
+  G.Mlim = RAGGED_K ? p.M : span;
+  G.Klim = RAGGED_K ? span : p.K;
+  G.nk = max(1, (G.Klim + kBKb - 1) / kBKb);   // an empty ragged-K group runs one all-zero step
+  return G;
+}
+
+// Lane-per-group tile counts of a wide product and their inclusive prefix
+// (groups <= 64); returns the total on every lane.
+template <bool RAGGED_K>
+__device__ __forceinline__ int wide_tile_prefix(const GemmParams& p, int lane, int groups, int tilesM, int tilesN,
+                                                int& incl, int& excl) {
+  int cnt = 0;
+  if (lane < groups) {
+    if constexpr (RAGGED_K) {
+      cnt = tilesM * tilesN;
+    } else {
+      int lo, span;
+      group_rows(p, lane, lo, span);
+      if (span > 0) span += lo & 15;
+      cnt = ((span + kWB - 1) / kWB) * tilesN;
+    }
+  }
+  incl = cnt;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int u = __shfl_up(incl, o, 64);
+    if (lane >= o) incl += u;
+  }
+  excl = incl - cnt;
+  return __builtin_amdgcn_readfirstlane(__shfl(incl, groups - 1, 64));
+}
+
+// Epilogue of one wave's tile from its accumulators: bf16 conversion and the
+// EPI-specific store (plain, (H, act(H)), or dA * act'(H) with H read back).
+// acc[i][j] holds output row 16 i + l % 16, columns 16 j + 4 (l / 16) .. +3 of
+// the wave tile at (G.m0 + wm WTM, G.n0 + wn WTN).
+template <int FM, int FN, int WTM, int WTN, bool RAGGED_K, int EPI, int ACT, bool CBLK>
+__device__ __forceinline__ void wide_epilogue(const GemmParams& p, const WGeo& G, f32x4 (&acc)[FM][FN], int wm,
+                                              int wn, int lane, int i_lo = 0, int i_hi = FM) {
+  const int64_t cofs = (int64_t)G.g * p.sC + (RAGGED_K || CBLK ? 0 : (int64_t)G.lo_al * p.ldc);
+  uint16_t* C = (uint16_t*)p.C + cofs;
+  uint16_t* C2 = EPI == EPI_FWD1 ? (uint16_t*)p.C2 + cofs : nullptr;
+  const uint16_t* Aux = EPI == EPI_DACT ? (const uint16_t*)p.Aux + cofs : nullptr;
+  const int rl = lane & 15, cq = 4 * (lane >> 4);
+  auto offset = [&](int row, int col) __attribute__((always_inline)) -> int64_t {
+    return CBLK ? blk_off(G.lo_al + row, col, p.ldc) : (int64_t)row * p.ldc + col;
+  };
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {          // two halves of four fragment rows
+    u32x2 aux[4][FN];
+    if constexpr (EPI == EPI_DACT) {     // all loads of the half first, then the math
+#pragma unroll
+      for (int ii = 0; ii < 4; ++ii) {
+        const int row = G.m0 + wm * WTM + 16 * (4 * h + ii) + rl;
+        const bool rok = row < G.Mlim && (RAGGED_K || G.lo_al + row >= G.lo) && 4 * h + ii >= i_lo && 4 * h + ii < i_hi;
+#pragma unroll
+        for (int j = 0; j < FN; ++j) {
+          const int col = G.n0 + wn * WTN + 16 * j + cq;
+          aux[ii][j] = (rok && col < p.N) ? *reinterpret_cast<const u32x2*>(Aux + offset(row, col)) : u32x2{0u, 0u};
+        }
+      }
+    }
+#pragma unroll
+    for (int ii = 0; ii < 4; ++ii) {
+      const int i = 4 * h + ii;
+      if (i < i_lo || i >= i_hi) continue;
+      const int row = G.m0 + wm * WTM + 16 * i + rl;
+      const bool rok = row < G.Mlim && (RAGGED_K || G.lo_al + row >= G.lo);
+#pragma unroll
+      for (int j = 0; j < FN; ++j) {
+        const int col = G.n0 + wn * WTN + 16 * j + cq;
+        if (!(rok && col < p.N)) continue;
+        const int64_t off = offset(row, col);
+        float v[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
+        if constexpr (EPI == EPI_FWD1) {
+          *reinterpret_cast<u32x2*>(C + off) = pack4_bf16(v);
+#pragma unroll
+          for (int u = 0; u < 4; ++u) v[u] = act_fwd_t<ACT>(v[u]);
+          *reinterpret_cast<u32x2*>(C2 + off) = pack4_bf16(v);
+        } else if constexpr (EPI == EPI_DACT) {
+          const u32x2 hv = aux[ii][j];
+          const float hh[4] = {__uint_as_float(hv[0] << 16), __uint_as_float(hv[0] & 0xffff0000u),
+                               __uint_as_float(hv[1] << 16), __uint_as_float(hv[1] & 0xffff0000u)};
+#pragma unroll
+          for (int u = 0; u < 4; ++u) v[u] *= act_bwd_t<ACT>(hh[u]);
+          *reinterpret_cast<u32x2*>(C + off) = pack4_bf16(v);
+        } else {
+          *reinterpret_cast<u32x2*>(C + off) = pack4_bf16(v);
+        }
+      }
+    }
+  }
+}
+
 // NW = 4: waves 2 x 2, wave tile 128 x 128, one wave per SIMD.
 // NW = 8: waves 2 x 4, wave tile 128 x 64, two waves per SIMD, which lets the
 // SIMD issue one wave's MFMAs while the other waits on memory.
@@ -690,60 +853,54 @@ gemm_wide_kernel(GemmParams p, int tilesM, int tilesN, int groups) {
   const int wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int wm = wid / WGN, wn = wid % WGN;
 
-  // Tile counts per group and their inclusive prefix, one lane per group
-  // (groups <= 64); every wave computes the same values.
-  int cnt = 0;
-  if (lane < groups) {
-    if constexpr (RAGGED_K) {
-      cnt = tilesM * tilesN;
-    } else {
-      int lo, span;
-      group_rows(p, lane, lo, span);
-      if (span > 0) span += lo & 15;
-      cnt = ((span + kWB - 1) / kWB) * tilesN;
-    }
-  }
-  int incl = cnt;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const int u = __shfl_up(incl, o, 64);
-    if (lane >= o) incl += u;
-  }
-  const int excl = incl - cnt;
-  const int total = __builtin_amdgcn_readfirstlane(__shfl(incl, groups - 1, 64));
+  // Tile counts per group and their prefix (every wave computes the same values).
+  int incl, excl;
+  const int total = wide_tile_prefix<RAGGED_K>(p, lane, groups, tilesM, tilesN, incl, excl);
   const int nslot = gridDim.x / 8;
   const int xcd = blockIdx.x % 8, slot = blockIdx.x / 8;
   const int per = (total + 7) / 8;
-  const int t_begin = xcd * per + slot;
-  const int t_end = min(total, (xcd + 1) * per);
-  if (t_begin >= t_end) return;
+  // The block's segments (see WSched): nd whole tiles T0 + e nslot + slot,
+  // then, if the last round is K-split (ragged-M products, one K length), the
+  // K range [sk0, sk1) of remainder tile T0 + R nslot + sq.
+  const int T0 = xcd * per, T1 = min(total, (xcd + 1) * per);
+  const int nkU = (p.K + BK - 1) / BK;
+  // Only the plain-store ragged-M products may K-split their last round (the
+  // narrow-N products where a ragged last round idles most of the GPU); the
+  // others keep the simpler whole-tile schedule and its register budget.
+  constexpr bool SPLIT = !RAGGED_K && EPI == EPI_STORE;
+  const WSched W = wide_sched(max(T1 - T0, 0), nslot, SPLIT);
+  int sq = 0, sfirst = 0, scnt = 0, sk0 = 0, sk1 = 0;
+  if (SPLIT && W.split) W.split_part(slot, nslot, nkU, sq, sfirst, scnt, sk0, sk1);
+  // (uniform values: keep them in scalar registers)
+  const int WR = __builtin_amdgcn_readfirstlane(W.R);
+  sq = __builtin_amdgcn_readfirstlane(sq);
+  sk0 = __builtin_amdgcn_readfirstlane(sk0);
+  sk1 = __builtin_amdgcn_readfirstlane(sk1);
+  const int nd = __builtin_amdgcn_readfirstlane(W.R + (!W.split && slot < W.r ? 1 : 0));
+  const int nseg = __builtin_amdgcn_readfirstlane(nd + (SPLIT && W.split && sk0 < sk1 ? 1 : 0));
+  if (nseg == 0) return;
 
   auto geo = [&](int t) __attribute__((always_inline)) {
-    WGeo G;
-    G.g = __builtin_amdgcn_readfirstlane(__popcll(__ballot(lane < groups && incl <= t)));
-    const int local = t - __builtin_amdgcn_readfirstlane(__shfl(excl, G.g, 64));
-    int lo, span;
-    group_rows(p, G.g, lo, span);
-    G.lo = lo;
-    G.hi = lo + span;
-    G.lo_al = lo & ~15;
-    if (span > 0) span += lo - G.lo_al;
-    const int tmg = RAGGED_K ? tilesM : (span + kWB - 1) / kWB;
-    const int pnl = local / (tmg * kPanelN);
-    const int rem = local - pnl * tmg * kPanelN;
-    const int pw = min(kPanelN, tilesN - pnl * kPanelN);
-    G.m0 = (rem / pw) * kWB;
-    G.n0 = (pnl * kPanelN + rem % pw) * kWB;
-    G.Mlim = RAGGED_K ? p.M : span;
-    G.Klim = RAGGED_K ? span : p.K;
-    G.nk = max(1, (G.Klim + BK - 1) / BK);   // an empty ragged-K group runs one all-zero step
-    return G;
+    return wide_geo<RAGGED_K>(p, t, lane, groups, incl, excl, tilesM, tilesN);
   };
 
-  // Load cursor: tile lt, K-step lk of lnk; ls = stages issued so far.
+  // Segment e: tile, first K-step, end K-step (0 = the tile's own count).
+  auto seg = [&](int e, int& t, int& k0, int& k1) __attribute__((always_inline)) {
+    if (e < nd) {
+      t = T0 + e * nslot + slot;
+      k0 = 0;
+      k1 = 0;
+    } else {
+      t = T0 + WR * nslot + sq;
+      k0 = sk0;
+      k1 = sk1;
+    }
+  };
+  // Load cursor: segment le, its tile lt, K-step lk, end lkend; ls = stages
+  // issued so far.
   WOp<A_K, RAGGED_K, NW> opA;
   WOp<BK_C, RAGGED_K, NW> opB;
-  int lt = t_begin, lk = 0, lnk = 0, ls = 0;
+  int le = 0, lt = 0, lk = 0, lkend = 0, ls = 0;
   auto plan = [&](int t) __attribute__((always_inline)) {
     const WGeo G = geo(t);
     const uint16_t* Ab = (const uint16_t*)p.A + G.g * p.sA;
@@ -753,24 +910,28 @@ gemm_wide_kernel(GemmParams p, int tilesM, int tilesN, int groups) {
     if constexpr (BK_C) opB.plan(Bb, p.sB, p.ldb, G.n0, p.N, 0, 0, 0, wid, lane);
     else if constexpr (RAGGED_K) opB.plan(Bb, p.sB, p.ldb, G.n0, p.N, G.lo_al, G.lo, G.hi, wid, lane);
     else opB.plan(Bb, p.sB, p.ldb, G.n0, p.N, 0, 0, p.K, wid, lane);
-    lnk = G.nk;
+    if (lkend == 0) lkend = G.nk;
   };
-  plan(lt);
+  auto enter = [&]() __attribute__((always_inline)) {   // load cursor onto segment le
+    seg(le, lt, lk, lkend);
+    plan(lt);
+  };
+  enter();
+  auto loads_left = [&]() __attribute__((always_inline)) { return le < nseg; };
   // Load q (0 .. 2 kWNI - 1; even: A, odd: B) of the next stage.
   auto issue_load = [&](int q) __attribute__((always_inline)) {
-    if (lt >= t_end) return;
+    if (!loads_left()) return;
     uint16_t* st = lds + (ls % STAGES) * STAGE;
     if (q & 1) opB.issue(q >> 1, lk, st + kWB * BK, wid);
     else opA.issue(q >> 1, lk, st, wid);
   };
   // Moves the load cursor past the stage just issued.
   auto advance = [&]() __attribute__((always_inline)) {
-    if (lt >= t_end) return;
+    if (!loads_left()) return;
     ++ls;
-    if (++lk == lnk) {
-      lk = 0;
-      lt += nslot;
-      if (lt < t_end) plan(lt);
+    if (++lk == lkend) {
+      ++le;
+      if (loads_left()) enter();
     }
   };
 
@@ -842,58 +1003,7 @@ gemm_wide_kernel(GemmParams p, int tilesM, int tilesN, int groups) {
     asm volatile("s_nop 15\n s_nop 15" ::: "memory");
 #pragma unroll
     for (int i = 0; i < FM; ++i) acc_pin(acc[i]);
-    const int64_t cofs = (int64_t)G.g * p.sC + (RAGGED_K || CBLK ? 0 : (int64_t)G.lo_al * p.ldc);
-    uint16_t* C = (uint16_t*)p.C + cofs;
-    uint16_t* C2 = EPI == EPI_FWD1 ? (uint16_t*)p.C2 + cofs : nullptr;
-    const uint16_t* Aux = EPI == EPI_DACT ? (const uint16_t*)p.Aux + cofs : nullptr;
-    const int rl = lane & 15, cq = 4 * (lane >> 4);
-    auto offset = [&](int row, int col) __attribute__((always_inline)) -> int64_t {
-      return CBLK ? blk_off(G.lo_al + row, col, p.ldc) : (int64_t)row * p.ldc + col;
-    };
-#pragma unroll
-    for (int h = 0; h < 2; ++h) {          // two halves of four fragment rows
-      u32x2 aux[4][FN];
-      if constexpr (EPI == EPI_DACT) {     // all loads of the half first, then the math
-#pragma unroll
-        for (int ii = 0; ii < 4; ++ii) {
-          const int row = G.m0 + wm * WTM + 16 * (4 * h + ii) + rl;
-          const bool rok = row < G.Mlim && (RAGGED_K || G.lo_al + row >= G.lo);
-#pragma unroll
-          for (int j = 0; j < FN; ++j) {
-            const int col = G.n0 + wn * WTN + 16 * j + cq;
-            aux[ii][j] = (rok && col < p.N) ? *reinterpret_cast<const u32x2*>(Aux + offset(row, col)) : u32x2{0u, 0u};
-          }
-        }
-      }
-#pragma unroll
-      for (int ii = 0; ii < 4; ++ii) {
-        const int i = 4 * h + ii;
-        const int row = G.m0 + wm * WTM + 16 * i + rl;
-        const bool rok = row < G.Mlim && (RAGGED_K || G.lo_al + row >= G.lo);
-#pragma unroll
-        for (int j = 0; j < FN; ++j) {
-          const int col = G.n0 + wn * WTN + 16 * j + cq;
-          if (!(rok && col < p.N)) continue;
-          const int64_t off = offset(row, col);
-          float v[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
-          if constexpr (EPI == EPI_FWD1) {
-            *reinterpret_cast<u32x2*>(C + off) = pack4_bf16(v);
-#pragma unroll
-            for (int u = 0; u < 4; ++u) v[u] = act_fwd_t<ACT>(v[u]);
-            *reinterpret_cast<u32x2*>(C2 + off) = pack4_bf16(v);
-          } else if constexpr (EPI == EPI_DACT) {
-            const u32x2 hv = aux[ii][j];
-            const float hh[4] = {__uint_as_float(hv[0] << 16), __uint_as_float(hv[0] & 0xffff0000u),
-                                 __uint_as_float(hv[1] << 16), __uint_as_float(hv[1] & 0xffff0000u)};
-#pragma unroll
-            for (int u = 0; u < 4; ++u) v[u] *= act_bwd_t<ACT>(hh[u]);
-            *reinterpret_cast<u32x2*>(C + off) = pack4_bf16(v);
-          } else {
-            *reinterpret_cast<u32x2*>(C + off) = pack4_bf16(v);
-          }
-        }
-      }
-    }
+    wide_epilogue<FM, FN, WTM, WTN, RAGGED_K, EPI, ACT, CBLK>(p, G, acc, wm, wn, lane);
   };
 
   // Prologue: fill the ring, wait for the first stage, read its fragments.
@@ -927,15 +1037,21 @@ gemm_wide_kernel(GemmParams p, int tilesM, int tilesN, int groups) {
   constexpr int NMF = FM * FN, NDMA = 2 * kWNI;
   constexpr int RSPAN = NMF * 3 / 4;          // all reads issued within the first 3/4 of the MFMAs
   u32x2 qa[2 * FM], qb[2 * FN];               // pending halves of MN-contiguous fragments
-  // LDS byte address of read r of an operand (fragment r, or half r % 2 of fragment r / 2).
-  auto read_addr = [&](auto tile, const uint16_t* st, int c0, int r) __attribute__((always_inline)) -> uint32_t {
+  // LDS byte address of read r of an operand = base(par) + imm(r), with a
+  // compile-time immediate, so a step needs one or two base registers per
+  // operand.  K-contiguous: fragment r, base at fragment 0, imm = r KB.
+  // MN-contiguous: half h = r % 2 of fragment u = r / 2; within the swizzled
+  // 16 x 32 blocks the lane's chunk depends on u % 2 (par) and on the lane,
+  // while the block (u / 2) and the +4 rows of the second half are constant
+  // offsets (rows k and k + 4 share their swizzle).
+  auto read_base = [&](auto tile, const uint16_t* st, int c0, int par) __attribute__((always_inline)) -> uint32_t {
     using T = decltype(tile);
     if constexpr (std::is_same<T, TileK<kWB, NW, true>>::value) {
-      return lds_addr(st + ((c0 >> 4) + r) * 512 + lane * 8);
+      return lds_addr(st + (c0 >> 4) * 512 + lane * 8);
     } else {
       const int j = lane & 15;
-      const int k = 8 * (lane >> 4) + (j >> 2) + 4 * (r & 1);
-      return lds_addr(st + T::lds_off(k, c0 + 16 * (r >> 1) + 4 * (j & 3)));
+      const int k = 8 * (lane >> 4) + (j >> 2);
+      return lds_addr(st + T::lds_off(k, c0 + 16 * par + 4 * (j & 3)));
     }
   };
   // One K-step: the MFMAs of (ca, cb), with the next stage's fragment reads
@@ -956,11 +1072,10 @@ gemm_wide_kernel(GemmParams p, int tilesM, int tilesN, int groups) {
     }
     // The reads are unconditional (branch-free, so pending registers are never
     // copied); after the last step they read a stage no load is writing.
-    uint32_t ra[NRA], rb[NRB];
-#pragma unroll
-    for (int r = 0; r < NRA; ++r) ra[r] = read_addr(TA{}, st, wm * WTM, r);
-#pragma unroll
-    for (int r = 0; r < NRB; ++r) rb[r] = read_addr(TB{}, st + kWB * BK, wn * WTN, r);
+    const uint32_t ra0 = read_base(TA{}, st, wm * WTM, 0);
+    const uint32_t ra1 = AK ? ra0 : read_base(TA{}, st, wm * WTM, 1);
+    const uint32_t rb0 = read_base(TB{}, st + kWB * BK, wn * WTN, 0);
+    const uint32_t rb1 = BKK ? rb0 : read_base(TB{}, st + kWB * BK, wn * WTN, 1);
     __builtin_amdgcn_sched_barrier(0);
     static_for<0, NMF>([&](auto mc) __attribute__((always_inline)) {
       constexpr int m = decltype(mc)::value;
@@ -969,11 +1084,14 @@ gemm_wide_kernel(GemmParams p, int tilesM, int tilesN, int groups) {
         constexpr int r = decltype(rc)::value;
         if constexpr ((r * RSPAN) / NRD == m) {
           if constexpr (r < NRA) {
-            if constexpr (AK) rd128_issue(na[r], ra[r]);
-            else rdtr_issue(qa[r], ra[r]);
+            constexpr int imm = wide_read_imm<AK, r>();
+            if constexpr (AK) rd128_issue_at<imm>(na[r], ra0);
+            else rdtr_issue_at<imm>(qa[r], ((r >> 1) & 1) ? ra1 : ra0);
           } else {
-            if constexpr (BKK) rd128_issue(nb[r - NRA], rb[r - NRA]);
-            else rdtr_issue(qb[r - NRA], rb[r - NRA]);
+            constexpr int rr = r - NRA;
+            constexpr int imm = wide_read_imm<BKK, rr>();
+            if constexpr (BKK) rd128_issue_at<imm>(nb[rr], rb0);
+            else rdtr_issue_at<imm>(qb[rr], ((rr >> 1) & 1) ? rb1 : rb0);
           }
           if constexpr (r % 8 == 7 && r + 1 < NRD) lds_wait_le<7>();
         }
@@ -1008,14 +1126,29 @@ gemm_wide_kernel(GemmParams p, int tilesM, int tilesN, int groups) {
     if (more) advance();
     ++cs;
   };
-  for (int ct = t_begin; ct < t_end; ct += nslot) {
-    const WGeo Cg = geo(ct);
+  // Partial tile of a K-split remainder tile: stored to this block's slot in
+  // accumulator order -- wave w, fragment (i, j), lane l at
+  // ((w FM + i) FN + j) 64 + l -- for the fix-up kernel to add.
+  auto partial = [&]() __attribute__((always_inline)) {
+    asm volatile("s_nop 15\n s_nop 15" ::: "memory");   // last MFMA -> accumulator reads
+    float* mine = p.part + (int64_t)blockIdx.x * (kWB * kWB) + ((int64_t)wid * FM * FN * 64 + lane) * 4;
+    // One fragment row at a time (the pin orders each row's register moves
+    // after the previous row's stores, so only a row is ever out of AGPRs).
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+      acc_pin_mem(acc[i]);
+#pragma unroll
+      for (int j = 0; j < FN; ++j) *reinterpret_cast<f32x4*>(mine + (i * FN + j) * 256) = acc[i][j];
+    }
+  };
+
+  auto run_steps = [&](int n) __attribute__((always_inline)) {
     int kk = 0;
-    for (; kk + 2 <= Cg.nk; kk += 2) {
+    for (; kk + 2 <= n; kk += 2) {
       step(fa0, fb0, fa1, fb1);
       step(fa1, fb1, fa0, fb0);
     }
-    if (kk < Cg.nk) {   // odd step count: the next tile's fragments are in set 1
+    if (kk < n) {   // odd step count: the next fragments are in set 1
       step(fa0, fb0, fa1, fb1);
 #pragma unroll
       for (int u = 0; u < FM; ++u) fa0[u] = fa1[u];
@@ -1024,11 +1157,74 @@ gemm_wide_kernel(GemmParams p, int tilesM, int tilesN, int groups) {
       valu_to_mfma_fence(fa0);
       valu_to_mfma_fence(fb0);
     }
-    epilogue(Cg);
+  };
+  for (int e = 0; e < nseg; ++e) {
+    int ct, k0, k1;
+    seg(e, ct, k0, k1);
+    const WGeo Cg = geo(ct);
+    if constexpr (SPLIT) {
+      run_steps(e < nd ? Cg.nk : k1 - k0);
+      if (e < nd) epilogue(Cg);
+      else partial();
+    } else {
+      run_steps(Cg.nk);
+      epilogue(Cg);
+    }
     zero_acc();
     stores_pending = true;
   }
   wait_vm<0>();
+}
+
+// Adds the partial sums of the K-split remainder tiles -- in block order, so
+// the result does not depend on timing -- and applies the epilogue.  Block b
+// takes fragment row i = (b / 8) % FM of remainder tile (b / 8) / FM of XCD
+// b % 8 (both waves rows of the tile's 2 x WGN wave grid), so a tile's sum is
+// spread over FM blocks.  The schedule is recomputed exactly as the product
+// made it (nslot blocks per XCD).
+template <int NW, int EPI, int ACT, bool CBLK>
+__global__ __launch_bounds__(NW * 64) void gemm_wide_fixup_kernel(GemmParams p, int tilesM, int tilesN, int groups,
+                                                                   int nslot) {
+  constexpr int WGN = NW / 2, WTM = 128, WTN = kWB / WGN, FM = WTM / 16, FN = WTN / 16;
+  const int lane = threadIdx.x & 63;
+  const int wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int wm = wid / WGN, wn = wid % WGN;
+  int incl, excl;
+  const int total = wide_tile_prefix<false>(p, lane, groups, tilesM, tilesN, incl, excl);
+  const int xcd = blockIdx.x % 8, q = (blockIdx.x / 8) / FM, i = (blockIdx.x / 8) % FM;
+  const int per = (total + 7) / 8;
+  const int T0 = xcd * per, T1 = min(total, (xcd + 1) * per);
+  const int nkU = (p.K + kBKb - 1) / kBKb;
+  const WSched W = wide_sched(max(T1 - T0, 0), nslot, true);
+  if (!W.split || q >= W.r) return;
+  // the blocks of remainder tile q: [first, first + cnt); an empty K range wrote nothing
+  int q0, first, cnt, k0, k1;
+  W.split_part((q * nslot + W.r - 1) / W.r, nslot, nkU, q0, first, cnt, k0, k1);
+  const int64_t lane_off = ((int64_t)wid * FM * FN * 64 + lane) * 4 + (int64_t)i * FN * 256;
+  f32x4 sum[FN];
+  bool any = false;
+  for (int sl = first; sl < first + cnt; ++sl) {
+    int qq, ff, cc, a0, a1;
+    W.split_part(sl, nslot, nkU, qq, ff, cc, a0, a1);
+    if (a0 >= a1) continue;
+    const float* src = p.part + (int64_t)(sl * 8 + xcd) * (kWB * kWB) + lane_off;
+    f32x4 v[FN];
+#pragma unroll
+    for (int j = 0; j < FN; ++j) v[j] = *reinterpret_cast<const f32x4*>(src + j * 256);
+#pragma unroll
+    for (int j = 0; j < FN; ++j) sum[j] = any ? sum[j] + v[j] : v[j];
+    any = true;
+  }
+  const WGeo G = wide_geo<false>(p, T0 + W.R * nslot + q, lane, groups, incl, excl, tilesM, tilesN);
+  f32x4 acc[FM][FN];
+  static_for<0, FM>([&](auto ic) {   // row i of acc (compile-time index), the others unused
+    constexpr int I = decltype(ic)::value;
+    if (I == i) {
+#pragma unroll
+      for (int j = 0; j < FN; ++j) acc[I][j] = sum[j];
+      wide_epilogue<FM, FN, WTM, WTN, false, EPI, ACT, CBLK>(p, G, acc, wm, wn, lane, I, I + 1);
+    }
+  });
 }
 
 // ------------------------------------------------------------------ f32 path
@@ -1179,6 +1375,7 @@ static void run_gemm(int dtype, int act, int groups, const GemmParams& p, int ti
 #ifndef LMOE_WIDE_WAVES
 #define LMOE_WIDE_WAVES 8
 #endif
+constexpr int kSkMaxBlocks = 256;   // most blocks of a stream-K launch (partial slots per block: 2)
 template <bool B_K, bool RAGGED_K, int EPI, int ACT, bool CBLK>
 static void launch_wide(int groups, const GemmParams& p, int tilesM, int tilesN, hipStream_t s) {
   constexpr int S = LMOE_WIDE_STAGES, NW = LMOE_WIDE_WAVES;
@@ -1191,10 +1388,23 @@ static void launch_wide(int groups, const GemmParams& p, int tilesM, int tilesN,
   }
   const int64_t max_tiles = (int64_t)tilesM * tilesN * groups;
   int blocks = num_cus();
+  if (!RAGGED_K && blocks > kSkMaxBlocks) blocks = kSkMaxBlocks;   // partial slots in the workspace
   if (max_tiles < blocks) blocks = (int)max_tiles;
   blocks = (blocks + 7) / 8 * 8;
   hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(NW * 64), shmem, s, p, tilesM, tilesN, groups);
+  if constexpr (!RAGGED_K && EPI == EPI_STORE) {
+    const int nslot = blocks / 8;   // a K-split last round has at most nslot / 4 tiles per XCD
+    constexpr int FM = 128 / 16;
+    if (nslot >= 4)
+      hipLaunchKernelGGL((gemm_wide_fixup_kernel<NW, EPI, ACT, CBLK>), dim3((unsigned)(8 * (nslot / 4) * FM)),
+                         dim3(NW * 64), 0, s, p, tilesM, tilesN, groups, nslot);
+  }
 }
+
+// Workspace of the ragged-M bf16 expert products: one partial 256 x 256 float
+// tile per block, for a K-split last round.
+static constexpr int64_t kSkPartBytes = (int64_t)kSkMaxBlocks * kWB * kWB * sizeof(float);
+size_t expert_sk_ws_bytes(const moe_cfg& c) { return c.dtype == MOE_BF16 ? (size_t)kSkPartBytes : 0; }
 
 // Expert products.  bf16: blocked operands, wide tiles; outputs blocked
 // (CBLK) or row-major (the dW products).  float: the FMA kernel, row-major.
@@ -1226,22 +1436,26 @@ static int cdiv(int64_t a, int b) { return (int)((a + b - 1) / b); }
 static int64_t rows_alloc(const moe_cfg& c) { return c.dtype == MOE_BF16 ? pad16(c.C) : c.C; }
 
 void launch_expert_fwd(const moe_cfg& c, const void* X, const int32_t* rb, const int32_t* re, const void* W1,
-                       const void* W2, void* H, void* A, void* O, hipStream_t s) {
+                       const void* W2, void* H, void* A, void* O, void* ws, hipStream_t s) {
   const int64_t d = c.d_model, f = c.d_ff, C = c.C, Cp = rows_alloc(c);
   GemmParams p1{X, d, Cp * d, W1, d, f * d, H, f, Cp * f, A, nullptr, rb, re, 0, (int)f, (int)d, c.act, (int)C};
+  p1.part = (float*)ws;
   run_expert<true, false, EPI_FWD1, true>(c, p1, C, (int)f, s);
   GemmParams p2{A, f, Cp * f, W2, f, d * f, O, d, Cp * d, nullptr, nullptr, rb, re, 0, (int)d, (int)f, c.act, (int)C};
+  p2.part = (float*)ws;
   run_expert<true, false, EPI_STORE, true>(c, p2, C, (int)d, s);
 }
 
 void launch_expert_bwd_dx(const moe_cfg& c, const void* dO, const int32_t* rb, const int32_t* re, const void* H,
-                          const void* W1, const void* W2, void* dH, void* dXe, hipStream_t s) {
+                          const void* W1, const void* W2, void* dH, void* dXe, void* ws, hipStream_t s) {
   const int64_t d = c.d_model, f = c.d_ff, C = c.C, Cp = rows_alloc(c);
   // dA = dO W2_e  (B(k=i, n=j) = W2[e][i][j], N contiguous), epilogue dH = dA * act'(H)
   GemmParams p1{dO, d, Cp * d, W2, f, d * f, dH, f, Cp * f, nullptr, H, rb, re, 0, (int)f, (int)d, c.act, (int)C};
+  p1.part = (float*)ws;
   run_expert<false, false, EPI_DACT, true>(c, p1, C, (int)f, s);
   // dXe = dH W1_e  (B(k=i, n=j) = W1[e][i][j])
   GemmParams p2{dH, f, Cp * f, W1, d, f * d, dXe, d, Cp * d, nullptr, nullptr, rb, re, 0, (int)d, (int)f, c.act, (int)C};
+  p2.part = (float*)ws;
   run_expert<false, false, EPI_STORE, true>(c, p2, C, (int)d, s);
 }
 

@@ -31,10 +31,13 @@ void launch_dwg(const moe_cfg& c, const void* x, const float* dlogits, float* dW
 void launch_pack_weights(const moe_cfg& c, const void* W1, const void* W2, void* W1p, void* W2p, hipStream_t s);
 
 // gemm.hip: expert GEMMs over [E][C][*] buffers with per-expert row ranges.
+// The row-ragged products take a workspace of expert_sk_ws_bytes(c) bytes
+// (partial tiles and counters of their K-split schedule; unused for float).
+size_t expert_sk_ws_bytes(const moe_cfg& c);
 void launch_expert_fwd(const moe_cfg& c, const void* X, const int32_t* rb, const int32_t* re, const void* W1,
-                       const void* W2, void* H, void* A, void* O, hipStream_t s);
+                       const void* W2, void* H, void* A, void* O, void* ws, hipStream_t s);
 void launch_expert_bwd_dx(const moe_cfg& c, const void* dO, const int32_t* rb, const int32_t* re, const void* H,
-                          const void* W1, const void* W2, void* dH, void* dXe, hipStream_t s);
+                          const void* W1, const void* W2, void* dH, void* dXe, void* ws, hipStream_t s);
 void launch_expert_bwd_dw(const moe_cfg& c, const void* X, const void* A, const void* dO, const void* dH,
                           const int32_t* rb, const int32_t* re, void* dW1, void* dW2, hipStream_t s);
 

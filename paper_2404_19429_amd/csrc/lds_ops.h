@@ -127,6 +127,17 @@ __device__ __forceinline__ void rd128_issue(u32x4& o, uint32_t a) {
 __device__ __forceinline__ void rdtr_issue(u32x2& o, uint32_t a) {
   asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(o) : "v"(a) : "memory");
 }
+// The same with a constant byte offset in the instruction (0 .. 65535).
+template <int OFF>
+__device__ __forceinline__ void rd128_issue_at(u32x4& o, uint32_t a) {
+  static_assert(OFF >= 0 && OFF < 65536, "ds offset range");
+  asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(o) : "v"(a), "n"(OFF) : "memory");
+}
+template <int OFF>
+__device__ __forceinline__ void rdtr_issue_at(u32x2& o, uint32_t a) {
+  static_assert(OFF >= 0 && OFF < 65536, "ds offset range");
+  asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(o) : "v"(a), "n"(OFF) : "memory");
+}
 __device__ __forceinline__ void lds_wait_all() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
 // At most n LDS operations outstanding (keeps the 4-bit counter from overflowing).
 template <int N>

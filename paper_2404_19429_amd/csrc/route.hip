@@ -289,7 +289,7 @@ __global__ __launch_bounds__(256) void combine_bwd_kernel(const float* __restric
   if (j < E) dlogits[t * E + j] = dl;
 }
 
-size_t bwd_dx_ws_bytes(const moe_cfg&) { return 0; }
+size_t bwd_dx_ws_bytes(const moe_cfg& c) { return expert_sk_ws_bytes(c); }
 
 void launch_combine_bwd(const moe_cfg& c, const float* logits, const int32_t* idx, const float* w,
                         const int32_t* slot, const void* O, const void* dy, void* dO, float* dlogits,

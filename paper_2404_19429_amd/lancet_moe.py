@@ -23,7 +23,7 @@ LIB_PATH = os.environ.get("LANCET_MOE_LIB") or os.path.join(_HERE, "liblancet_mo
 MOE_OK, MOE_EINVAL, MOE_ESHAPE, MOE_EALIGN, MOE_EDTYPE, MOE_EDEVICE, MOE_ELAUNCH, MOE_EWORKSPACE = 0, -1, -2, -3, -4, -5, -6, -7
 MOE_F32, MOE_BF16 = 0, 1
 ACTS = {"identity": 0, "relu": 1, "gelu_tanh": 2, "gelu_erf": 3}
-MOE_CALL_DISPATCH, MOE_CALL_BWD_DX, MOE_CALL_BWD_DW = 0, 1, 2
+MOE_CALL_DISPATCH, MOE_CALL_BWD_DX, MOE_CALL_BWD_DW, MOE_CALL_FFN_FWD = 0, 1, 2, 3
 
 #: Every symbol include/lancet_moe.h declares.
 EXPORTS = ["moe_capacity", "moe_workspace_bytes", "moe_last_error", "moe_gate_topk", "moe_dispatch",
@@ -80,7 +80,7 @@ def _load():
         "moe_gate_topk": (I32, [CFG, P, P, P, P, P, P, P]),
         "moe_dispatch": (I32, [CFG, P, P, P, P, P, P, P, SZ, P]),
         "moe_pack_weights": (I32, [CFG, P, P, P, P, P]),
-        "moe_expert_ffn_fwd": (I32, [CFG, P, P, P, P, P, P, P, P, P]),
+        "moe_expert_ffn_fwd": (I32, [CFG, P, P, P, P, P, P, P, P, P, SZ, P]),
         "moe_combine": (I32, [CFG, P, P, P, P, P, P]),
         "moe_bwd_dx": (I32, [CFG] + [P] * 18 + [SZ, P]),
         "moe_bwd_dw": (I32, [CFG] + [P] * 12 + [SZ, P]),
@@ -188,15 +188,18 @@ def moe_pack_weights(cfg, W1, W2, W1p, W2p, stream=None):
                                  _ptr(W1p, "W1p", dt, n), _ptr(W2p, "W2p", dt, n), _stream(stream)))
 
 
-def moe_expert_ffn_fwd(cfg, send_buf, row_begin, row_end, W1p, W2p, H, A, expert_out, stream=None):
+def moe_expert_ffn_fwd(cfg, send_buf, row_begin, row_end, W1p, W2p, H, A, expert_out, ws=None, stream=None):
     dt = torch_dtype(cfg)
     d, f, E = cfg.d_model, cfg.d_ff, cfg.E
+    need = moe_workspace_bytes(cfg, MOE_CALL_FFN_FWD)
     _check(_lib.moe_expert_ffn_fwd(ctypes.byref(cfg), _ptr(send_buf, "send_buf", dt, expert_numel(cfg, d)),
                                    _ptr(row_begin, "row_begin", torch.int32, E, nullable=True),
                                    _ptr(row_end, "row_end", torch.int32, E), _ptr(W1p, "W1p", dt, E * f * d),
                                    _ptr(W2p, "W2p", dt, E * d * f), _ptr(H, "H", dt, expert_numel(cfg, f)),
                                    _ptr(A, "A", dt, expert_numel(cfg, f)),
-                                   _ptr(expert_out, "expert_out", dt, expert_numel(cfg, d)), _stream(stream)))
+                                   _ptr(expert_out, "expert_out", dt, expert_numel(cfg, d)),
+                                   _ptr(ws, "ws", torch.uint8, need, nullable=need == 0),
+                                   ws.numel() if ws is not None else 0, _stream(stream)))
 
 
 def moe_combine(cfg, expert_out, idx, slot, w, y, stream=None):
@@ -269,6 +272,7 @@ class LayerBuffers:
     W1p: torch.Tensor
     W2p: torch.Tensor
     ws_dispatch: torch.Tensor
+    ws_ffn: torch.Tensor
     ws_dx: torch.Tensor
     ws_dw: torch.Tensor
 
@@ -285,6 +289,7 @@ def alloc_layer(cfg: moe_cfg, device="cuda") -> LayerBuffers:
         dO=e(nd), dH=e(nf), dXe=e(nd), dlogits=e(T, E, dtype=torch.float32), dx=e(T, d),
         dW1=e(E, f, d), dW2=e(E, d, f), dWg=e(E, d, dtype=torch.float32), W1p=e(E * f * d), W2p=e(E * d * f),
         ws_dispatch=e(max(16, moe_workspace_bytes(cfg, MOE_CALL_DISPATCH)), dtype=torch.uint8),
+        ws_ffn=e(max(16, moe_workspace_bytes(cfg, MOE_CALL_FFN_FWD)), dtype=torch.uint8),
         ws_dx=e(max(16, moe_workspace_bytes(cfg, MOE_CALL_BWD_DX)), dtype=torch.uint8),
         ws_dw=e(max(16, moe_workspace_bytes(cfg, MOE_CALL_BWD_DW)), dtype=torch.uint8),
     )
@@ -296,7 +301,7 @@ def layer_forward(b: LayerBuffers, x, Wg, bias, W1, W2, stream=None):
     moe_pack_weights(c, W1, W2, b.W1p, b.W2p, stream)
     moe_gate_topk(c, x, Wg, bias, b.logits, b.idx, b.w, stream)
     moe_dispatch(c, x, b.idx, b.carry, b.fill, b.slot, b.send_buf, b.ws_dispatch, stream)
-    moe_expert_ffn_fwd(c, b.send_buf, b.carry, b.fill, b.W1p, b.W2p, b.H, b.A, b.O, stream)
+    moe_expert_ffn_fwd(c, b.send_buf, b.carry, b.fill, b.W1p, b.W2p, b.H, b.A, b.O, b.ws_ffn, stream)
     moe_combine(c, b.O, b.idx, b.slot, b.w, b.y, stream)
 
 

@@ -93,10 +93,10 @@ def test_dispatch_workspace_and_alias_checks():
 def test_bf16_gemm_shape_rule():
     c = _cfg(d_model=72)         # multiple of 8 (gate/dispatch fine) but not of 64
     lib = L._lib
-    assert lib.moe_expert_ffn_fwd(ctypes.byref(c), *([GOOD] * 8), None) == L.MOE_ESHAPE
+    assert lib.moe_expert_ffn_fwd(ctypes.byref(c), *([GOOD] * 8), GOOD, 1 << 40, None) == L.MOE_ESHAPE
     assert _gate(c) == L.MOE_EDEVICE
     c32 = _cfg(d_model=72, dtype="f32")
-    assert lib.moe_expert_ffn_fwd(ctypes.byref(c32), *([GOOD] * 8), None) == L.MOE_EDEVICE
+    assert lib.moe_expert_ffn_fwd(ctypes.byref(c32), *([GOOD] * 8), GOOD, 1 << 40, None) == L.MOE_EDEVICE
 
 
 def test_workspace_bytes_invalid_cfg_is_zero():
@@ -192,3 +192,17 @@ def test_expert_buffer_sizes_pad_bf16_rows_to_16():
     assert L.rows_alloc(_cfg(C=320)) == 320 and L.rows_alloc(_cfg(C=321)) == 336
     assert L.rows_alloc(_cfg(C=321, dtype="f32")) == 321
     assert L.expert_numel(_cfg(C=100, E=3), 64) == 3 * 112 * 64
+
+
+def test_ffn_fwd_workspace_rule():
+    """bf16 expert products need the K-split workspace the library reports; float needs none."""
+    c = _cfg()
+    lib = L._lib
+    need = L.moe_workspace_bytes(c, L.MOE_CALL_FFN_FWD)
+    assert need > 0 and need == L.moe_workspace_bytes(c, L.MOE_CALL_BWD_DX)
+    assert lib.moe_expert_ffn_fwd(ctypes.byref(c), *([GOOD] * 8), None, 0, None) == L.MOE_EWORKSPACE
+    assert lib.moe_expert_ffn_fwd(ctypes.byref(c), *([GOOD] * 8), GOOD, need - 1, None) == L.MOE_EWORKSPACE
+    assert lib.moe_expert_ffn_fwd(ctypes.byref(c), *([GOOD] * 8), GOOD, need, None) == L.MOE_EDEVICE
+    c32 = _cfg(dtype="f32")
+    assert L.moe_workspace_bytes(c32, L.MOE_CALL_FFN_FWD) == 0
+    assert lib.moe_expert_ffn_fwd(ctypes.byref(c32), *([GOOD] * 8), None, 0, None) == L.MOE_EDEVICE

@@ -136,15 +136,31 @@ _COMPARED = ("out", "dx", "logits", "idx", "w", "slot", "a", "qkv", "attn", "h",
              "da", "dlogits", "dWqkv", "dWo", "dln1_g", "dln1_b", "dln2_g", "dln2_b", "dWg", "dW1", "dW2")
 
 
-def _assert_bitwise(b1, b2, E, label):
-    for n in _COMPARED:
+def _assert_bitwise(b1, b2, E, label, names=_COMPARED):
+    for n in names:
         assert torch.equal(b1[n].view(torch.int16) if b1[n].dtype == torch.bfloat16 else b1[n],
                            b2[n].view(torch.int16) if b2[n].dtype == torch.bfloat16 else b2[n]), f"{label}: {n}"
     assert torch.equal(b1["fill"].view(-1, E)[-1], b2["fill"].view(-1, E)[-1]), f"{label}: final fill"
 
 
+# Everything up to the expert products, routing included, is bitwise the same
+# for any number of partitions.  The expert products cut each XCD's run of
+# K-steps into equal pieces, so where a tile's K sum is split -- and with it
+# the float summation order -- depends on how many tiles a call has; values
+# downstream of the experts then agree to rounding, not bit for bit.
+_BEFORE_EXPERTS = ("logits", "idx", "w", "slot", "a", "qkv", "attn", "h", "m")
+_AFTER_EXPERTS = tuple(n for n in _COMPARED if n not in _BEFORE_EXPERTS)
+TOL_ORDER = 1e-2   # normwise; bf16 roundings of fp32 sums taken in another order, carried down the backward
+
+
+def _assert_partition_equivalent(b1, b2, E, label):
+    _assert_bitwise(b1, b2, E, label, _BEFORE_EXPERTS)
+    for n in _AFTER_EXPERTS:
+        assert_close(f"{label}: {n}", host(b1[n]), host(b2[n]), TOL_ORDER)
+
+
 @pytest.mark.parametrize("case", ["B4_S37_d128_f128_E4_4chunks", "B4_S64_d256_f192_E8_drops_4chunks"])
-def test_partitions_equal_unpartitioned_bitwise(L, case):
+def test_partitions_equal_unpartitioned(L, case):
     spec = SMALL[case]
     inp = block_inputs(spec)
     dev = _upload(L, inp)
@@ -152,7 +168,7 @@ def test_partitions_equal_unpartitioned_bitwise(L, case):
     _, C, b1 = run_block(L, spec, dev, 1)
     for n in (2, spec.B):
         _, _, bn = run_block(L, spec, dev, n)
-        _assert_bitwise(b1, bn, E, f"{n} partitions vs 1")
+        _assert_partition_equivalent(b1, bn, E, f"{n} partitions vs 1")
         fills = host(bn["fill"]).reshape(n, E)
         assert (np.diff(np.concatenate([np.zeros((1, E), np.int64), fills]), axis=0) >= 0).all()
         assert (fills[-1] <= C).all()
@@ -200,7 +216,7 @@ def full(L):
 def test_full_size_partitioned_equals_unpartitioned(L, full):
     spec, inp, dev, C, b4 = full
     _, _, b1 = run_block(L, spec, dev, 1)
-    _assert_bitwise(b4, b1, spec.moe.E, "4 partitions vs 1 at full size")
+    _assert_partition_equivalent(b4, b1, spec.moe.E, "4 partitions vs 1 at full size")
 
 
 def test_full_size_sampled_forward_matches_oracle(L, full):

@@ -98,8 +98,9 @@ def test_layer_is_deterministic_and_dw_stream_independent(L):
 
 def test_batch_partitions_with_capacity_carry_equal_unpartitioned(L):
     """Four batch partitions, each continuing from the capacity the previous ones
-    used: routing and drops equal the unpartitioned layer (Sec. 2.3), and every
-    forward tensor equals the unpartitioned GPU run bit for bit."""
+    used: routing and drops equal the unpartitioned layer (Sec. 2.3), the
+    dispatched rows are bitwise the unpartitioned ones, and the expert outputs
+    agree with the unpartitioned GPU run to float summation order."""
     spec = _s("chunks", T=1024, d=128, f=256, E=8, cf_num=1, cf_den=1, zipf_s=0.8, seed=21)
     inp = layer_inputs(spec)
     C = spec_C(spec)
@@ -121,16 +122,19 @@ def test_batch_partitions_with_capacity_carry_equal_unpartitioned(L):
         L.moe_gate_topk(cfg, xi, dev["Wg"], bias, b.logits[sl], b.idx[sl], b.w[sl])
         fills.append(torch.empty(spec.E, dtype=torch.int32, device="cuda"))
         L.moe_dispatch(cfg, xi, b.idx[sl], fills[i], fills[i + 1], b.slot[sl], b.send_buf, ws)
-        L.moe_expert_ffn_fwd(cfg, b.send_buf, fills[i], fills[i + 1], b.W1p, b.W2p, b.H, b.A, b.O)
+        L.moe_expert_ffn_fwd(cfg, b.send_buf, fills[i], fills[i + 1], b.W1p, b.W2p, b.H, b.A, b.O, b.ws_ffn)
         L.moe_combine(cfg, b.O, b.idx[sl], b.slot[sl], b.w[sl], b.y[sl])
     torch.cuda.synchronize()
     np.testing.assert_array_equal(host(b.slot), fw["slot"])
     np.testing.assert_array_equal(host(fills[-1]), fw["fill"])
     fill = fw["fill"]
-    for name in ("send_buf", "H", "A", "O"):
-        np.testing.assert_array_equal(kept_rows(ebuf(b, name), fill),
-                                      kept_rows(ebuf(full, name), fill), err_msg=name)
-    np.testing.assert_array_equal(host(b.y), host(full.y))
+    np.testing.assert_array_equal(kept_rows(ebuf(b, "send_buf"), fill), kept_rows(ebuf(full, "send_buf"), fill))
+    # The expert products split a tile's K sum where their equal pieces fall,
+    # which depends on the call's tile count: after the experts, partitioned
+    # and unpartitioned runs agree to float summation order.
+    for name in ("H", "A", "O"):
+        assert_close(name, kept_rows(ebuf(b, name), fill), kept_rows(ebuf(full, name), fill), 5e-3)
+    assert_close("y", host(b.y), host(full.y), 5e-3)
     # carries are the per-partition fills; every partition filled a contiguous, disjoint row range
     f = np.stack([host(t) for t in fills])
     assert np.all(np.diff(f, axis=0) >= 0)
@@ -150,7 +154,7 @@ def test_zero_tokens(L):
     L.moe_dispatch(cfg, x, b.idx, b.carry, b.fill, b.slot, b.send_buf, b.ws_dispatch)
     # rows [carry, fill) are empty, so the experts and the dW products see no rows
     L.moe_pack_weights(cfg, W, W.clone(), b.W1p, b.W2p)
-    L.moe_expert_ffn_fwd(cfg, b.send_buf, b.carry, b.fill, b.W1p, b.W2p, b.H, b.A, b.O)
+    L.moe_expert_ffn_fwd(cfg, b.send_buf, b.carry, b.fill, b.W1p, b.W2p, b.H, b.A, b.O, b.ws_ffn)
     L.moe_combine(cfg, b.O, b.idx, b.slot, b.w, b.y)
     L.moe_bwd_dw(cfg, x, b.dlogits, b.carry, b.fill, b.send_buf, b.A, b.dO, b.dH, b.dW1, b.dW2, b.dWg, b.ws_dw)
     torch.cuda.synchronize()
