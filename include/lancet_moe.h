@@ -31,13 +31,15 @@
  *     moe_last_error() describes the problem.  T == 0 is valid.
  *   - Rows of an [E][C][*] buffer past an expert's filled range are
  *     unspecified: never read and never written by these calls.
- *   - Expert buffers [E][C][X] (send_buf, H, A, expert_out, dO, dH, dXe) and
- *     packed weights: for MOE_BF16 each expert's [C][X] matrix is stored in
- *     16-row x 32-column blocks of 1 KiB, rows padded to Cp = C rounded up to
- *     16: element (e, r, c) is at e*Cp*X + ((r/16)*(X/32) + c/32)*512 +
- *     (r%16)*32 + c%32, so a buffer holds E*Cp*X elements.  (Each block is
- *     one MFMA operand fragment; the GEMMs load it as one contiguous 1 KiB
- *     run.)  For MOE_F32 they are plain row-major with Cp = C.
+ *   - Expert buffers [E][C][X] hold E*Cp*X elements, with Cp = C rounded up
+ *     to 16 for MOE_BF16 and Cp = C for MOE_F32.  The buffers an expert
+ *     product reads (send_buf, H, A, dO, dH) and the packed weights are, for
+ *     MOE_BF16, stored in 16-row x 32-column blocks of 1 KiB: element
+ *     (e, r, c) is at e*Cp*X + ((r/16)*(X/32) + c/32)*512 + (r%16)*32 + c%32.
+ *     (Each block is one MFMA operand fragment; the GEMMs load it as one
+ *     contiguous 1 KiB run.)  The product outputs that only the gathers read
+ *     (expert_out, dXe) are row-major: (e, r, c) at (e*Cp + r)*X + c, so a
+ *     row is one contiguous run.  For MOE_F32 every buffer is row-major.
  *   - A device other than gfx950 gives MOE_EDEVICE; a failed launch
  *     MOE_ELAUNCH.
  *

@@ -1406,8 +1406,10 @@ static void launch_wide(int groups, const GemmParams& p, int tilesM, int tilesN,
 static constexpr int64_t kSkPartBytes = (int64_t)kSkMaxBlocks * kWB * kWB * sizeof(float);
 size_t expert_sk_ws_bytes(const moe_cfg& c) { return c.dtype == MOE_BF16 ? (size_t)kSkPartBytes : 0; }
 
-// Expert products.  bf16: blocked operands, wide tiles; outputs blocked
-// (CBLK) or row-major (the dW products).  float: the FMA kernel, row-major.
+// Expert products.  bf16: blocked operands, wide tiles; outputs that a later
+// product reads (H, A, dH) blocked (CBLK), the others (expert_out, dXe, which
+// only the gathers read, and the dW products) row-major.  float: the FMA
+// kernel, row-major.
 // rows: rows of the output per group (ragged-M: the capacity C, with up to 15
 // alignment rows; ragged-K: M); cols: N.
 template <bool B_K, bool RAGGED_K, int EPI, bool CBLK>
@@ -1443,7 +1445,7 @@ void launch_expert_fwd(const moe_cfg& c, const void* X, const int32_t* rb, const
   run_expert<true, false, EPI_FWD1, true>(c, p1, C, (int)f, s);
   GemmParams p2{A, f, Cp * f, W2, f, d * f, O, d, Cp * d, nullptr, nullptr, rb, re, 0, (int)d, (int)f, c.act, (int)C};
   p2.part = (float*)ws;
-  run_expert<true, false, EPI_STORE, true>(c, p2, C, (int)d, s);
+  run_expert<true, false, EPI_STORE, false>(c, p2, C, (int)d, s);   // expert_out row-major
 }
 
 void launch_expert_bwd_dx(const moe_cfg& c, const void* dO, const int32_t* rb, const int32_t* re, const void* H,
@@ -1456,7 +1458,7 @@ void launch_expert_bwd_dx(const moe_cfg& c, const void* dO, const int32_t* rb, c
   // dXe = dH W1_e  (B(k=i, n=j) = W1[e][i][j])
   GemmParams p2{dH, f, Cp * f, W1, d, f * d, dXe, d, Cp * d, nullptr, nullptr, rb, re, 0, (int)d, (int)f, c.act, (int)C};
   p2.part = (float*)ws;
-  run_expert<false, false, EPI_STORE, true>(c, p2, C, (int)d, s);
+  run_expert<false, false, EPI_STORE, false>(c, p2, C, (int)d, s);   // dXe row-major
 }
 
 void launch_expert_bwd_dw(const moe_cfg& c, const void* X, const void* A, const void* dO, const void* dH,

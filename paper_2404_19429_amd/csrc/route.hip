@@ -4,71 +4,39 @@
 // Slot assignment walks assignments token by token, rank by rank; the row an
 // assignment receives is carry_e plus the number of earlier assignments to
 // the same expert.  It is computed without order-defining atomics in three
-// launches: per-chunk expert histograms, a per-expert exclusive scan over
-// chunks (starting at carry, which makes batch partitions exact), and
-// in-chunk ranks from wavefront ballots.  Rows are then copied with 16-byte
+// launches: in-chunk ranks and per-chunk expert histograms (wavefront
+// ballots), a per-expert exclusive scan over chunks (starting at carry, which
+// makes batch partitions exact), and a final pass that adds the chunk base to
+// each rank, applies the capacity and copies the kept rows with 16-byte
 // vector accesses, one thread per (token, 16-byte column chunk).
 #include "internal.h"
 
 namespace lmoe {
 
-// Element offset of (expert e, row s, column col) in an [E][C][d] buffer:
-// blocked for bf16 (rows padded to 16), row-major for float.
+// Element offset of (expert e, row s, column col) in an [E][C][d] buffer that
+// the expert products read (send_buf, dO): blocked for bf16 (rows padded to
+// 16), row-major for float.
 template <typename T>
 __device__ __forceinline__ int64_t eoff(int e, int s, int col, int d, int C) {
   const int64_t rows = sizeof(T) == 2 ? pad16(C) : C;
   return (int64_t)e * rows * d + ebuf_off<T>(s, col, d);
 }
+// The same for the row-major product outputs (expert_out, dXe).
+template <typename T>
+__device__ __forceinline__ int64_t erow(int e, int s, int col, int d, int C) {
+  const int64_t rows = sizeof(T) == 2 ? pad16(C) : C;
+  return ((int64_t)e * rows + s) * d + col;
+}
 
 // ------------------------------------------------------------ slot assignment
-// counts[chunk][E]: assignments of each expert inside one chunk of tokens.
-__global__ __launch_bounds__(kRouteChunk) void route_count_kernel(const int32_t* __restrict__ idx,
-                                                                  int32_t* __restrict__ counts,
-                                                                  int64_t T_tokens, int E, int k) {
-  __shared__ int32_t hist[kMaxE];
-  for (int e = threadIdx.x; e < E; e += blockDim.x) hist[e] = 0;
-  __syncthreads();
-  const int64_t t = (int64_t)blockIdx.x * kRouteChunk + threadIdx.x;
-  if (t < T_tokens)
-    for (int r = 0; r < k; ++r) {
-      const int e = idx[t * k + r];
-      if (e >= 0 && e < E) atomicAdd(&hist[e], 1);  // counts only: order-free
-    }
-  __syncthreads();
-  for (int e = threadIdx.x; e < E; e += blockDim.x) counts[(int64_t)blockIdx.x * E + e] = hist[e];
-}
-
-// base[chunk][e] = carry_e + assignments to e in earlier chunks; fill_e = min(C, carry_e + all).
-__global__ __launch_bounds__(256) void route_scan_kernel(const int32_t* __restrict__ counts,
-                                                         int32_t* __restrict__ base,
-                                                         const int32_t* __restrict__ carry,
-                                                         int32_t* __restrict__ fill, int nchunks, int E,
-                                                         int C) {
-  const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
-  for (int e = wave; e < E; e += (blockDim.x >> 6)) {
-    int running = carry ? carry[e] : 0;
-    for (int c0 = 0; c0 < nchunks; c0 += kWave) {
-      const int c = c0 + lane;
-      const int v = c < nchunks ? counts[(int64_t)c * E + e] : 0;
-      int incl = v;
-#pragma unroll
-      for (int o = 1; o < kWave; o <<= 1) {
-        const int u = __shfl_up(incl, o, kWave);
-        if (lane >= o) incl += u;
-      }
-      if (c < nchunks) base[(int64_t)c * E + e] = running + incl - v;
-      running += __shfl(incl, kWave - 1, kWave);
-    }
-    if (lane == 0) fill[e] = running < C ? running : C;
-  }
-}
-
-// slot[t][r] = base[chunk][e] + rank among earlier same-expert assignments in the chunk, or -1.
-__global__ __launch_bounds__(kRouteChunk) void route_slots_kernel(const int32_t* __restrict__ idx,
-                                                                  const int32_t* __restrict__ base,
-                                                                  int32_t* __restrict__ slot,
-                                                                  int64_t T_tokens, int E, int k, int C) {
+// For every assignment (t, r) of a chunk: rank[t][r] = assignments to the same
+// expert earlier in (token, rank) order inside the chunk; counts[chunk][e] =
+// the chunk's assignments to e.  Lanes holding the same expert are found with
+// one ballot per expert-index bit.
+__global__ __launch_bounds__(kRouteChunk) void route_rank_kernel(const int32_t* __restrict__ idx,
+                                                                 int32_t* __restrict__ counts,
+                                                                 int32_t* __restrict__ rank_out,
+                                                                 int64_t T_tokens, int E, int k) {
   constexpr int NW = kRouteChunk / kWave;
   __shared__ int32_t wcnt[NW][kMaxE];
   const int lane = threadIdx.x & 63;
@@ -78,33 +46,51 @@ __global__ __launch_bounds__(kRouteChunk) void route_slots_kernel(const int32_t*
 
   const int64_t t = (int64_t)blockIdx.x * kRouteChunk + threadIdx.x;
   const bool active = t < T_tokens;
-  int my[kMaxK];
-  int rank[kMaxK];
+  int my[kMaxK], rank[kMaxK];
 #pragma unroll
   for (int r = 0; r < kMaxK; ++r) {
     const int e = (active && r < k) ? idx[t * k + r] : -1;
     my[r] = (e >= 0 && e < E) ? e : -1;  // an out-of-range expert is treated as dropped
     rank[r] = 0;
   }
+  // Earlier choices of the same token (only if a row repeats an expert).
+#pragma unroll
+  for (int r = 1; r < kMaxK; ++r)
+#pragma unroll
+    for (int q = 0; q < r; ++q) rank[r] += (my[r] >= 0 && my[q] == my[r]) ? 1 : 0;
+
+  // Round rp: the bit masks of every lane's rp-th choice let each lane count,
+  // for each of its own choices, the lower lanes whose rp-th choice matches.
   const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
 #pragma unroll
   for (int rp = 0; rp < kMaxK; ++rp) {
     if (rp >= k) break;
     const int v = my[rp];
-    uint64_t rem = __ballot(v >= 0);
-    while (rem) {
-      const int leader = __ffsll((unsigned long long)rem) - 1;
-      const int ev = __shfl(v, leader, kWave);
-      const uint64_t m = __ballot(v == ev);
-      rem &= ~m;
-      const int before = __popcll(m & lt);
+    const uint64_t valid = __ballot(v >= 0);
+    uint64_t mb[6];
 #pragma unroll
-      for (int r = 0; r < kMaxK; ++r)
-        if (my[r] == ev) rank[r] += before;
-      if (lane == 0) wcnt[wave][ev] += __popcll(m);
+    for (int b = 0; b < 6; ++b) mb[b] = __ballot(v >= 0 && ((v >> b) & 1));
+    auto holders = [&](int e) __attribute__((always_inline)) {   // lanes whose rp-th choice is e
+      uint64_t m = valid;
+#pragma unroll
+      for (int b = 0; b < 6; ++b) m &= ((e >> b) & 1) ? mb[b] : ~mb[b];
+      return m;
+    };
+#pragma unroll
+    for (int r = 0; r < kMaxK; ++r)
+      if (r < k && my[r] >= 0) rank[r] += __popcll(holders(my[r]) & lt);
+    if (v >= 0) {
+      const uint64_t peers = holders(v);
+      if ((peers & lt) == 0) wcnt[wave][v] += __popcll(peers);  // one leader per expert
     }
   }
   __syncthreads();
+  for (int e = threadIdx.x; e < E; e += blockDim.x) {
+    int n = 0;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) n += wcnt[w][e];
+    counts[(int64_t)blockIdx.x * E + e] = n;
+  }
   if (!active) return;
 #pragma unroll
   for (int r = 0; r < kMaxK; ++r) {
@@ -112,38 +98,113 @@ __global__ __launch_bounds__(kRouteChunk) void route_slots_kernel(const int32_t*
       const int e = my[r];
       int s = -1;
       if (e >= 0) {
-        s = base[(int64_t)blockIdx.x * E + e] + rank[r];
+        s = rank[r];
         for (int w = 0; w < wave; ++w) s += wcnt[w][e];
       }
-      slot[t * k + r] = (s >= 0 && s < C) ? s : -1;
+      rank_out[t * k + r] = s;
     }
   }
 }
 
+// base[chunk][e] = carry_e + assignments to e in earlier chunks; fill_e = min(C, carry_e + all).
+// One wave per expert (grid = E).
+__global__ __launch_bounds__(64) void route_scan_kernel(const int32_t* __restrict__ counts,
+                                                        int32_t* __restrict__ base,
+                                                        const int32_t* __restrict__ carry,
+                                                        int32_t* __restrict__ fill, int nchunks, int E, int C) {
+  const int lane = threadIdx.x;
+  const int e = blockIdx.x;
+  int running = carry ? carry[e] : 0;
+  for (int c0 = 0; c0 < nchunks; c0 += kWave) {
+    const int c = c0 + lane;
+    const int v = c < nchunks ? counts[(int64_t)c * E + e] : 0;
+    int incl = v;
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+      const int u = __shfl_up(incl, o, kWave);
+      if (lane >= o) incl += u;
+    }
+    if (c < nchunks) base[(int64_t)c * E + e] = running + incl - v;
+    running += __shfl(incl, kWave - 1, kWave);
+  }
+  if (lane == 0) fill[e] = running < C ? running : C;
+}
+
+// Row kernels (dispatch copy, combine, dispatch backward) give each thread one
+// 16-byte column chunk of U tokens and issue every load of those tokens
+// before any store, so a thread keeps U * k row loads in flight.  KT is the
+// top-k as a constant (0: a runtime k up to kMaxK, with U = 1).
+
+// slot[t][r] = base[chunk][e] + rank (or -1 past the capacity), and
 // send_buf[e][slot][:] = x[t][:] for every kept (t, r).
-template <typename T>
+template <typename T, int KT, int U>
 __global__ __launch_bounds__(256) void dispatch_copy_kernel(const T* __restrict__ x, const int32_t* __restrict__ idx,
-                                                            const int32_t* __restrict__ slot, T* __restrict__ send,
-                                                            int64_t T_tokens, int d, int E, int k, int C) {
+                                                            const int32_t* __restrict__ rank,
+                                                            const int32_t* __restrict__ base,
+                                                            int32_t* __restrict__ slot, T* __restrict__ send,
+                                                            int64_t T_tokens, int d, int E, int kr, int C) {
   constexpr int V = Vec<T>::N;
+  constexpr int KK = KT > 0 ? KT : kMaxK;
+  const int k = KT > 0 ? KT : kr;
   const int nc = d / V;
   const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const int64_t t = gid / nc;
-  const int c = (int)(gid - t * nc);
-  if (t >= T_tokens) return;
-  const u32x4 v = *reinterpret_cast<const u32x4*>(x + t * d + (int64_t)c * V);
-  for (int r = 0; r < k; ++r) {
-    const int s = slot[t * k + r];
-    const int e = idx[t * k + r];
-    if (s >= 0 && s < C && e >= 0 && e < E) {
-      *reinterpret_cast<u32x4*>(send + eoff<T>(e, s, c * V, d, C)) = v;
+  const int64_t g = gid / nc;
+  const int c = (int)(gid - g * nc);
+  const int64_t t0 = g * U;
+  if (t0 >= T_tokens) return;
+  u32x4 v[U];
+  int er[U][KK], sr[U][KK];
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    const int64_t t = t0 + u;
+    const bool tok = t < T_tokens;
+    v[u] = tok ? *reinterpret_cast<const u32x4*>(x + t * d + (int64_t)c * V) : u32x4{0u, 0u, 0u, 0u};
+#pragma unroll
+    for (int r = 0; r < KK; ++r) {
+      er[u][r] = -1;
+      sr[u][r] = -1;
+      if (tok && r < k) {
+        const int e = idx[t * k + r];
+        const int rk = rank[t * k + r];
+        if (rk >= 0 && e >= 0 && e < E) {
+          const int sl = base[(t / kRouteChunk) * E + e] + rk;
+          if (sl < C) {
+            er[u][r] = e;
+            sr[u][r] = sl;
+          }
+        }
+        if (c == 0) slot[t * k + r] = sr[u][r];
+      }
     }
   }
+#pragma unroll
+  for (int u = 0; u < U; ++u)
+#pragma unroll
+    for (int r = 0; r < KK; ++r)
+      if (sr[u][r] >= 0) *reinterpret_cast<u32x4*>(send + eoff<T>(er[u][r], sr[u][r], c * V, d, C)) = v[u];
 }
+
+// Launch a row kernel F::kernel<T, KT, U> over T tokens: one thread per
+// (group of U tokens, 16-byte chunk).
+// U1 / U2: tokens per thread for top-1 / top-2.
+template <template <typename, int, int> class F, typename T, int U1, int U2, typename... Args>
+static void row_launch(const moe_cfg& c, hipStream_t s, Args... args) {
+  const int nc = c.d_model / Vec<T>::N;
+  auto go = [&](auto kern, int U) {
+    const int64_t n = (c.T + U - 1) / U * nc;
+    hipLaunchKernelGGL(kern, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, args...);
+  };
+  if (c.k == 1) go(F<T, 1, U1>::kernel(), U1);
+  else if (c.k == 2) go(F<T, 2, U2>::kernel(), U2);
+  else go(F<T, 0, 1>::kernel(), 1);
+}
+template <typename T, int KT, int U> struct DispatchCopy {
+  static constexpr auto kernel() { return dispatch_copy_kernel<T, KT, U>; }
+};
 
 size_t dispatch_ws_bytes(const moe_cfg& c) {
   const int64_t nch = (c.T + kRouteChunk - 1) / kRouteChunk;
-  return (size_t)(2 * nch * c.E) * sizeof(int32_t);
+  return (size_t)(2 * nch * c.E + c.T * c.k) * sizeof(int32_t);
 }
 
 void launch_dispatch(const moe_cfg& c, const void* x, const int32_t* idx, const int32_t* carry, int32_t* fill,
@@ -151,71 +212,97 @@ void launch_dispatch(const moe_cfg& c, const void* x, const int32_t* idx, const 
   const int64_t nch = (c.T + kRouteChunk - 1) / kRouteChunk;
   int32_t* counts = (int32_t*)ws;
   int32_t* base = counts + nch * c.E;
+  int32_t* rank = base + nch * c.E;
   if (nch > 0)
-    hipLaunchKernelGGL(route_count_kernel, dim3((unsigned)nch), dim3(kRouteChunk), 0, s, idx, counts, c.T, c.E, c.k);
-  hipLaunchKernelGGL(route_scan_kernel, dim3(1), dim3(256), 0, s, counts, base, carry, fill, (int)nch, c.E, c.C);
+    hipLaunchKernelGGL(route_rank_kernel, dim3((unsigned)nch), dim3(kRouteChunk), 0, s, idx, counts, rank, c.T, c.E,
+                       c.k);
+  if (c.E > 0)
+    hipLaunchKernelGGL(route_scan_kernel, dim3((unsigned)c.E), dim3(64), 0, s, counts, base, carry, fill, (int)nch, c.E,
+                       c.C);
   if (nch == 0) return;
-  hipLaunchKernelGGL(route_slots_kernel, dim3((unsigned)nch), dim3(kRouteChunk), 0, s, idx, base, slot, c.T, c.E,
-                     c.k, c.C);
-  if (c.dtype == MOE_BF16) {
-    const int64_t n = c.T * (c.d_model / 8);
-    hipLaunchKernelGGL(dispatch_copy_kernel<uint16_t>, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s,
-                       (const uint16_t*)x, idx, slot, (uint16_t*)send_buf, c.T, c.d_model, c.E, c.k, c.C);
-  } else {
-    const int64_t n = c.T * (c.d_model / 4);
-    hipLaunchKernelGGL(dispatch_copy_kernel<float>, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s,
-                       (const float*)x, idx, slot, (float*)send_buf, c.T, c.d_model, c.E, c.k, c.C);
-  }
+  if (c.dtype == MOE_BF16)
+    row_launch<DispatchCopy, uint16_t, 4, 2>(c, s, (const uint16_t*)x, idx, rank, base, slot, (uint16_t*)send_buf, c.T,
+                                       c.d_model, c.E, c.k, c.C);
+  else
+    row_launch<DispatchCopy, float, 4, 2>(c, s, (const float*)x, idx, rank, base, slot, (float*)send_buf, c.T, c.d_model,
+                                    c.E, c.k, c.C);
 }
 
 // -------------------------------------------------------------------- combine
 // y[t][:] = resid[t][:] + sum_r kept w[t][r] * O[e][s][:], in rank order, float
 // accumulation (resid NULL = 0; the block passes its residual stream).
-template <typename T>
+template <typename T, int KT, int U>
 __global__ __launch_bounds__(256) void combine_kernel(const T* __restrict__ O, const int32_t* __restrict__ idx,
                                                       const int32_t* __restrict__ slot, const float* __restrict__ w,
                                                       const T* __restrict__ resid, T* __restrict__ y, int64_t T_tokens,
-                                                      int d, int E, int k, int C) {
+                                                      int d, int E, int kr, int C) {
   constexpr int V = Vec<T>::N;
+  constexpr int KK = KT > 0 ? KT : kMaxK;
+  const int k = KT > 0 ? KT : kr;
   const int nc = d / V;
   const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const int64_t t = gid / nc;
-  const int c = (int)(gid - t * nc);
-  if (t >= T_tokens) return;
-  float acc[V];
-  if (resid) {
-    Vec<T>::load(resid + t * d + (int64_t)c * V, acc);
-  } else {
+  const int64_t g = gid / nc;
+  const int c = (int)(gid - g * nc);
+  const int64_t t0 = g * U;
+  if (t0 >= T_tokens) return;
+  int64_t off[U][KK];
+  float wr[U][KK];
 #pragma unroll
-    for (int i = 0; i < V; ++i) acc[i] = 0.f;
-  }
-  for (int r = 0; r < k; ++r) {
-    const int s = slot[t * k + r];
-    const int e = idx[t * k + r];
-    if (s >= 0 && s < C && e >= 0 && e < E) {
-      const float wr = w[t * k + r];
-      float v[V];
-      Vec<T>::load(O + eoff<T>(e, s, c * V, d, C), v);
+  for (int u = 0; u < U; ++u) {
+    const int64_t t = t0 + u;
 #pragma unroll
-      for (int i = 0; i < V; ++i) acc[i] = fmaf(wr, v[i], acc[i]);
+    for (int r = 0; r < KK; ++r) {
+      off[u][r] = -1;
+      wr[u][r] = 0.f;
+      if (t < T_tokens && r < k) {
+        const int sl = slot[t * k + r];
+        const int e = idx[t * k + r];
+        if (sl >= 0 && sl < C && e >= 0 && e < E) {
+          off[u][r] = erow<T>(e, sl, c * V, d, C);
+          wr[u][r] = w[t * k + r];
+        }
+      }
     }
   }
-  Vec<T>::store(y + t * d + (int64_t)c * V, acc);
+  float acc[U][V], v[U][KK][V];
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    const int64_t t = t0 + u;
+    if (resid && t < T_tokens) {
+      Vec<T>::load(resid + t * d + (int64_t)c * V, acc[u]);
+    } else {
+#pragma unroll
+      for (int i = 0; i < V; ++i) acc[u][i] = 0.f;
+    }
+#pragma unroll
+    for (int r = 0; r < KK; ++r)
+      if (off[u][r] >= 0) Vec<T>::load(O + off[u][r], v[u][r]);
+  }
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    const int64_t t = t0 + u;
+    if (t >= T_tokens) break;
+#pragma unroll
+    for (int r = 0; r < KK; ++r)
+      if (off[u][r] >= 0)
+#pragma unroll
+        for (int i = 0; i < V; ++i) acc[u][i] = fmaf(wr[u][r], v[u][r][i], acc[u][i]);
+    Vec<T>::store(y + t * d + (int64_t)c * V, acc[u]);
+  }
 }
+template <typename T, int KT, int U> struct Combine {
+  static constexpr auto kernel() { return combine_kernel<T, KT, U>; }
+};
 
 void launch_combine(const moe_cfg& c, const void* O, const int32_t* idx, const int32_t* slot, const float* w,
                     void* y, hipStream_t s, const void* resid) {
   if (c.T == 0) return;
-  if (c.dtype == MOE_BF16) {
-    const int64_t n = c.T * (c.d_model / 8);
-    hipLaunchKernelGGL(combine_kernel<uint16_t>, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s,
-                       (const uint16_t*)O, idx, slot, w, (const uint16_t*)resid, (uint16_t*)y, c.T, c.d_model, c.E,
-                       c.k, c.C);
-  } else {
-    const int64_t n = c.T * (c.d_model / 4);
-    hipLaunchKernelGGL(combine_kernel<float>, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s,
-                       (const float*)O, idx, slot, w, (const float*)resid, (float*)y, c.T, c.d_model, c.E, c.k, c.C);
-  }
+  if (c.dtype == MOE_BF16)
+    row_launch<Combine, uint16_t, 4, 2>(c, s, (const uint16_t*)O, idx, slot, w, (const uint16_t*)resid, (uint16_t*)y, c.T,
+                                  c.d_model, c.E, c.k, c.C);
+  else
+    row_launch<Combine, float, 4, 2>(c, s, (const float*)O, idx, slot, w, (const float*)resid, (float*)y, c.T, c.d_model,
+                               c.E, c.k, c.C);
 }
 
 // ------------------------------------------------------ combine + gate backward
@@ -249,15 +336,14 @@ __global__ __launch_bounds__(256) void combine_bwd_kernel(const float* __restric
 #pragma unroll
     for (int r = 0; r < kMaxK; ++r) {
       if (sr[r] >= 0) {
-        const int64_t off = eoff<T>(er[r], sr[r], c * V, d, C);
         float o[V], out[V];
-        Vec<T>::load(O + off, o);
+        Vec<T>::load(O + erow<T>(er[r], sr[r], c * V, d, C), o);
 #pragma unroll
         for (int i = 0; i < V; ++i) {
           gp[r] = fmaf(g[i], o[i], gp[r]);
           out[i] = wr[r] * g[i];
         }
-        Vec<T>::store(dO + off, out);
+        Vec<T>::store(dO + eoff<T>(er[r], sr[r], c * V, d, C), out);
       }
     }
   }
@@ -308,78 +394,119 @@ void launch_combine_bwd(const moe_cfg& c, const float* logits, const int32_t* id
 
 // ----------------------------------------------------------- dispatch backward
 // dx[t] = sum_r kept dXe[e][s] + sum_j dlogits[t][j] Wg[j]  (renorm: only the k selected j are nonzero).
-template <typename T>
+template <typename T, int KT, int U>
 __global__ __launch_bounds__(256) void dispatch_bwd_kernel(const T* __restrict__ Wg, const float* __restrict__ dl,
                                                            const int32_t* __restrict__ idx,
                                                            const int32_t* __restrict__ slot,
                                                            const T* __restrict__ dXe, T* __restrict__ dx,
-                                                           int64_t T_tokens, int d, int E, int k, int C, int renorm) {
+                                                           int64_t T_tokens, int d, int E, int kr, int C, int renorm) {
   constexpr int V = Vec<T>::N;
+  constexpr int KK = KT > 0 ? KT : kMaxK;
+  const int k = KT > 0 ? KT : kr;
   const int nc = d / V;
   const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const int64_t t = gid / nc;
-  const int c = (int)(gid - t * nc);
-  if (t >= T_tokens) return;
-  float acc[V];
+  const int64_t g = gid / nc;
+  const int c = (int)(gid - g * nc);
+  const int64_t t0 = g * U;
+  if (t0 >= T_tokens) return;
+  int64_t off[U][KK];
+  int ej[U][KK];      // renorm: the selected experts whose Wg rows enter dx
+  float aj[U][KK];
 #pragma unroll
-  for (int i = 0; i < V; ++i) acc[i] = 0.f;
-  for (int r = 0; r < k; ++r) {
-    const int s = slot[t * k + r];
-    const int e = idx[t * k + r];
-    if (s >= 0 && s < C && e >= 0 && e < E) {
-      float v[V];
-      Vec<T>::load(dXe + eoff<T>(e, s, c * V, d, C), v);
+  for (int u = 0; u < U; ++u) {
+    const int64_t t = t0 + u;
 #pragma unroll
-      for (int i = 0; i < V; ++i) acc[i] += v[i];
+    for (int r = 0; r < KK; ++r) {
+      off[u][r] = -1;
+      ej[u][r] = -1;
+      aj[u][r] = 0.f;
+      if (t < T_tokens && r < k) {
+        const int sl = slot[t * k + r];
+        const int e = idx[t * k + r];
+        const bool ev = e >= 0 && e < E;
+        if (sl >= 0 && sl < C && ev) off[u][r] = erow<T>(e, sl, c * V, d, C);
+        if (renorm && ev) {
+          ej[u][r] = e;
+          aj[u][r] = dl[t * E + e];
+        }
+      }
     }
   }
-  const int nj = renorm ? k : E;
-  for (int q = 0; q < nj; ++q) {
-    const int j = renorm ? idx[t * k + q] : q;
-    if (j < 0 || j >= E) continue;
-    const float a = dl[t * E + j];
-    float g[V];
-    Vec<T>::load(Wg + (int64_t)j * d + (int64_t)c * V, g);
+  float v[U][KK][V], gw[U][KK][V];
 #pragma unroll
-    for (int i = 0; i < V; ++i) acc[i] = fmaf(a, g[i], acc[i]);
+  for (int u = 0; u < U; ++u)
+#pragma unroll
+    for (int r = 0; r < KK; ++r) {
+      if (off[u][r] >= 0) Vec<T>::load(dXe + off[u][r], v[u][r]);
+      if (ej[u][r] >= 0) Vec<T>::load(Wg + (int64_t)ej[u][r] * d + (int64_t)c * V, gw[u][r]);
+    }
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    const int64_t t = t0 + u;
+    if (t >= T_tokens) break;
+    float acc[V];
+#pragma unroll
+    for (int i = 0; i < V; ++i) acc[i] = 0.f;
+#pragma unroll
+    for (int r = 0; r < KK; ++r)
+      if (off[u][r] >= 0)
+#pragma unroll
+        for (int i = 0; i < V; ++i) acc[i] += v[u][r][i];
+#pragma unroll
+    for (int r = 0; r < KK; ++r)
+      if (ej[u][r] >= 0)
+#pragma unroll
+        for (int i = 0; i < V; ++i) acc[i] = fmaf(aj[u][r], gw[u][r][i], acc[i]);
+    if (!renorm) {
+      for (int j = 0; j < E; ++j) {
+        const float a = dl[t * E + j];
+        float gv[V];
+        Vec<T>::load(Wg + (int64_t)j * d + (int64_t)c * V, gv);
+#pragma unroll
+        for (int i = 0; i < V; ++i) acc[i] = fmaf(a, gv[i], acc[i]);
+      }
+    }
+    Vec<T>::store(dx + t * d + (int64_t)c * V, acc);
   }
-  Vec<T>::store(dx + t * d + (int64_t)c * V, acc);
 }
+template <typename T, int KT, int U> struct DispatchBwd {
+  static constexpr auto kernel() { return dispatch_bwd_kernel<T, KT, U>; }
+};
 
 void launch_dispatch_bwd(const moe_cfg& c, const void* Wg, const float* dlogits, const int32_t* idx,
                          const int32_t* slot, const void* dXe, void* dx, hipStream_t s) {
   if (c.T == 0) return;
-  if (c.dtype == MOE_BF16) {
-    const int64_t n = c.T * (c.d_model / 8);
-    hipLaunchKernelGGL(dispatch_bwd_kernel<uint16_t>, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s,
-                       (const uint16_t*)Wg, dlogits, idx, slot, (const uint16_t*)dXe, (uint16_t*)dx, c.T,
-                       c.d_model, c.E, c.k, c.C, c.renorm);
-  } else {
-    const int64_t n = c.T * (c.d_model / 4);
-    hipLaunchKernelGGL(dispatch_bwd_kernel<float>, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s,
-                       (const float*)Wg, dlogits, idx, slot, (const float*)dXe, (float*)dx, c.T, c.d_model, c.E,
-                       c.k, c.C, c.renorm);
-  }
+  if (c.dtype == MOE_BF16)
+    row_launch<DispatchBwd, uint16_t, 2, 1>(c, s, (const uint16_t*)Wg, dlogits, idx, slot, (const uint16_t*)dXe,
+                                      (uint16_t*)dx, c.T, c.d_model, c.E, c.k, c.C, c.renorm);
+  else
+    row_launch<DispatchBwd, float, 2, 1>(c, s, (const float*)Wg, dlogits, idx, slot, (const float*)dXe, (float*)dx, c.T,
+                                   c.d_model, c.E, c.k, c.C, c.renorm);
 }
 
 // -------------------------------------------------------------------- dWg
 // dWg[e][:] = sum_t dlogits[t][e] x[t][:].  Stage 1: a block owns a slab of
-// 512 columns (each lane 8 consecutive columns, one 16-byte load per token),
-// a chunk of tokens and a group of up to 16 experts; its four waves take
-// every fourth token of the chunk, and their sums meet in LDS in wave order.
+// 256 columns (each lane 4 consecutive columns), a chunk of tokens and a
+// group of up to kDwgEG experts; its eight waves take every eighth token of
+// the chunk, and their sums meet in LDS in wave order.  A dlogits entry that
+// is zero (every unselected expert under renormalised top-k) skips its
+// products: the branch is uniform, since a wave works on one token at a time.
 // Stage 2 adds the chunk partials in chunk order.  Deterministic.
-constexpr int kDwgSlab = 512;     // columns per block
-constexpr int kDwgEG = 16;        // experts per block
+constexpr int kDwgCPL = 4;                 // columns per lane
+constexpr int kDwgSlab = 64 * kDwgCPL;     // columns per block
+constexpr int kDwgWaves = 8;
+constexpr int kDwgRound = 4;               // experts per LDS reduction round
 
 struct DwgPlan {
   int64_t tch, nch;
-  int slabs, egroups;
+  int slabs, egroups, eg;
 };
 static DwgPlan dwg_plan(const moe_cfg& c) {
   DwgPlan q;
+  q.eg = c.E <= 16 ? 16 : 32;
   q.slabs = (c.d_model + kDwgSlab - 1) / kDwgSlab;
-  q.egroups = (c.E + kDwgEG - 1) / kDwgEG;
-  // about 256 blocks over the chunks, at least 64 tokens per chunk
+  q.egroups = (c.E + q.eg - 1) / q.eg;
+  // about 256 blocks (two waves per SIMD) over the chunks, at least 64 tokens per chunk
   int64_t want = 256 / (q.slabs * q.egroups);
   if (want < 1) want = 1;
   int64_t tch = (c.T + want - 1) / want;
@@ -389,80 +516,123 @@ static DwgPlan dwg_plan(const moe_cfg& c) {
   return q;
 }
 
-template <typename T> __device__ __forceinline__ void load8(const T* p, float (&v)[8]);
-template <> __device__ __forceinline__ void load8<uint16_t>(const uint16_t* p, float (&v)[8]) { Vec<uint16_t>::load(p, v); }
-template <> __device__ __forceinline__ void load8<float>(const float* p, float (&v)[8]) {
-  float a[4], b[4];
-  Vec<float>::load(p, a);
-  Vec<float>::load(p + 4, b);
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    v[i] = a[i];
-    v[4 + i] = b[i];
-  }
+template <typename T> __device__ __forceinline__ void load4(const T* p, float (&v)[4]);
+template <> __device__ __forceinline__ void load4<uint16_t>(const uint16_t* p, float (&v)[4]) {
+  const u32x2 r = *reinterpret_cast<const u32x2*>(p);
+  v[0] = __uint_as_float(r[0] << 16);
+  v[1] = __uint_as_float(r[0] & 0xffff0000u);
+  v[2] = __uint_as_float(r[1] << 16);
+  v[3] = __uint_as_float(r[1] & 0xffff0000u);
 }
+template <> __device__ __forceinline__ void load4<float>(const float* p, float (&v)[4]) { Vec<float>::load(p, v); }
 
-template <typename T, int EG>
-__global__ __launch_bounds__(256) void dwg_partial_kernel(const T* __restrict__ x, const float* __restrict__ dl,
-                                                          float* __restrict__ part, int64_t T_tokens, int d, int E,
-                                                          int64_t tch) {
-  __shared__ float red[3][EG][kDwgSlab];
+// SPARSE: a wave reads each token's dlogits row with one vector load (lane j
+// holds expert j), and visits only the nonzero entries of its group (under
+// renormalised top-k, the k selected experts).  Otherwise every expert of the
+// group, with a uniform skip of zero entries.  Both orders are the same: per
+// expert, the wave's tokens in sequence.
+template <typename T, int EG, bool SPARSE>
+__global__ __launch_bounds__(64 * kDwgWaves) void dwg_partial_kernel(const T* __restrict__ x,
+                                                                     const float* __restrict__ dl,
+                                                                     float* __restrict__ part, int64_t T_tokens,
+                                                                     int d, int E, int64_t tch) {
+  constexpr int NW = kDwgWaves, CPL = kDwgCPL;
+  __shared__ float red[NW - 1][kDwgRound][kDwgSlab];
   const int lane = threadIdx.x & 63;
   const int wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int col = blockIdx.x * kDwgSlab + 8 * lane;
-  const int e0 = blockIdx.z * kDwgEG;
+  const int col = blockIdx.x * kDwgSlab + CPL * lane;
+  const int e0 = blockIdx.z * EG;
   const int64_t ch = blockIdx.y;
   const int64_t t_begin = ch * tch;
   const int64_t t_end = min(t_begin + tch, T_tokens);
-  float acc[EG][8];
+  float acc[EG][CPL];
 #pragma unroll
   for (int e = 0; e < EG; ++e)
 #pragma unroll
-    for (int j = 0; j < 8; ++j) acc[e][j] = 0.f;
+    for (int j = 0; j < CPL; ++j) acc[e][j] = 0.f;
   const bool colok = col < d;
-  constexpr int U = 4;   // tokens in flight per wave
-  for (int64_t t0 = t_begin + wid; t0 < t_end; t0 += 4 * U) {
-    float xv[U][8];
+  const bool full = (E % 4 == 0) && (e0 + EG <= E);   // whole group inside each dlogits row
+  const bool mine = lane >= e0 && lane < e0 + EG && lane < E;
+  constexpr int U = SPARSE ? 8 : 4;   // tokens in flight per wave
+  for (int64_t t0 = t_begin + wid; t0 < t_end; t0 += NW * U) {
+    float xv[U][CPL];
+    float gl[U];
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int64_t t = t0 + 4 * u;
-      if (colok && t < t_end) load8<T>(x + t * d + col, xv[u]);
-      else
-#pragma unroll
-        for (int j = 0; j < 8; ++j) xv[u][j] = 0.f;
+    for (int u = 0; u < U; ++u) {   // unconditional loads (clamped), so all U are in flight together
+      int64_t t = t0 + NW * u;
+      if (t >= t_end) t = t_end - 1;
+      load4<T>(x + t * d + (colok ? col : 0), xv[u]);
+      if constexpr (SPARSE) gl[u] = dl[t * E + (mine ? lane : 0)];
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const int64_t t = t0 + 4 * u;
-      const bool tok = t < t_end;
-      const float* dr = dl + (tok ? t : t_begin) * E + e0;
+      const int64_t t = t0 + NW * u;
+      if (t >= t_end) break;
+      if constexpr (SPARSE) {
+        uint64_t m = __ballot(mine && gl[u] != 0.f);
+        while (m) {
+          const int e = __ffsll((unsigned long long)m) - 1;
+          m &= m - 1;
+          const float g = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, gl[u]), e));
+          const int rel = e - e0;
 #pragma unroll
-      for (int e = 0; e < EG; ++e) {
-        const float g = (tok && e0 + e < E) ? dr[e] : 0.f;
+          for (int R = 0; R < EG; ++R) {   // uniform compare chain: acc indices stay static
+            if (rel == R) {
 #pragma unroll
-        for (int j = 0; j < 8; ++j) acc[e][j] = fmaf(g, xv[u][j], acc[e][j]);
+              for (int j = 0; j < CPL; ++j) acc[R][j] = fmaf(g, xv[u][j], acc[R][j]);
+            }
+          }
+        }
+      } else {
+        const float* dr = dl + t * E + e0;
+        float g[EG];
+        if (full) {   // the group's dlogits as 16-byte (scalar-cache) loads
+#pragma unroll
+          for (int q = 0; q < EG / 4; ++q) {
+            const f32x4 v = *reinterpret_cast<const f32x4*>(dr + 4 * q);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) g[4 * q + i] = v[i];
+          }
+        } else {
+#pragma unroll
+          for (int e = 0; e < EG; ++e) g[e] = (e0 + e < E) ? dr[e] : 0.f;
+        }
+#pragma unroll
+        for (int e = 0; e < EG; ++e) {
+          if (g[e] != 0.f) {
+#pragma unroll
+            for (int j = 0; j < CPL; ++j) acc[e][j] = fmaf(g[e], xv[u][j], acc[e][j]);
+          }
+        }
       }
     }
   }
-  // Block sum in wave order: waves 1..3 hand their sums to wave 0 through LDS.
-  if (wid > 0) {
+  // Block sum in wave order, kDwgRound experts per round through LDS.
+  float* out = part + (ch * E + e0) * (int64_t)d + col;
 #pragma unroll
-    for (int e = 0; e < EG; ++e)
+  for (int r0 = 0; r0 < EG; r0 += kDwgRound) {
+    if (wid > 0) {
 #pragma unroll
-      for (int j = 0; j < 8; ++j) red[wid - 1][e][8 * lane + j] = acc[e][j];
-  }
-  __syncthreads();
-  if (wid == 0 && colok) {
-    float* out = part + (ch * E + e0) * (int64_t)d + col;
+      for (int i = 0; i < kDwgRound; ++i)
 #pragma unroll
-    for (int e = 0; e < EG; ++e) {
-      if (e0 + e >= E) continue;
-      float v[8];
-#pragma unroll
-      for (int j = 0; j < 8; ++j) v[j] = ((acc[e][j] + red[0][e][8 * lane + j]) + red[1][e][8 * lane + j]) + red[2][e][8 * lane + j];
-      Vec<float>::store(out + (int64_t)e * d, v);
-      Vec<float>::store(out + (int64_t)e * d + 4, v + 4);
+        for (int j = 0; j < CPL; ++j) red[wid - 1][i][CPL * lane + j] = acc[r0 + i][j];
     }
+    __syncthreads();
+    if (wid == 0 && colok) {
+#pragma unroll
+      for (int i = 0; i < kDwgRound; ++i) {
+        if (e0 + r0 + i >= E) continue;
+        float v[CPL];
+#pragma unroll
+        for (int j = 0; j < CPL; ++j) {
+          v[j] = acc[r0 + i][j];
+#pragma unroll
+          for (int w = 0; w < NW - 1; ++w) v[j] += red[w][i][CPL * lane + j];
+        }
+        Vec<float>::store(out + (int64_t)(r0 + i) * d, v);
+      }
+    }
+    __syncthreads();
   }
 }
 
@@ -496,16 +666,22 @@ size_t bwd_dw_ws_bytes(const moe_cfg& c) {
   return (size_t)(q.nch * c.E * (int64_t)c.d_model) * sizeof(float);
 }
 
+template <typename T, int EG>
+static void launch_dwg_eg(const moe_cfg& c, const void* x, const float* dl, float* part, const DwgPlan& q,
+                          hipStream_t s) {
+  dim3 grid((unsigned)q.slabs, (unsigned)q.nch, (unsigned)q.egroups);
+  if (c.renorm)
+    hipLaunchKernelGGL((dwg_partial_kernel<T, EG, true>), grid, dim3(64 * kDwgWaves), 0, s, (const T*)x, dl, part,
+                       c.T, c.d_model, c.E, q.tch);
+  else
+    hipLaunchKernelGGL((dwg_partial_kernel<T, EG, false>), grid, dim3(64 * kDwgWaves), 0, s, (const T*)x, dl, part,
+                       c.T, c.d_model, c.E, q.tch);
+}
 template <typename T>
 static void launch_dwg_t(const moe_cfg& c, const void* x, const float* dl, float* part, const DwgPlan& q,
                          hipStream_t s) {
-  dim3 grid((unsigned)q.slabs, (unsigned)q.nch, (unsigned)q.egroups);
-  if (c.E <= 4)
-    hipLaunchKernelGGL((dwg_partial_kernel<T, 4>), grid, dim3(256), 0, s, (const T*)x, dl, part, c.T, c.d_model, c.E, q.tch);
-  else if (c.E <= 8)
-    hipLaunchKernelGGL((dwg_partial_kernel<T, 8>), grid, dim3(256), 0, s, (const T*)x, dl, part, c.T, c.d_model, c.E, q.tch);
-  else
-    hipLaunchKernelGGL((dwg_partial_kernel<T, 16>), grid, dim3(256), 0, s, (const T*)x, dl, part, c.T, c.d_model, c.E, q.tch);
+  if (q.eg == 16) launch_dwg_eg<T, 16>(c, x, dl, part, q, s);
+  else launch_dwg_eg<T, 32>(c, x, dl, part, q, s);
 }
 
 void launch_dwg(const moe_cfg& c, const void* x, const float* dlogits, float* dWg, void* ws, hipStream_t s) {

@@ -55,13 +55,19 @@ def host(t):
 EXPERT_X = {"send_buf": "d", "H": "f", "A": "f", "O": "d", "expert_out": "d", "dO": "d", "dH": "f", "dXe": "d"}
 
 
-def expert_host(t, cfg, X):
-    """An [E][C][X] expert buffer as a row-major numpy array (bf16 buffers are
-    stored in 16 x 32 blocks with C padded to a multiple of 16)."""
+ROW_MAJOR_BUFFERS = ("O", "expert_out", "dXe")   # product outputs only the gathers read
+
+
+def expert_host(t, cfg, X, blocked=True):
+    """An [E][C][X] expert buffer as a row-major numpy array (bf16 buffers
+    have C padded to a multiple of 16 and, if `blocked`, are stored in
+    16 x 32 blocks)."""
     a = host(t)
     E, C = cfg.E, cfg.C
     if cfg.dtype == 1:  # bf16
         Cp = (C + 15) // 16 * 16
+        if not blocked:
+            return a.reshape(E, Cp, X)[:, :C]
         return a.reshape(E, Cp // 16, X // 32, 16, 32).transpose(0, 1, 3, 2, 4).reshape(E, Cp, X)[:, :C]
     return a.reshape(E, C, X)
 
@@ -70,7 +76,7 @@ def ebuf(b, name):
     """Expert buffer `name` of LayerBuffers b, row-major [E][C][X]."""
     c = b.cfg
     X = c.d_model if EXPERT_X[name] == "d" else c.d_ff
-    return expert_host(getattr(b, name), c, X)
+    return expert_host(getattr(b, name), c, X, blocked=name not in ROW_MAJOR_BUFFERS)
 
 
 def kept_rows(buf, fill, lo=None):
