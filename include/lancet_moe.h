@@ -91,6 +91,9 @@ typedef struct {
   int32_t dtype;   /* moe_dtype */
   int32_t act;     /* moe_act */
   int32_t renorm;  /* 1: top-k weights renormalised over the selected experts; 0: w = softmax(l)[e] */
+  int32_t wpacked; /* 1: moe_bwd_dw writes dW1, dW2 in the packed layout of moe_pack_weights (a
+                      training loop that keeps the packed copies as its parameters updates them
+                      in place and never re-packs); 0: row-major [out][in] */
 } moe_cfg;
 
 /* Expert capacity C = ceil(k*T*cf_num / (E*cf_den)) in exact integer
@@ -191,7 +194,8 @@ moe_status moe_bwd_dx(const moe_cfg* cfg, const void* Wg, const float* logits, c
  *   dW2_e = dO_e^T A_e  [d][f],  dW1_e = dH_e^T X_e  [f][d]  over rows
  *   [row_begin_e, row_end_e) of the expert (X_e = send_buf rows); an expert
  *   with no rows gets exact zeros;  dWg = dlogits^T x  [E][d] float.
- *   dW1, dW2 dtype (float accumulation).  x [T][d] dtype.
+ *   dW1, dW2 dtype (float accumulation), row-major, or for cfg->wpacked = 1
+ *   and MOE_BF16 in the blocked layout of W1p, W2p.  x [T][d] dtype.
  *   ws: moe_workspace_bytes(cfg, MOE_CALL_BWD_DW) bytes. */
 moe_status moe_bwd_dw(const moe_cfg* cfg, const void* x, const float* dlogits,
                       const int32_t* row_begin, const int32_t* row_end, const void* send_buf,

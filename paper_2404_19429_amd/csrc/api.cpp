@@ -50,6 +50,7 @@ moe_status check_cfg(const moe_cfg* c, const char* fn, bool need_gemm_shape) {
   if (c->dtype != MOE_F32 && c->dtype != MOE_BF16) return fail(MOE_EDTYPE, "%s: unknown dtype %d", fn, c->dtype);
   if (c->act < MOE_ACT_IDENTITY || c->act > MOE_ACT_GELU_ERF) return fail(MOE_EINVAL, "%s: unknown act %d", fn, c->act);
   if (c->renorm != 0 && c->renorm != 1) return fail(MOE_EINVAL, "%s: renorm must be 0 or 1", fn);
+  if (c->wpacked != 0 && c->wpacked != 1) return fail(MOE_EINVAL, "%s: wpacked must be 0 or 1", fn);
   if (c->T < 0) return fail(MOE_EINVAL, "%s: T < 0", fn);
   if (c->T > (int64_t)1 << 31) return fail(MOE_ESHAPE, "%s: T > 2^31 unsupported", fn);
   if (c->E < 1 || c->E > lmoe::kMaxE) return fail(MOE_ESHAPE, "%s: E=%d outside 1..%d", fn, c->E, lmoe::kMaxE);

@@ -779,7 +779,7 @@ __device__ __forceinline__ void wide_epilogue(const GemmParams& p, const WGeo& G
   const uint16_t* Aux = EPI == EPI_DACT ? (const uint16_t*)p.Aux + cofs : nullptr;
   const int rl = lane & 15, cq = 4 * (lane >> 4);
   auto offset = [&](int row, int col) __attribute__((always_inline)) -> int64_t {
-    return CBLK ? blk_off(G.lo_al + row, col, p.ldc) : (int64_t)row * p.ldc + col;
+    return CBLK ? blk_off((RAGGED_K ? 0 : G.lo_al) + row, col, p.ldc) : (int64_t)row * p.ldc + col;
   };
 #pragma unroll
   for (int h = 0; h < 2; ++h) {          // two halves of four fragment rows
@@ -1465,11 +1465,17 @@ void launch_expert_bwd_dw(const moe_cfg& c, const void* X, const void* A, const 
                           const int32_t* rb, const int32_t* re, void* dW1, void* dW2, hipStream_t s) {
   const int64_t d = c.d_model, f = c.d_ff, C = c.C, Cp = rows_alloc(c);
   // dW2_e [d][f] = dO_e^T A_e : A-operand(m, k) = dO[e][k][m], B(k, n) = A[e][k][n]
+  // (wpacked: written in the blocked layout of the packed weights)
   GemmParams p2{dO, d, Cp * d, A, f, Cp * f, dW2, f, d * f, nullptr, nullptr, rb, re, (int)d, (int)f, 0, c.act, (int)C};
-  run_expert<false, true, EPI_STORE, false>(c, p2, d, (int)f, s);
   // dW1_e [f][d] = dH_e^T X_e
   GemmParams p1{dH, f, Cp * f, X, d, Cp * d, dW1, d, f * d, nullptr, nullptr, rb, re, (int)f, (int)d, 0, c.act, (int)C};
-  run_expert<false, true, EPI_STORE, false>(c, p1, f, (int)d, s);
+  if (c.wpacked && c.dtype == MOE_BF16) {
+    run_expert<false, true, EPI_STORE, true>(c, p2, d, (int)f, s);
+    run_expert<false, true, EPI_STORE, true>(c, p1, f, (int)d, s);
+  } else {
+    run_expert<false, true, EPI_STORE, false>(c, p2, d, (int)f, s);
+    run_expert<false, true, EPI_STORE, false>(c, p1, f, (int)d, s);
+  }
 }
 
 // Dense bf16 products of the transformer block (one group, every row, row-major).

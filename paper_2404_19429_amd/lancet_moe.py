@@ -41,7 +41,8 @@ class MoeError(RuntimeError):
 class moe_cfg(ctypes.Structure):
     _fields_ = [("T", ctypes.c_int64), ("d_model", ctypes.c_int32), ("d_ff", ctypes.c_int32),
                 ("E", ctypes.c_int32), ("k", ctypes.c_int32), ("C", ctypes.c_int32), ("G", ctypes.c_int32),
-                ("dtype", ctypes.c_int32), ("act", ctypes.c_int32), ("renorm", ctypes.c_int32)]
+                ("dtype", ctypes.c_int32), ("act", ctypes.c_int32), ("renorm", ctypes.c_int32),
+                ("wpacked", ctypes.c_int32)]
 
 
 class moe_block_cfg(ctypes.Structure):
@@ -99,10 +100,10 @@ _lib = _load()
 
 
 # ----------------------------------------------------------------------- helpers
-def make_cfg(T, d_model, d_ff, E, k, C, G=1, dtype="bf16", act="gelu_tanh", renorm=1) -> moe_cfg:
+def make_cfg(T, d_model, d_ff, E, k, C, G=1, dtype="bf16", act="gelu_tanh", renorm=1, wpacked=0) -> moe_cfg:
     dt = {"bf16": MOE_BF16, "f32": MOE_F32}[dtype] if isinstance(dtype, str) else int(dtype)
     return moe_cfg(int(T), int(d_model), int(d_ff), int(E), int(k), int(C), int(G), dt,
-                   ACTS[act] if isinstance(act, str) else int(act), int(renorm))
+                   ACTS[act] if isinstance(act, str) else int(act), int(renorm), int(wpacked))
 
 
 def torch_dtype(cfg: moe_cfg):

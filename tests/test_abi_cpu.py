@@ -206,3 +206,10 @@ def test_ffn_fwd_workspace_rule():
     c32 = _cfg(dtype="f32")
     assert L.moe_workspace_bytes(c32, L.MOE_CALL_FFN_FWD) == 0
     assert lib.moe_expert_ffn_fwd(ctypes.byref(c32), *([GOOD] * 8), None, 0, None) == L.MOE_EDEVICE
+
+
+def test_wpacked_flag_validation():
+    assert _gate(_cfg(wpacked=2)) == L.MOE_EINVAL
+    assert "wpacked" in L.moe_last_error()
+    assert _gate(_cfg(wpacked=1)) == L.MOE_EDEVICE   # valid; no GPU here
+    assert ctypes.sizeof(L.moe_cfg) == 48

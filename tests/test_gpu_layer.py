@@ -96,6 +96,28 @@ def test_layer_is_deterministic_and_dw_stream_independent(L):
                                       kept_rows(ebuf(b2, name), fill), err_msg=name)
 
 
+def _unpack_weights(t, E, R, X):
+    """[E][R][X] packed (16 x 32 blocks) bf16 matrices as row-major numpy."""
+    return host(t).reshape(E, R // 16, X // 32, 16, 32).transpose(0, 1, 3, 2, 4).reshape(E, R, X)
+
+
+def test_packed_weight_gradients_equal_row_major(L):
+    """wpacked = 1: dW1/dW2 are the same values as the row-major gradients,
+    bit for bit, stored in the blocked layout of the packed weights."""
+    spec = SMALL["bf16_zipf_T777_d128_f192_E16_drops"]
+    inp = layer_inputs(spec)
+    C = spec_C(spec)
+    b, dev = run_layer(L, spec, inp, C)
+    cfg = L.make_cfg(spec.T, spec.d, spec.f, spec.E, spec.k, C, spec.G, spec.dtype, spec.act, spec.renorm,
+                     wpacked=1)
+    dW1p, dW2p, dWg = torch.full_like(b.dW1, float("nan")), torch.full_like(b.dW2, float("nan")), b.dWg.clone()
+    L.moe_bwd_dw(cfg, dev["x"], b.dlogits, b.carry, b.fill, b.send_buf, b.A, b.dO, b.dH, dW1p, dW2p, dWg, b.ws_dw)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(_unpack_weights(dW1p, spec.E, spec.f, spec.d), host(b.dW1).reshape(spec.E, spec.f, spec.d))
+    np.testing.assert_array_equal(_unpack_weights(dW2p, spec.E, spec.d, spec.f), host(b.dW2).reshape(spec.E, spec.d, spec.f))
+    np.testing.assert_array_equal(host(dWg), host(b.dWg))
+
+
 def test_batch_partitions_with_capacity_carry_equal_unpartitioned(L):
     """Four batch partitions, each continuing from the capacity the previous ones
     used: routing and drops equal the unpartitioned layer (Sec. 2.3), the
