@@ -133,13 +133,17 @@ __device__ __forceinline__ float act_bwd(float h, int act) {
 
 // Compile-time activation for the bf16 GEMM epilogues, whose outputs are
 // rounded to bf16: GELU-tanh is evaluated as h * sigmoid(2u), the same function
-// as 0.5 h (1 + tanh u), with the hardware exponential (relative error ~1e-7).
+// as 0.5 h (1 + tanh u), with the hardware exponential and reciprocal
+// (v_exp_f32, v_rcp_f32: about 1 ulp each, far below the bf16 rounding of the
+// result; an IEEE division would cost about ten instructions per element).
+__device__ __forceinline__ float sigmoid_fast(float z) { return __builtin_amdgcn_rcpf(1.f + __expf(-z)); }
+
 template <int ACT>
 __device__ __forceinline__ float act_fwd_t(float h) {
   if constexpr (ACT == MOE_ACT_RELU) return h > 0.f ? h : 0.f;
   else if constexpr (ACT == MOE_ACT_GELU_TANH) {
     const float u2 = 1.5957691216057308f * (h + 0.044715f * h * h * h);  // 2u
-    return h / (1.f + __expf(-u2));
+    return h * sigmoid_fast(u2);
   } else if constexpr (ACT == MOE_ACT_GELU_ERF) return 0.5f * h * (1.f + erff(h * 0.7071067811865476f));
   else return h;
 }
@@ -150,7 +154,7 @@ __device__ __forceinline__ float act_bwd_t(float h) {
   else if constexpr (ACT == MOE_ACT_GELU_TANH) {
     // d/dh [h s(2u)] = s + 2 h s (1 - s) u',  u' = sqrt(2/pi) (1 + 3 * 0.044715 h^2)
     const float u2 = 1.5957691216057308f * (h + 0.044715f * h * h * h);
-    const float sg = 1.f / (1.f + __expf(-u2));
+    const float sg = sigmoid_fast(u2);
     const float du2 = 1.5957691216057308f * (1.f + 0.134145f * h * h);
     return sg + h * sg * (1.f - sg) * du2;
   } else if constexpr (ACT == MOE_ACT_GELU_ERF)

@@ -1058,7 +1058,12 @@ gemm_wide_kernel(GemmParams p, int tilesM, int tilesN, int groups) {
   // into (na, nb) and the refill of this step's stage interleaved between
   // them one instruction at a time, so the wave keeps issuing MFMAs while the
   // memory operations queue.
-  auto step = [&](u32x4 (&ca)[FM], u32x4 (&cb)[FN], u32x4 (&na)[FM], u32x4 (&nb)[FN]) __attribute__((always_inline)) {
+  // MMA false: a wave whose rows of the tile are all past the group's last
+  // row keeps its share of the loads and reads but issues no MFMAs, leaving
+  // the matrix core to the other wave on its SIMD.
+  auto step = [&](auto mmac, u32x4 (&ca)[FM], u32x4 (&cb)[FN], u32x4 (&na)[FM], u32x4 (&nb)[FN])
+                  __attribute__((always_inline)) {
+    constexpr bool MMA = decltype(mmac)::value;
     const uint16_t* st = lds + ((cs + 1) % STAGES) * STAGE;
     const bool more = cs + 1 < ls;
     if (more) {
@@ -1079,7 +1084,7 @@ gemm_wide_kernel(GemmParams p, int tilesM, int tilesN, int groups) {
     __builtin_amdgcn_sched_barrier(0);
     static_for<0, NMF>([&](auto mc) __attribute__((always_inline)) {
       constexpr int m = decltype(mc)::value;
-      mfma_acc(acc[m / FN][m % FN], cb[m % FN], ca[m / FN]);
+      if constexpr (MMA) mfma_acc(acc[m / FN][m % FN], cb[m % FN], ca[m / FN]);
       static_for<0, NRD>([&](auto rc) __attribute__((always_inline)) {
         constexpr int r = decltype(rc)::value;
         if constexpr ((r * RSPAN) / NRD == m) {
@@ -1142,14 +1147,14 @@ gemm_wide_kernel(GemmParams p, int tilesM, int tilesN, int groups) {
     }
   };
 
-  auto run_steps = [&](int n) __attribute__((always_inline)) {
+  auto run_steps_t = [&](int n, auto mmac) __attribute__((always_inline)) {
     int kk = 0;
     for (; kk + 2 <= n; kk += 2) {
-      step(fa0, fb0, fa1, fb1);
-      step(fa1, fb1, fa0, fb0);
+      step(mmac, fa0, fb0, fa1, fb1);
+      step(mmac, fa1, fb1, fa0, fb0);
     }
     if (kk < n) {   // odd step count: the next fragments are in set 1
-      step(fa0, fb0, fa1, fb1);
+      step(mmac, fa0, fb0, fa1, fb1);
 #pragma unroll
       for (int u = 0; u < FM; ++u) fa0[u] = fa1[u];
 #pragma unroll
@@ -1158,16 +1163,22 @@ gemm_wide_kernel(GemmParams p, int tilesM, int tilesN, int groups) {
       valu_to_mfma_fence(fb0);
     }
   };
+  auto run_steps = [&](int n, bool mma) __attribute__((always_inline)) {
+    if (mma) run_steps_t(n, std::true_type{});
+    else run_steps_t(n, std::false_type{});
+  };
   for (int e = 0; e < nseg; ++e) {
     int ct, k0, k1;
     seg(e, ct, k0, k1);
     const WGeo Cg = geo(ct);
+    // Ragged-M: does the wave hold any of the group's rows in this tile?
+    const bool mma = RAGGED_K || __builtin_amdgcn_readfirstlane((int)(Cg.m0 + wm * WTM < Cg.Mlim));
     if constexpr (SPLIT) {
-      run_steps(e < nd ? Cg.nk : k1 - k0);
+      run_steps(e < nd ? Cg.nk : k1 - k0, mma);
       if (e < nd) epilogue(Cg);
       else partial();
     } else {
-      run_steps(Cg.nk);
+      run_steps(Cg.nk, mma);
       epilogue(Cg);
     }
     zero_acc();
