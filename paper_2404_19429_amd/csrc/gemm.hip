@@ -680,6 +680,21 @@ struct WOp {
     }
     __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void*)(stage + (i * NW + wid) * 512), 16, vo, 0, 0, 0);
   }
+  // The same, branch-free, with the K-step's descriptor made once per step:
+  // with live false the descriptor is empty, so the load writes zeros into
+  // the stage (a stage no later step reads).
+  __device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(int kk, bool live) const {
+    const uint32_t adv = (uint32_t)kk * stride;
+    return __builtin_amdgcn_make_buffer_rsrc((void*)(base + adv), (short)0, live ? (int)(bytes - adv) : 0, kBufCfg);
+  }
+  __device__ __forceinline__ void issue_r(int i, __amdgpu_buffer_rsrc_t r, int kk, uint16_t* stage, int wid) const {
+    uint32_t vo = voff[i];
+    if constexpr (KCHK) {
+      const int k = kr[i] + 32 * kk;
+      if (k < klo || k >= khi) vo |= kOob;
+    }
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void*)(stage + (i * NW + wid) * 512), 16, vo, 0, 0, 0);
+  }
 };
 
 // Schedule of one XCD's tiles [T0, T0 + n) over its nslot blocks.  Rounds of
@@ -1065,6 +1080,13 @@ gemm_wide_kernel(GemmParams p, int tilesM, int tilesN, int groups) {
                   __attribute__((always_inline)) {
     constexpr bool MMA = decltype(mmac)::value;
     const uint16_t* st = lds + ((cs + 1) % STAGES) * STAGE;
+    // This step's refill: stage ls, K-step lk of the load cursor (issued
+    // unconditionally; past the block's last load it writes zeros into the
+    // stage of step cs, which no later step reads).
+    uint16_t* const dst = lds + (ls % STAGES) * STAGE;
+    const bool live = loads_left();
+    const int kdma = lk;
+    const __amdgpu_buffer_rsrc_t rsa = opA.rsrc(kdma, live), rsb = opB.rsrc(kdma, live);
     const bool more = cs + 1 < ls;
     if (more) {
       if (stores_pending) {
@@ -1105,7 +1127,8 @@ gemm_wide_kernel(GemmParams p, int tilesM, int tilesN, int groups) {
         constexpr int d = decltype(dc)::value;
         if constexpr ((d * NMF) / NDMA + 1 == m) {
           __builtin_amdgcn_sched_barrier(0);
-          issue_load(d);
+          if constexpr (d & 1) opB.issue_r(d >> 1, rsb, kdma, dst + kWB * BK, wid);
+          else opA.issue_r(d >> 1, rsa, kdma, dst, wid);
           __builtin_amdgcn_sched_barrier(0);
         }
       });
