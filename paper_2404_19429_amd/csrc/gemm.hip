@@ -788,13 +788,21 @@ __device__ __forceinline__ int wide_tile_prefix(const GemmParams& p, int lane, i
 template <int FM, int FN, int WTM, int WTN, bool RAGGED_K, int EPI, int ACT, bool CBLK>
 __device__ __forceinline__ void wide_epilogue(const GemmParams& p, const WGeo& G, f32x4 (&acc)[FM][FN], int wm,
                                               int wn, int lane, int i_lo = 0, int i_hi = FM) {
+  // Buffer stores and loads over the group's output: a lane outside the
+  // product carries an out-of-range offset (store dropped, load zero), so
+  // the epilogue is branch-free and dA * act'(H) issues all of a half's H
+  // loads together.  Group offsets fit 31 bits (validated on the host).
   const int64_t cofs = (int64_t)G.g * p.sC + (RAGGED_K || CBLK ? 0 : (int64_t)G.lo_al * p.ldc);
-  uint16_t* C = (uint16_t*)p.C + cofs;
-  uint16_t* C2 = EPI == EPI_FWD1 ? (uint16_t*)p.C2 + cofs : nullptr;
-  const uint16_t* Aux = EPI == EPI_DACT ? (const uint16_t*)p.Aux + cofs : nullptr;
+  const __amdgpu_buffer_rsrc_t rC = __builtin_amdgcn_make_buffer_rsrc((uint16_t*)p.C + cofs, (short)0, 0x7fffffff, kBufCfg);
+  __amdgpu_buffer_rsrc_t rC2 = rC, rAux = rC;
+  if constexpr (EPI == EPI_FWD1)
+    rC2 = __builtin_amdgcn_make_buffer_rsrc((uint16_t*)p.C2 + cofs, (short)0, 0x7fffffff, kBufCfg);
+  if constexpr (EPI == EPI_DACT)
+    rAux = __builtin_amdgcn_make_buffer_rsrc((uint16_t*)p.Aux + cofs, (short)0, 0x7fffffff, kBufCfg);
   const int rl = lane & 15, cq = 4 * (lane >> 4);
-  auto offset = [&](int row, int col) __attribute__((always_inline)) -> int64_t {
-    return CBLK ? blk_off((RAGGED_K ? 0 : G.lo_al) + row, col, p.ldc) : (int64_t)row * p.ldc + col;
+  auto voff = [&](bool ok, int row, int col) __attribute__((always_inline)) -> uint32_t {
+    const int64_t e = CBLK ? blk_off((RAGGED_K ? 0 : G.lo_al) + row, col, p.ldc) : (int64_t)row * p.ldc + col;
+    return ok ? (uint32_t)(e * 2) : kOob;
   };
 #pragma unroll
   for (int h = 0; h < 2; ++h) {          // two halves of four fragment rows
@@ -807,7 +815,7 @@ __device__ __forceinline__ void wide_epilogue(const GemmParams& p, const WGeo& G
 #pragma unroll
         for (int j = 0; j < FN; ++j) {
           const int col = G.n0 + wn * WTN + 16 * j + cq;
-          aux[ii][j] = (rok && col < p.N) ? *reinterpret_cast<const u32x2*>(Aux + offset(row, col)) : u32x2{0u, 0u};
+          aux[ii][j] = __builtin_amdgcn_raw_buffer_load_b64(rAux, (int)voff(rok && col < p.N, row, col), 0, 0);
         }
       }
     }
@@ -820,23 +828,22 @@ __device__ __forceinline__ void wide_epilogue(const GemmParams& p, const WGeo& G
 #pragma unroll
       for (int j = 0; j < FN; ++j) {
         const int col = G.n0 + wn * WTN + 16 * j + cq;
-        if (!(rok && col < p.N)) continue;
-        const int64_t off = offset(row, col);
+        const int vo = (int)voff(rok && col < p.N, row, col);
         float v[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
         if constexpr (EPI == EPI_FWD1) {
-          *reinterpret_cast<u32x2*>(C + off) = pack4_bf16(v);
+          __builtin_amdgcn_raw_buffer_store_b64(pack4_bf16(v), rC, vo, 0, 0);
 #pragma unroll
           for (int u = 0; u < 4; ++u) v[u] = act_fwd_t<ACT>(v[u]);
-          *reinterpret_cast<u32x2*>(C2 + off) = pack4_bf16(v);
+          __builtin_amdgcn_raw_buffer_store_b64(pack4_bf16(v), rC2, vo, 0, 0);
         } else if constexpr (EPI == EPI_DACT) {
           const u32x2 hv = aux[ii][j];
           const float hh[4] = {__uint_as_float(hv[0] << 16), __uint_as_float(hv[0] & 0xffff0000u),
                                __uint_as_float(hv[1] << 16), __uint_as_float(hv[1] & 0xffff0000u)};
 #pragma unroll
           for (int u = 0; u < 4; ++u) v[u] *= act_bwd_t<ACT>(hh[u]);
-          *reinterpret_cast<u32x2*>(C + off) = pack4_bf16(v);
+          __builtin_amdgcn_raw_buffer_store_b64(pack4_bf16(v), rC, vo, 0, 0);
         } else {
-          *reinterpret_cast<u32x2*>(C + off) = pack4_bf16(v);
+          __builtin_amdgcn_raw_buffer_store_b64(pack4_bf16(v), rC, vo, 0, 0);
         }
       }
     }
@@ -936,7 +943,7 @@ gemm_wide_kernel(GemmParams p, int tilesM, int tilesN, int groups) {
   // Load q (0 .. 2 kWNI - 1; even: A, odd: B) of the next stage.
   auto issue_load = [&](int q) __attribute__((always_inline)) {
     if (!loads_left()) return;
-    uint16_t* st = lds + (ls % STAGES) * STAGE;
+    uint16_t* st = lds + ((unsigned)ls % STAGES) * STAGE;
     if (q & 1) opB.issue(q >> 1, lk, st + kWB * BK, wid);
     else opA.issue(q >> 1, lk, st, wid);
   };
@@ -1039,6 +1046,8 @@ gemm_wide_kernel(GemmParams p, int tilesM, int tilesN, int groups) {
   zero_acc();
 
   int cs = 0;                // compute steps done (over all of the block's tiles)
+  // The first step after an epilogue drains every store before its barrier
+  // (measured faster than letting the stores overlap the next tile's loads).
   bool stores_pending = false;
   // One K-step: multiply the fragments in (ca, cb) while the next stage's
   // loads are issued and its fragments read into (na, nb).
@@ -1079,11 +1088,11 @@ gemm_wide_kernel(GemmParams p, int tilesM, int tilesN, int groups) {
   auto step = [&](auto mmac, u32x4 (&ca)[FM], u32x4 (&cb)[FN], u32x4 (&na)[FM], u32x4 (&nb)[FN])
                   __attribute__((always_inline)) {
     constexpr bool MMA = decltype(mmac)::value;
-    const uint16_t* st = lds + ((cs + 1) % STAGES) * STAGE;
+    const uint16_t* st = lds + ((unsigned)(cs + 1) % STAGES) * STAGE;
     // This step's refill: stage ls, K-step lk of the load cursor (issued
     // unconditionally; past the block's last load it writes zeros into the
     // stage of step cs, which no later step reads).
-    uint16_t* const dst = lds + (ls % STAGES) * STAGE;
+    uint16_t* const dst = lds + ((unsigned)ls % STAGES) * STAGE;
     const bool live = loads_left();
     const int kdma = lk;
     const __amdgpu_buffer_rsrc_t rsa = opA.rsrc(kdma, live), rsb = opB.rsrc(kdma, live);
