@@ -751,7 +751,7 @@ __device__ __forceinline__ WGeo wide_geo(const GemmParams& p, int t, int lane, i
   G.n0 = (pnl * kPanelN + rem % pw) * kWB;
   G.Mlim = RAGGED_K ? p.M : span;
   G.Klim = RAGGED_K ? span : p.K;
-  G.nk = max(1, (G.Klim + kBKb - 1) / kBKb);   // an empty ragged-K group runs one all-zero step
+  G.nk = max(1, (G.Klim + kBKb - 1) / kBKb);
   return G;
 }
 
@@ -763,7 +763,9 @@ __device__ __forceinline__ int wide_tile_prefix(const GemmParams& p, int lane, i
   int cnt = 0;
   if (lane < groups) {
     if constexpr (RAGGED_K) {
-      cnt = tilesM * tilesN;
+      int lo, span;
+      group_rows(p, lane, lo, span);
+      cnt = span > 0 ? tilesM * tilesN : 0;   // an empty group's product is zeroed by zero_empty_groups_kernel
     } else {
       int lo, span;
       group_rows(p, lane, lo, span);
@@ -881,16 +883,24 @@ gemm_wide_kernel(GemmParams p, int tilesM, int tilesN, int groups) {
   const int nslot = gridDim.x / 8;
   const int xcd = blockIdx.x % 8, slot = blockIdx.x / 8;
   const int per = (total + 7) / 8;
-  // The block's segments (see WSched): nd whole tiles T0 + e nslot + slot,
+  // The XCD's tiles: ragged-M products (one K length, equal tiles) take a
+  // contiguous range, so the XCD's L2 holds neighbouring operand panels;
+  // ragged-K products, whose tiles cost as many K-steps as their group has
+  // rows, take every eighth tile, so each XCD gets an even share of every
+  // group (with skewed routing, a contiguous range could hold the few large
+  // groups).  xtile(j) = the XCD's j-th tile.
+  // The block's segments (see WSched): nd whole tiles xtile(e nslot + slot),
   // then, if the last round is K-split (ragged-M products, one K length), the
-  // K range [sk0, sk1) of remainder tile T0 + R nslot + sq.
-  const int T0 = xcd * per, T1 = min(total, (xcd + 1) * per);
+  // K range [sk0, sk1) of remainder tile xtile(R nslot + sq).
+  const int T0 = RAGGED_K ? 0 : xcd * per;
+  const int nx = RAGGED_K ? (total > xcd ? (total - xcd + 7) / 8 : 0) : max(min(total, (xcd + 1) * per) - T0, 0);
+  auto xtile = [&](int j) __attribute__((always_inline)) { return RAGGED_K ? xcd + 8 * j : T0 + j; };
   const int nkU = (p.K + BK - 1) / BK;
   // Only the plain-store ragged-M products may K-split their last round (the
   // narrow-N products where a ragged last round idles most of the GPU); the
   // others keep the simpler whole-tile schedule and its register budget.
   constexpr bool SPLIT = !RAGGED_K && EPI == EPI_STORE;
-  const WSched W = wide_sched(max(T1 - T0, 0), nslot, SPLIT);
+  const WSched W = wide_sched(nx, nslot, SPLIT);
   int sq = 0, sfirst = 0, scnt = 0, sk0 = 0, sk1 = 0;
   if (SPLIT && W.split) W.split_part(slot, nslot, nkU, sq, sfirst, scnt, sk0, sk1);
   // (uniform values: keep them in scalar registers)
@@ -909,11 +919,11 @@ gemm_wide_kernel(GemmParams p, int tilesM, int tilesN, int groups) {
   // Segment e: tile, first K-step, end K-step (0 = the tile's own count).
   auto seg = [&](int e, int& t, int& k0, int& k1) __attribute__((always_inline)) {
     if (e < nd) {
-      t = T0 + e * nslot + slot;
+      t = xtile(e * nslot + slot);
       k0 = 0;
       k1 = 0;
     } else {
-      t = T0 + WR * nslot + sq;
+      t = xtile(WR * nslot + sq);
       k0 = sk0;
       k1 = sk1;
     }
@@ -1504,6 +1514,24 @@ void launch_expert_bwd_dx(const moe_cfg& c, const void* dO, const int32_t* rb, c
   run_expert<false, false, EPI_STORE, false>(c, p2, C, (int)d, s);   // dXe row-major
 }
 
+// Zeroes the per-group outputs ([per_group] elements each) of the groups with
+// no rows, whose tiles the ragged-K schedule leaves out: 16-byte stores.
+__global__ __launch_bounds__(256) void zero_empty_groups_kernel(uint16_t* __restrict__ out, int64_t per_group,
+                                                                const int32_t* __restrict__ rb,
+                                                                const int32_t* __restrict__ re, int cap) {
+  GemmParams q{};
+  q.rb = rb;
+  q.re = re;
+  q.cap = cap;
+  int lo, span;
+  group_rows(q, blockIdx.y, lo, span);
+  if (span > 0) return;
+  u32x4* base = reinterpret_cast<u32x4*>(out + (int64_t)blockIdx.y * per_group);
+  const int64_t n = per_group / 8;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
+    base[i] = u32x4{0u, 0u, 0u, 0u};
+}
+
 void launch_expert_bwd_dw(const moe_cfg& c, const void* X, const void* A, const void* dO, const void* dH,
                           const int32_t* rb, const int32_t* re, void* dW1, void* dW2, hipStream_t s) {
   const int64_t d = c.d_model, f = c.d_ff, C = c.C, Cp = rows_alloc(c);
@@ -1512,6 +1540,12 @@ void launch_expert_bwd_dw(const moe_cfg& c, const void* X, const void* A, const 
   GemmParams p2{dO, d, Cp * d, A, f, Cp * f, dW2, f, d * f, nullptr, nullptr, rb, re, (int)d, (int)f, 0, c.act, (int)C};
   // dW1_e [f][d] = dH_e^T X_e
   GemmParams p1{dH, f, Cp * f, X, d, Cp * d, dW1, d, f * d, nullptr, nullptr, rb, re, (int)f, (int)d, 0, c.act, (int)C};
+  if (c.dtype == MOE_BF16 && c.E > 0) {   // groups without rows: zeros, outside the products' schedule
+    hipLaunchKernelGGL(zero_empty_groups_kernel, dim3(64, (unsigned)c.E), dim3(256), 0, s, (uint16_t*)dW2, d * f, rb,
+                       re, (int)C);
+    hipLaunchKernelGGL(zero_empty_groups_kernel, dim3(64, (unsigned)c.E), dim3(256), 0, s, (uint16_t*)dW1, f * d, rb,
+                       re, (int)C);
+  }
   if (c.wpacked && c.dtype == MOE_BF16) {
     run_expert<false, true, EPI_STORE, true>(c, p2, d, (int)f, s);
     run_expert<false, true, EPI_STORE, true>(c, p1, f, (int)d, s);

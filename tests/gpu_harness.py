@@ -87,7 +87,8 @@ def kept_rows(buf, fill, lo=None):
 
 
 def nan_fill(b):
-    for name in ("send_buf", "H", "A", "O", "dO", "dH", "dXe"):
+    """Poison every output, so a value a kernel fails to write shows up."""
+    for name in ("send_buf", "H", "A", "O", "dO", "dH", "dXe", "dW1", "dW2", "dWg"):
         getattr(b, name).fill_(float("nan"))
 
 

@@ -250,6 +250,9 @@ def _sampled_full(L, n, n_tok=40, seed=0):
         for c in rng.choice(spec.f, size=3, replace=False):
             ref = O.expert_dw2_col(X, dO, inp["W1"][e], spec.act, int(c))
             assert_close(f"dW2[{e}][:, {c}]", host(dW2[e, :, int(c)]), ref, tol)
+    # experts that received no rows: exact-zero weight gradients (written by their own fill)
+    for e in [e for e in range(spec.E) if fill[e] == 0][:8]:
+        assert torch.count_nonzero(dW1[e]).item() == 0 and torch.count_nonzero(dW2[e]).item() == 0, e
     # dWg is the product dlogits^T x of the kernel's own dlogits (checked above on samples)
     dWg_ref = host(b.dlogits).astype(np.float64).T @ x.astype(np.float64)
     assert_close("dWg (= dlogits^T x)", host(b.dWg), dWg_ref, 1e-5)
