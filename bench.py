@@ -331,7 +331,8 @@ def main():
         "config": {"workload": spec.name, "T": T, "d_model": d, "d_ff": f, "E": spec.E, "k": spec.k,
                    "C": C, "capacity_factor": f"{spec.cf_num}/{spec.cf_den}", "act": spec.act,
                    "kept_rows": N, "parallelism": "single GPU (one GPU's share; all-to-all not run)"},
-        "roofline": {"kernel": "expert FFN forward: 2 grouped bf16 MFMA GEMMs (gemm_bf16_kernel FWD1 + FWD2)",
+        "roofline": {"kernel": "expert FFN forward: grouped bf16 MFMA GEMMs gemm_wide_kernel FWD1 + FWD2 "
+                               "(+ the K-split fix-up launch)",
                      "bound": "mfma", "achieved": achieved_tflops, "peak": MI355X_PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": achieved_tflops / MI355X_PEAK_BF16_TFLOPS,
                      "traffic": measured_traffic(spec.name)},
