@@ -9,6 +9,8 @@
 // makes batch partitions exact), and a final pass that adds the chunk base to
 // each rank, applies the capacity and copies the kept rows with 16-byte
 // vector accesses, one thread per (token, 16-byte column chunk).
+#include <type_traits>
+
 #include "internal.h"
 
 namespace lmoe {
@@ -137,7 +139,7 @@ __global__ __launch_bounds__(64) void route_scan_kernel(const int32_t* __restric
 
 // slot[t][r] = base[chunk][e] + rank (or -1 past the capacity), and
 // send_buf[e][slot][:] = x[t][:] for every kept (t, r).
-template <typename T, int KT, int U>
+template <typename T, int KT, int U, bool UNI>
 __global__ __launch_bounds__(256) void dispatch_copy_kernel(const T* __restrict__ x, const int32_t* __restrict__ idx,
                                                             const int32_t* __restrict__ rank,
                                                             const int32_t* __restrict__ base,
@@ -148,7 +150,7 @@ __global__ __launch_bounds__(256) void dispatch_copy_kernel(const T* __restrict_
   const int k = KT > 0 ? KT : kr;
   const int nc = d / V;
   const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const int64_t g = gid / nc;
+  const int64_t g = UNI ? (int64_t)__builtin_amdgcn_readfirstlane((int)(gid / nc)) : gid / nc;
   const int c = (int)(gid - g * nc);
   const int64_t t0 = g * U;
   if (t0 >= T_tokens) return;
@@ -186,20 +188,29 @@ __global__ __launch_bounds__(256) void dispatch_copy_kernel(const T* __restrict_
 
 // Launch a row kernel F::kernel<T, KT, U> over T tokens: one thread per
 // (group of U tokens, 16-byte chunk).
-// U1 / U2: tokens per thread for top-1 / top-2.
-template <template <typename, int, int> class F, typename T, int U1, int U2, typename... Args>
+// U1 / U2: tokens per thread for top-1 / top-2.  When a row is a multiple of
+// 64 chunks, every lane of a wave works on the same tokens: the token index
+// is made wave-uniform (UNI), so the tokens' idx / slot / w come through
+// scalar loads.
+template <template <typename, int, int, bool> class F, typename T, int U1, int U2, typename... Args>
 static void row_launch(const moe_cfg& c, hipStream_t s, Args... args) {
   const int nc = c.d_model / Vec<T>::N;
   auto go = [&](auto kern, int U) {
     const int64_t n = (c.T + U - 1) / U * nc;
     hipLaunchKernelGGL(kern, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, args...);
   };
-  if (c.k == 1) go(F<T, 1, U1>::kernel(), U1);
-  else if (c.k == 2) go(F<T, 2, U2>::kernel(), U2);
-  else go(F<T, 0, 1>::kernel(), 1);
+  const bool uni = nc % kWave == 0 && c.T < ((int64_t)1 << 30);
+  auto pick = [&](auto ucst) {
+    constexpr bool UNI = decltype(ucst)::value;
+    if (c.k == 1) go(F<T, 1, U1, UNI>::kernel(), U1);
+    else if (c.k == 2) go(F<T, 2, U2, UNI>::kernel(), U2);
+    else go(F<T, 0, 1, UNI>::kernel(), 1);
+  };
+  if (uni) pick(std::true_type{});
+  else pick(std::false_type{});
 }
-template <typename T, int KT, int U> struct DispatchCopy {
-  static constexpr auto kernel() { return dispatch_copy_kernel<T, KT, U>; }
+template <typename T, int KT, int U, bool UNI> struct DispatchCopy {
+  static constexpr auto kernel() { return dispatch_copy_kernel<T, KT, U, UNI>; }
 };
 
 size_t dispatch_ws_bytes(const moe_cfg& c) {
@@ -231,7 +242,7 @@ void launch_dispatch(const moe_cfg& c, const void* x, const int32_t* idx, const 
 // -------------------------------------------------------------------- combine
 // y[t][:] = resid[t][:] + sum_r kept w[t][r] * O[e][s][:], in rank order, float
 // accumulation (resid NULL = 0; the block passes its residual stream).
-template <typename T, int KT, int U>
+template <typename T, int KT, int U, bool UNI>
 __global__ __launch_bounds__(256) void combine_kernel(const T* __restrict__ O, const int32_t* __restrict__ idx,
                                                       const int32_t* __restrict__ slot, const float* __restrict__ w,
                                                       const T* __restrict__ resid, T* __restrict__ y, int64_t T_tokens,
@@ -241,7 +252,7 @@ __global__ __launch_bounds__(256) void combine_kernel(const T* __restrict__ O, c
   const int k = KT > 0 ? KT : kr;
   const int nc = d / V;
   const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const int64_t g = gid / nc;
+  const int64_t g = UNI ? (int64_t)__builtin_amdgcn_readfirstlane((int)(gid / nc)) : gid / nc;
   const int c = (int)(gid - g * nc);
   const int64_t t0 = g * U;
   if (t0 >= T_tokens) return;
@@ -290,8 +301,8 @@ __global__ __launch_bounds__(256) void combine_kernel(const T* __restrict__ O, c
     Vec<T>::store(y + t * d + (int64_t)c * V, acc[u]);
   }
 }
-template <typename T, int KT, int U> struct Combine {
-  static constexpr auto kernel() { return combine_kernel<T, KT, U>; }
+template <typename T, int KT, int U, bool UNI> struct Combine {
+  static constexpr auto kernel() { return combine_kernel<T, KT, U, UNI>; }
 };
 
 void launch_combine(const moe_cfg& c, const void* O, const int32_t* idx, const int32_t* slot, const float* w,
@@ -394,7 +405,7 @@ void launch_combine_bwd(const moe_cfg& c, const float* logits, const int32_t* id
 
 // ----------------------------------------------------------- dispatch backward
 // dx[t] = sum_r kept dXe[e][s] + sum_j dlogits[t][j] Wg[j]  (renorm: only the k selected j are nonzero).
-template <typename T, int KT, int U>
+template <typename T, int KT, int U, bool UNI>
 __global__ __launch_bounds__(256) void dispatch_bwd_kernel(const T* __restrict__ Wg, const float* __restrict__ dl,
                                                            const int32_t* __restrict__ idx,
                                                            const int32_t* __restrict__ slot,
@@ -405,7 +416,7 @@ __global__ __launch_bounds__(256) void dispatch_bwd_kernel(const T* __restrict__
   const int k = KT > 0 ? KT : kr;
   const int nc = d / V;
   const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const int64_t g = gid / nc;
+  const int64_t g = UNI ? (int64_t)__builtin_amdgcn_readfirstlane((int)(gid / nc)) : gid / nc;
   const int c = (int)(gid - g * nc);
   const int64_t t0 = g * U;
   if (t0 >= T_tokens) return;
@@ -469,8 +480,8 @@ __global__ __launch_bounds__(256) void dispatch_bwd_kernel(const T* __restrict__
     Vec<T>::store(dx + t * d + (int64_t)c * V, acc);
   }
 }
-template <typename T, int KT, int U> struct DispatchBwd {
-  static constexpr auto kernel() { return dispatch_bwd_kernel<T, KT, U>; }
+template <typename T, int KT, int U, bool UNI> struct DispatchBwd {
+  static constexpr auto kernel() { return dispatch_bwd_kernel<T, KT, U, UNI>; }
 };
 
 void launch_dispatch_bwd(const moe_cfg& c, const void* Wg, const float* dlogits, const int32_t* idx,
