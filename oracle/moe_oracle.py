@@ -30,7 +30,13 @@ Readings of points the paper leaves open (each also listed in the design doc):
   (NaN here) and never read;
 * no gradient flows through the top-k choice or the capacity rule, only
   through the weights; there is no auxiliary loss;
-* the loss is ``L = sum_t <dy_t, y_t>`` for a given upstream gradient dy.
+* the loss is ``L = sum_t <dy_t, y_t>`` for a given upstream gradient dy;
+* Batch-prioritized Routing (named in Sec. 2.3 as a gate that decides over
+  the whole batch): a token's importance is the sum of the softmax
+  probabilities of its k selected experts (over all E, not renormalised),
+  evaluated in float64 and rounded once to float32; tokens are visited by
+  importance descending, equal importance in token order, each token's
+  choices in rank order, under the same capacity rule.
 
 Parity pins for every function live in tests/test_oracle_*.py (not gpu).
 """
@@ -42,7 +48,8 @@ import numpy as np
 
 __all__ = [
     "capacity", "gate_logits", "topk_route", "softmax", "gate_weights",
-    "assign_slots", "assign_slots_direct_microbatch", "dispatch", "send_counts",
+    "assign_slots", "assign_slots_direct_microbatch", "bpr_importance", "bpr_order",
+    "assign_slots_bpr", "dispatch", "send_counts",
     "act", "act_grad", "expert_ffn", "combine",
     "combine_bwd", "expert_bwd_dx", "expert_bwd_dw", "dispatch_bwd", "gate_bwd",
     "layer_forward", "layer_backward", "expert_row_forward", "expert_row_backward",
@@ -145,6 +152,44 @@ def dispatch(x: np.ndarray, idx: np.ndarray, slot: np.ndarray, E: int, C: int) -
             if s >= 0:
                 buf[int(idx[t, r]), s] = x[t]
     return buf
+
+
+# ------------------------------------------------------- batch-prioritized routing
+def bpr_importance(logits32: np.ndarray, idx: np.ndarray) -> np.ndarray:
+    """Importance score of each token for Batch-prioritized Routing (Sec. 2.3,
+    "Opportunities and Challenges", the gating methods that decide over the
+    whole batch): the sum of the token's k largest gating scores, i.e. of the
+    softmax probabilities (over all E experts) of its selected experts, not
+    renormalised.  Evaluated in float64 from the float32 logits and rounded
+    once to float32: the ordering decision is taken on these float32 values."""
+    p = softmax(np.asarray(logits32).astype(F64))
+    sel = np.take_along_axis(p, np.asarray(idx, np.int64), axis=1)
+    imp = np.zeros(sel.shape[0], F64)
+    for r in range(sel.shape[1]):       # rank order
+        imp = imp + sel[:, r]
+    return imp.astype(np.float32)
+
+
+def bpr_order(importance32: np.ndarray) -> np.ndarray:
+    """Order in which Batch-prioritized Routing visits the tokens: importance
+    descending; equal importance keeps token order (a stable sort)."""
+    imp = np.asarray(importance32, np.float32).astype(F64)
+    return np.argsort(-imp, kind="stable").astype(np.int32)
+
+
+def assign_slots_bpr(idx: np.ndarray, E: int, C: int, importance32: np.ndarray):
+    """Batch-prioritized capacity rule (Sec. 2.3): tokens are sorted by
+    importance first and then assigned to experts, so the least important
+    tokens are the ones dropped.  The capacity rule of ``assign_slots`` runs
+    over the tokens in ``bpr_order`` (each token's choices in rank order), so
+    an expert's rows hold its kept tokens by descending importance.  The whole
+    batch decides the order, so there is no carry from earlier partitions.
+    Returns (slot [T][k] in token order, fill [E], order [T])."""
+    order = bpr_order(importance32)
+    slot_sorted, fill = assign_slots(np.asarray(idx)[order], E, C)
+    slot = np.empty_like(slot_sorted)
+    slot[order] = slot_sorted
+    return slot, fill, order
 
 
 def send_counts(fill: np.ndarray, G: int) -> np.ndarray:

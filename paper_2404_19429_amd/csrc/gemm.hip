@@ -765,7 +765,7 @@ __device__ __forceinline__ int wide_tile_prefix(const GemmParams& p, int lane, i
     if constexpr (RAGGED_K) {
       int lo, span;
       group_rows(p, lane, lo, span);
-      cnt = span > 0 ? tilesM * tilesN : 0;   // an empty group's product is zeroed by zero_empty_groups_kernel
+      cnt = span > 0 ? tilesM * tilesN : 0;   // an empty group's output is zeroed in the prologue
     } else {
       int lo, span;
       group_rows(p, lane, lo, span);
@@ -880,6 +880,19 @@ gemm_wide_kernel(GemmParams p, int tilesM, int tilesN, int groups) {
   // Tile counts per group and their prefix (every wave computes the same values).
   int incl, excl;
   const int total = wide_tile_prefix<RAGGED_K>(p, lane, groups, tilesM, tilesN, incl, excl);
+  if constexpr (RAGGED_K) {
+    // Groups without rows have no tiles: their [M][N] outputs are zeroed here,
+    // spread over the whole grid (16-byte stores; no tile writes them).
+    uint64_t empty = __ballot(lane < groups && incl == excl);
+    const int64_t chunks = (int64_t)p.M * p.N / 8;
+    const int64_t gtid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x, gstride = (int64_t)gridDim.x * blockDim.x;
+    while (empty) {
+      const int g = __builtin_ctzll(empty);
+      empty &= empty - 1;
+      u32x4* o = reinterpret_cast<u32x4*>((uint16_t*)p.C + (int64_t)g * p.sC);
+      for (int64_t i = gtid; i < chunks; i += gstride) o[i] = u32x4{0u, 0u, 0u, 0u};
+    }
+  }
   const int nslot = gridDim.x / 8;
   const int xcd = blockIdx.x % 8, slot = blockIdx.x / 8;
   const int per = (total + 7) / 8;
@@ -1514,24 +1527,6 @@ void launch_expert_bwd_dx(const moe_cfg& c, const void* dO, const int32_t* rb, c
   run_expert<false, false, EPI_STORE, false>(c, p2, C, (int)d, s);   // dXe row-major
 }
 
-// Zeroes the per-group outputs ([per_group] elements each) of the groups with
-// no rows, whose tiles the ragged-K schedule leaves out: 16-byte stores.
-__global__ __launch_bounds__(256) void zero_empty_groups_kernel(uint16_t* __restrict__ out, int64_t per_group,
-                                                                const int32_t* __restrict__ rb,
-                                                                const int32_t* __restrict__ re, int cap) {
-  GemmParams q{};
-  q.rb = rb;
-  q.re = re;
-  q.cap = cap;
-  int lo, span;
-  group_rows(q, blockIdx.y, lo, span);
-  if (span > 0) return;
-  u32x4* base = reinterpret_cast<u32x4*>(out + (int64_t)blockIdx.y * per_group);
-  const int64_t n = per_group / 8;
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
-    base[i] = u32x4{0u, 0u, 0u, 0u};
-}
-
 void launch_expert_bwd_dw(const moe_cfg& c, const void* X, const void* A, const void* dO, const void* dH,
                           const int32_t* rb, const int32_t* re, void* dW1, void* dW2, hipStream_t s) {
   const int64_t d = c.d_model, f = c.d_ff, C = c.C, Cp = rows_alloc(c);
@@ -1540,12 +1535,6 @@ void launch_expert_bwd_dw(const moe_cfg& c, const void* X, const void* A, const 
   GemmParams p2{dO, d, Cp * d, A, f, Cp * f, dW2, f, d * f, nullptr, nullptr, rb, re, (int)d, (int)f, 0, c.act, (int)C};
   // dW1_e [f][d] = dH_e^T X_e
   GemmParams p1{dH, f, Cp * f, X, d, Cp * d, dW1, d, f * d, nullptr, nullptr, rb, re, (int)f, (int)d, 0, c.act, (int)C};
-  if (c.dtype == MOE_BF16 && c.E > 0) {   // groups without rows: zeros, outside the products' schedule
-    hipLaunchKernelGGL(zero_empty_groups_kernel, dim3(64, (unsigned)c.E), dim3(256), 0, s, (uint16_t*)dW2, d * f, rb,
-                       re, (int)C);
-    hipLaunchKernelGGL(zero_empty_groups_kernel, dim3(64, (unsigned)c.E), dim3(256), 0, s, (uint16_t*)dW1, f * d, rb,
-                       re, (int)C);
-  }
   if (c.wpacked && c.dtype == MOE_BF16) {
     run_expert<false, true, EPI_STORE, true>(c, p2, d, (int)f, s);
     run_expert<false, true, EPI_STORE, true>(c, p1, f, (int)d, s);

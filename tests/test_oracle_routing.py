@@ -206,3 +206,98 @@ def test_dispatch_is_exact_permutation_and_send_counts():
     sc = O.send_counts(fill, G)
     assert sc.shape == (G,) and int(sc.sum()) == int(kept.sum())
     np.testing.assert_array_equal(sc, [fill[g * 2:(g + 1) * 2].sum() for g in range(G)])
+
+
+# ------------------------------------------------------- batch-prioritized routing
+def test_bpr_hand_worked_example():
+    g = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "bpr_small_example.json")))
+    l = np.array(g["logits"], np.float32)
+    idx = O.topk_route(l, g["k"])
+    np.testing.assert_array_equal(idx, g["expected"]["idx"])
+    imp = O.bpr_importance(l, idx)
+    slot, fill, order = O.assign_slots_bpr(idx, g["E"], g["C"], imp)
+    np.testing.assert_array_equal(order, g["expected"]["order"])
+    np.testing.assert_array_equal(slot, g["expected"]["slot"])
+    np.testing.assert_array_equal(fill, g["expected"]["fill"])
+    s_tok, _ = O.assign_slots(idx, g["E"], g["C"])
+    np.testing.assert_array_equal(s_tok, g["expected"]["token_order_slot"])
+
+
+def test_bpr_importance_closed_forms():
+    rng = np.random.default_rng(11)
+    l = (rng.standard_normal((64, 6)) * 2).astype(np.float32)
+    # top-1: the largest probability, 1 / sum_e exp(l_e - max)
+    i1 = O.topk_route(l, 1)
+    ld = l.astype(np.float64)
+    want = 1.0 / np.exp(ld - ld.max(axis=1, keepdims=True)).sum(axis=1)
+    np.testing.assert_array_equal(O.bpr_importance(l, i1), want.astype(np.float32))
+    # every expert selected: the probabilities sum to one
+    iE = O.topk_route(l, 6)
+    np.testing.assert_array_equal(O.bpr_importance(l, iE), np.ones(64, np.float32))
+    # E = 2, top-1: the logistic function of the logit gap
+    l2 = l[:, :2]
+    gap = np.abs(l2[:, 0].astype(np.float64) - l2[:, 1])
+    np.testing.assert_allclose(O.bpr_importance(l2, O.topk_route(l2, 1)), 1 / (1 + np.exp(-gap)), rtol=1e-6)
+
+
+@pytest.mark.parametrize("seed,T,E,k,C", [(0, 300, 8, 2, 40), (1, 257, 4, 1, 50), (2, 500, 16, 2, 30),
+                                          (3, 100, 8, 3, 25)])
+def test_bpr_kept_outrank_dropped(seed, T, E, k, C):
+    rng = np.random.default_rng(seed)
+    l = rng.standard_normal((T, E)).astype(np.float32)
+    l[rng.random(T) < 0.1] = l[0]                    # equal-importance ties
+    idx = O.topk_route(l, k)
+    imp = O.bpr_importance(l, idx)
+    slot, fill, order = O.assign_slots_bpr(idx, E, C, imp)
+    assert sorted(order.tolist()) == list(range(T))
+    demand = np.bincount(idx.ravel(), minlength=E)
+    np.testing.assert_array_equal(fill, np.minimum(demand, C))      # order changes who, not how many
+    pri = {int(t): i for i, t in enumerate(order)}                  # position in the visiting order
+    for e in range(E):
+        kept = [(t, int(slot[t, r])) for t in range(T) for r in range(k) if idx[t, r] == e and slot[t, r] >= 0]
+        drop = [t for t in range(T) for r in range(k) if idx[t, r] == e and slot[t, r] < 0]
+        assert sorted(s for _, s in kept) == list(range(len(kept)))
+        # rows in priority order; every kept token is ahead of every dropped one:
+        # higher importance, or equal importance and a lower token index
+        ks = sorted(kept, key=lambda ts: ts[1])
+        for (a, _), (b, _) in zip(ks, ks[1:]):
+            assert imp[a] > imp[b] or (imp[a] == imp[b] and a < b)
+        if kept and drop:
+            a = ks[-1][0]
+            for b in drop:
+                assert imp[a] > imp[b] or (imp[a] == imp[b] and a < b)
+                assert pri[a] < pri[b]
+
+
+def test_bpr_equal_importance_is_token_order():
+    # every row a permutation of one logit vector: one importance for all tokens
+    rng = np.random.default_rng(4)
+    base = rng.standard_normal(8).astype(np.float32)
+    l = np.stack([rng.permutation(base) for _ in range(200)])
+    idx = O.topk_route(l, 2)
+    imp = O.bpr_importance(l, idx)
+    assert np.unique(imp).size == 1
+    slot, fill, order = O.assign_slots_bpr(idx, 8, 30, imp)
+    s_tok, f_tok = O.assign_slots(idx, 8, 30)
+    np.testing.assert_array_equal(order, np.arange(200))
+    np.testing.assert_array_equal(slot, s_tok)
+    np.testing.assert_array_equal(fill, f_tok)
+
+
+def test_bpr_monotone_importance():
+    # importance strictly decreasing in t: token order; increasing: reversed
+    T, E, C = 120, 4, 20
+    a = np.linspace(3.0, 0.5, T).astype(np.float32)
+    l = np.zeros((T, E), np.float32)
+    l[:, 0] = a
+    l[np.arange(T) % 2 == 1] = np.roll(l[np.arange(T) % 2 == 1], 1, axis=1)   # half the tokens on expert 1
+    idx = O.topk_route(l, 1)
+    imp = O.bpr_importance(l, idx)
+    assert np.all(np.diff(imp.astype(np.float64)) < 0)
+    slot, _, order = O.assign_slots_bpr(idx, E, C, imp)
+    np.testing.assert_array_equal(order, np.arange(T))
+    np.testing.assert_array_equal(slot, O.assign_slots(idx, E, C)[0])
+    lr, ir = l[::-1].copy(), idx[::-1].copy()
+    slot_r, _, order_r = O.assign_slots_bpr(ir, E, C, O.bpr_importance(lr, ir))
+    np.testing.assert_array_equal(order_r, np.arange(T)[::-1])
+    np.testing.assert_array_equal(slot_r[::-1], O.assign_slots(idx, E, C)[0])
