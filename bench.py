@@ -26,8 +26,12 @@ the line also reports forward and backward times with 1 partition and with
 all work on a single stream, which isolate the pipelining and the deferred
 weight gradients.
 
+With --routing bpr the step's dispatch is the batch-prioritized one
+(moe_dispatch_bpr: tokens visited by importance); either way the line reports
+the other order's dispatch time on the same gate output (dispatch_*_ms).
+
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 2|3|4] [--workload layer|block]
-                       [--no-cpu-baseline]
+                       [--routing token|bpr] [--no-cpu-baseline]
 """
 from __future__ import annotations
 
@@ -84,6 +88,8 @@ def _args():
                     help="run one plain device copy of this many MiB first (calibrates HBM byte counters)")
     ap.add_argument("--cpu-sample-tokens", type=int, default=8192)
     ap.add_argument("--workload", default="layer", choices=["layer", "block"])
+    ap.add_argument("--routing", default="token", choices=["token", "bpr"],
+                    help="capacity order of the layer step: token order, or batch-prioritized (importance order)")
     return ap.parse_args()
 
 
@@ -253,7 +259,10 @@ def main():
         mark(0)
         L.moe_gate_topk(cfg, dev["x"], dev["Wg"], bias, b.logits, b.idx, b.w)
         mark(1)
-        L.moe_dispatch(cfg, dev["x"], b.idx, b.carry, b.fill, b.slot, b.send_buf, b.ws_dispatch)
+        if a.routing == "bpr":
+            L.moe_dispatch_bpr(cfg, dev["x"], b.logits, b.idx, b.fill, b.slot, b.send_buf, None, b.ws_bpr)
+        else:
+            L.moe_dispatch(cfg, dev["x"], b.idx, b.carry, b.fill, b.slot, b.send_buf, b.ws_dispatch)
         mark(2)
         L.moe_expert_ffn_fwd(cfg, b.send_buf, b.carry, b.fill, b.W1p, b.W2p, b.H, b.A, b.O, b.ws_ffn)
         mark(3)
@@ -303,6 +312,24 @@ def main():
     torch.cuda.synchronize()
     pack_ms = pe[0].elapsed_time(pe[1]) / 5
 
+    # The other capacity order's dispatch on the same gate output (not part of the step).
+    alt = {}
+    for name in ("token", "bpr"):
+        if name == a.routing:
+            continue
+        de = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        de[0].record(stream)
+        for _ in range(10):
+            if name == "bpr":
+                L.moe_dispatch_bpr(cfg, dev["x"], b.logits, b.idx, b.fill, b.slot, b.send_buf, None, b.ws_bpr)
+            else:
+                L.moe_dispatch(cfg, dev["x"], b.idx, b.carry, b.fill, b.slot, b.send_buf, b.ws_dispatch)
+        de[1].record(stream)
+        torch.cuda.synchronize()
+        alt[f"dispatch_{name}_ms"] = de[0].elapsed_time(de[1]) / 10
+    step()                       # leave the buffers as the step's own routing left them
+    torch.cuda.synchronize()
+
     fill = b.fill.cpu().numpy()
     N = int(fill.sum())                                           # kept (token, expert) rows
     d, f, T = spec.d, spec.f, spec.T
@@ -330,6 +357,7 @@ def main():
         "data": "synthetic (seeded Gaussian hidden states and weights; no dataset)",
         "config": {"workload": spec.name, "T": T, "d_model": d, "d_ff": f, "E": spec.E, "k": spec.k,
                    "C": C, "capacity_factor": f"{spec.cf_num}/{spec.cf_den}", "act": spec.act,
+                   "routing": a.routing,
                    "kept_rows": N, "parallelism": "single GPU (one GPU's share; all-to-all not run)"},
         "roofline": {"kernel": "expert FFN forward: grouped bf16 MFMA GEMMs gemm_wide_kernel FWD1 + FWD2 "
                                "(+ the K-split fix-up launch)",
@@ -343,6 +371,7 @@ def main():
         "event_ms_per_step": step_ms,
         "weights": "packed once before the timed steps; dW1/dW2 written packed (wpacked=1)",
         "pack_weights_ms": pack_ms,
+        **alt,
         "ms_per_step_with_repack": wall / a.steps * 1e3 + pack_ms,
     }
     if not a.no_cpu_baseline:

@@ -77,7 +77,13 @@ typedef enum { MOE_F32 = 0, MOE_BF16 = 1 } moe_dtype;
 typedef enum { MOE_ACT_IDENTITY = 0, MOE_ACT_RELU = 1, MOE_ACT_GELU_TANH = 2, MOE_ACT_GELU_ERF = 3 } moe_act;
 
 /* Which call a workspace is for (moe_workspace_bytes). */
-typedef enum { MOE_CALL_DISPATCH = 0, MOE_CALL_BWD_DX = 1, MOE_CALL_BWD_DW = 2, MOE_CALL_FFN_FWD = 3 } moe_call;
+typedef enum {
+  MOE_CALL_DISPATCH = 0,
+  MOE_CALL_BWD_DX = 1,
+  MOE_CALL_BWD_DW = 2,
+  MOE_CALL_FFN_FWD = 3,
+  MOE_CALL_DISPATCH_BPR = 4
+} moe_call;
 
 /* Host-side description of one MoE layer call. */
 typedef struct {
@@ -138,6 +144,30 @@ moe_status moe_gate_topk(const moe_cfg* cfg, const void* x, const void* Wg, cons
 moe_status moe_dispatch(const moe_cfg* cfg, const void* x, const int32_t* idx, const int32_t* carry,
                         int32_t* fill, int32_t* slot, void* send_buf, void* ws, size_t ws_bytes,
                         moe_stream_t stream);
+
+/* Capacity-bounded dispatch with Batch-prioritized Routing (Sec. 2.3,
+ * "Opportunities and Challenges": the tokens of the batch are sorted by
+ * importance, the sum of their top-k gating scores, before they are assigned
+ * to experts, so the least important tokens are dropped first).
+ *   importance[t] = sum over r of softmax(logits[t])[idx[t][r]] (softmax over
+ *   all E experts, not renormalised), evaluated in double and rounded once to
+ *   float.  The tokens are visited by importance descending, equal importance
+ *   in token order, each token's choices in rank order; an assignment takes
+ *   the next free row of its expert below C, else it is dropped.  An expert's
+ *   rows therefore hold its kept tokens by descending importance.
+ *   In: x [T][d] dtype, logits [T][E] float (moe_gate_topk), idx [T][k] int32.
+ *   Out: fill [E] int32 = rows taken (min(C, demand_e)); slot [T][k] int32
+ *   (token order; -1 = dropped); send_buf as in moe_dispatch, rows 0..fill_e-1;
+ *   order [T] int32 (nullable): the visiting order, order[j] = the token
+ *   visited j-th.
+ *   The whole batch decides the order, so there is no carry-in: partitions of
+ *   the batch may only start after this call (the paper's pipelining after the
+ *   gate).  ws: moe_workspace_bytes(cfg, MOE_CALL_DISPATCH_BPR) bytes of device
+ *   memory.  The sort: 4096-token tiles sorted in LDS, then merged by binary
+ *   search (deterministic, no atomics on device memory). */
+moe_status moe_dispatch_bpr(const moe_cfg* cfg, const void* x, const float* logits, const int32_t* idx,
+                            int32_t* fill, int32_t* slot, void* send_buf, int32_t* order, void* ws, size_t ws_bytes,
+                            moe_stream_t stream);
 
 /* Expert weights in the layout the expert GEMMs read, written once per
  * weight update and used by moe_expert_ffn_fwd and moe_bwd_dx:

@@ -363,11 +363,13 @@ def gate_bwd(g: np.ndarray, p: np.ndarray, w: np.ndarray, idx: np.ndarray, renor
 
 
 # ------------------------------------------------------------------------ composite
-def layer_forward(spec, inp, carry=None, C=None, exact_logits: bool = False):
+def layer_forward(spec, inp, carry=None, C=None, exact_logits: bool = False, routing: str = "token"):
     """The whole MoE layer forward for a LayerSpec-like object ``spec`` (fields
     T, E, k, cf_num, cf_den, act, renorm) and inputs dict (x, Wg, bias, W1, W2).
-    ``C`` defaults to the capacity of the unpartitioned T tokens.  Returns every
-    intermediate, so each stage can be compared on its own."""
+    ``C`` defaults to the capacity of the unpartitioned T tokens.  ``routing``
+    "bpr" fills capacity in batch-prioritized order (``assign_slots_bpr``; no
+    carry).  Returns every intermediate, so each stage can be compared on its
+    own."""
     x = np.asarray(inp["x"], F64)
     T = x.shape[0]
     if C is None:
@@ -376,12 +378,17 @@ def layer_forward(spec, inp, carry=None, C=None, exact_logits: bool = False):
     idx = topk_route(logits, spec.k)
     p, w = gate_weights(logits, idx, spec.renorm)
     carry0 = np.zeros(spec.E, np.int64) if carry is None else np.asarray(carry, np.int64)
-    slot, fill = assign_slots(idx, spec.E, C, carry0)
+    order = None
+    if routing == "bpr":
+        assert carry is None, "batch-prioritized routing orders the whole batch: no carry"
+        slot, fill, order = assign_slots_bpr(idx, spec.E, C, bpr_importance(logits, idx))
+    else:
+        slot, fill = assign_slots(idx, spec.E, C, carry0)
     buf = dispatch(x, idx, slot, spec.E, C)
     H, A, O = expert_ffn(buf, carry0, fill, inp["W1"], inp["W2"], spec.act)
     y = combine(O, idx, slot, w)
     return dict(C=C, logits=logits, idx=idx, p=p, w=w, slot=slot, fill=fill, carry=carry0,
-                buf=buf, H=H, A=A, O=O, y=y)
+                buf=buf, H=H, A=A, O=O, y=y, order=order)
 
 
 def layer_backward(spec, inp, fw):

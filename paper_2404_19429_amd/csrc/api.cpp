@@ -120,6 +120,7 @@ size_t moe_workspace_bytes(const moe_cfg* cfg, int32_t call) {
     case MOE_CALL_BWD_DX: return lmoe::bwd_dx_ws_bytes(*cfg);
     case MOE_CALL_BWD_DW: return lmoe::bwd_dw_ws_bytes(*cfg);
     case MOE_CALL_FFN_FWD: return lmoe::expert_sk_ws_bytes(*cfg);
+    case MOE_CALL_DISPATCH_BPR: return lmoe::dispatch_bpr_ws_bytes(*cfg);
     default: fail(MOE_EINVAL, "%s: unknown call %d", fn, call); return 0;
   }
 }
@@ -153,6 +154,24 @@ moe_status moe_dispatch(const moe_cfg* cfg, const void* x, const int32_t* idx, c
   }
   CHECK(check_device(fn));
   lmoe::launch_dispatch(*cfg, x, idx, carry, fill, slot, send_buf, ws, (hipStream_t)stream);
+  return check_launch(fn);
+}
+
+moe_status moe_dispatch_bpr(const moe_cfg* cfg, const void* x, const float* logits, const int32_t* idx,
+                            int32_t* fill, int32_t* slot, void* send_buf, int32_t* order, void* ws, size_t ws_bytes,
+                            moe_stream_t stream) {
+  const char* fn = "moe_dispatch_bpr";
+  CHECK(check_cfg(cfg, fn, false));
+  REQUIRE_TPTR(x); REQUIRE_TPTR(logits); REQUIRE_TPTR(idx); REQUIRE_PTR(fill);
+  REQUIRE_TPTR(slot); REQUIRE_PTR(send_buf); OPTIONAL_PTR(order);
+  const size_t need = lmoe::dispatch_bpr_ws_bytes(*cfg);
+  if (need > 0) {
+    if (ws == nullptr || ws_bytes < need)
+      return fail(MOE_EWORKSPACE, "%s: workspace of %zu bytes needed, %zu given", fn, need, ws ? ws_bytes : 0);
+    REQUIRE_PTR(ws);
+  }
+  CHECK(check_device(fn));
+  lmoe::launch_dispatch_bpr(*cfg, x, logits, idx, fill, slot, send_buf, order, ws, (hipStream_t)stream);
   return check_launch(fn);
 }
 

@@ -17,6 +17,9 @@ void launch_gate(const moe_cfg& c, const void* x, const void* Wg, const float* b
 size_t dispatch_ws_bytes(const moe_cfg& c);
 void launch_dispatch(const moe_cfg& c, const void* x, const int32_t* idx, const int32_t* carry, int32_t* fill,
                      int32_t* slot, void* send_buf, void* ws, hipStream_t s);
+size_t dispatch_bpr_ws_bytes(const moe_cfg& c);
+void launch_dispatch_bpr(const moe_cfg& c, const void* x, const float* logits, const int32_t* idx, int32_t* fill,
+                         int32_t* slot, void* send_buf, int32_t* order, void* ws, hipStream_t s);
 void launch_combine(const moe_cfg& c, const void* O, const int32_t* idx, const int32_t* slot, const float* w,
                     void* y, hipStream_t s, const void* resid = nullptr);
 size_t bwd_dx_ws_bytes(const moe_cfg& c);

@@ -35,7 +35,10 @@ __device__ __forceinline__ int64_t erow(int e, int s, int col, int d, int C) {
 // expert earlier in (token, rank) order inside the chunk; counts[chunk][e] =
 // the chunk's assignments to e.  Lanes holding the same expert are found with
 // one ballot per expert-index bit.
+// perm (nullable): position j of the walk holds token perm[j] (batch-prioritized
+// order); NULL = token order.  rank_out and the chunks are indexed by position.
 __global__ __launch_bounds__(kRouteChunk) void route_rank_kernel(const int32_t* __restrict__ idx,
+                                                                 const int32_t* __restrict__ perm,
                                                                  int32_t* __restrict__ counts,
                                                                  int32_t* __restrict__ rank_out,
                                                                  int64_t T_tokens, int E, int k) {
@@ -48,10 +51,15 @@ __global__ __launch_bounds__(kRouteChunk) void route_rank_kernel(const int32_t* 
 
   const int64_t t = (int64_t)blockIdx.x * kRouteChunk + threadIdx.x;
   const bool active = t < T_tokens;
+  int64_t tok = t;
+  if (active && perm) {
+    tok = perm[t];
+    if (tok < 0 || tok >= T_tokens) tok = t;   // (a valid order is a permutation of 0 .. T-1)
+  }
   int my[kMaxK], rank[kMaxK];
 #pragma unroll
   for (int r = 0; r < kMaxK; ++r) {
-    const int e = (active && r < k) ? idx[t * k + r] : -1;
+    const int e = (active && r < k) ? idx[tok * k + r] : -1;
     my[r] = (e >= 0 && e < E) ? e : -1;  // an out-of-range expert is treated as dropped
     rank[r] = 0;
   }
@@ -139,8 +147,10 @@ __global__ __launch_bounds__(64) void route_scan_kernel(const int32_t* __restric
 
 // slot[t][r] = base[chunk][e] + rank (or -1 past the capacity), and
 // send_buf[e][slot][:] = x[t][:] for every kept (t, r).
+// perm as in route_rank_kernel: the thread's positions j hold tokens perm[j].
 template <typename T, int KT, int U, bool UNI>
 __global__ __launch_bounds__(256) void dispatch_copy_kernel(const T* __restrict__ x, const int32_t* __restrict__ idx,
+                                                            const int32_t* __restrict__ perm,
                                                             const int32_t* __restrict__ rank,
                                                             const int32_t* __restrict__ base,
                                                             int32_t* __restrict__ slot, T* __restrict__ send,
@@ -158,8 +168,13 @@ __global__ __launch_bounds__(256) void dispatch_copy_kernel(const T* __restrict_
   int er[U][KK], sr[U][KK];
 #pragma unroll
   for (int u = 0; u < U; ++u) {
-    const int64_t t = t0 + u;
-    const bool tok = t < T_tokens;
+    const int64_t j = t0 + u;                 // position of the walk
+    const bool tok = j < T_tokens;
+    int64_t t = j;
+    if (tok && perm) {
+      t = perm[j];
+      if (t < 0 || t >= T_tokens) t = j;       // (a valid order is a permutation of 0 .. T-1)
+    }
     v[u] = tok ? *reinterpret_cast<const u32x4*>(x + t * d + (int64_t)c * V) : u32x4{0u, 0u, 0u, 0u};
 #pragma unroll
     for (int r = 0; r < KK; ++r) {
@@ -167,9 +182,9 @@ __global__ __launch_bounds__(256) void dispatch_copy_kernel(const T* __restrict_
       sr[u][r] = -1;
       if (tok && r < k) {
         const int e = idx[t * k + r];
-        const int rk = rank[t * k + r];
+        const int rk = rank[j * k + r];
         if (rk >= 0 && e >= 0 && e < E) {
-          const int sl = base[(t / kRouteChunk) * E + e] + rk;
+          const int sl = base[(j / kRouteChunk) * E + e] + rk;
           if (sl < C) {
             er[u][r] = e;
             sr[u][r] = sl;
@@ -218,25 +233,248 @@ size_t dispatch_ws_bytes(const moe_cfg& c) {
   return (size_t)(2 * nch * c.E + c.T * c.k) * sizeof(int32_t);
 }
 
-void launch_dispatch(const moe_cfg& c, const void* x, const int32_t* idx, const int32_t* carry, int32_t* fill,
-                     int32_t* slot, void* send_buf, void* ws, hipStream_t s) {
+// Slot assignment and copy over the walk order perm (NULL = token order).
+static void dispatch_walk(const moe_cfg& c, const void* x, const int32_t* idx, const int32_t* perm,
+                          const int32_t* carry, int32_t* fill, int32_t* slot, void* send_buf, void* ws, hipStream_t s) {
   const int64_t nch = (c.T + kRouteChunk - 1) / kRouteChunk;
   int32_t* counts = (int32_t*)ws;
   int32_t* base = counts + nch * c.E;
   int32_t* rank = base + nch * c.E;
   if (nch > 0)
-    hipLaunchKernelGGL(route_rank_kernel, dim3((unsigned)nch), dim3(kRouteChunk), 0, s, idx, counts, rank, c.T, c.E,
-                       c.k);
+    hipLaunchKernelGGL(route_rank_kernel, dim3((unsigned)nch), dim3(kRouteChunk), 0, s, idx, perm, counts, rank, c.T,
+                       c.E, c.k);
   if (c.E > 0)
     hipLaunchKernelGGL(route_scan_kernel, dim3((unsigned)c.E), dim3(64), 0, s, counts, base, carry, fill, (int)nch, c.E,
                        c.C);
   if (nch == 0) return;
   if (c.dtype == MOE_BF16)
-    row_launch<DispatchCopy, uint16_t, 4, 2>(c, s, (const uint16_t*)x, idx, rank, base, slot, (uint16_t*)send_buf, c.T,
-                                       c.d_model, c.E, c.k, c.C);
+    row_launch<DispatchCopy, uint16_t, 4, 2>(c, s, (const uint16_t*)x, idx, perm, rank, base, slot, (uint16_t*)send_buf,
+                                       c.T, c.d_model, c.E, c.k, c.C);
   else
-    row_launch<DispatchCopy, float, 4, 2>(c, s, (const float*)x, idx, rank, base, slot, (float*)send_buf, c.T, c.d_model,
-                                    c.E, c.k, c.C);
+    row_launch<DispatchCopy, float, 4, 2>(c, s, (const float*)x, idx, perm, rank, base, slot, (float*)send_buf, c.T,
+                                    c.d_model, c.E, c.k, c.C);
+}
+
+void launch_dispatch(const moe_cfg& c, const void* x, const int32_t* idx, const int32_t* carry, int32_t* fill,
+                     int32_t* slot, void* send_buf, void* ws, hipStream_t s) {
+  dispatch_walk(c, x, idx, nullptr, carry, fill, slot, send_buf, ws, s);
+}
+
+// ------------------------------------------------------ batch-prioritized routing
+// The tokens are visited by importance (the sum of the selected experts'
+// softmax probabilities) descending, equal importance in token order; the
+// capacity rule then runs over that walk exactly as over token order.
+
+// elem[t] = (key << 32) | t, key = ~bits of the float importance (ascending
+// key = descending importance; importance >= 0), so the 64-bit elements are
+// distinct and their ascending order is the visiting order: importance
+// descending, then token ascending.  One wave per token, lane e for
+// expert e: the softmax over all E experts in double, then the selected
+// experts' probabilities summed in rank order, rounded once to float; the
+// ordering decision is taken on the float values.
+__global__ __launch_bounds__(256) void bpr_key_kernel(const float* __restrict__ logits, const int32_t* __restrict__ idx,
+                                                      uint64_t* __restrict__ elem, int64_t T_tokens, int E, int k) {
+  const int lane = threadIdx.x & 63;
+  const int64_t t = (int64_t)blockIdx.x * (blockDim.x / kWave) + (threadIdx.x >> 6);
+  if (t >= T_tokens) return;
+  const bool has = lane < E;
+  const float l = has ? logits[t * E + lane] : -INFINITY;
+  float mf = l;
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) mf = fmaxf(mf, __shfl_xor(mf, o, kWave));
+  const double ex = has ? exp((double)l - (double)mf) : 0.0;
+  double z = ex;
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) z += __shfl_xor(z, o, kWave);
+  const double p = ex / z;
+  double imp = 0.0;
+  for (int r = 0; r < k; ++r) {
+    const int e = idx[t * k + r];
+    const double pe = __shfl(p, (e >= 0 && e < E) ? e : 0, kWave);
+    if (e >= 0 && e < E) imp += pe;
+  }
+  if (lane == 0) elem[t] = ((uint64_t)~__float_as_uint((float)imp) << 32) | (uint64_t)t;
+}
+
+constexpr int kSortThreads = 1024;
+constexpr int kSortWaves = kSortThreads / kWave;
+constexpr int kDigitBits = 8;
+constexpr int kRadix = 1 << kDigitBits;
+constexpr int kSortPasses = 4;             // the key's low 30 bits: digits of 8, 8, 8, 6 bits
+constexpr int kCntStride = kSortWaves + 1; // counters of one digit (one per wave), padded
+constexpr int kSortTile = 4096;            // elements per sorted tile: 16 waves x 4 rounds of 64
+constexpr int kWaveSpan = kSortTile / kSortWaves;
+constexpr size_t kTileSortLds = 2 * kSortTile * sizeof(uint64_t) + kSortWaves * kRadix * sizeof(uint64_t) +
+                                (kRadix * kCntStride + kSortWaves) * sizeof(int32_t);
+static_assert(kRadix * kSortWaves == 4 * kSortThreads, "scan layout");
+
+// Sorts one tile of up to kSortTile elements in LDS by the key's low 30 bits
+// (importance keys: ~bits of a float in [0, 1], whose two top bits are
+// constant), stably: an LSD radix sort of four passes.  Wave w owns elements
+// [w kWaveSpan, (w + 1) kWaveSpan) of the tile and takes them in rounds of
+// 64 in order; cnt[digit][w] counts the digit in w's range, and its
+// exclusive prefix in (digit, wave) order is where w's next element with
+// that digit goes.  In a round, each lane ORs its lane bit into the wave's
+// table entry of its digit and reads the entry back: the lanes sharing its
+// digit.  They are ranked by lane, and the lowest of them claims their
+// positions with one returning LDS add and clears the entry (a wave's LDS
+// operations complete in order, so the rounds claim in order).  Equal keys
+// keep their input order, which within a tile is token order: the sorted
+// tile is in ascending order of the 64-bit elements.
+__global__ __launch_bounds__(kSortThreads) void bpr_tile_sort_kernel(const uint64_t* __restrict__ in,
+                                                                     uint64_t* __restrict__ out, int64_t n) {
+  extern __shared__ __attribute__((aligned(16))) unsigned char bpr_lds[];
+  uint64_t* buf0 = reinterpret_cast<uint64_t*>(bpr_lds);
+  uint64_t* buf1 = buf0 + kSortTile;
+  uint64_t* table = buf1 + kSortTile;                                  // [kSortWaves][kRadix]
+  int32_t* cnt = reinterpret_cast<int32_t*>(table + kSortWaves * kRadix);   // [kRadix][kCntStride]
+  int32_t* wsum = cnt + kRadix * kCntStride;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int64_t t0 = (int64_t)blockIdx.x * kSortTile;
+  const int m = (int)min((int64_t)kSortTile, n - t0);
+  for (int i = tid; i < m; i += kSortThreads) buf0[i] = in[t0 + i];
+  for (int i = lane; i < kRadix; i += kWave) table[wave * kRadix + i] = 0ull;
+  const int lo = min(m, wave * kWaveSpan), hi = min(m, lo + kWaveSpan);
+  const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+  for (int pass = 0; pass < kSortPasses; ++pass) {
+    const int sh = 32 + kDigitBits * pass;
+    const uint32_t dmask = pass == kSortPasses - 1 ? 0x3fu : 0xffu;
+    const uint64_t* src = (pass & 1) ? buf1 : buf0;   // 0 -> 1 -> 0 -> 1 -> 0
+    uint64_t* dst = (pass & 1) ? buf0 : buf1;
+    for (int i = tid; i < kRadix * kCntStride; i += kSortThreads) cnt[i] = 0;
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < kWaveSpan / kWave; ++j) {
+      const int i = lo + kWave * j + lane;
+      if (i < hi) atomicAdd(&cnt[(int)((src[i] >> sh) & dmask) * kCntStride + wave], 1);
+    }
+    __syncthreads();
+    // Exclusive scan of the counters in (digit, wave) order; thread tid owns
+    // digit tid / 4, waves 4 (tid % 4) .. + 3.
+    const int d0 = tid >> 2, w0 = (tid & 3) * 4;
+    int v[4];
+    int sum = 0;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      v[q] = cnt[d0 * kCntStride + w0 + q];
+      sum += v[q];
+    }
+    int incl = sum;
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+      const int u = __shfl_up(incl, o, kWave);
+      if (lane >= o) incl += u;
+    }
+    if (lane == kWave - 1) wsum[wave] = incl;
+    __syncthreads();
+    int ex = incl - sum;
+    for (int w = 0; w < wave; ++w) ex += wsum[w];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      cnt[d0 * kCntStride + w0 + q] = ex;
+      ex += v[q];
+    }
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < kWaveSpan / kWave; ++j) {
+      const int i = lo + kWave * j + lane;
+      const bool ok = i < hi;
+      const uint64_t e = ok ? src[i] : 0ull;
+      const int dg = (int)((e >> sh) & dmask);
+      uint64_t peers = 0ull;
+      if (ok) {
+        atomicOr((unsigned long long*)&table[wave * kRadix + dg], (unsigned long long)(1ull << lane));
+        peers = table[wave * kRadix + dg];
+      }
+      int first = 0;
+      if (ok && (peers & lt) == 0) {
+        first = atomicAdd(&cnt[dg * kCntStride + wave], __popcll(peers));
+        table[wave * kRadix + dg] = 0ull;
+      }
+      const int srcl = ok ? (int)__builtin_ctzll(peers) : lane;
+      const int pos = __shfl(first, srcl, kWave) + __popcll(peers & lt);
+      if (ok && pos >= 0 && pos < m) dst[pos] = e;   // always true for a consistent count; keeps stores in bounds
+    }
+    __syncthreads();
+  }
+  for (int i = tid; i < m; i += kSortThreads) out[t0 + i] = buf0[i];
+}
+
+// Merges the sorted tiles: element i of tile a goes to its rank in the tile
+// plus, for every other tile, the number of its elements below it (a binary
+// search; the elements are distinct), and perm[pos] = its token.  Every
+// position is below n.
+constexpr int kMergeTiles = 16;   // tiles searched side by side (more: one after another)
+__global__ __launch_bounds__(256) void bpr_merge_kernel(const uint64_t* __restrict__ sorted, int32_t* __restrict__ perm,
+                                                        int64_t n) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  const uint64_t v = sorted[i];
+  const int64_t a = i / kSortTile;
+  const int64_t ntiles = (n + kSortTile - 1) / kSortTile;
+  int64_t pos = i - a * kSortTile;
+  for (int64_t g0 = 0; g0 < ntiles; g0 += kMergeTiles) {
+    int64_t base[kMergeTiles];
+    int len[kMergeTiles];
+#pragma unroll
+    for (int q = 0; q < kMergeTiles; ++q) {
+      const int64_t b = g0 + q;
+      base[q] = b * kSortTile;
+      len[q] = (b < ntiles && b != a) ? (int)min((int64_t)kSortTile, n - base[q]) : 0;
+    }
+    // lower bound of v in every tile of the group, the probes of all tiles in flight together
+    for (int it = 0; it < 14; ++it) {
+#pragma unroll
+      for (int q = 0; q < kMergeTiles; ++q) {
+        if (len[q] > 0) {
+          const int half = len[q] >> 1;
+          if (sorted[base[q] + half] < v) {
+            base[q] += half + 1;
+            len[q] -= half + 1;
+          } else {
+            len[q] = half;
+          }
+        }
+      }
+    }
+#pragma unroll
+    for (int q = 0; q < kMergeTiles; ++q) {
+      const int64_t b = g0 + q;
+      if (b < ntiles && b != a) pos += base[q] - b * kSortTile;
+    }
+  }
+  if (pos >= 0 && pos < n) perm[pos] = (int32_t)(v & 0xffffffffu);
+}
+
+size_t dispatch_bpr_ws_bytes(const moe_cfg& c) {
+  const size_t a = (dispatch_ws_bytes(c) + 255) / 256 * 256;
+  const size_t eb = ((size_t)c.T * sizeof(uint64_t) + 255) / 256 * 256;
+  const size_t tb = ((size_t)c.T * sizeof(int32_t) + 255) / 256 * 256;
+  return a + 2 * eb + tb;
+}
+
+void launch_dispatch_bpr(const moe_cfg& c, const void* x, const float* logits, const int32_t* idx, int32_t* fill,
+                         int32_t* slot, void* send_buf, int32_t* order, void* ws, hipStream_t s) {
+  const size_t a = (dispatch_ws_bytes(c) + 255) / 256 * 256;
+  const size_t eb = ((size_t)c.T * sizeof(uint64_t) + 255) / 256 * 256;
+  char* w = (char*)ws + a;
+  uint64_t* e0 = (uint64_t*)w;
+  uint64_t* e1 = (uint64_t*)(w + eb);
+  int32_t* perm = order ? order : (int32_t*)(w + 2 * eb);
+  if (c.T > 0) {
+    static bool attr_set = false;
+    if (!attr_set) {
+      (void)hipFuncSetAttribute((const void*)bpr_tile_sort_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                (int)kTileSortLds);
+      attr_set = true;
+    }
+    const int64_t ntiles = (c.T + kSortTile - 1) / kSortTile;
+    hipLaunchKernelGGL(bpr_key_kernel, dim3((unsigned)((c.T + 3) / 4)), dim3(256), 0, s, logits, idx, e0, c.T, c.E,
+                       c.k);
+    hipLaunchKernelGGL(bpr_tile_sort_kernel, dim3((unsigned)ntiles), dim3(kSortThreads), kTileSortLds, s, e0, e1, c.T);
+    hipLaunchKernelGGL(bpr_merge_kernel, dim3((unsigned)((c.T + 255) / 256)), dim3(256), 0, s, e1, perm, c.T);
+  }
+  dispatch_walk(c, x, idx, perm, nullptr, fill, slot, send_buf, ws, s);
 }
 
 // -------------------------------------------------------------------- combine

@@ -23,11 +23,11 @@ LIB_PATH = os.environ.get("LANCET_MOE_LIB") or os.path.join(_HERE, "liblancet_mo
 MOE_OK, MOE_EINVAL, MOE_ESHAPE, MOE_EALIGN, MOE_EDTYPE, MOE_EDEVICE, MOE_ELAUNCH, MOE_EWORKSPACE = 0, -1, -2, -3, -4, -5, -6, -7
 MOE_F32, MOE_BF16 = 0, 1
 ACTS = {"identity": 0, "relu": 1, "gelu_tanh": 2, "gelu_erf": 3}
-MOE_CALL_DISPATCH, MOE_CALL_BWD_DX, MOE_CALL_BWD_DW, MOE_CALL_FFN_FWD = 0, 1, 2, 3
+MOE_CALL_DISPATCH, MOE_CALL_BWD_DX, MOE_CALL_BWD_DW, MOE_CALL_FFN_FWD, MOE_CALL_DISPATCH_BPR = 0, 1, 2, 3, 4
 
 #: Every symbol include/lancet_moe.h declares.
 EXPORTS = ["moe_capacity", "moe_workspace_bytes", "moe_last_error", "moe_gate_topk", "moe_dispatch",
-           "moe_pack_weights", "moe_expert_ffn_fwd", "moe_combine", "moe_bwd_dx", "moe_bwd_dw",
+           "moe_dispatch_bpr", "moe_pack_weights", "moe_expert_ffn_fwd", "moe_combine", "moe_bwd_dx", "moe_bwd_dw",
            "moe_block_workspace_bytes", "moe_block_chunked"]
 MOE_BLOCK_FWD, MOE_BLOCK_BWD = 1, 2
 
@@ -80,6 +80,7 @@ def _load():
         "moe_last_error": (ctypes.c_char_p, []),
         "moe_gate_topk": (I32, [CFG, P, P, P, P, P, P, P]),
         "moe_dispatch": (I32, [CFG, P, P, P, P, P, P, P, SZ, P]),
+        "moe_dispatch_bpr": (I32, [CFG, P, P, P, P, P, P, P, P, SZ, P]),
         "moe_pack_weights": (I32, [CFG, P, P, P, P, P]),
         "moe_expert_ffn_fwd": (I32, [CFG, P, P, P, P, P, P, P, P, P, SZ, P]),
         "moe_combine": (I32, [CFG, P, P, P, P, P, P]),
@@ -182,6 +183,20 @@ def moe_dispatch(cfg, x, idx, carry, fill, slot, send_buf, ws, stream=None):
                              ws.numel() if ws is not None else 0, _stream(stream)))
 
 
+def moe_dispatch_bpr(cfg, x, logits, idx, fill, slot, send_buf, order, ws, stream=None):
+    dt = torch_dtype(cfg)
+    T, d, E, k = cfg.T, cfg.d_model, cfg.E, cfg.k
+    need = moe_workspace_bytes(cfg, MOE_CALL_DISPATCH_BPR)
+    _check(_lib.moe_dispatch_bpr(ctypes.byref(cfg), _ptr(x, "x", dt, T * d),
+                                 _ptr(logits, "logits", torch.float32, T * E), _ptr(idx, "idx", torch.int32, T * k),
+                                 _ptr(fill, "fill", torch.int32, E), _ptr(slot, "slot", torch.int32, T * k),
+                                 _ptr(send_buf, "send_buf", dt, expert_numel(cfg, d)),
+                                 _ptr(order, "order", torch.int32, T, nullable=True),
+                                 _ptr(ws, "ws", torch.uint8, need, nullable=need == 0),
+                                 ws.numel() if ws is not None else 0,
+                                 _stream(stream)))
+
+
 def moe_pack_weights(cfg, W1, W2, W1p, W2p, stream=None):
     dt = torch_dtype(cfg)
     n = cfg.E * cfg.d_ff * cfg.d_model
@@ -276,6 +291,8 @@ class LayerBuffers:
     ws_ffn: torch.Tensor
     ws_dx: torch.Tensor
     ws_dw: torch.Tensor
+    order: torch.Tensor       # batch-prioritized routing: the visiting order
+    ws_bpr: torch.Tensor
 
 
 def alloc_layer(cfg: moe_cfg, device="cuda") -> LayerBuffers:
@@ -293,15 +310,21 @@ def alloc_layer(cfg: moe_cfg, device="cuda") -> LayerBuffers:
         ws_ffn=e(max(16, moe_workspace_bytes(cfg, MOE_CALL_FFN_FWD)), dtype=torch.uint8),
         ws_dx=e(max(16, moe_workspace_bytes(cfg, MOE_CALL_BWD_DX)), dtype=torch.uint8),
         ws_dw=e(max(16, moe_workspace_bytes(cfg, MOE_CALL_BWD_DW)), dtype=torch.uint8),
+        order=e(max(1, T), dtype=torch.int32),
+        ws_bpr=e(max(16, moe_workspace_bytes(cfg, MOE_CALL_DISPATCH_BPR)), dtype=torch.uint8),
     )
 
 
-def layer_forward(b: LayerBuffers, x, Wg, bias, W1, W2, stream=None):
-    """weight packing -> gate -> dispatch -> experts -> combine, all on one stream."""
+def layer_forward(b: LayerBuffers, x, Wg, bias, W1, W2, stream=None, routing="token"):
+    """weight packing -> gate -> dispatch -> experts -> combine, all on one stream.
+    routing "bpr": batch-prioritized capacity order (no carry-in; b.carry must be zero)."""
     c = b.cfg
     moe_pack_weights(c, W1, W2, b.W1p, b.W2p, stream)
     moe_gate_topk(c, x, Wg, bias, b.logits, b.idx, b.w, stream)
-    moe_dispatch(c, x, b.idx, b.carry, b.fill, b.slot, b.send_buf, b.ws_dispatch, stream)
+    if routing == "bpr":
+        moe_dispatch_bpr(c, x, b.logits, b.idx, b.fill, b.slot, b.send_buf, b.order, b.ws_bpr, stream)
+    else:
+        moe_dispatch(c, x, b.idx, b.carry, b.fill, b.slot, b.send_buf, b.ws_dispatch, stream)
     moe_expert_ffn_fwd(c, b.send_buf, b.carry, b.fill, b.W1p, b.W2p, b.H, b.A, b.O, b.ws_ffn, stream)
     moe_combine(c, b.O, b.idx, b.slot, b.w, b.y, stream)
 

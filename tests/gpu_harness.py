@@ -92,7 +92,7 @@ def nan_fill(b):
         getattr(b, name).fill_(float("nan"))
 
 
-def run_layer(L, spec, inp, C, backward=True, dw_stream=None, carry=None):
+def run_layer(L, spec, inp, C, backward=True, dw_stream=None, carry=None, routing="token"):
     """Run gate -> dispatch -> experts -> combine (and the backward) on cuda:0."""
     dt = torch.bfloat16 if spec.dtype == "bf16" else torch.float32
     cfg = L.make_cfg(inp["x"].shape[0], spec.d, spec.f, spec.E, spec.k, C, spec.G, spec.dtype, spec.act,
@@ -103,7 +103,7 @@ def run_layer(L, spec, inp, C, backward=True, dw_stream=None, carry=None):
         b.carry.copy_(torch.as_tensor(np.asarray(carry), dtype=torch.int32))
     dev = {n: to_dev(inp[n], dt) for n in ("x", "Wg", "W1", "W2", "dy")}
     bias = None if inp.get("bias") is None else torch.as_tensor(inp["bias"], dtype=torch.float32).cuda()
-    L.layer_forward(b, dev["x"], dev["Wg"], bias, dev["W1"], dev["W2"])
+    L.layer_forward(b, dev["x"], dev["Wg"], bias, dev["W1"], dev["W2"], routing=routing)
     if backward:
         L.layer_backward(b, dev["x"], dev["Wg"], dev["dy"], dw_stream=dw_stream)
     torch.cuda.synchronize()

@@ -213,3 +213,19 @@ def test_wpacked_flag_validation():
     assert "wpacked" in L.moe_last_error()
     assert _gate(_cfg(wpacked=1)) == L.MOE_EDEVICE   # valid; no GPU here
     assert ctypes.sizeof(L.moe_cfg) == 48
+
+
+def test_dispatch_bpr_validation():
+    c = _cfg()
+    need = L.moe_workspace_bytes(c, L.MOE_CALL_DISPATCH_BPR)
+    # the dispatch workspace plus two token-sized 64-bit element arrays and the order
+    assert need >= L.moe_workspace_bytes(c, L.MOE_CALL_DISPATCH) + 16 * c.T
+    lib = L._lib
+    f = lib.moe_dispatch_bpr
+    assert f(ctypes.byref(c), GOOD, GOOD, GOOD, GOOD, GOOD, GOOD, None, None, 0, None) == L.MOE_EWORKSPACE
+    assert f(ctypes.byref(c), GOOD, GOOD, GOOD, GOOD, GOOD, GOOD, None, GOOD, need - 1, None) == L.MOE_EWORKSPACE
+    assert f(ctypes.byref(c), GOOD, None, GOOD, GOOD, GOOD, GOOD, None, GOOD, need, None) == L.MOE_EINVAL
+    assert "logits" in L.moe_last_error()
+    assert f(ctypes.byref(c), GOOD, GOOD, GOOD, GOOD, GOOD, GOOD, GOOD + 4, GOOD, need, None) == L.MOE_EALIGN
+    assert f(ctypes.byref(c), GOOD, GOOD, GOOD, GOOD, GOOD, GOOD, None, GOOD, need, None) == L.MOE_EDEVICE
+    assert f(ctypes.byref(c), GOOD, GOOD, GOOD, GOOD, GOOD, GOOD, GOOD, GOOD, need, None) == L.MOE_EDEVICE
