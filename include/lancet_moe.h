@@ -349,6 +349,33 @@ moe_status moe_block_chunked(const moe_block_cfg* cfg, const moe_block_weights* 
                              void* dx, const moe_block_acts* acts, int32_t passes, int32_t n_chunks,
                              const moe_stream_t* streams, void* ws, size_t ws_bytes);
 
+/* ------------------------------------------------------------ host planner */
+
+/* Weight-gradient computation schedule pass (Sec. 4; Alg. 1).  Host only:
+ * every pointer is a host pointer and no GPU is touched.
+ *   The instance: n instructions in a valid execution order, kind[i] = 0
+ *   (other), 1 (all-to-all) or 2 (weight-gradient computation), time[i] >= 0
+ *   (one unit for all), and n_edges dependencies src[e] -> dst[e] (dst
+ *   consumes an output of src; src < dst).
+ *   Labelling (Sec. 4.1): the candidates of an all-to-all a are the
+ *   weight-gradient instructions with no directed path to or from a.
+ *   Assignment (Sec. 4.2): all-to-alls in sequence order; for each, while its
+ *   unoverlapped time t_u > 0 and an unused candidate is left, the candidate
+ *   whose time is closest to t_u (ties: the lower index) is assigned to it and
+ *   t_u decreases by its time.
+ *   Reordering: each assigned instruction moves right after its all-to-all
+ *   (after its last predecessor, if that comes later; an instruction that
+ *   consumes an assigned one not yet placed pulls it in first), so the result
+ *   is always a valid execution order.
+ *   Out: assign[n] = the all-to-all that instruction i overlaps, -1 if none
+ *   (always -1 for other kinds); order[n] = the new sequence (a permutation
+ *   of 0..n-1); *overlap = sum over all-to-alls of min(t_a, assigned time),
+ *   the integer program's objective.  n <= 16384.
+ *   Errors (MOE_EINVAL): unknown kind, negative or non-finite time, an edge
+ *   with src >= dst or outside 0..n-1, a NULL required pointer. */
+moe_status moe_dw_schedule(int32_t n, const int32_t* kind, const double* time, int32_t n_edges, const int32_t* src,
+                           const int32_t* dst, int32_t* assign, int32_t* order, double* overlap);
+
 #ifdef __cplusplus
 }
 #endif

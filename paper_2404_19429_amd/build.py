@@ -18,7 +18,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "liblancet_moe.so")
-SOURCES = ["api.cpp", "block.cpp", "gate.hip", "route.hip", "gemm.hip", "attn.hip", "norm.hip"]
+SOURCES = ["api.cpp", "block.cpp", "plan.cpp", "gate.hip", "route.hip", "gemm.hip", "attn.hip", "norm.hip"]
 ARCH = "gfx950"
 
 HIPCC_FLAGS = [

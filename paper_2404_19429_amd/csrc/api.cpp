@@ -175,6 +175,18 @@ moe_status moe_dispatch_bpr(const moe_cfg* cfg, const void* x, const float* logi
   return check_launch(fn);
 }
 
+moe_status moe_dw_schedule(int32_t n, const int32_t* kind, const double* time, int32_t n_edges, const int32_t* src,
+                           const int32_t* dst, int32_t* assign, int32_t* order, double* overlap) {
+  const char* fn = "moe_dw_schedule";
+  if (overlap == nullptr) return fail(MOE_EINVAL, "%s: overlap is NULL", fn);
+  if (n > 0 && (kind == nullptr || time == nullptr || assign == nullptr || order == nullptr))
+    return fail(MOE_EINVAL, "%s: kind, time, assign and order are required", fn);
+  if (n_edges > 0 && (src == nullptr || dst == nullptr)) return fail(MOE_EINVAL, "%s: src and dst are required", fn);
+  const std::string err = lmoe::dw_schedule(n, kind, time, n_edges, src, dst, assign, order, overlap);
+  if (!err.empty()) return fail(MOE_EINVAL, "%s: %s", fn, err.c_str());
+  return ok();
+}
+
 moe_status moe_pack_weights(const moe_cfg* cfg, const void* W1, const void* W2, void* W1p, void* W2p,
                             moe_stream_t stream) {
   const char* fn = "moe_pack_weights";

@@ -1,6 +1,9 @@
 // Internal launchers shared between the kernel files and the C-ABI layer.
 #pragma once
 
+#include <algorithm>
+#include <string>
+
 #include "common.h"
 
 namespace lmoe {
@@ -8,6 +11,11 @@ namespace lmoe {
 constexpr int kMaxK = 8;       // largest supported top-k
 constexpr int kMaxE = 64;      // largest supported expert count (one lane per expert in the gate)
 constexpr int kRouteChunk = 256;  // tokens per slot-assignment chunk
+
+// plan.cpp (host only): the weight-gradient computation schedule pass.
+constexpr int kMaxPlanInstr = 1 << 14;
+std::string dw_schedule(int n, const int32_t* kind, const double* time, int n_edges, const int32_t* src,
+                        const int32_t* dst, int32_t* assign, int32_t* order, double* overlap);
 
 // gate.hip
 void launch_gate(const moe_cfg& c, const void* x, const void* Wg, const float* bias, float* logits,

@@ -1,0 +1,142 @@
+// Host-side planner: the weight-gradient computation schedule pass (Sec. 4:
+// labelling by dependency paths, Sec. 4.1; the greedy best-fit assignment of
+// weight-gradient operations to all-to-alls, Sec. 4.2 and Alg. 1; and the
+// reordering that places each assigned operation right after its
+// all-to-all).  Plain C++, no device code; the C ABI entry is
+// moe_dw_schedule.
+#include <cmath>
+#include <cstdint>
+#include <string>
+#include <vector>
+
+#include "internal.h"
+
+namespace lmoe {
+
+namespace {
+
+constexpr int kOther = 0, kA2A = 1, kDW = 2;
+
+struct Reorder {
+  const std::vector<std::vector<int>>& pred;   // ascending
+  const std::vector<int32_t>& asg;             // DW -> all-to-all, or -1
+  std::vector<char> emitted;
+  std::vector<int32_t> out;
+
+  // Emits i after the not-yet-emitted assigned operations it consumes.
+  void pull(int i) {
+    for (int p : pred[i])
+      if (!emitted[p]) pull(p);
+    if (!emitted[i]) {
+      emitted[i] = 1;
+      out.push_back(i);
+    }
+  }
+  // Emits, in index order and until nothing changes, every assigned operation
+  // whose all-to-all and predecessors are out.
+  void flush(const std::vector<int>& assigned) {
+    for (bool changed = true; changed;) {
+      changed = false;
+      for (int j : assigned) {
+        if (emitted[j] || !emitted[asg[j]]) continue;
+        bool ready = true;
+        for (int p : pred[j]) ready = ready && emitted[p];
+        if (ready) {
+          emitted[j] = 1;
+          out.push_back(j);
+          changed = true;
+        }
+      }
+    }
+  }
+};
+
+}  // namespace
+
+std::string dw_schedule(int n, const int32_t* kind, const double* time, int n_edges, const int32_t* src,
+                        const int32_t* dst, int32_t* assign, int32_t* order, double* overlap) {
+  if (n < 0 || n > kMaxPlanInstr) return "n outside 0.." + std::to_string(kMaxPlanInstr);
+  if (n_edges < 0) return "n_edges < 0";
+  for (int i = 0; i < n; ++i) {
+    if (kind[i] != kOther && kind[i] != kA2A && kind[i] != kDW) return "kind[" + std::to_string(i) + "] unknown";
+    if (!std::isfinite(time[i]) || time[i] < 0) return "time[" + std::to_string(i) + "] not a finite value >= 0";
+  }
+  std::vector<std::vector<int>> succ(n), pred(n);
+  for (int e = 0; e < n_edges; ++e) {
+    if (src[e] < 0 || dst[e] >= n || src[e] >= dst[e])
+      return "edge " + std::to_string(e) + " is not src < dst within 0..n-1 (the sequence must be an execution order)";
+    succ[src[e]].push_back(dst[e]);
+    pred[dst[e]].push_back(src[e]);
+  }
+  for (auto& p : pred) std::sort(p.begin(), p.end()), p.erase(std::unique(p.begin(), p.end()), p.end());
+
+  // Labelling: reach[i] = the operations with a path from i, as bit rows,
+  // built from the end of the sequence (every edge points forward).
+  const int words = (n + 63) / 64;
+  std::vector<uint64_t> reach((size_t)n * words, 0ull);
+  for (int i = n - 1; i >= 0; --i) {
+    uint64_t* ri = &reach[(size_t)i * words];
+    for (int j : succ[i]) {
+      const uint64_t* rj = &reach[(size_t)j * words];
+      for (int w = 0; w < words; ++w) ri[w] |= rj[w];
+      ri[j >> 6] |= 1ull << (j & 63);
+    }
+  }
+  auto path = [&](int a, int b) { return (reach[(size_t)a * words + (b >> 6)] >> (b & 63)) & 1ull; };
+
+  // Greedy assignment, all-to-alls in sequence order.
+  std::vector<int32_t> asg(n, -1);
+  std::vector<char> used(n, 0);
+  std::vector<int> cand;
+  std::vector<double> assigned_time(n, 0.0);
+  for (int a = 0; a < n; ++a) {
+    if (kind[a] != kA2A) continue;
+    cand.clear();
+    for (int j = 0; j < n; ++j)
+      if (j != a && kind[j] == kDW && !path(a, j) && !path(j, a)) cand.push_back(j);
+    double t_u = time[a];
+    while (t_u > 0) {
+      int best = -1;
+      double bd = 0.0;
+      for (int j : cand) {
+        if (used[j]) continue;
+        const double dj = std::fabs(t_u - time[j]);
+        if (best < 0 || dj < bd) {   // ties keep the lower index
+          best = j;
+          bd = dj;
+        }
+      }
+      if (best < 0) break;
+      t_u -= time[best];
+      used[best] = 1;
+      asg[best] = a;
+      assigned_time[a] += time[best];
+    }
+  }
+  double ov = 0.0;
+  for (int a = 0; a < n; ++a)
+    if (kind[a] == kA2A) ov += std::min(time[a], assigned_time[a]);
+
+  // Reordering.
+  std::vector<int> assigned;
+  for (int j = 0; j < n; ++j)
+    if (asg[j] >= 0) assigned.push_back(j);
+  Reorder R{pred, asg, std::vector<char>(n, 0), {}};
+  R.out.reserve(n);
+  for (int i = 0; i < n; ++i) {
+    if (asg[i] >= 0 || R.emitted[i]) continue;
+    R.pull(i);
+    R.flush(assigned);
+  }
+  for (int j : assigned)
+    if (!R.emitted[j]) R.pull(j);
+
+  for (int i = 0; i < n; ++i) {
+    assign[i] = asg[i];
+    order[i] = R.out[i];
+  }
+  *overlap = ov;
+  return "";
+}
+
+}  // namespace lmoe

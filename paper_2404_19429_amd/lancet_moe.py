@@ -28,7 +28,7 @@ MOE_CALL_DISPATCH, MOE_CALL_BWD_DX, MOE_CALL_BWD_DW, MOE_CALL_FFN_FWD, MOE_CALL_
 #: Every symbol include/lancet_moe.h declares.
 EXPORTS = ["moe_capacity", "moe_workspace_bytes", "moe_last_error", "moe_gate_topk", "moe_dispatch",
            "moe_dispatch_bpr", "moe_pack_weights", "moe_expert_ffn_fwd", "moe_combine", "moe_bwd_dx", "moe_bwd_dw",
-           "moe_block_workspace_bytes", "moe_block_chunked"]
+           "moe_block_workspace_bytes", "moe_block_chunked", "moe_dw_schedule"]
 MOE_BLOCK_FWD, MOE_BLOCK_BWD = 1, 2
 
 
@@ -86,6 +86,7 @@ def _load():
         "moe_combine": (I32, [CFG, P, P, P, P, P, P]),
         "moe_bwd_dx": (I32, [CFG] + [P] * 18 + [SZ, P]),
         "moe_bwd_dw": (I32, [CFG] + [P] * 12 + [SZ, P]),
+        "moe_dw_schedule": (I32, [I32, P, P, I32, P, P, P, P, P]),
         "moe_block_workspace_bytes": (SZ, [ctypes.POINTER(moe_block_cfg), I32]),
         "moe_block_chunked": (I32, [ctypes.POINTER(moe_block_cfg), ctypes.POINTER(moe_block_weights),
                                     ctypes.POINTER(moe_block_grads), P, P, P, P, ctypes.POINTER(moe_block_acts),
@@ -195,6 +196,25 @@ def moe_dispatch_bpr(cfg, x, logits, idx, fill, slot, send_buf, order, ws, strea
                                  _ptr(ws, "ws", torch.uint8, need, nullable=need == 0),
                                  ws.numel() if ws is not None else 0,
                                  _stream(stream)))
+
+
+def moe_dw_schedule(kinds, times, edges):
+    """Weight-gradient schedule pass on the host (see include/lancet_moe.h).
+    kinds: 0 other / 1 all-to-all / 2 weight gradient; times: per instruction;
+    edges: (src, dst) pairs.  Returns (assign [n] int32, order [n] int32, overlap)."""
+    import numpy as np
+    kinds = np.ascontiguousarray(kinds, np.int32)
+    times = np.ascontiguousarray(times, np.float64)
+    e = np.ascontiguousarray(np.asarray(edges, np.int32).reshape(-1, 2))
+    src, dst = np.ascontiguousarray(e[:, 0]), np.ascontiguousarray(e[:, 1])
+    n = int(kinds.size)
+    assign = np.empty(n, np.int32)
+    order = np.empty(n, np.int32)
+    ov = ctypes.c_double(0.0)
+    p = lambda a: a.ctypes.data_as(ctypes.c_void_p) if a.size else None
+    _check(_lib.moe_dw_schedule(n, p(kinds), p(times), int(src.size), p(src), p(dst), p(assign), p(order),
+                                ctypes.byref(ov)))
+    return assign, order, ov.value
 
 
 def moe_pack_weights(cfg, W1, W2, W1p, W2p, stream=None):
