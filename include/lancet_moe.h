@@ -376,6 +376,36 @@ moe_status moe_block_chunked(const moe_block_cfg* cfg, const moe_block_weights* 
 moe_status moe_dw_schedule(int32_t n, const int32_t* kind, const double* time, int32_t n_edges, const int32_t* src,
                            const int32_t* dst, int32_t* assign, int32_t* order, double* overlap);
 
+/* Operator-partition pass: pipeline cost and partition-range choice (Sec. 5.1
+ * dynamic program; Sec. 5.3 pipeline scheduler).  Host only.
+ *   The instance: N forward instructions in execution order, kind[j] = 0
+ *   (computation) or 1 (communication); times[j * K + (k - 1)] = the time of
+ *   one of k parts of instruction j when its range is split k ways (k = 1:
+ *   unsplit; +inf: it cannot be split k ways; the k = 1 time must be finite);
+ *   join[k - 1] = the cost of splitting a range's inputs and joining its
+ *   outputs for k parts (join[0] is not used).
+ *   Range cost P(i, n, k) of instructions i..n (1-based): k = 1, the sum of
+ *   the times; otherwise the range's stages (maximal runs of one kind) are
+ *   laid out for k partitions, each partition's stage after its previous
+ *   stage and after the previous instruction of the same kind in the order
+ *   stage by stage, partition by partition; P = the end of the last one plus
+ *   join[k - 1].
+ *   Plan: T(0) = 0, T(n) = min over ranges i..n of at most G instructions
+ *   (G <= 0: no limit) and k = 1..K of T(i - 1) + P(i, n, k); ties take the
+ *   smaller i, then the smaller k.
+ *   Out: *n_seg ranges seg_begin..seg_end (1-based, in order) with their
+ *   seg_k (arrays of N entries); *total = T(N).  N <= 16384, K <= 64.
+ *   Errors (MOE_EINVAL): bad kinds, NaN or negative times, infinite unsplit
+ *   times, bad join values, NULL required pointers. */
+moe_status moe_pipeline_plan(int32_t N, int32_t K, const int32_t* kind, const double* times, const double* join,
+                             int32_t G, int32_t* seg_begin, int32_t* seg_end, int32_t* seg_k, int32_t* n_seg,
+                             double* total);
+
+/* P(i, n, k) of moe_pipeline_plan alone (same instance arguments): the
+ * predicted time of instructions i..n split k ways. */
+moe_status moe_pipeline_range_cost(int32_t N, int32_t K, const int32_t* kind, const double* times,
+                                   const double* join, int32_t i, int32_t n, int32_t k, double* cost);
+
 #ifdef __cplusplus
 }
 #endif

@@ -187,6 +187,29 @@ moe_status moe_dw_schedule(int32_t n, const int32_t* kind, const double* time, i
   return ok();
 }
 
+moe_status moe_pipeline_plan(int32_t N, int32_t K, const int32_t* kind, const double* times, const double* join,
+                             int32_t G, int32_t* seg_begin, int32_t* seg_end, int32_t* seg_k, int32_t* n_seg,
+                             double* total) {
+  const char* fn = "moe_pipeline_plan";
+  if (n_seg == nullptr || total == nullptr || join == nullptr) return fail(MOE_EINVAL, "%s: join, n_seg and total are required", fn);
+  if (N > 0 && (kind == nullptr || times == nullptr || seg_begin == nullptr || seg_end == nullptr || seg_k == nullptr))
+    return fail(MOE_EINVAL, "%s: kind, times and the segment arrays are required", fn);
+  const std::string err = lmoe::pipeline_plan(N, K, kind, times, join, G, seg_begin, seg_end, seg_k, n_seg, total);
+  if (!err.empty()) return fail(MOE_EINVAL, "%s: %s", fn, err.c_str());
+  return ok();
+}
+
+moe_status moe_pipeline_range_cost(int32_t N, int32_t K, const int32_t* kind, const double* times,
+                                   const double* join, int32_t i, int32_t n, int32_t k, double* cost) {
+  const char* fn = "moe_pipeline_range_cost";
+  if (cost == nullptr || kind == nullptr || times == nullptr || join == nullptr)
+    return fail(MOE_EINVAL, "%s: kind, times, join and cost are required", fn);
+  if (K < 1 || K > 64 || k < 1 || k > K || i < 1 || n < i || n > N)
+    return fail(MOE_EINVAL, "%s: need 1 <= i <= n <= N and 1 <= k <= K <= 64", fn);
+  *cost = lmoe::pipeline_range_cost(N, K, kind, times, join, i, n, k);
+  return ok();
+}
+
 moe_status moe_pack_weights(const moe_cfg* cfg, const void* W1, const void* W2, void* W1p, void* W2p,
                             moe_stream_t stream) {
   const char* fn = "moe_pack_weights";

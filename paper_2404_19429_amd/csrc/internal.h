@@ -17,6 +17,11 @@ constexpr int kMaxPlanInstr = 1 << 14;
 std::string dw_schedule(int n, const int32_t* kind, const double* time, int n_edges, const int32_t* src,
                         const int32_t* dst, int32_t* assign, int32_t* order, double* overlap);
 
+double pipeline_range_cost(int N, int K, const int32_t* kind, const double* times, const double* join, int i, int n,
+                           int k);
+std::string pipeline_plan(int N, int K, const int32_t* kind, const double* times, const double* join, int G,
+                          int32_t* seg_begin, int32_t* seg_end, int32_t* seg_k, int32_t* n_seg, double* total);
+
 // gate.hip
 void launch_gate(const moe_cfg& c, const void* x, const void* Wg, const float* bias, float* logits,
                  int32_t* idx, float* w, hipStream_t s);

@@ -1,9 +1,12 @@
-// Host-side planner: the weight-gradient computation schedule pass (Sec. 4:
-// labelling by dependency paths, Sec. 4.1; the greedy best-fit assignment of
-// weight-gradient operations to all-to-alls, Sec. 4.2 and Alg. 1; and the
-// reordering that places each assigned operation right after its
-// all-to-all).  Plain C++, no device code; the C ABI entry is
-// moe_dw_schedule.
+// Host-side planners, plain C++ with no device code:
+// * the weight-gradient computation schedule pass (Sec. 4: labelling by
+//   dependency paths, Sec. 4.1; the greedy best-fit assignment of
+//   weight-gradient operations to all-to-alls, Sec. 4.2 and Alg. 1; and the
+//   reordering that places each assigned operation right after its
+//   all-to-all) -- C ABI moe_dw_schedule;
+// * the operator-partition pass's pipeline cost and range choice (Sec. 5.1's
+//   dynamic program over Sec. 5.3's timeline simulation) -- C ABI
+//   moe_pipeline_plan.
 #include <cmath>
 #include <cstdint>
 #include <string>
@@ -136,6 +139,93 @@ std::string dw_schedule(int n, const int32_t* kind, const double* time, int n_ed
     order[i] = R.out[i];
   }
   *overlap = ov;
+  return "";
+}
+
+// ----------------------------------------------------------- partition ranges
+
+namespace {
+
+// End time of k partitions of the stages (kind, one partition's time): a
+// partition's stage starts after its previous stage and after the previous
+// instruction of its kind in the order stage by stage, partition by
+// partition.
+double simulate_stages(const std::vector<std::pair<int, double>>& st, int k, std::vector<double>& prev) {
+  prev.assign(k, 0.0);
+  double free_[2] = {0.0, 0.0};
+  double last = 0.0;
+  for (const auto& sd : st) {
+    for (int p = 0; p < k; ++p) {
+      const double s = std::max(prev[p], free_[sd.first]);
+      const double e = s + sd.second;
+      prev[p] = e;
+      free_[sd.first] = e;
+      last = std::max(last, e);
+    }
+  }
+  return last;
+}
+
+}  // namespace
+
+double pipeline_range_cost(int N, int K, const int32_t* kind, const double* times, const double* join, int i, int n,
+                           int k) {
+  (void)N;
+  std::vector<std::pair<int, double>> st;
+  double sum = 0.0;
+  for (int j = i - 1; j < n; ++j) {
+    const double t = times[(size_t)j * K + (k - 1)];
+    if (std::isinf(t)) return INFINITY;
+    sum += t;
+    if (!st.empty() && st.back().first == kind[j]) st.back().second += t;
+    else st.emplace_back(kind[j], t);
+  }
+  if (k == 1) return sum;
+  std::vector<double> prev;
+  return simulate_stages(st, k, prev) + join[k - 1];
+}
+
+std::string pipeline_plan(int N, int K, const int32_t* kind, const double* times, const double* join, int G,
+                          int32_t* seg_begin, int32_t* seg_end, int32_t* seg_k, int32_t* n_seg, double* total) {
+  if (N < 0 || N > kMaxPlanInstr) return "N outside 0.." + std::to_string(kMaxPlanInstr);
+  if (K < 1 || K > 64) return "K outside 1..64";
+  for (int j = 0; j < N; ++j) {
+    if (kind[j] != 0 && kind[j] != 1) return "kind[" + std::to_string(j) + "] is neither 0 nor 1";
+    for (int k = 0; k < K; ++k) {
+      const double t = times[(size_t)j * K + k];
+      if (std::isnan(t) || t < 0 || (k == 0 && std::isinf(t)))
+        return "times[" + std::to_string(j) + "][" + std::to_string(k) + "] invalid (unsplit times must be finite)";
+    }
+  }
+  for (int k = 0; k < K; ++k)
+    if (!std::isfinite(join[k]) || join[k] < 0) return "join[" + std::to_string(k) + "] not a finite value >= 0";
+  if (G <= 0 || G > N) G = N;
+  std::vector<double> T(N + 1, INFINITY);
+  std::vector<int> ai(N + 1, 0), ak(N + 1, 0);
+  T[0] = 0.0;
+  for (int n = 1; n <= N; ++n) {
+    for (int i = std::max(1, n - G + 1); i <= n; ++i) {
+      for (int k = 1; k <= K; ++k) {
+        const double c = T[i - 1] + pipeline_range_cost(N, K, kind, times, join, i, n, k);
+        if (c < T[n]) {
+          T[n] = c;
+          ai[n] = i;
+          ak[n] = k;
+        }
+      }
+    }
+  }
+  int cnt = 0;
+  for (int n = N; n > 0; n = ai[n] - 1) ++cnt;
+  int q = cnt;
+  for (int n = N; n > 0; n = ai[n] - 1) {
+    --q;
+    seg_begin[q] = ai[n];
+    seg_end[q] = n;
+    seg_k[q] = ak[n];
+  }
+  *n_seg = cnt;
+  *total = T[N];
   return "";
 }
 

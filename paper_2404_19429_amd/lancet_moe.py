@@ -28,7 +28,8 @@ MOE_CALL_DISPATCH, MOE_CALL_BWD_DX, MOE_CALL_BWD_DW, MOE_CALL_FFN_FWD, MOE_CALL_
 #: Every symbol include/lancet_moe.h declares.
 EXPORTS = ["moe_capacity", "moe_workspace_bytes", "moe_last_error", "moe_gate_topk", "moe_dispatch",
            "moe_dispatch_bpr", "moe_pack_weights", "moe_expert_ffn_fwd", "moe_combine", "moe_bwd_dx", "moe_bwd_dw",
-           "moe_block_workspace_bytes", "moe_block_chunked", "moe_dw_schedule"]
+           "moe_block_workspace_bytes", "moe_block_chunked", "moe_dw_schedule", "moe_pipeline_plan",
+           "moe_pipeline_range_cost"]
 MOE_BLOCK_FWD, MOE_BLOCK_BWD = 1, 2
 
 
@@ -87,6 +88,8 @@ def _load():
         "moe_bwd_dx": (I32, [CFG] + [P] * 18 + [SZ, P]),
         "moe_bwd_dw": (I32, [CFG] + [P] * 12 + [SZ, P]),
         "moe_dw_schedule": (I32, [I32, P, P, I32, P, P, P, P, P]),
+        "moe_pipeline_plan": (I32, [I32, I32, P, P, P, I32, P, P, P, P, P]),
+        "moe_pipeline_range_cost": (I32, [I32, I32, P, P, P, I32, I32, I32, P]),
         "moe_block_workspace_bytes": (SZ, [ctypes.POINTER(moe_block_cfg), I32]),
         "moe_block_chunked": (I32, [ctypes.POINTER(moe_block_cfg), ctypes.POINTER(moe_block_weights),
                                     ctypes.POINTER(moe_block_grads), P, P, P, P, ctypes.POINTER(moe_block_acts),
@@ -215,6 +218,37 @@ def moe_dw_schedule(kinds, times, edges):
     _check(_lib.moe_dw_schedule(n, p(kinds), p(times), int(src.size), p(src), p(dst), p(assign), p(order),
                                 ctypes.byref(ov)))
     return assign, order, ov.value
+
+
+def _pipeline_args(kinds, times, join):
+    import numpy as np
+    kinds = np.ascontiguousarray(kinds, np.int32)
+    times = np.ascontiguousarray(times, np.float64).reshape(kinds.size, -1)
+    join = np.ascontiguousarray(join, np.float64)
+    assert times.shape[1] == join.size, "times needs one column per k = 1..K"
+    p = lambda a: a.ctypes.data_as(ctypes.c_void_p) if a.size else None
+    return kinds, times, join, p
+
+
+def moe_pipeline_plan(kinds, times, join, G=0):
+    """Partition-range plan on the host (see include/lancet_moe.h).  times [N][K],
+    join [K].  Returns (T(N), [(begin, end, k), ...] 1-based inclusive)."""
+    import numpy as np
+    kinds, times, join, p = _pipeline_args(kinds, times, join)
+    N, K = int(kinds.size), int(join.size)
+    b, e, k = (np.zeros(max(N, 1), np.int32) for _ in range(3))
+    n_seg, total = ctypes.c_int32(0), ctypes.c_double(0.0)
+    _check(_lib.moe_pipeline_plan(N, K, p(kinds), p(times), p(join), int(G), p(b), p(e), p(k), ctypes.byref(n_seg),
+                                  ctypes.byref(total)))
+    return total.value, [(int(b[q]), int(e[q]), int(k[q])) for q in range(n_seg.value)]
+
+
+def moe_pipeline_range_cost(kinds, times, join, i, n, k):
+    kinds, times, join, p = _pipeline_args(kinds, times, join)
+    c = ctypes.c_double(0.0)
+    _check(_lib.moe_pipeline_range_cost(int(kinds.size), int(join.size), p(kinds), p(times), p(join), int(i), int(n),
+                                        int(k), ctypes.byref(c)))
+    return c.value
 
 
 def moe_pack_weights(cfg, W1, W2, W1p, W2p, stream=None):

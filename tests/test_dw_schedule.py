@@ -127,3 +127,37 @@ def test_block_backward_schedule():
     # every all-to-all of the lower block has weight gradients of the upper block to hide behind
     lower = [i for i in range(len(BLOCK_OPS), n) if kinds[i] == A2A]
     assert all(any(x == i for x in asg.values()) for i in lower)
+
+
+# ------------------------------------------------ partition-range planner
+from oracle import pipeline_oracle as PO  # noqa: E402
+
+
+@pytest.mark.parametrize("seed", range(30))
+def test_pipeline_planner_matches_oracle(seed):
+    rng = np.random.default_rng(500 + seed)
+    N = int(rng.integers(1, 40))
+    K = int(rng.integers(1, 9))
+    kinds = [int(rng.integers(0, 2)) for _ in range(N)]
+    times = []
+    for _ in range(N):
+        t1 = float(rng.integers(1, 50)) if rng.random() < 0.5 else float(rng.random() * 40)
+        row = [t1] + [t1 / k + float(rng.random()) for k in range(2, K + 1)]
+        if rng.random() < 0.1 and K > 1:
+            row[int(rng.integers(1, K))] = float("inf")
+        times.append(row)
+    join = [0.0] + [float(rng.random() * 3) for _ in range(K - 1)]
+    G = int(rng.integers(0, N + 1))
+    T, segs = PO.plan(kinds, times, join, G)
+    t2, s2 = L.moe_pipeline_plan(kinds, times, join, G)
+    assert t2 == T and s2 == segs
+    i, n = sorted(int(v) for v in rng.integers(1, N + 1, 2))
+    for k in range(1, K + 1):
+        assert L.moe_pipeline_range_cost(kinds, times, join, i, n, k) == PO.range_cost(kinds, times, join, i, n, k)
+
+
+def test_pipeline_planner_rejects_invalid():
+    for kinds, times, join in [([2], [[1.0]], [0.0]), ([0], [[float("nan")]], [0.0]), ([0], [[float("inf")]], [0.0]),
+                               ([0], [[1.0, 1.0]], [0.0, -1.0])]:
+        with pytest.raises(L.MoeError):
+            L.moe_pipeline_plan(kinds, times, join)
