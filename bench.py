@@ -88,6 +88,9 @@ def _args():
                     help="run one plain device copy of this many MiB first (calibrates HBM byte counters)")
     ap.add_argument("--cpu-sample-tokens", type=int, default=8192)
     ap.add_argument("--workload", default="layer", choices=["layer", "block"])
+    ap.add_argument("--pipeline-check", action="store_true",
+                    help="block workload: predict the partitioned forward's time for 1, 2, 4, 8 partitions with the "
+                         "library's pipeline simulator from measured stage times, and compare with the measured time")
     ap.add_argument("--routing", default="token", choices=["token", "bpr"],
                     help="capacity order of the layer step: token order, or batch-prioritized (importance order)")
     return ap.parse_args()
@@ -224,9 +227,105 @@ def main_block(a):
         "pipelining_gain_fwd_ms": variants["fwd_4part_1stream"] - variants["fwd_4part_3streams"],
         "deferred_dw_gain_bwd_ms": variants["bwd_1stream"] - variants["bwd_3streams"],
     }
+    if a.pipeline_check:
+        del bufs
+        res["pipeline_check"] = pipeline_check(L, torch, spec, cfg, w, x, out, dy, dx, main, three, one)
     if not a.no_cpu_baseline:
         res["cpu_baseline"] = block_cpu_baseline(spec, inp, 512)
     print(json.dumps(res), flush=True)
+
+
+def pipeline_check(L, torch, spec, cfg, w, x, out, dy, dx, main, three, one):
+    """The block forward split into k = 1, 2, 4, 8 batch partitions: stage times
+    of one partition (pre-MoE computation up to the gate; dispatch; experts;
+    combine) measured at T / k tokens, plus the expert weight packing the
+    forward does once, the pipelined time the library's
+    simulator predicts from them (moe_pipeline_range_cost: compute stages on
+    one resource, dispatch/combine on another), and the measured time of the
+    partitioned forward on three streams.  On one GPU the dispatch/combine
+    stream shares the compute units, which the simulator does not model."""
+    m = spec.moe
+    ks = [k for k in (1, 2, 4, 8) if spec.B % k == 0]
+    ev = lambda: torch.cuda.Event(enable_timing=True)
+
+    def avg_ms(fn, reps=5, warm=2):
+        for _ in range(warm):
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = ev(), ev()
+        e0.record(main)
+        for _ in range(reps):
+            fn()
+        e1.record(main)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps
+
+    stage = {}
+    for k in ks:
+        B1 = spec.B // k
+        T1 = B1 * spec.S
+        C1 = L.moe_capacity(T1, m.E, m.k, m.cf_num, m.cf_den)
+        c1 = L.make_block_cfg(B1, spec.S, spec.heads, m.f, m.E, m.k, C1, m.G, m.act, m.renorm)
+        b = L.alloc_block(c1, 1)
+        n1 = T1 * spec.d
+        xs, outs = x[:n1], out[:n1]
+        fwd = avg_ms(lambda: L.moe_block_chunked(c1, w, b, xs, outs, None, None, b, L.MOE_BLOCK_FWD, 1, one, b["ws"]))
+        mc = c1.moe
+        ws_d = torch.empty(max(16, L.moe_workspace_bytes(mc, L.MOE_CALL_DISPATCH)), dtype=torch.uint8, device="cuda")
+        ws_f = torch.empty(max(16, L.moe_workspace_bytes(mc, L.MOE_CALL_FFN_FWD)), dtype=torch.uint8, device="cuda")
+        y = b["dm"][:n1]
+        disp = avg_ms(lambda: L.moe_dispatch(mc, b["m"], b["idx"], None, b["fill"], b["slot"], b["send_buf"], ws_d))
+        ffn = avg_ms(lambda: L.moe_expert_ffn_fwd(mc, b["send_buf"], None, b["fill"], b["W1p"], b["W2p"], b["H"],
+                                                  b["A"], b["expert_out"], ws_f))
+        comb = avg_ms(lambda: L.moe_combine(mc, b["expert_out"], b["idx"], b["slot"], b["w"], y))
+        pack = avg_ms(lambda: L.moe_pack_weights(mc, w["W1"], w["W2"], b["W1p"], b["W2p"]))
+        stage[k] = [pack, max(0.0, fwd - pack - disp - ffn - comb), disp, ffn, comb]
+        if k == 1:
+            kept_rows = int(b["fill"].sum().item())
+        del b, ws_d, ws_f
+        torch.cuda.empty_cache()
+    # expert weight packing (once per forward, not split), then per partition:
+    # computation up to the gate, dispatch, experts, combine
+    kinds = [0, 0, 1, 0, 1]
+    K = max(ks)
+    inf = float("inf")
+    times = [[stage[1][0]] + [inf] * (K - 1)]
+    times += [[stage[k][j] if k in stage else inf for k in range(1, K + 1)] for j in range(1, 5)]
+    join = [0.0] * K                         # partitions are contiguous slices of the batch: no split/join work
+    outk = {}
+    for k in ks:
+        bk = L.alloc_block(cfg, k)
+
+        def fwd_k(streams, bk=bk, k=k):
+            L.moe_block_chunked(cfg, w, bk, x, out, None, None, bk, L.MOE_BLOCK_FWD, k, streams, bk["ws"])
+        meas = avg_ms(lambda: fwd_k(three), reps=5)
+        meas1 = avg_ms(lambda: fwd_k(one), reps=5)
+        pred = times[0][0] + L.moe_pipeline_range_cost(kinds, times, join, 2, 5, k)
+        outk[str(k)] = {"stage_ms": [round(v, 4) for v in stage[k]], "predicted_ms": pred,
+                        "measured_3streams_ms": meas, "measured_1stream_ms": meas1,
+                        "error": (pred - meas) / meas}
+        del bk
+        torch.cuda.empty_cache()
+    total, segs = L.moe_pipeline_plan(kinds, times, join)
+    # What the same plan does when dispatch and combine are real all-to-alls
+    # between 8 GPUs (2 experts each): a GPU sends 7/8 of its kept rows, over 7
+    # xGMI links of 153 GB/s, or over one 100 Gb/s network port.
+    a2a_mb = kept_rows * spec.d * 2 * 7 / 8 / 1e6
+    what_if = {}
+    for net, gbps in (("xgmi_7x153GBps", 7 * 153.0), ("nic_100Gbps", 12.5)):
+        tw = [row[:] for row in times]
+        for j in (2, 4):
+            for k in range(1, K + 1):
+                if tw[j][k - 1] != inf:
+                    tw[j][k - 1] = a2a_mb / k / gbps       # ms: MB / (GB/s)
+        tot_w, segs_w = L.moe_pipeline_plan(kinds, tw, join)
+        what_if[net] = {"a2a_ms_unsplit": a2a_mb / gbps,
+                        "predicted_ms": {str(k): tw[0][0] + L.moe_pipeline_range_cost(kinds, tw, join, 2, 5, k)
+                                         for k in ks},
+                        "dp_plan": {"predicted_ms": tot_w, "ranges": segs_w}}
+    return {"per_partitions": outk, "dp_plan": {"predicted_ms": total, "ranges": segs},
+            "what_if_all_to_all": what_if,
+            "stages": ["weight packing", "pre-MoE computation + gate", "dispatch", "experts", "combine"]}
 
 
 def main():
