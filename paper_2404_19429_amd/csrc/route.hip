@@ -556,37 +556,56 @@ void launch_combine(const moe_cfg& c, const void* O, const int32_t* idx, const i
 
 // ------------------------------------------------------ combine + gate backward
 // One wavefront per token: dO[e][s] = w dy, g_r = <dy, O[e][s]>, then dlogits.
-template <typename T>
+template <typename T, int KT>
 __global__ __launch_bounds__(256) void combine_bwd_kernel(const float* __restrict__ logits,
                                                           const int32_t* __restrict__ idx,
                                                           const float* __restrict__ w,
                                                           const int32_t* __restrict__ slot,
                                                           const T* __restrict__ O, const T* __restrict__ dy,
                                                           T* __restrict__ dO, float* __restrict__ dlogits,
-                                                          int64_t T_tokens, int d, int E, int k, int C, int renorm) {
+                                                          int64_t T_tokens, int d, int E, int kr, int C, int renorm) {
   constexpr int V = Vec<T>::N;
+  constexpr int KK = KT > 0 ? KT : kMaxK;
+  const int k = KT > 0 ? KT : kr;
   const int lane = threadIdx.x & 63;
   const int64_t t = (int64_t)blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6);
   if (t >= T_tokens) return;
-  int er[kMaxK], sr[kMaxK];
-  float wr[kMaxK], gp[kMaxK];
+  int er[KK], sr[KK];
+  float wr[KK], gp[KK];
 #pragma unroll
-  for (int r = 0; r < kMaxK; ++r) {
+  for (int r = 0; r < KK; ++r) {
     er[r] = r < k ? idx[t * k + r] : 0;
     sr[r] = r < k ? slot[t * k + r] : -1;
     if (er[r] < 0 || er[r] >= E || sr[r] >= C) { er[r] = 0; sr[r] = -1; }
     wr[r] = r < k ? w[t * k + r] : 0.f;
     gp[r] = 0.f;
   }
+  // Two 16-byte chunks per lane per round: every dy and O load of the round
+  // is issued before the first product and store.
   const int nc = d / V;
-  for (int c = lane; c < nc; c += kWave) {
-    float g[V];
-    Vec<T>::load(dy + t * d + (int64_t)c * V, g);
+  for (int c0 = lane; c0 < nc; c0 += 2 * kWave) {
+    u32x4 gv[2], ov[2][KK];
 #pragma unroll
-    for (int r = 0; r < kMaxK; ++r) {
-      if (sr[r] >= 0) {
+    for (int h = 0; h < 2; ++h) {
+      const int c = c0 + h * kWave;
+      const bool ok = c < nc;
+      gv[h] = ok ? *reinterpret_cast<const u32x4*>(dy + t * d + (int64_t)c * V) : u32x4{0u, 0u, 0u, 0u};
+#pragma unroll
+      for (int r = 0; r < KK; ++r)
+        ov[h][r] = (ok && sr[r] >= 0) ? *reinterpret_cast<const u32x4*>(O + erow<T>(er[r], sr[r], c * V, d, C))
+                                      : u32x4{0u, 0u, 0u, 0u};
+    }
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int c = c0 + h * kWave;
+      if (c >= nc) continue;
+      float g[V];
+      Vec<T>::load(&gv[h], g);
+#pragma unroll
+      for (int r = 0; r < KK; ++r) {
+        if (sr[r] < 0) continue;
         float o[V], out[V];
-        Vec<T>::load(O + erow<T>(er[r], sr[r], c * V, d, C), o);
+        Vec<T>::load(&ov[h][r], o);
 #pragma unroll
         for (int i = 0; i < V; ++i) {
           gp[r] = fmaf(g[i], o[i], gp[r]);
@@ -598,7 +617,7 @@ __global__ __launch_bounds__(256) void combine_bwd_kernel(const float* __restric
   }
   float gsum = 0.f;  // sum_r w_r g_r
 #pragma unroll
-  for (int r = 0; r < kMaxK; ++r) {
+  for (int r = 0; r < KK; ++r) {
     gp[r] = wave_sum(gp[r]);
     gsum = fmaf(wr[r], gp[r], gsum);
   }
@@ -607,7 +626,7 @@ __global__ __launch_bounds__(256) void combine_bwd_kernel(const float* __restric
   float dl = 0.f;
   if (renorm) {
 #pragma unroll
-    for (int r = 0; r < kMaxK; ++r)
+    for (int r = 0; r < KK; ++r)
       if (r < k && er[r] == j) dl = wr[r] * (gp[r] - gsum);
   } else {
     const float lj = j < E ? logits[t * E + j] : -INFINITY;
@@ -618,7 +637,7 @@ __global__ __launch_bounds__(256) void combine_bwd_kernel(const float* __restric
     const float pj = ex / wave_sum(ex);
     dl = -pj * gsum;
 #pragma unroll
-    for (int r = 0; r < kMaxK; ++r)
+    for (int r = 0; r < KK; ++r)
       if (r < k && er[r] == j) dl += gp[r] * wr[r];
   }
   if (j < E) dlogits[t * E + j] = dl;
@@ -631,14 +650,20 @@ void launch_combine_bwd(const moe_cfg& c, const float* logits, const int32_t* id
                         hipStream_t s) {
   if (c.T == 0) return;
   const unsigned blocks = (unsigned)((c.T + 3) / 4);
-  if (c.dtype == MOE_BF16)
-    hipLaunchKernelGGL(combine_bwd_kernel<uint16_t>, dim3(blocks), dim3(256), 0, s, logits, idx, w, slot,
-                       (const uint16_t*)O, (const uint16_t*)dy, (uint16_t*)dO, dlogits, c.T, c.d_model, c.E, c.k,
-                       c.C, c.renorm);
-  else
-    hipLaunchKernelGGL(combine_bwd_kernel<float>, dim3(blocks), dim3(256), 0, s, logits, idx, w, slot,
-                       (const float*)O, (const float*)dy, (float*)dO, dlogits, c.T, c.d_model, c.E, c.k, c.C,
-                       c.renorm);
+  auto go = [&](auto kern, auto tag) {
+    using T = decltype(tag);
+    hipLaunchKernelGGL(kern, dim3(blocks), dim3(256), 0, s, logits, idx, w, slot, (const T*)O, (const T*)dy,
+                       (T*)dO, dlogits, c.T, c.d_model, c.E, c.k, c.C, c.renorm);
+  };
+  if (c.dtype == MOE_BF16) {
+    if (c.k == 1) go(combine_bwd_kernel<uint16_t, 1>, uint16_t{});
+    else if (c.k == 2) go(combine_bwd_kernel<uint16_t, 2>, uint16_t{});
+    else go(combine_bwd_kernel<uint16_t, 0>, uint16_t{});
+  } else {
+    if (c.k == 1) go(combine_bwd_kernel<float, 1>, float{});
+    else if (c.k == 2) go(combine_bwd_kernel<float, 2>, float{});
+    else go(combine_bwd_kernel<float, 0>, float{});
+  }
 }
 
 // ----------------------------------------------------------- dispatch backward
