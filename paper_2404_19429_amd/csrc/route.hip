@@ -148,13 +148,21 @@ __global__ __launch_bounds__(64) void route_scan_kernel(const int32_t* __restric
 // slot[t][r] = base[chunk][e] + rank (or -1 past the capacity), and
 // send_buf[e][slot][:] = x[t][:] for every kept (t, r).
 // perm as in route_rank_kernel: the thread's positions j hold tokens perm[j].
+// nfused > 0 (wave-uniform tokens, at most 64 chunks): the chunk bases are
+// not read from `base` but summed here from the chunk counts (one wave
+// reduction per token and choice; the scan launch is skipped), and the first
+// wave of block b writes fill[e] = min(C, carry_e + all counts of e) for
+// e = b, b + gridDim.x, ...
 template <typename T, int KT, int U, bool UNI>
 __global__ __launch_bounds__(256) void dispatch_copy_kernel(const T* __restrict__ x, const int32_t* __restrict__ idx,
                                                             const int32_t* __restrict__ perm,
                                                             const int32_t* __restrict__ rank,
                                                             const int32_t* __restrict__ base,
                                                             int32_t* __restrict__ slot, T* __restrict__ send,
-                                                            int64_t T_tokens, int d, int E, int kr, int C) {
+                                                            int64_t T_tokens, int d, int E, int kr, int C,
+                                                            const int32_t* __restrict__ counts,
+                                                            const int32_t* __restrict__ carry,
+                                                            int32_t* __restrict__ fill, int nfused) {
   constexpr int V = Vec<T>::N;
   constexpr int KK = KT > 0 ? KT : kMaxK;
   const int k = KT > 0 ? KT : kr;
@@ -163,6 +171,20 @@ __global__ __launch_bounds__(256) void dispatch_copy_kernel(const T* __restrict_
   const int64_t g = UNI ? (int64_t)__builtin_amdgcn_readfirstlane((int)(gid / nc)) : gid / nc;
   const int c = (int)(gid - g * nc);
   const int64_t t0 = g * U;
+  const int lane = threadIdx.x & 63;
+  // Sum over the first n chunks of expert e's counts (wave-uniform n and e, n <= 64).
+  auto counts_before = [&](int n, int e) __attribute__((always_inline)) {
+    int v = lane < n ? counts[(int64_t)lane * E + e] : 0;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
+    return v;
+  };
+  if (nfused > 0 && threadIdx.x < kWave) {
+    for (int e = blockIdx.x; e < E; e += gridDim.x) {
+      const int tot = (carry ? carry[e] : 0) + counts_before(nfused, e);
+      if (lane == 0) fill[e] = tot < C ? tot : C;
+    }
+  }
   if (t0 >= T_tokens) return;
   u32x4 v[U];
   int er[U][KK], sr[U][KK];
@@ -184,7 +206,8 @@ __global__ __launch_bounds__(256) void dispatch_copy_kernel(const T* __restrict_
         const int e = idx[t * k + r];
         const int rk = rank[j * k + r];
         if (rk >= 0 && e >= 0 && e < E) {
-          const int sl = base[(j / kRouteChunk) * E + e] + rk;
+          const int sl = (UNI && nfused > 0 ? (carry ? carry[e] : 0) + counts_before((int)(j / kRouteChunk), e)
+                                            : base[(j / kRouteChunk) * E + e]) + rk;
           if (sl < C) {
             er[u][r] = e;
             sr[u][r] = sl;
@@ -240,19 +263,28 @@ static void dispatch_walk(const moe_cfg& c, const void* x, const int32_t* idx, c
   int32_t* counts = (int32_t*)ws;
   int32_t* base = counts + nch * c.E;
   int32_t* rank = base + nch * c.E;
+  // The copy launch sums the chunk bases itself when its waves are token-uniform
+  // (as row_launch decides) and there are at most 64 chunks (one count per
+  // lane); else a scan launch (with 128 chunks the in-copy sums cost more than
+  // the launch they save).
+  const int V = c.dtype == MOE_BF16 ? 8 : 4;
+  const bool fused = nch > 0 && nch <= kWave && (c.d_model / V) % kWave == 0 && c.T < ((int64_t)1 << 30);
+  const int nfused = fused ? (int)nch : 0;
   if (nch > 0)
     hipLaunchKernelGGL(route_rank_kernel, dim3((unsigned)nch), dim3(kRouteChunk), 0, s, idx, perm, counts, rank, c.T,
                        c.E, c.k);
-  if (c.E > 0)
+  if (c.E > 0 && !fused)
     hipLaunchKernelGGL(route_scan_kernel, dim3((unsigned)c.E), dim3(64), 0, s, counts, base, carry, fill, (int)nch, c.E,
                        c.C);
   if (nch == 0) return;
   if (c.dtype == MOE_BF16)
-    row_launch<DispatchCopy, uint16_t, 4, 2>(c, s, (const uint16_t*)x, idx, perm, rank, base, slot, (uint16_t*)send_buf,
-                                       c.T, c.d_model, c.E, c.k, c.C);
+    row_launch<DispatchCopy, uint16_t, 4, 2>(c, s, (const uint16_t*)x, idx, perm, rank, (const int32_t*)base, slot,
+                                       (uint16_t*)send_buf, c.T, c.d_model, c.E, c.k, c.C, (const int32_t*)counts,
+                                       carry, fill, nfused);
   else
-    row_launch<DispatchCopy, float, 4, 2>(c, s, (const float*)x, idx, perm, rank, base, slot, (float*)send_buf, c.T,
-                                    c.d_model, c.E, c.k, c.C);
+    row_launch<DispatchCopy, float, 4, 2>(c, s, (const float*)x, idx, perm, rank, (const int32_t*)base, slot,
+                                    (float*)send_buf, c.T, c.d_model, c.E, c.k, c.C, (const int32_t*)counts, carry,
+                                    fill, nfused);
 }
 
 void launch_dispatch(const moe_cfg& c, const void* x, const int32_t* idx, const int32_t* carry, int32_t* fill,
