@@ -697,8 +697,8 @@ struct WOp {
   }
 };
 
-// Schedule of one XCD's tiles [T0, T0 + n) over its nslot blocks.  Rounds of
-// whole tiles run in lock step (block s takes tiles T0 + q nslot + s), so the
+// Schedule of one XCD's n tiles xtile(0 .. n-1) over its nslot blocks.  Rounds
+// of whole tiles run in lock step (block s takes tiles xtile(q nslot + s)), so the
 // tiles in flight share their K position and their operand slices in L2.  A
 // last round that would leave most blocks idle (r <= nslot / 4 tiles) is
 // split instead: the r tiles' K-steps go to all nslot blocks, each tile to a
@@ -727,60 +727,107 @@ __device__ __forceinline__ WSched wide_sched(int n, int nslot, bool allow_split)
   return w;
 }
 
-// Geometry of tile t of a wide product.  incl / excl: the lane-per-group
-// inclusive / exclusive prefix of tile counts.  Within a group, tiles are
-// numbered panel by panel (kPanelN tile columns), m-tiles within a panel, n
-// fastest, so the tiles one XCD has in flight form a square-ish patch.
-template <bool RAGGED_K>
-__device__ __forceinline__ WGeo wide_geo(const GemmParams& p, int t, int lane, int groups, int incl, int excl,
+// Lane-per-group tile counts of a wide product and their prefixes (groups <= 64).
+// Ragged-K, or ragged-M without SEP: every tile of a group (with rows).
+// Ragged-M with SEP: the full M-tiles (256 rows) and, separately, the short
+// last M-tile of a group whose rows are not a multiple of 256; tile numbers
+// [0, NF) are the full tiles, [NF, NF + NP) the short ones, so a schedule can
+// place the short (cheaper) tiles last.
+struct WPrefix {
+  int incl, excl;     // full tiles (ragged-K: all tiles), lane = group
+  int inclP, exclP;   // ragged-M short tiles, lane = group
+  int NF, NP;         // totals (uniform)
+};
+template <bool RAGGED_K, bool SEP>
+__device__ __forceinline__ WPrefix wide_tile_prefix(const GemmParams& p, int lane, int groups, int tilesM,
+                                                    int tilesN) {
+  int cnt = 0, cntP = 0;
+  if (lane < groups) {
+    int lo, span;
+    group_rows(p, lane, lo, span);
+    if constexpr (RAGGED_K) {
+      cnt = span > 0 ? tilesM * tilesN : 0;   // an empty group's output is zeroed in the prologue
+    } else {
+      if (span > 0) span += lo & 15;
+      const int tm = (span + kWB - 1) / kWB;
+      const int sh = (SEP && (span % kWB) != 0) ? 1 : 0;
+      cnt = (tm - sh) * tilesN;
+      cntP = sh * tilesN;
+    }
+  }
+  WPrefix P;
+  P.incl = cnt;
+  P.inclP = cntP;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int u = __shfl_up(P.incl, o, 64);
+    const int v = __shfl_up(P.inclP, o, 64);
+    if (lane >= o) {
+      P.incl += u;
+      P.inclP += v;
+    }
+  }
+  P.excl = P.incl - cnt;
+  P.exclP = P.inclP - cntP;
+  P.NF = __builtin_amdgcn_readfirstlane(__shfl(P.incl, groups - 1, 64));
+  P.NP = __builtin_amdgcn_readfirstlane(__shfl(P.inclP, groups - 1, 64));
+  return P;
+}
+
+// Geometry of tile t of a wide product.  Within a group, tiles (with SEP: the
+// full tiles) are numbered panel by panel (kPanelN tile columns), m-tiles
+// within a panel, n fastest, so the tiles one XCD has in flight form a
+// square-ish patch; with SEP a group's short last M-tile has its own numbers
+// (t >= NF), n order.
+template <bool RAGGED_K, bool SEP>
+__device__ __forceinline__ WGeo wide_geo(const GemmParams& p, int t, int lane, int groups, const WPrefix& P,
                                          int tilesM, int tilesN) {
   WGeo G;
-  G.g = __builtin_amdgcn_readfirstlane(__popcll(__ballot(lane < groups && incl <= t)));
-  const int local = t - __builtin_amdgcn_readfirstlane(__shfl(excl, G.g, 64));
+  const bool shrt = SEP && !RAGGED_K && t >= P.NF;
+  const int tt = shrt ? t - P.NF : t;
+  const int inc = shrt ? P.inclP : P.incl;
+  const int exc = shrt ? P.exclP : P.excl;
+  G.g = __builtin_amdgcn_readfirstlane(__popcll(__ballot(lane < groups && inc <= tt)));
+  const int local = tt - __builtin_amdgcn_readfirstlane(__shfl(exc, G.g, 64));
   int lo, span;
   group_rows(p, G.g, lo, span);
   G.lo = lo;
   G.hi = lo + span;
   G.lo_al = lo & ~15;
   if (span > 0) span += lo - G.lo_al;
-  const int tmg = RAGGED_K ? tilesM : (span + kWB - 1) / kWB;
-  const int pnl = local / (tmg * kPanelN);
-  const int rem = local - pnl * tmg * kPanelN;
-  const int pw = min(kPanelN, tilesN - pnl * kPanelN);
-  G.m0 = (rem / pw) * kWB;
-  G.n0 = (pnl * kPanelN + rem % pw) * kWB;
+  if (shrt) {
+    G.m0 = ((span + kWB - 1) / kWB - 1) * kWB;
+    G.n0 = local * kWB;
+  } else {
+    const int tmg = RAGGED_K ? tilesM : (SEP ? span / kWB : (span + kWB - 1) / kWB);   // (full) M-tiles
+    const int pnl = local / (tmg * kPanelN);
+    const int rem = local - pnl * tmg * kPanelN;
+    const int pw = min(kPanelN, tilesN - pnl * kPanelN);
+    G.m0 = (rem / pw) * kWB;
+    G.n0 = (pnl * kPanelN + rem % pw) * kWB;
+  }
   G.Mlim = RAGGED_K ? p.M : span;
   G.Klim = RAGGED_K ? span : p.K;
   G.nk = max(1, (G.Klim + kBKb - 1) / kBKb);
   return G;
 }
 
-// Lane-per-group tile counts of a wide product and their inclusive prefix
-// (groups <= 64); returns the total on every lane.
-template <bool RAGGED_K>
-__device__ __forceinline__ int wide_tile_prefix(const GemmParams& p, int lane, int groups, int tilesM, int tilesN,
-                                                int& incl, int& excl) {
-  int cnt = 0;
-  if (lane < groups) {
-    if constexpr (RAGGED_K) {
-      int lo, span;
-      group_rows(p, lane, lo, span);
-      cnt = span > 0 ? tilesM * tilesN : 0;   // an empty group's output is zeroed in the prologue
-    } else {
-      int lo, span;
-      group_rows(p, lane, lo, span);
-      if (span > 0) span += lo & 15;
-      cnt = ((span + kWB - 1) / kWB) * tilesN;
-    }
-  }
-  incl = cnt;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const int u = __shfl_up(incl, o, 64);
-    if (lane >= o) incl += u;
-  }
-  excl = incl - cnt;
-  return __builtin_amdgcn_readfirstlane(__shfl(incl, groups - 1, 64));
+// One XCD's tiles of a ragged-M product: an even share of the full tiles, as
+// one contiguous range (neighbouring operand panels in the XCD's L2), then an
+// even share of the short tiles.  tile(j) = the XCD's j-th tile.
+struct WRange {
+  int f0, nf, p0, np, NF;
+  __device__ __forceinline__ int tile(int j) const { return j < nf ? f0 + j : NF + p0 + (j - nf); }
+};
+__device__ __forceinline__ WRange wide_range(const WPrefix& P, int xcd) {
+  WRange r;
+  const int perF = (P.NF + 7) / 8, perP = (P.NP + 7) / 8;
+  r.f0 = xcd * perF;
+  r.nf = max(min(P.NF, r.f0 + perF) - r.f0, 0);
+  r.p0 = xcd * perP;
+  r.np = max(min(P.NP, r.p0 + perP) - r.p0, 0);
+  r.NF = P.NF;
+  return r;
 }
 
 // Epilogue of one wave's tile from its accumulators: bf16 conversion and the
@@ -878,12 +925,18 @@ gemm_wide_kernel(GemmParams p, int tilesM, int tilesN, int groups) {
   const int wm = wid / WGN, wn = wid % WGN;
 
   // Tile counts per group and their prefix (every wave computes the same values).
-  int incl, excl;
-  const int total = wide_tile_prefix<RAGGED_K>(p, lane, groups, tilesM, tilesN, incl, excl);
+  // Only the plain-store ragged-M products may K-split their last round (the
+  // narrow-N products where a ragged last round idles most of the GPU); the
+  // others keep the simpler whole-tile schedule and its register budget.
+  // The K-split products place their short tiles last (SEP), so the split
+  // round holds the short tiles, whose partial sums stop at the group's rows.
+  constexpr bool SPLIT = !RAGGED_K && EPI == EPI_STORE;
+  const WPrefix P = wide_tile_prefix<RAGGED_K, SPLIT>(p, lane, groups, tilesM, tilesN);
+  const int total = P.NF + P.NP;
   if constexpr (RAGGED_K) {
     // Groups without rows have no tiles: their [M][N] outputs are zeroed here,
     // spread over the whole grid (16-byte stores; no tile writes them).
-    uint64_t empty = __ballot(lane < groups && incl == excl);
+    uint64_t empty = __ballot(lane < groups && P.incl == P.excl);
     const int64_t chunks = (int64_t)p.M * p.N / 8;
     const int64_t gtid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x, gstride = (int64_t)gridDim.x * blockDim.x;
     while (empty) {
@@ -895,9 +948,9 @@ gemm_wide_kernel(GemmParams p, int tilesM, int tilesN, int groups) {
   }
   const int nslot = gridDim.x / 8;
   const int xcd = blockIdx.x % 8, slot = blockIdx.x / 8;
-  const int per = (total + 7) / 8;
-  // The XCD's tiles: ragged-M products (one K length, equal tiles) take a
-  // contiguous range, so the XCD's L2 holds neighbouring operand panels;
+  // The XCD's tiles: ragged-M products (one K length) take a contiguous range
+  // of the (full) tiles, so the XCD's L2 holds neighbouring operand panels,
+  // then with SEP their share of the short last M-tiles;
   // ragged-K products, whose tiles cost as many K-steps as their group has
   // rows, take every eighth tile, so each XCD gets an even share of every
   // group (with skewed routing, a contiguous range could hold the few large
@@ -905,14 +958,10 @@ gemm_wide_kernel(GemmParams p, int tilesM, int tilesN, int groups) {
   // The block's segments (see WSched): nd whole tiles xtile(e nslot + slot),
   // then, if the last round is K-split (ragged-M products, one K length), the
   // K range [sk0, sk1) of remainder tile xtile(R nslot + sq).
-  const int T0 = RAGGED_K ? 0 : xcd * per;
-  const int nx = RAGGED_K ? (total > xcd ? (total - xcd + 7) / 8 : 0) : max(min(total, (xcd + 1) * per) - T0, 0);
-  auto xtile = [&](int j) __attribute__((always_inline)) { return RAGGED_K ? xcd + 8 * j : T0 + j; };
+  const WRange XR = wide_range(P, xcd);
+  const int nx = RAGGED_K ? (total > xcd ? (total - xcd + 7) / 8 : 0) : XR.nf + XR.np;
+  auto xtile = [&](int j) __attribute__((always_inline)) { return RAGGED_K ? xcd + 8 * j : XR.tile(j); };
   const int nkU = (p.K + BK - 1) / BK;
-  // Only the plain-store ragged-M products may K-split their last round (the
-  // narrow-N products where a ragged last round idles most of the GPU); the
-  // others keep the simpler whole-tile schedule and its register budget.
-  constexpr bool SPLIT = !RAGGED_K && EPI == EPI_STORE;
   const WSched W = wide_sched(nx, nslot, SPLIT);
   int sq = 0, sfirst = 0, scnt = 0, sk0 = 0, sk1 = 0;
   if (SPLIT && W.split) W.split_part(slot, nslot, nkU, sq, sfirst, scnt, sk0, sk1);
@@ -926,7 +975,7 @@ gemm_wide_kernel(GemmParams p, int tilesM, int tilesN, int groups) {
   if (nseg == 0) return;
 
   auto geo = [&](int t) __attribute__((always_inline)) {
-    return wide_geo<RAGGED_K>(p, t, lane, groups, incl, excl, tilesM, tilesN);
+    return wide_geo<RAGGED_K, SPLIT>(p, t, lane, groups, P, tilesM, tilesN);
   };
 
   // Segment e: tile, first K-step, end K-step (0 = the tile's own count).
@@ -1189,16 +1238,21 @@ gemm_wide_kernel(GemmParams p, int tilesM, int tilesN, int groups) {
   // Partial tile of a K-split remainder tile: stored to this block's slot in
   // accumulator order -- wave w, fragment (i, j), lane l at
   // ((w FM + i) FN + j) 64 + l -- for the fix-up kernel to add.
-  auto partial = [&]() __attribute__((always_inline)) {
+  // Fragment rows past the group's rows are not stored (the fix-up never
+  // reads them).
+  auto partial = [&](const WGeo& Cg) __attribute__((always_inline)) {
     asm volatile("s_nop 15\n s_nop 15" ::: "memory");   // last MFMA -> accumulator reads
     float* mine = p.part + (int64_t)blockIdx.x * (kWB * kWB) + ((int64_t)wid * FM * FN * 64 + lane) * 4;
+    const int rows = Cg.Mlim - (Cg.m0 + wm * WTM);   // the wave's rows in the group (uniform)
     // One fragment row at a time (the pin orders each row's register moves
     // after the previous row's stores, so only a row is ever out of AGPRs).
 #pragma unroll
     for (int i = 0; i < FM; ++i) {
       acc_pin_mem(acc[i]);
+      if (16 * i < rows) {
 #pragma unroll
-      for (int j = 0; j < FN; ++j) *reinterpret_cast<f32x4*>(mine + (i * FN + j) * 256) = acc[i][j];
+        for (int j = 0; j < FN; ++j) *reinterpret_cast<f32x4*>(mine + (i * FN + j) * 256) = acc[i][j];
+      }
     }
   };
 
@@ -1231,7 +1285,7 @@ gemm_wide_kernel(GemmParams p, int tilesM, int tilesN, int groups) {
     if constexpr (SPLIT) {
       run_steps(e < nd ? Cg.nk : k1 - k0, mma);
       if (e < nd) epilogue(Cg);
-      else partial();
+      else partial(Cg);
     } else {
       run_steps(Cg.nk, mma);
       epilogue(Cg);
@@ -1255,14 +1309,15 @@ __global__ __launch_bounds__(NW * 64) void gemm_wide_fixup_kernel(GemmParams p, 
   const int lane = threadIdx.x & 63;
   const int wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int wm = wid / WGN, wn = wid % WGN;
-  int incl, excl;
-  const int total = wide_tile_prefix<false>(p, lane, groups, tilesM, tilesN, incl, excl);
+  const WPrefix P = wide_tile_prefix<false, true>(p, lane, groups, tilesM, tilesN);
   const int xcd = blockIdx.x % 8, q = (blockIdx.x / 8) / FM, i = (blockIdx.x / 8) % FM;
-  const int per = (total + 7) / 8;
-  const int T0 = xcd * per, T1 = min(total, (xcd + 1) * per);
+  const WRange XR = wide_range(P, xcd);
   const int nkU = (p.K + kBKb - 1) / kBKb;
-  const WSched W = wide_sched(max(T1 - T0, 0), nslot, true);
+  const WSched W = wide_sched(XR.nf + XR.np, nslot, true);
   if (!W.split || q >= W.r) return;
+  const WGeo G = wide_geo<false, true>(p, XR.tile(W.R * nslot + q), lane, groups, P, tilesM, tilesN);
+  // fragment row i of the wave's rows: nothing to add past the group's rows
+  const bool live = 16 * i < G.Mlim - (G.m0 + wm * WTM);
   // the blocks of remainder tile q: [first, first + cnt); an empty K range wrote nothing
   int q0, first, cnt, k0, k1;
   W.split_part((q * nslot + W.r - 1) / W.r, nslot, nkU, q0, first, cnt, k0, k1);
@@ -1272,7 +1327,7 @@ __global__ __launch_bounds__(NW * 64) void gemm_wide_fixup_kernel(GemmParams p, 
   for (int sl = first; sl < first + cnt; ++sl) {
     int qq, ff, cc, a0, a1;
     W.split_part(sl, nslot, nkU, qq, ff, cc, a0, a1);
-    if (a0 >= a1) continue;
+    if (a0 >= a1 || !live) continue;
     const float* src = p.part + (int64_t)(sl * 8 + xcd) * (kWB * kWB) + lane_off;
     f32x4 v[FN];
 #pragma unroll
@@ -1281,7 +1336,10 @@ __global__ __launch_bounds__(NW * 64) void gemm_wide_fixup_kernel(GemmParams p, 
     for (int j = 0; j < FN; ++j) sum[j] = any ? sum[j] + v[j] : v[j];
     any = true;
   }
-  const WGeo G = wide_geo<false>(p, T0 + W.R * nslot + q, lane, groups, incl, excl, tilesM, tilesN);
+  if (!any) {   // rows past the group, or an empty K range everywhere: nothing stored
+#pragma unroll
+    for (int j = 0; j < FN; ++j) sum[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
   f32x4 acc[FM][FN];
   static_for<0, FM>([&](auto ic) {   // row i of acc (compile-time index), the others unused
     constexpr int I = decltype(ic)::value;
