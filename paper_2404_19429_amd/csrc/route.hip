@@ -353,8 +353,11 @@ static_assert(kRadix * kSortWaves == 4 * kSortThreads, "scan layout");
 // operations complete in order, so the rounds claim in order).  Equal keys
 // keep their input order, which within a tile is token order: the sorted
 // tile is in ascending order of the 64-bit elements.
+constexpr int kSplStep = 64;                          // a splitter every 64 sorted elements
+constexpr int kSplPerTile = kSortTile / kSplStep;
 __global__ __launch_bounds__(kSortThreads) void bpr_tile_sort_kernel(const uint64_t* __restrict__ in,
-                                                                     uint64_t* __restrict__ out, int64_t n) {
+                                                                     uint64_t* __restrict__ out,
+                                                                     uint64_t* __restrict__ spl, int64_t n) {
   extern __shared__ __attribute__((aligned(16))) unsigned char bpr_lds[];
   uint64_t* buf0 = reinterpret_cast<uint64_t*>(bpr_lds);
   uint64_t* buf1 = buf0 + kSortTile;
@@ -407,64 +410,108 @@ __global__ __launch_bounds__(kSortThreads) void bpr_tile_sort_kernel(const uint6
       ex += v[q];
     }
     __syncthreads();
+    constexpr int NR = kWaveSpan / kWave;
+    uint64_t el[NR];
 #pragma unroll
-    for (int j = 0; j < kWaveSpan / kWave; ++j) {
+    for (int j = 0; j < NR; ++j) {   // the wave's elements of the pass, read up front
       const int i = lo + kWave * j + lane;
-      const bool ok = i < hi;
-      const uint64_t e = ok ? src[i] : 0ull;
+      el[j] = i < hi ? src[i] : 0ull;
+    }
+#pragma unroll
+    for (int j = 0; j < NR; ++j) {
+      // One LDS round trip per round: OR the lane bit into the digit's table
+      // entry, then read the entry (the lanes sharing the digit) and the
+      // digit's running position together; the lowest of those lanes then
+      // advances the position and clears the entry.  A wave's LDS operations
+      // complete in order, so every lane's reads precede the leader's writes.
+      const bool ok = lo + kWave * j + lane < hi;
+      const uint64_t e = el[j];
       const int dg = (int)((e >> sh) & dmask);
       uint64_t peers = 0ull;
+      int base = 0;
       if (ok) {
         atomicOr((unsigned long long*)&table[wave * kRadix + dg], (unsigned long long)(1ull << lane));
         peers = table[wave * kRadix + dg];
+        base = cnt[dg * kCntStride + wave];
       }
-      int first = 0;
+      const int pos = base + __popcll(peers & lt);
       if (ok && (peers & lt) == 0) {
-        first = atomicAdd(&cnt[dg * kCntStride + wave], __popcll(peers));
+        cnt[dg * kCntStride + wave] = base + __popcll(peers);
         table[wave * kRadix + dg] = 0ull;
       }
-      const int srcl = ok ? (int)__builtin_ctzll(peers) : lane;
-      const int pos = __shfl(first, srcl, kWave) + __popcll(peers & lt);
       if (ok && pos >= 0 && pos < m) dst[pos] = e;   // always true for a consistent count; keeps stores in bounds
     }
     __syncthreads();
   }
   for (int i = tid; i < m; i += kSortThreads) out[t0 + i] = buf0[i];
+  for (int i = tid; i * kSplStep < m; i += kSortThreads) spl[(int64_t)blockIdx.x * kSplPerTile + i] = buf0[i * kSplStep];
 }
 
 // Merges the sorted tiles: element i of tile a goes to its rank in the tile
-// plus, for every other tile, the number of its elements below it (a binary
-// search; the elements are distinct), and perm[pos] = its token.  Every
-// position is below n.
-constexpr int kMergeTiles = 16;   // tiles searched side by side (more: one after another)
-__global__ __launch_bounds__(256) void bpr_merge_kernel(const uint64_t* __restrict__ sorted, int32_t* __restrict__ perm,
+// plus, for every other tile, the number of its elements below it, and
+// perm[pos] = its token (the elements are distinct, so the positions are a
+// permutation; every position is checked below n).  The count in tile b: the
+// splitters of b (every 64th element, in LDS) bound it to a window of at most
+// 63 elements, searched in device memory.
+constexpr int kMergeTiles = 16;   // tiles whose splitters are in LDS at a time
+__global__ __launch_bounds__(256) void bpr_merge_kernel(const uint64_t* __restrict__ sorted,
+                                                        const uint64_t* __restrict__ spl, int32_t* __restrict__ perm,
                                                         int64_t n) {
+  __shared__ uint64_t sp[kMergeTiles * kSplPerTile];
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= n) return;
-  const uint64_t v = sorted[i];
-  const int64_t a = i / kSortTile;
+  const bool act = i < n;
+  const uint64_t v = act ? sorted[i] : 0ull;
+  const int64_t a = act ? i / kSortTile : -1;
   const int64_t ntiles = (n + kSortTile - 1) / kSortTile;
-  int64_t pos = i - a * kSortTile;
+  int64_t pos = act ? i - a * kSortTile : 0;
   for (int64_t g0 = 0; g0 < ntiles; g0 += kMergeTiles) {
-    int64_t base[kMergeTiles];
-    int len[kMergeTiles];
+    const int ng = (int)min((int64_t)kMergeTiles, ntiles - g0);
+    __syncthreads();
+    for (int q = threadIdx.x; q < ng * kSplPerTile; q += blockDim.x) {
+      const int64_t b = g0 + q / kSplPerTile;
+      const int s = q % kSplPerTile;
+      const int64_t len = min((int64_t)kSortTile, n - b * kSortTile);
+      sp[q] = (int64_t)s * kSplStep < len ? spl[b * kSplPerTile + s] : ~0ull;   // past the tile: above every element
+    }
+    __syncthreads();
+    if (!act) continue;
+    int64_t wb[kMergeTiles];
+    int wl[kMergeTiles];
 #pragma unroll
     for (int q = 0; q < kMergeTiles; ++q) {
       const int64_t b = g0 + q;
-      base[q] = b * kSortTile;
-      len[q] = (b < ntiles && b != a) ? (int)min((int64_t)kSortTile, n - base[q]) : 0;
+      wb[q] = b * kSortTile;
+      wl[q] = 0;
+      if (q < ng && b != a) {
+        // splitters below v (they are sorted): a binary search in LDS
+        int lo = 0, cnt = kSplPerTile;
+        while (cnt > 0) {
+          const int half = cnt >> 1;
+          if (sp[q * kSplPerTile + lo + half] < v) {
+            lo += half + 1;
+            cnt -= half + 1;
+          } else {
+            cnt = half;
+          }
+        }
+        // the lower bound lies in (64 (lo - 1), 64 lo]: a window of at most 63
+        if (lo > 0) {
+          const int64_t len = min((int64_t)kSortTile, n - b * kSortTile);
+          wb[q] = b * kSortTile + (int64_t)(lo - 1) * kSplStep + 1;
+          wl[q] = (int)(min((int64_t)lo * kSplStep, len) - ((int64_t)(lo - 1) * kSplStep + 1));
+        }
+      }
     }
-    // lower bound of v in every tile of the group, the probes of all tiles in flight together
-    for (int it = 0; it < 14; ++it) {
+    for (int it = 0; it < 7; ++it) {   // lower bound in every window, the probes of all tiles in flight together
 #pragma unroll
       for (int q = 0; q < kMergeTiles; ++q) {
-        if (len[q] > 0) {
-          const int half = len[q] >> 1;
-          if (sorted[base[q] + half] < v) {
-            base[q] += half + 1;
-            len[q] -= half + 1;
+        if (wl[q] > 0) {
+          const int half = wl[q] >> 1;
+          if (sorted[wb[q] + half] < v) {
+            wb[q] += half + 1;
+            wl[q] -= half + 1;
           } else {
-            len[q] = half;
+            wl[q] = half;
           }
         }
       }
@@ -472,17 +519,21 @@ __global__ __launch_bounds__(256) void bpr_merge_kernel(const uint64_t* __restri
 #pragma unroll
     for (int q = 0; q < kMergeTiles; ++q) {
       const int64_t b = g0 + q;
-      if (b < ntiles && b != a) pos += base[q] - b * kSortTile;
+      if (q < ng && b != a) pos += wb[q] - b * kSortTile;
     }
   }
-  if (pos >= 0 && pos < n) perm[pos] = (int32_t)(v & 0xffffffffu);
+  if (act && pos >= 0 && pos < n) perm[pos] = (int32_t)(v & 0xffffffffu);
 }
 
+static size_t bpr_spl_bytes(const moe_cfg& c) {
+  const int64_t ntiles = (c.T + kSortTile - 1) / kSortTile;
+  return ((size_t)ntiles * kSplPerTile * sizeof(uint64_t) + 255) / 256 * 256;
+}
 size_t dispatch_bpr_ws_bytes(const moe_cfg& c) {
   const size_t a = (dispatch_ws_bytes(c) + 255) / 256 * 256;
   const size_t eb = ((size_t)c.T * sizeof(uint64_t) + 255) / 256 * 256;
   const size_t tb = ((size_t)c.T * sizeof(int32_t) + 255) / 256 * 256;
-  return a + 2 * eb + tb;
+  return a + 2 * eb + tb + bpr_spl_bytes(c);
 }
 
 void launch_dispatch_bpr(const moe_cfg& c, const void* x, const float* logits, const int32_t* idx, int32_t* fill,
@@ -492,7 +543,9 @@ void launch_dispatch_bpr(const moe_cfg& c, const void* x, const float* logits, c
   char* w = (char*)ws + a;
   uint64_t* e0 = (uint64_t*)w;
   uint64_t* e1 = (uint64_t*)(w + eb);
+  const size_t tb = ((size_t)c.T * sizeof(int32_t) + 255) / 256 * 256;
   int32_t* perm = order ? order : (int32_t*)(w + 2 * eb);
+  uint64_t* spl = (uint64_t*)(w + 2 * eb + tb);
   if (c.T > 0) {
     static bool attr_set = false;
     if (!attr_set) {
@@ -503,8 +556,9 @@ void launch_dispatch_bpr(const moe_cfg& c, const void* x, const float* logits, c
     const int64_t ntiles = (c.T + kSortTile - 1) / kSortTile;
     hipLaunchKernelGGL(bpr_key_kernel, dim3((unsigned)((c.T + 3) / 4)), dim3(256), 0, s, logits, idx, e0, c.T, c.E,
                        c.k);
-    hipLaunchKernelGGL(bpr_tile_sort_kernel, dim3((unsigned)ntiles), dim3(kSortThreads), kTileSortLds, s, e0, e1, c.T);
-    hipLaunchKernelGGL(bpr_merge_kernel, dim3((unsigned)((c.T + 255) / 256)), dim3(256), 0, s, e1, perm, c.T);
+    hipLaunchKernelGGL(bpr_tile_sort_kernel, dim3((unsigned)ntiles), dim3(kSortThreads), kTileSortLds, s, e0, e1, spl,
+                       c.T);
+    hipLaunchKernelGGL(bpr_merge_kernel, dim3((unsigned)((c.T + 255) / 256)), dim3(256), 0, s, e1, spl, perm, c.T);
   }
   dispatch_walk(c, x, idx, perm, nullptr, fill, slot, send_buf, ws, s);
 }
