@@ -101,6 +101,16 @@ def _args():
     return ap.parse_args()
 
 
+def cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(spec, inp, n_tokens):
     """The oracle, as it stands, on the first n_tokens tokens of the workload."""
     from dataclasses import replace
@@ -116,7 +126,7 @@ def cpu_baseline(spec, inp, n_tokens):
     fw = O.layer_forward(s, sub)
     O.layer_backward(s, sub, fw)
     dt = time.perf_counter() - t0
-    return {"value": n_tokens / dt, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
+    return {"value": n_tokens / dt, "unit": "tokens/s", "cores": int(threads), "kind": "oracle", "cpu": cpu_model(),
             "sample": f"float64 oracle layer forward+backward on the first {n_tokens} tokens of the same "
                       f"workload (capacity recomputed for {n_tokens} tokens), {dt:.1f} s wall"}
 
@@ -137,7 +147,7 @@ def block_cpu_baseline(spec, inp, S_sample):
     fw = BO.block_forward(s, sub)
     BO.block_backward(s, sub, fw)
     dt = time.perf_counter() - t0
-    return {"value": S_sample / dt, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
+    return {"value": S_sample / dt, "unit": "tokens/s", "cores": int(threads), "kind": "oracle", "cpu": cpu_model(),
             "sample": f"float64 oracle block forward+backward on the first {S_sample} tokens of sequence 0 "
                       f"(one sequence of {S_sample}; capacity recomputed), {dt:.1f} s wall"}
 
@@ -462,6 +472,8 @@ def main():
     disp_bytes = (T * d + N * d) * eb + T * spec.k * 4 * 2          # read x, write kept rows, idx + slot
     dispatch_gbps = disp_bytes / (per_call["dispatch"] * 1e-3) / 1e9
     eager_ms = wall / a.steps * 1e3
+    working_set = sum(t.numel() * t.element_size() for t in vars(b).values() if isinstance(t, torch.Tensor))
+    working_set += sum(t.numel() * t.element_size() for t in dev.values())
     step_ms_timed = graph_ms if graph_ms is not None else eager_ms
     tokens_per_s = T / (step_ms_timed * 1e-3)
 
@@ -478,6 +490,9 @@ def main():
         "vs_baseline": None,
         "dtype": spec.dtype,
         "data": "synthetic (seeded Gaussian hidden states and weights; no dataset)",
+        "cache": f"steps repeat over the same buffers with no cache flush; the layer's buffers (weights, packed "
+                 f"weights, activations, gradients, workspaces) total {working_set / 2**30:.2f} GiB, above the "
+                 f"256 MiB Infinity Cache",
         "config": {"workload": spec.name, "T": T, "d_model": d, "d_ff": f, "E": spec.E, "k": spec.k,
                    "C": C, "capacity_factor": f"{spec.cf_num}/{spec.cf_den}", "act": spec.act,
                    "routing": a.routing,

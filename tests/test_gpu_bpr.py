@@ -37,6 +37,7 @@ SMALL = {
     "f32_k3_T300_E5_cf1/2": _s("d", T=300, d=40, f=24, E=5, k=3, cf_den=2, dtype="f32", act="gelu_erf", seed=24),
     "f32_T37_E2_top1": _s("e", T=37, d=16, f=8, E=2, k=1, renorm=0, act="relu", dtype="f32", seed=25),
     "f32_T1_E4": _s("f", T=1, d=64, f=64, E=4, dtype="f32", seed=26),
+    "bf16_G4_T640_E8_cf3/4": _s("h", T=640, d=128, f=128, E=8, G=4, cf_num=3, cf_den=4, seed=28),
 }
 
 
