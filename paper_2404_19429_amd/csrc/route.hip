@@ -353,6 +353,29 @@ static_assert(kRadix * kSortWaves == 4 * kSortThreads, "scan layout");
 // operations complete in order, so the rounds claim in order).  Equal keys
 // keep their input order, which within a tile is token order: the sorted
 // tile is in ascending order of the 64-bit elements.
+// Lanes of a round by digit when the round holds at most two digits: m0 =
+// the active lanes with the first active lane's digit (returned), m1 = the
+// other active lanes if they all share one digit, rest = any active lanes
+// left (nonzero: more than two digits; m1 then means nothing).
+__device__ __forceinline__ int few_digits(int dg, bool ok, uint64_t& m0, uint64_t& m1, uint64_t& rest) {
+  const uint64_t act = __ballot(ok);
+  if (act == 0) {
+    m0 = m1 = rest = 0ull;
+    return 0;
+  }
+  const int d0 = __builtin_amdgcn_readlane(dg, (int)__builtin_ctzll(act));
+  m0 = __ballot(ok && dg == d0);
+  const uint64_t r = act & ~m0;
+  if (r == 0) {
+    m1 = rest = 0ull;
+    return d0;
+  }
+  const int d1 = __builtin_amdgcn_readlane(dg, (int)__builtin_ctzll(r));
+  m1 = __ballot(ok && dg == d1);
+  rest = r & ~m1;
+  return d0;
+}
+
 constexpr int kSplStep = 64;                          // a splitter every 64 sorted elements
 constexpr int kSplPerTile = kSortTile / kSplStep;
 __global__ __launch_bounds__(kSortThreads) void bpr_tile_sort_kernel(const uint64_t* __restrict__ in,
@@ -381,7 +404,18 @@ __global__ __launch_bounds__(kSortThreads) void bpr_tile_sort_kernel(const uint6
 #pragma unroll
     for (int j = 0; j < kWaveSpan / kWave; ++j) {
       const int i = lo + kWave * j + lane;
-      if (i < hi) atomicAdd(&cnt[(int)((src[i] >> sh) & dmask) * kCntStride + wave], 1);
+      const bool ok = i < hi;
+      const int dg = ok ? (int)((src[i] >> sh) & dmask) : 0;
+      // A round with at most two digits (the high digits of nearby importances)
+      // is counted by one lane per digit; otherwise one LDS add per lane.
+      uint64_t m0, m1, rest;
+      const int d0 = few_digits(dg, ok, m0, m1, rest);
+      if (rest == 0) {
+        if (m0 != 0 && lane == (int)__builtin_ctzll(m0)) atomicAdd(&cnt[d0 * kCntStride + wave], __popcll(m0));
+        if (m1 != 0 && lane == (int)__builtin_ctzll(m1)) atomicAdd(&cnt[dg * kCntStride + wave], __popcll(m1));
+      } else if (ok) {
+        atomicAdd(&cnt[dg * kCntStride + wave], 1);
+      }
     }
     __syncthreads();
     // Exclusive scan of the counters in (digit, wave) order; thread tid owns
@@ -427,9 +461,14 @@ __global__ __launch_bounds__(kSortThreads) void bpr_tile_sort_kernel(const uint6
       const bool ok = lo + kWave * j + lane < hi;
       const uint64_t e = el[j];
       const int dg = (int)((e >> sh) & dmask);
+      uint64_t m0, m1, rest;
+      few_digits(dg, ok, m0, m1, rest);
       uint64_t peers = 0ull;
       int base = 0;
-      if (ok) {
+      if (rest == 0) {   // at most two digits: the lanes sharing a digit are a ballot
+        peers = ok ? (((m0 >> lane) & 1) ? m0 : m1) : 0ull;
+        if (ok) base = cnt[dg * kCntStride + wave];
+      } else if (ok) {
         atomicOr((unsigned long long*)&table[wave * kRadix + dg], (unsigned long long)(1ull << lane));
         peers = table[wave * kRadix + dg];
         base = cnt[dg * kCntStride + wave];
@@ -437,7 +476,7 @@ __global__ __launch_bounds__(kSortThreads) void bpr_tile_sort_kernel(const uint6
       const int pos = base + __popcll(peers & lt);
       if (ok && (peers & lt) == 0) {
         cnt[dg * kCntStride + wave] = base + __popcll(peers);
-        table[wave * kRadix + dg] = 0ull;
+        if (rest != 0) table[wave * kRadix + dg] = 0ull;
       }
       if (ok && pos >= 0 && pos < m) dst[pos] = e;   // always true for a consistent count; keeps stores in bounds
     }
