@@ -103,3 +103,11 @@ def test_schedule_constraints_bound_and_order(seed):
         anchor = max([pos[a]] + [pos[p] for p in pred[j]])
         between = order[anchor + 1:pos[j]]
         assert all(v in asg for v in between), (j, a, between)
+
+
+def test_equal_times_take_the_lower_index():
+    # reading: equal |t_u - t_w| goes to the lower instruction index
+    kinds = [A2A, DW, DW, DW]
+    times = [3.0, 3.0, 3.0, 1.0]
+    asg = D.greedy_assign(kinds, times, D.label(4, kinds, []))
+    assert asg == {1: 0}

@@ -80,3 +80,12 @@ def test_dp_equals_enumeration(seed):
     assert segs[0][0] == 1 and segs[-1][1] == N
     assert all(a[1] + 1 == b[0] for a, b in zip(segs, segs[1:]))
     assert sum(P.range_cost(kinds, times, join, i, n, k) for i, n, k in segs) == pytest.approx(T)
+
+
+def test_split_range_pays_its_join_cost():
+    # two stages a = 4 (compute), b = 3 (communication), split 2 ways, join 1.5:
+    # a + b + (k - 1) max(a, b) + join = 4 + 3 + 4 + 1.5
+    kinds = [COMP, COMM]
+    times = [[8.0, 4.0], [6.0, 3.0]]
+    assert P.range_cost(kinds, times, [0.0, 1.5], 1, 2, 2) == 12.5
+    assert P.range_cost(kinds, times, [0.0, 1.5], 1, 2, 1) == 14.0   # unsplit: the sum, no join
