@@ -83,3 +83,44 @@ def test_graph_replays_equal_eager(L, routing):
                         np.testing.assert_array_equal(got[e, :nb], want[e, :nb], err_msg=f"{n} replay {rep}")
             else:
                 np.testing.assert_array_equal(got, want, err_msg=f"{n} replay {rep}")
+
+
+def test_graph_replay_full_size_equals_eager(L):
+    """The configuration bench.py times: the 8192-token layer (d_model 1024,
+    d_ff 4096, 16 experts, top-2), packed weights, the step as one HIP graph.
+    Two replays reproduce the eager step's outputs bit for bit."""
+    from synth import layer_spec
+    spec = layer_spec(2)
+    inp = layer_inputs(spec)
+    C = spec_C(spec)
+    log(f"[graph full] {spec.name} C={C}")
+    cfg = L.make_cfg(spec.T, spec.d, spec.f, spec.E, spec.k, C, spec.G, spec.dtype, spec.act, spec.renorm,
+                     wpacked=1)
+    b, ref_b = L.alloc_layer(cfg), L.alloc_layer(cfg)
+    dev = {n: to_dev(inp[n], torch.bfloat16) for n in ("x", "Wg", "W1", "W2", "dy")}
+
+    def step(bb):
+        L.moe_gate_topk(cfg, dev["x"], dev["Wg"], None, bb.logits, bb.idx, bb.w)
+        L.moe_dispatch(cfg, dev["x"], bb.idx, bb.carry, bb.fill, bb.slot, bb.send_buf, bb.ws_dispatch)
+        L.moe_expert_ffn_fwd(cfg, bb.send_buf, bb.carry, bb.fill, bb.W1p, bb.W2p, bb.H, bb.A, bb.O, bb.ws_ffn)
+        L.moe_combine(cfg, bb.O, bb.idx, bb.slot, bb.w, bb.y)
+        L.moe_bwd_dx(cfg, dev["Wg"], bb.logits, bb.idx, bb.w, bb.slot, bb.carry, bb.fill, bb.H, bb.O, bb.W1p, bb.W2p,
+                     dev["dy"], bb.dO, bb.dH, bb.dXe, bb.dlogits, bb.dx, bb.ws_dx)
+        L.moe_bwd_dw(cfg, dev["x"], bb.dlogits, bb.carry, bb.fill, bb.send_buf, bb.A, bb.dO, bb.dH, bb.dW1, bb.dW2,
+                     bb.dWg, bb.ws_dw)
+
+    for bb in (b, ref_b):
+        L.moe_pack_weights(cfg, dev["W1"], dev["W2"], bb.W1p, bb.W2p)
+    step(ref_b)
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        step(b)
+    names = ("logits", "idx", "w", "slot", "fill", "y", "dlogits", "dx", "dW1", "dW2", "dWg")
+    for rep in range(2):
+        for n in names:
+            t = getattr(b, n)
+            t.fill_(float("nan") if t.is_floating_point() else -3)
+        graph.replay()
+        torch.cuda.synchronize()
+        for n in names:
+            assert torch.equal(getattr(b, n), getattr(ref_b, n)), f"{n} differs on replay {rep}"
