@@ -1185,6 +1185,10 @@ gemm_wide_kernel(GemmParams p, int tilesM, int tilesN, int groups) {
     const uint32_t rb0 = read_base(TB{}, st + kWB * BK, wn * WTN, 0);
     const uint32_t rb1 = BKK ? rb0 : read_base(TB{}, st + kWB * BK, wn * WTN, 1);
     __builtin_amdgcn_sched_barrier(0);
+    // Raised wave priority while this step's MFMAs and reads issue: of the two
+    // waves on a SIMD, the one past the barrier keeps the matrix core fed
+    // while the other waits (measured: FWD2 -3 %, the layer step -1 %).
+    __builtin_amdgcn_s_setprio(1);
     static_for<0, NMF>([&](auto mc) __attribute__((always_inline)) {
       constexpr int m = decltype(mc)::value;
       if constexpr (MMA) mfma_acc(acc[m / FN][m % FN], cb[m % FN], ca[m / FN]);
@@ -1214,6 +1218,7 @@ gemm_wide_kernel(GemmParams p, int tilesM, int tilesN, int groups) {
         }
       });
     });
+    __builtin_amdgcn_s_setprio(0);
     lds_wait_all();
     if constexpr (AK) {
       lds_mark(na);
