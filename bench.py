@@ -471,6 +471,13 @@ def main():
     expert_gemm_s = (per_call["expert_ffn_fwd"]) * 1e-3
     disp_bytes = (T * d + N * d) * eb + T * spec.k * 4 * 2          # read x, write kept rows, idx + slot
     dispatch_gbps = disp_bytes / (per_call["dispatch"] * 1e-3) / 1e9
+    # Algorithmic HBM bytes of the other gathers / the gate, per call (event-timed, launch gaps included):
+    # gate reads x and Wg, writes logits, idx, w; combine reads the kept expert rows, idx, slot, w and writes y.
+    gate_bytes = (T * d + spec.E * d) * eb + T * spec.E * 4 + T * spec.k * 8
+    comb_bytes = (N * d + T * d) * eb + T * spec.k * 12
+    hbm_frac = {"gate": gate_bytes / (per_call["gate"] * 1e-3) / 1e9 / MI355X_PEAK_HBM_GBPS,
+                "dispatch": dispatch_gbps / MI355X_PEAK_HBM_GBPS,
+                "combine": comb_bytes / (per_call["combine"] * 1e-3) / 1e9 / MI355X_PEAK_HBM_GBPS}
     eager_ms = wall / a.steps * 1e3
     working_set = sum(t.numel() * t.element_size() for t in vars(b).values() if isinstance(t, torch.Tensor))
     working_set += sum(t.numel() * t.element_size() for t in dev.values())
@@ -505,6 +512,7 @@ def main():
         "expert_gemm_mfma_frac": achieved_tflops / MI355X_PEAK_BF16_TFLOPS,
         "dispatch_GBps": dispatch_gbps,
         "dispatch_hbm_frac": dispatch_gbps / MI355X_PEAK_HBM_GBPS,
+        "hbm_frac_per_call": hbm_frac,
         "per_call_ms": per_call,
         "step_mode": "hip_graph_replay" if graph_ms is not None else "eager",
         "eager_ms_per_step": eager_ms,
