@@ -7,8 +7,10 @@
 // * the operator-partition pass's pipeline cost and range choice (Sec. 5.1's
 //   dynamic program over Sec. 5.3's timeline simulation) -- C ABI
 //   moe_pipeline_plan.
+#include <algorithm>
 #include <cmath>
 #include <cstdint>
+#include <iterator>
 #include <string>
 #include <vector>
 
@@ -36,12 +38,14 @@ struct Reorder {
     }
   }
   // Emits, in index order and until nothing changes, every assigned operation
-  // whose all-to-all and predecessors are out.
-  void flush(const std::vector<int>& assigned) {
+  // whose all-to-all and predecessors are out.  Only the operations whose
+  // all-to-all is already out (`active`, ascending) can qualify; all-to-alls
+  // are emitted only outside this loop.
+  void flush(std::vector<int>& active) {
     for (bool changed = true; changed;) {
       changed = false;
-      for (int j : assigned) {
-        if (emitted[j] || !emitted[asg[j]]) continue;
+      for (int j : active) {
+        if (emitted[j]) continue;
         bool ready = true;
         for (int p : pred[j]) ready = ready && emitted[p];
         if (ready) {
@@ -51,6 +55,7 @@ struct Reorder {
         }
       }
     }
+    active.erase(std::remove_if(active.begin(), active.end(), [&](int j) { return emitted[j] != 0; }), active.end());
   }
 };
 
@@ -122,14 +127,24 @@ std::string dw_schedule(int n, const int32_t* kind, const double* time, int n_ed
 
   // Reordering.
   std::vector<int> assigned;
+  std::vector<std::vector<int>> of_a2a(n);   // the operations assigned to each all-to-all, ascending
   for (int j = 0; j < n; ++j)
-    if (asg[j] >= 0) assigned.push_back(j);
+    if (asg[j] >= 0) {
+      assigned.push_back(j);
+      of_a2a[asg[j]].push_back(j);
+    }
   Reorder R{pred, asg, std::vector<char>(n, 0), {}};
   R.out.reserve(n);
+  std::vector<int> active;
   for (int i = 0; i < n; ++i) {
     if (asg[i] >= 0 || R.emitted[i]) continue;
     R.pull(i);
-    R.flush(assigned);
+    if (kind[i] == kA2A && !of_a2a[i].empty()) {
+      std::vector<int> merged;
+      std::merge(active.begin(), active.end(), of_a2a[i].begin(), of_a2a[i].end(), std::back_inserter(merged));
+      active.swap(merged);
+    }
+    R.flush(active);
   }
   for (int j : assigned)
     if (!R.emitted[j]) R.pull(j);

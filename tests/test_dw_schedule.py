@@ -161,3 +161,19 @@ def test_pipeline_planner_rejects_invalid():
                                ([0], [[1.0, 1.0]], [0.0, -1.0])]:
         with pytest.raises(L.MoeError):
             L.moe_pipeline_plan(kinds, times, join)
+
+
+def test_planner_large_instance_is_fast():
+    import time
+    rng = np.random.default_rng(7)
+    n = 6000
+    kinds = [int(k) for k in rng.choice([OTHER, A2A, DW], size=n, p=[0.5, 0.1, 0.4])]
+    times = [float(t) for t in rng.integers(1, 20, n)]
+    edges = sorted({(int(j), int(i)) for i in range(1, n) for j in rng.integers(max(0, i - 50), i, 3)})
+    t0 = time.perf_counter()
+    a, o, v = L.moe_dw_schedule(kinds, times, edges)
+    assert time.perf_counter() - t0 < 5.0
+    pos = np.empty(n, np.int64)
+    pos[o] = np.arange(n)
+    assert all(pos[s] < pos[d] for s, d in edges)          # a valid execution order
+    assert sorted(o.tolist()) == list(range(n))
