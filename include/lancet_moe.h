@@ -395,6 +395,8 @@ moe_status moe_dw_schedule(int32_t n, const int32_t* kind, const double* time, i
  *   smaller i, then the smaller k.
  *   Out: *n_seg ranges seg_begin..seg_end (1-based, in order) with their
  *   seg_k (arrays of N entries); *total = T(N).  N <= 16384, K <= 64.
+ *   Cost: O(N * G * K) range evaluations of O(G * K) each; group instructions
+ *   (as the paper does) or bound G for long sequences.
  *   Errors (MOE_EINVAL): bad kinds, NaN or negative times, infinite unsplit
  *   times, bad join values, NULL required pointers. */
 moe_status moe_pipeline_plan(int32_t N, int32_t K, const int32_t* kind, const double* times, const double* join,
