@@ -137,3 +137,28 @@ def test_bpr_many_tiles(L):
     np.testing.assert_array_equal(g["order"], order)
     np.testing.assert_array_equal(g["slot"], slot)
     np.testing.assert_array_equal(g["fill"], fill)
+
+
+def test_bpr_all_equal_importance_keeps_token_order(L):
+    """Every token's logits a permutation of one vector: one importance for all
+    9000 tokens, so the order is token order and the slots equal moe_dispatch's."""
+    T, E, k, d = 9000, 8, 2, 64
+    rng = np.random.default_rng(29)
+    base = rng.standard_normal(E).astype(np.float32)
+    logits = np.stack([rng.permutation(base) for _ in range(T)])
+    idx = O.topk_route(logits, k)
+    C = O.capacity(T, E, k, 1, 1)
+    cfg = L.make_cfg(T, d, d, E, k, C, 1, "bf16", "gelu_tanh", 1)
+    i32 = dict(dtype=torch.int32, device="cuda")
+    x = torch.zeros(T, d, dtype=torch.bfloat16, device="cuda")
+    lg = torch.from_numpy(logits).cuda()
+    ix = torch.from_numpy(idx).cuda()
+    fill, slot, order = torch.empty(E, **i32), torch.empty(T, k, **i32), torch.empty(T, **i32)
+    send = torch.empty(L.expert_numel(cfg, d), dtype=torch.bfloat16, device="cuda")
+    ws = torch.empty(L.moe_workspace_bytes(cfg, L.MOE_CALL_DISPATCH_BPR), dtype=torch.uint8, device="cuda")
+    L.moe_dispatch_bpr(cfg, x, lg, ix, fill, slot, send, order, ws)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(host(order), np.arange(T))
+    s_tok, f_tok = O.assign_slots(idx, E, C)
+    np.testing.assert_array_equal(host(slot), s_tok)
+    np.testing.assert_array_equal(host(fill), f_tok)
