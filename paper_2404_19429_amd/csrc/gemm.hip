@@ -548,9 +548,13 @@ gemm_bf16_kernel(GemmParams p, int tilesM, int tilesN, int groups) {
 // = an A fragment), so each lane's four accumulator values are four
 // consecutive output columns of one row: the epilogue converts them with
 // v_cvt_pk_bf16_f32 and stores 8-byte vectors straight from registers.
-#ifndef LMOE_WIDE_STAGES
-#define LMOE_WIDE_STAGES 4
-#endif
+//
+// LDS stages: four with one block barrier per K-step; five (the whole LDS)
+// with one barrier per two K-steps (PAIR: the barrier before an even step
+// covers the stages of both steps of the pair).  The products whose B operand
+// is MN-contiguous (read transposed) run PAIR -- measured faster there (the
+// ragged-K weight-gradient products -7 % at d_model 2048) -- and the
+// K-contiguous ones four stages (PAIR measured +4 % there).
 constexpr int kWB = 256;       // block tile (rows and columns)
 
 // Immediate byte offset of fragment read r from its base (see read_base in the
@@ -918,6 +922,7 @@ gemm_wide_kernel(GemmParams p, int tilesM, int tilesN, int groups) {
   static_assert(TA::NI == kWNI && TB::NI == kWNI, "load plan");
   constexpr int LPS = 2 * kWNI;                  // loads per wave per stage
   static_assert(STAGES >= 2 && LPS * (STAGES - 1) < 64, "vmcnt range");
+  constexpr bool PAIR = STAGES >= 5;
   extern __shared__ __attribute__((aligned(16))) uint16_t lds[];
 
   const int lane = threadIdx.x & 63;
@@ -1100,9 +1105,10 @@ gemm_wide_kernel(GemmParams p, int tilesM, int tilesN, int groups) {
     wide_epilogue<FM, FN, WTM, WTN, RAGGED_K, EPI, ACT, CBLK>(p, G, acc, wm, wn, lane);
   };
 
-  // Prologue: fill the ring, wait for the first stage, read its fragments.
+  // Prologue: fill the ring (PAIR: all but one stage, the slot the first
+  // step refills), wait for the first stage, read its fragments.
 #pragma unroll
-  for (int s = 0; s < STAGES; ++s) {
+  for (int s = 0; s < (PAIR ? STAGES - 1 : STAGES); ++s) {
 #pragma unroll
     for (int q = 0; q < 2 * kWNI; ++q) issue_load(q);
     advance();
@@ -1163,13 +1169,34 @@ gemm_wide_kernel(GemmParams p, int tilesM, int tilesN, int groups) {
     const uint16_t* st = lds + ((unsigned)(cs + 1) % STAGES) * STAGE;
     // This step's refill: stage ls, K-step lk of the load cursor (issued
     // unconditionally; past the block's last load it writes zeros into the
-    // stage of step cs, which no later step reads).
+    // ring slot of a K-step already consumed, which no later step reads).
     uint16_t* const dst = lds + ((unsigned)ls % STAGES) * STAGE;
     const bool live = loads_left();
     const int kdma = lk;
     const __amdgpu_buffer_rsrc_t rsa = opA.rsrc(kdma, live), rsb = opB.rsrc(kdma, live);
     const bool more = cs + 1 < ls;
-    if (more) {
+    if constexpr (PAIR) {
+      // Even step: stages cs+1 and cs+2 have landed (at most stage cs+3 is
+      // pending) and, after the barrier, are in LDS for every wave; every wave
+      // is past step cs-1, so no wave reads the stages of K-steps cs-1 and cs
+      // any more -- the refills of steps cs and cs+1 (ls <= cs+4 and ls+1:
+      // ring slots of K-steps ls-5 <= cs-1 and cs).  Odd step: nothing to wait
+      // for but this wave's epilogue stores.
+      if ((cs & 1) == 0) {
+        if (more) {
+          if (stores_pending) {
+            wait_vm<0>();
+            stores_pending = false;
+          } else {
+            wait_vm_tiles<LPS, STAGES - 4>(ls - cs - 3);
+          }
+          lds_barrier();
+        }
+      } else if (stores_pending) {
+        wait_vm<0>();
+        stores_pending = false;
+      }
+    } else if (more) {
       if (stores_pending) {
         wait_vm<0>();
         stores_pending = false;
@@ -1507,7 +1534,7 @@ static void run_gemm(int dtype, int act, int groups, const GemmParams& p, int ti
 constexpr int kSkMaxBlocks = 256;   // most blocks of a stream-K launch (partial slots per block: 2)
 template <bool B_K, bool RAGGED_K, int EPI, int ACT, bool CBLK>
 static void launch_wide(int groups, const GemmParams& p, int tilesM, int tilesN, hipStream_t s) {
-  constexpr int S = LMOE_WIDE_STAGES, NW = LMOE_WIDE_WAVES;
+  constexpr int S = B_K ? 4 : 5, NW = LMOE_WIDE_WAVES;
   constexpr size_t shmem = S * (size_t)(2 * kWB) * kBKb * sizeof(uint16_t);
   auto kern = gemm_wide_kernel<NW, S, B_K, RAGGED_K, EPI, ACT, CBLK>;
   static bool attr_set = false;
