@@ -11,7 +11,7 @@ order), each of kind OTHER, A2A (all-to-all) or DW (weight-gradient
 computation), with an execution time, and dependency edges (src, dst):
 dst consumes an output of src, and src precedes dst in the sequence.
 
-Readings of points the paper leaves open (also listed in the design doc):
+Readings of points the paper leaves open:
 
 * the candidates of an all-to-all are the DW instructions with no directed
   path to or from it (the labelling admits any instruction; only DW ones

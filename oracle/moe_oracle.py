@@ -11,7 +11,7 @@ The paper's transformations (batch partitioning with capacity passing, dX/dW
 separation) are defined to leave the result unchanged (Introduction; Sec. 2.3
 "Challenge 1"), so the oracle is the unpartitioned layer.
 
-Readings of points the paper leaves open (each also listed in the design doc):
+Readings of points the paper leaves open:
 
 * capacity ``C = ceil(k*T*cf/E)`` in exact integer arithmetic, ``T`` the
   unpartitioned token count (the paper only states that each expert accepts at

@@ -13,7 +13,7 @@ is split into k parts, times[i][k - 1] for k = 1..K (one part's time; inf =
 the instruction cannot be split k ways), and the cost of splitting a range's
 inputs and joining its outputs, join[k - 1] (0 for k = 1).
 
-Readings of points the paper leaves open (also listed in the design doc):
+Readings of points the paper leaves open:
 
 * a stage is a maximal run of consecutive instructions of one kind in the
   range; a partition's stage depends on the same partition's previous stage
