@@ -1137,7 +1137,13 @@ gemm_wide_kernel(GemmParams p, int tilesM, int tilesN, int groups) {
   constexpr bool BKK = std::is_same<TB, TileK<kWB, NW, true>>::value;
   constexpr int NRA = AK ? FM : 2 * FM, NRB = BKK ? FN : 2 * FN, NRD = NRA + NRB;
   constexpr int NMF = FM * FN, NDMA = 2 * kWNI;
-  constexpr int RSPAN = NMF * 3 / 4;          // all reads issued within the first 3/4 of the MFMAs
+  // PRE: MFMAs of a step issued before its wait and barrier (they use the
+  // fragments read in the previous step); the reads and refills follow the
+  // barrier.  Measured on the ragged-M plain-store product with a transposed
+  // B (dXe): -7 % with 8 (8192-token layer), -4 % at d_model 2048; neutral or
+  // slower on the others, which keep 0.
+  constexpr int PRE = (!B_K && !RAGGED_K && EPI == EPI_STORE) ? 8 : 0;
+  constexpr int RSPAN = (NMF - PRE) * 3 / 4;  // reads issued within the first 3/4 of the MFMAs after PRE
   u32x2 qa[2 * FM], qb[2 * FN];               // pending halves of MN-contiguous fragments
   // LDS byte address of read r of an operand = base(par) + imm(r), with a
   // compile-time immediate, so a step needs one or two base registers per
@@ -1175,6 +1181,7 @@ gemm_wide_kernel(GemmParams p, int tilesM, int tilesN, int groups) {
     const int kdma = lk;
     const __amdgpu_buffer_rsrc_t rsa = opA.rsrc(kdma, live), rsb = opB.rsrc(kdma, live);
     const bool more = cs + 1 < ls;
+    auto sync = [&]() __attribute__((always_inline)) {
     if constexpr (PAIR) {
       // Even step: stages cs+1 and cs+2 have landed (at most stage cs+3 is
       // pending) and, after the barrier, are in LDS for every wave; every wave
@@ -1205,6 +1212,8 @@ gemm_wide_kernel(GemmParams p, int tilesM, int tilesN, int groups) {
       }
       lds_barrier();   // stage cs+1 is in LDS for every wave; no wave reads stage cs any more
     }
+    };
+    if constexpr (PRE == 0) sync();
     // The reads are unconditional (branch-free, so pending registers are never
     // copied); after the last step they read a stage no load is writing.
     const uint32_t ra0 = read_base(TA{}, st, wm * WTM, 0);
@@ -1218,10 +1227,15 @@ gemm_wide_kernel(GemmParams p, int tilesM, int tilesN, int groups) {
     __builtin_amdgcn_s_setprio(1);
     static_for<0, NMF>([&](auto mc) __attribute__((always_inline)) {
       constexpr int m = decltype(mc)::value;
+      if constexpr (PRE > 0 && m == PRE) {
+        __builtin_amdgcn_sched_barrier(0);
+        sync();
+        __builtin_amdgcn_sched_barrier(0);
+      }
       if constexpr (MMA) mfma_acc(acc[m / FN][m % FN], cb[m % FN], ca[m / FN]);
       static_for<0, NRD>([&](auto rc) __attribute__((always_inline)) {
         constexpr int r = decltype(rc)::value;
-        if constexpr ((r * RSPAN) / NRD == m) {
+        if constexpr (m >= PRE && (r * RSPAN) / NRD == m - PRE) {
           if constexpr (r < NRA) {
             constexpr int imm = wide_read_imm<AK, r>();
             if constexpr (AK) rd128_issue_at<imm>(na[r], ra0);
@@ -1237,7 +1251,7 @@ gemm_wide_kernel(GemmParams p, int tilesM, int tilesN, int groups) {
       });
       static_for<0, NDMA>([&](auto dc) __attribute__((always_inline)) {
         constexpr int d = decltype(dc)::value;
-        if constexpr ((d * NMF) / NDMA + 1 == m) {
+        if constexpr ((d * (NMF - PRE)) / NDMA + 1 + PRE == m) {
           __builtin_amdgcn_sched_barrier(0);
           if constexpr (d & 1) opB.issue_r(d >> 1, rsb, kdma, dst + kWB * BK, wid);
           else opA.issue_r(d >> 1, rsa, kdma, dst, wid);
