@@ -2,8 +2,11 @@
 
 One step = top-k gate -> capacity-bounded dispatch -> expert FFN grouped GEMMs
 -> weighted combine -> dX chain -> dW products, over one batch of seeded
-synthetic input already resident in HBM (the 8192-token, d_model 1024,
-d_ff 4096, 16-expert, top-2, bf16 layer by default).  Prints ONE JSON line.
+synthetic input already resident in HBM.  The default workload is one GPU's
+expert-parallel share (16384 tokens, d_model 2048, d_ff 8192, 8 local experts
+in 8 destination slices, top-2, capacity factor 1.25, bf16), the largest
+single-GPU MoE-layer workload; --config 2 and 4 select the 8192-token,
+16-expert layer and the Zipf-skewed 64-expert layer.  Prints ONE JSON line.
 
 The expert weights are held in the packed layout the GEMMs read, as a
 training loop on this library keeps them: they are packed once before the
@@ -18,10 +21,15 @@ the step (the launches go out together, without per-kernel host gaps; graph
 replays reproduce the eager step bit for bit, tests/test_gpu_graph.py); the
 eager step is timed too (eager_ms_per_step).  Per-call durations come from
 HIP events recorded around every C-ABI call on the stream the kernels run on,
-over the eager steps.  The roofline object
-reports the expert FFN forward (its two grouped bf16 MFMA GEMMs) against the
-dense bf16 MFMA peak.  The CPU baseline is the float64 oracle on a bounded
-sample of the same workload.
+over the eager steps.  Those steps run over the same buffers (hot caches:
+the 256 MiB Infinity Cache may hold what the previous call wrote); the cold
+variant writes a 512 MiB scratch buffer before every step and before every
+call, outside the timed events, so each call starts from HBM
+(cold_ms_per_step, cold_per_call_ms, cold_hbm_frac_per_call).  The roofline
+object reports the grouped expert GEMM call with the largest share of the
+step (its algorithmic 4 N d f flops over its event-timed duration, against
+the dense bf16 MFMA peak); roofline_calls lists all three.  The CPU
+baseline is the float64 oracle on a bounded sample of the same workload.
 
 With --workload block: one step = forward + backward of the pre-LN MoE block
 (8 sequences x 2048 tokens, d_model 2048, 16 heads, 16 experts, d_ff 8192,
@@ -50,8 +58,9 @@ import numpy as np
 MI355X_PEAK_BF16_TFLOPS = 2500.0   # dense bf16 MFMA
 MI355X_PEAK_HBM_GBPS = 8000.0
 ROOT = os.path.dirname(os.path.abspath(__file__))
-#: HBM bytes per expert-FFN-forward call from PMC counters, valid for the GEMM source it names.
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemm_expert_ffn_bf16_T8192_d1024_f4096_E16_pmc_traffic.md")
+#: HBM bytes per call from PMC counters (profiles/*_pmc_traffic.md), each valid for the
+#: workload, call and GEMM sources it names.
+PROFILES = os.path.join(ROOT, "profiles")
 GEMM_SOURCES = ["paper_2404_19429_amd/csrc/gemm.hip", "paper_2404_19429_amd/csrc/lds_ops.h",
                 "paper_2404_19429_amd/csrc/common.h"]
 
@@ -65,18 +74,20 @@ def gemm_source_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def measured_traffic(workload: str):
-    """Bytes per call recorded in the committed PMC summary, or None if it was
-    taken on another workload or on different GEMM sources."""
-    try:
-        text = open(TRAFFIC_FILE).read()
-    except OSError:
-        return None
-    kv = dict(line.split(":", 1) for line in text.splitlines() if line.startswith(("traffic_", "gemm_", "workload")))
-    kv = {k.strip(): v.strip() for k, v in kv.items()}
-    if kv.get("workload") != workload or kv.get("gemm_source_hash") != gemm_source_hash():
-        return None
-    return float(kv["traffic_bytes_per_call"])
+def measured_traffic(workload: str, call: str):
+    """HBM bytes per call of `call` recorded in a committed PMC summary, or None
+    if none was taken on this workload with the current GEMM sources."""
+    import glob
+    h = gemm_source_hash()
+    for path in sorted(glob.glob(os.path.join(PROFILES, "*_pmc_traffic.md"))):
+        kv = {}
+        for line in open(path).read().splitlines():
+            if line.startswith(("traffic_", "gemm_", "workload", "call")) and ":" in line:
+                k, v = line.split(":", 1)
+                kv[k.strip()] = v.strip()
+        if kv.get("workload") == workload and kv.get("call") == call and kv.get("gemm_source_hash") == h:
+            return float(kv["traffic_bytes_per_call"])
+    return None
 METRIC = "MoE layer fwd+bwd tokens/s on 1 MI355X; expert GEMM MFMA util; dispatch GB/s"
 CALLS = ["gate", "dispatch", "expert_ffn_fwd", "combine", "bwd_dx", "bwd_dw"]
 
@@ -86,12 +97,15 @@ def _args():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--config", type=int, default=2, choices=[2, 3, 4])
+    ap.add_argument("--config", type=int, default=3, choices=[2, 3, 4])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-graph", action="store_true", help="skip the HIP-graph replay of the layer step")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="run one plain device copy of this many MiB first (calibrates HBM byte counters)")
-    ap.add_argument("--cpu-sample-tokens", type=int, default=8192)
+    ap.add_argument("--cpu-sample-tokens", type=int, default=0,
+                    help="tokens of the oracle's CPU sample (0: 2^36 / (d_model d_ff) tokens, at most T: "
+                         "about 10-20 s on the GPU machine's host)")
+    ap.add_argument("--no-cold", action="store_true", help="skip the cold-cache steps")
     ap.add_argument("--workload", default="layer", choices=["layer", "block"])
     ap.add_argument("--pipeline-check", action="store_true",
                     help="block workload: predict the partitioned forward's time for 1, 2, 4, 8 partitions with the "
@@ -389,6 +403,20 @@ def main():
                      b.dWg, b.ws_dw)
         mark(6)
 
+    def step_calls():
+        """The step's six calls as separate callables (the cold-cache variant flushes between them)."""
+        disp = ((lambda: L.moe_dispatch_bpr(cfg, dev["x"], b.logits, b.idx, b.fill, b.slot, b.send_buf, None,
+                                            b.ws_bpr)) if a.routing == "bpr" else
+                (lambda: L.moe_dispatch(cfg, dev["x"], b.idx, b.carry, b.fill, b.slot, b.send_buf, b.ws_dispatch)))
+        return [lambda: L.moe_gate_topk(cfg, dev["x"], dev["Wg"], bias, b.logits, b.idx, b.w), disp,
+                lambda: L.moe_expert_ffn_fwd(cfg, b.send_buf, b.carry, b.fill, b.W1p, b.W2p, b.H, b.A, b.O,
+                                             b.ws_ffn),
+                lambda: L.moe_combine(cfg, b.O, b.idx, b.slot, b.w, b.y),
+                lambda: L.moe_bwd_dx(cfg, dev["Wg"], b.logits, b.idx, b.w, b.slot, b.carry, b.fill, b.H, b.O,
+                                     b.W1p, b.W2p, dev["dy"], b.dO, b.dH, b.dXe, b.dlogits, b.dx, b.ws_dx),
+                lambda: L.moe_bwd_dw(cfg, dev["x"], b.dlogits, b.carry, b.fill, b.send_buf, b.A, b.dO, b.dH,
+                                     b.dW1, b.dW2, b.dWg, b.ws_dw)]
+
     def pack():
         L.moe_pack_weights(cfg, dev["W1"], dev["W2"], b.W1p, b.W2p)
 
@@ -434,6 +462,37 @@ def main():
         graph_ms = (time.perf_counter() - g0) / a.steps * 1e3
     step_ms = sum(evs[i][0].elapsed_time(evs[i][len(CALLS)]) for i in range(a.steps)) / a.steps
 
+    # Cold caches: a 512 MiB scratch read (twice the Infinity Cache) before the
+    # step and before each call, outside the events, so every call reads its
+    # inputs from HBM.  A read leaves clean lines behind (a write would leave
+    # dirty ones, whose write-back the next kernel would pay for).
+    # cold_ms_per_step times whole steps flushed only before the step;
+    # cold_per_call_ms the calls flushed one by one.
+    cold = None
+    if not a.no_cold:
+        scratch = torch.ones(128 << 20, dtype=torch.float32, device="cuda")
+        sink = torch.empty(1, dtype=torch.float32, device="cuda")
+        flush = lambda: torch.sum(scratch, dim=0, keepdim=True, out=sink)
+        cs = max(3, a.steps // 2)
+        ce = [[torch.cuda.Event(enable_timing=True) for _ in range(len(CALLS) + 1)] for _ in range(cs)]
+        cstep = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(cs)]
+        for i in range(cs):
+            flush()
+            cstep[i][0].record(stream)
+            step()
+            cstep[i][1].record(stream)
+        for i in range(cs):
+            calls = step_calls()
+            for j, fn in enumerate(calls):
+                flush()
+                ce[i][j].record(stream)
+                fn()
+                ce[i][j + 1].record(stream)
+        torch.cuda.synchronize()
+        del scratch
+        cold = {"ms_per_step": sum(e[0].elapsed_time(e[1]) for e in cstep) / cs,
+                "per_call_ms": {c: sum(e[j].elapsed_time(e[j + 1]) for e in ce) / cs for j, c in enumerate(CALLS)}}
+
     # One re-pack of W1, W2 (not part of the step; reported for callers that re-pack every step).
     pe = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
     pe[0].record(stream)
@@ -465,24 +524,38 @@ def main():
     N = int(fill.sum())                                           # kept (token, expert) rows
     d, f, T = spec.d, spec.f, spec.T
     eb = 2 if spec.dtype == "bf16" else 4
-    gemm_fwd_flop = 4.0 * N * d * f
-    ffn_s = per_call["expert_ffn_fwd"] * 1e-3
-    achieved_tflops = gemm_fwd_flop / ffn_s / 1e12
-    expert_gemm_s = (per_call["expert_ffn_fwd"]) * 1e-3
-    disp_bytes = (T * d + N * d) * eb + T * spec.k * 4 * 2          # read x, write kept rows, idx + slot
-    dispatch_gbps = disp_bytes / (per_call["dispatch"] * 1e-3) / 1e9
-    # Algorithmic HBM bytes of the other gathers / the gate, per call (event-timed, launch gaps included):
-    # gate reads x and Wg, writes logits, idx, w; combine reads the kept expert rows, idx, slot, w and writes y.
+    gemm_call_flop = 4.0 * N * d * f                              # each of the three GEMM calls: two products
+    # Algorithmic HBM bytes per call: gate reads x and Wg, writes logits, idx, w; dispatch reads x, writes
+    # the kept rows, idx + slot; combine reads the kept expert rows, idx, slot, w and writes y.
+    disp_bytes = (T * d + N * d) * eb + T * spec.k * 4 * 2
     gate_bytes = (T * d + spec.E * d) * eb + T * spec.E * 4 + T * spec.k * 8
     comb_bytes = (N * d + T * d) * eb + T * spec.k * 12
-    hbm_frac = {"gate": gate_bytes / (per_call["gate"] * 1e-3) / 1e9 / MI355X_PEAK_HBM_GBPS,
-                "dispatch": dispatch_gbps / MI355X_PEAK_HBM_GBPS,
-                "combine": comb_bytes / (per_call["combine"] * 1e-3) / 1e9 / MI355X_PEAK_HBM_GBPS}
+    call_bytes = {"gate": gate_bytes, "dispatch": disp_bytes, "combine": comb_bytes}
+
+    def hbm_fracs(pc):
+        return {c: call_bytes[c] / (pc[c] * 1e-3) / 1e9 / MI355X_PEAK_HBM_GBPS for c in call_bytes}
+
+    dispatch_gbps = disp_bytes / (per_call["dispatch"] * 1e-3) / 1e9
+    gemm_calls = {
+        "expert_ffn_fwd": "moe_expert_ffn_fwd: FWD1 H = X W1^T with (H, act(H)) epilogue + FWD2 O = act(H) W2^T "
+                          "(gemm_wide_kernel, + the K-split fix-up launch when a last round is split)",
+        "bwd_dx": "moe_bwd_dx: dA = dO W2 with dA * act'(H) epilogue + dXe = dH W1 (gemm_wide_kernel, + fix-up), "
+                  "plus its combine-backward and dispatch-backward gathers",
+        "bwd_dw": "moe_bwd_dw: ragged-K dW2 = dO^T A + dW1 = dH^T X (gemm_wide_kernel), plus the dWg reduction",
+    }
+    rl_calls = {}
+    for c, what in gemm_calls.items():
+        ach = gemm_call_flop / (per_call[c] * 1e-3) / 1e12
+        rl_calls[c] = {"kernel": what, "bound": "mfma", "achieved": ach, "peak": MI355X_PEAK_BF16_TFLOPS,
+                       "unit": "TFLOP/s", "frac": ach / MI355X_PEAK_BF16_TFLOPS,
+                       "ms": per_call[c], "traffic": measured_traffic(spec.name, c)}
+    dominant = max(gemm_calls, key=lambda c: per_call[c])
     eager_ms = wall / a.steps * 1e3
     working_set = sum(t.numel() * t.element_size() for t in vars(b).values() if isinstance(t, torch.Tensor))
     working_set += sum(t.numel() * t.element_size() for t in dev.values())
     step_ms_timed = graph_ms if graph_ms is not None else eager_ms
     tokens_per_s = T / (step_ms_timed * 1e-3)
+    all_gemm_ms = sum(per_call[c] for c in gemm_calls)
 
     out = {
         "metric": METRIC,
@@ -497,22 +570,20 @@ def main():
         "vs_baseline": None,
         "dtype": spec.dtype,
         "data": "synthetic (seeded Gaussian hidden states and weights; no dataset)",
-        "cache": f"steps repeat over the same buffers with no cache flush; the layer's buffers (weights, packed "
-                 f"weights, activations, gradients, workspaces) total {working_set / 2**30:.2f} GiB, above the "
-                 f"256 MiB Infinity Cache",
+        "cache": f"timed steps repeat over the same buffers (hot: the layer's buffers total "
+                 f"{working_set / 2**30:.2f} GiB, above the 256 MiB Infinity Cache, but a call may find what "
+                 f"the previous call wrote there); 'cold' reads 512 MiB of scratch first",
         "config": {"workload": spec.name, "T": T, "d_model": d, "d_ff": f, "E": spec.E, "k": spec.k,
-                   "C": C, "capacity_factor": f"{spec.cf_num}/{spec.cf_den}", "act": spec.act,
+                   "C": C, "G": spec.G, "capacity_factor": f"{spec.cf_num}/{spec.cf_den}", "act": spec.act,
                    "routing": a.routing,
                    "kept_rows": N, "parallelism": "single GPU (one GPU's share; all-to-all not run)"},
-        "roofline": {"kernel": "expert FFN forward: grouped bf16 MFMA GEMMs gemm_wide_kernel FWD1 + FWD2 "
-                               "(+ the K-split fix-up launch)",
-                     "bound": "mfma", "achieved": achieved_tflops, "peak": MI355X_PEAK_BF16_TFLOPS,
-                     "unit": "TFLOP/s", "frac": achieved_tflops / MI355X_PEAK_BF16_TFLOPS,
-                     "traffic": measured_traffic(spec.name)},
-        "expert_gemm_mfma_frac": achieved_tflops / MI355X_PEAK_BF16_TFLOPS,
+        "roofline": {k: v for k, v in rl_calls[dominant].items() if k != "ms"},
+        "roofline_call": dominant,
+        "roofline_calls": rl_calls,
+        "expert_gemm_mfma_frac": 3 * gemm_call_flop / (all_gemm_ms * 1e-3) / 1e12 / MI355X_PEAK_BF16_TFLOPS,
         "dispatch_GBps": dispatch_gbps,
         "dispatch_hbm_frac": dispatch_gbps / MI355X_PEAK_HBM_GBPS,
-        "hbm_frac_per_call": hbm_frac,
+        "hbm_frac_per_call": hbm_fracs(per_call),
         "per_call_ms": per_call,
         "step_mode": "hip_graph_replay" if graph_ms is not None else "eager",
         "eager_ms_per_step": eager_ms,
@@ -522,8 +593,13 @@ def main():
         **alt,
         "ms_per_step_with_repack": step_ms_timed + pack_ms,
     }
+    if cold is not None:
+        out["cold_ms_per_step"] = cold["ms_per_step"]
+        out["cold_per_call_ms"] = cold["per_call_ms"]
+        out["cold_hbm_frac_per_call"] = hbm_fracs(cold["per_call_ms"])
     if not a.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(spec, inp, a.cpu_sample_tokens)
+        n_cpu = a.cpu_sample_tokens or min(T, max(256, int(2 ** 36 // (d * f)) // 256 * 256))
+        out["cpu_baseline"] = cpu_baseline(spec, inp, n_cpu)
     print(json.dumps(out), flush=True)
 
 

@@ -100,6 +100,16 @@ typedef struct {
   int32_t wpacked; /* 1: moe_bwd_dw writes dW1, dW2 in the packed layout of moe_pack_weights (a
                       training loop that keeps the packed copies as its parameters updates them
                       in place and never re-packs); 0: row-major [out][in] */
+  int32_t ksplit;  /* bf16 expert products that store a plain product (expert_out in
+                      moe_expert_ffn_fwd, dXe in moe_bwd_dx):
+                      1: when the call's tile count leaves a short last round, the K sums of
+                         those last tiles are split over several blocks and their float
+                         partials added in a fixed order (deterministic for a given call, but
+                         the summation order, hence the last bits, depends on how many rows
+                         the call covers);
+                      0: every output element is one K sum taken in order, so results are
+                         bitwise independent of how an expert's rows are split into calls
+                         (batch partitions) */
 } moe_cfg;
 
 /* Expert capacity C = ceil(k*T*cf_num / (E*cf_den)) in exact integer
@@ -332,7 +342,9 @@ size_t moe_block_workspace_bytes(const moe_block_cfg* cfg, int32_t n_chunks);
  *   slots and drops equal the unpartitioned layer -- and its combine (plus the
  *   residual h) as soon as its experts are done.  Partition i's dispatch thus
  *   overlaps partition i+1's attention, and its combine the next partition's
- *   experts.  Every output is bitwise independent of n_chunks.
+ *   experts.  The block's expert products never split a K sum (moe.ksplit
+ *   is ignored and taken as 0), so every output is bitwise independent of
+ *   n_chunks.
  *   Backward (unpartitioned; L = sum <dy, out>): the dX chain runs on
  *   streams[0]; every weight gradient (MoE dW1, dW2, dWg, dWo, dWqkv and the
  *   LayerNorm gains and biases) is deferred to streams[2] as soon as its

@@ -105,11 +105,13 @@ def attention_bwd(do, q, k, v, p, B, S, H):
     return _merge(dq), _merge(dk), _merge(dv)
 
 
-def block_forward(spec, inp, round_acts=None, exact_logits=False):
+def block_forward(spec, inp, round_acts=None, exact_logits=False, C=None, idx_override=None):
     """spec: BlockSpec-like (B, S, d, heads, moe=LayerSpec-like).  inp: x, ln1_g, ln1_b, Wqkv,
     Wo, ln2_g, ln2_b, Wg, W1, W2 (and dy for the backward).  ``round_acts`` (default: the
     block is bf16) rounds the stored activations to bf16; ``exact_logits`` keeps the gate
-    logits in float64 (for comparisons against float64 autograd)."""
+    logits in float64 (for comparisons against float64 autograd); ``C`` is the expert
+    capacity (default: that of the B*S tokens given); ``idx_override`` replaces the
+    MoE layer's top-k choice (see moe_oracle.layer_forward)."""
     B, S, d, H = spec.B, spec.S, spec.d, spec.heads
     if round_acts is None:
         round_acts = spec.moe.dtype == "bf16"
@@ -125,7 +127,7 @@ def block_forward(spec, inp, round_acts=None, exact_logits=False):
     m, m_hat, m_rstd = layernorm(h, inp["ln2_g"], inp["ln2_b"])
     m_in = rnd(m)
     moe_inp = {"x": m_in, "Wg": inp["Wg"], "W1": inp["W1"], "W2": inp["W2"], "bias": None}
-    mw = M.layer_forward(spec.moe, moe_inp, exact_logits=exact_logits)
+    mw = M.layer_forward(spec.moe, moe_inp, exact_logits=exact_logits, C=C, idx_override=idx_override)
     out = h + mw["y"]
     return dict(a=a, a_hat=a_hat, a_rstd=a_rstd, q=q, k=k, v=v, o=o, p=p, h=h, m=m, m_in=m_in,
                 m_hat=m_hat, m_rstd=m_rstd, moe=mw, moe_inp=moe_inp, out=out)

@@ -363,19 +363,22 @@ def gate_bwd(g: np.ndarray, p: np.ndarray, w: np.ndarray, idx: np.ndarray, renor
 
 
 # ------------------------------------------------------------------------ composite
-def layer_forward(spec, inp, carry=None, C=None, exact_logits: bool = False, routing: str = "token"):
+def layer_forward(spec, inp, carry=None, C=None, exact_logits: bool = False, routing: str = "token",
+                  idx_override=None):
     """The whole MoE layer forward for a LayerSpec-like object ``spec`` (fields
     T, E, k, cf_num, cf_den, act, renorm) and inputs dict (x, Wg, bias, W1, W2).
     ``C`` defaults to the capacity of the unpartitioned T tokens.  ``routing``
     "bpr" fills capacity in batch-prioritized order (``assign_slots_bpr``; no
-    carry).  Returns every intermediate, so each stage can be compared on its
-    own."""
+    carry).  ``idx_override`` [T][k] replaces the top-k choice (a test that has
+    checked another computation's choice to be a valid top-k of these logits,
+    differing only at near-ties, follows it from there on).  Returns every
+    intermediate, so each stage can be compared on its own."""
     x = np.asarray(inp["x"], F64)
     T = x.shape[0]
     if C is None:
         C = capacity(T, spec.E, spec.k, spec.cf_num, spec.cf_den)
     logits = gate_logits(inp["x"], inp["Wg"], inp.get("bias"), round_f32=not exact_logits)
-    idx = topk_route(logits, spec.k)
+    idx = topk_route(logits, spec.k) if idx_override is None else np.ascontiguousarray(idx_override, np.int32)
     p, w = gate_weights(logits, idx, spec.renorm)
     carry0 = np.zeros(spec.E, np.int64) if carry is None else np.asarray(carry, np.int64)
     order = None

@@ -1,12 +1,17 @@
 // C ABI of the MoE-layer library: host-side validation, then kernel launches.
 // Validation needs no GPU, so every error path can be exercised on a host
 // without one; only a call that passes validation touches the HIP runtime.
+#include <cstddef>
 #include <cstdio>
 #include <cstdarg>
 #include <cstring>
 #include <string>
 
 #include "internal.h"
+
+// The Python binding and other callers lay these structs out by hand.
+static_assert(sizeof(moe_cfg) == 56 && offsetof(moe_cfg, ksplit) == 48, "moe_cfg layout");
+static_assert(sizeof(moe_block_cfg) == 72 && offsetof(moe_block_cfg, moe) == 16, "moe_block_cfg layout");
 
 namespace {
 
@@ -51,6 +56,7 @@ moe_status check_cfg(const moe_cfg* c, const char* fn, bool need_gemm_shape) {
   if (c->act < MOE_ACT_IDENTITY || c->act > MOE_ACT_GELU_ERF) return fail(MOE_EINVAL, "%s: unknown act %d", fn, c->act);
   if (c->renorm != 0 && c->renorm != 1) return fail(MOE_EINVAL, "%s: renorm must be 0 or 1", fn);
   if (c->wpacked != 0 && c->wpacked != 1) return fail(MOE_EINVAL, "%s: wpacked must be 0 or 1", fn);
+  if (c->ksplit != 0 && c->ksplit != 1) return fail(MOE_EINVAL, "%s: ksplit must be 0 or 1", fn);
   if (c->T < 0) return fail(MOE_EINVAL, "%s: T < 0", fn);
   if (c->T > (int64_t)1 << 31) return fail(MOE_ESHAPE, "%s: T > 2^31 unsupported", fn);
   if (c->E < 1 || c->E > lmoe::kMaxE) return fail(MOE_ESHAPE, "%s: E=%d outside 1..%d", fn, c->E, lmoe::kMaxE);

@@ -9,7 +9,8 @@
 // its combine once its experts are done.  Partition i's dispatch starts from
 // the capacity partition i-1 left (fill[i-1]) and its experts work on rows
 // [fill[i-1], fill[i]) of the shared [E][C][*] buffers, so partitions touch
-// disjoint rows and the result equals the unpartitioned block bit for bit.
+// disjoint rows; the expert products take every K sum whole and in order
+// (moe.ksplit = 0), so the result equals the unpartitioned block bit for bit.
 //
 // Backward (unpartitioned): the activation-gradient chain runs on the compute
 // stream; each weight gradient goes to the weight stream as soon as the
@@ -99,7 +100,8 @@ hipError_t run_block(const moe_block_cfg& c, const moe_block_weights& W, const m
                      const hipStream_t st[3], void* ws) {
   g_events.next = 0;
   const hipStream_t Sc = st[0], Sx = st[1], Sw = st[2];
-  const moe_cfg& mc = c.moe;
+  moe_cfg mc = c.moe;
+  mc.ksplit = 0;   // one in-order K sum per output element: results independent of the partitioning
   const int64_t T = mc.T;
   const int d = mc.d_model, E = mc.E, k = mc.k, H = c.heads, S = c.S;
   const int64_t d3 = 3 * (int64_t)d;

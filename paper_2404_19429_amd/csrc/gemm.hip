@@ -38,6 +38,7 @@ struct GemmParams {
   int act;
   int cap;          // rows per expert block (C): row ranges are clamped to [0, cap]; re == NULL means [0, cap)
   float* part;      // wide ragged-M products: partial tiles of the K-split (stream-K) schedule
+  int ksplit;       // wide plain-store ragged-M products: 1 = a short last round may be K-split
 };
 
 // Row range of group g, clamped to the buffer so bad ranges cannot reach outside it.
@@ -265,13 +266,7 @@ struct TileMN {
 // 8 x 8 patch: each A row-slice and B column-slice it streams is shared by 8
 // tiles through that XCD's L2, instead of one A slice shared by a whole row of
 // tiles while every B slice of the row is fetched afresh.
-#ifndef LMOE_SPLIT_READS
-#define LMOE_SPLIT_READS 1
-#endif
-#ifndef LMOE_PANEL_N
-#define LMOE_PANEL_N 8
-#endif
-constexpr int kPanelN = LMOE_PANEL_N;
+constexpr int kPanelN = 8;
 // BLK: both operands in 16 x 32 blocks (expert buffers and packed weights),
 // ragged row ranges start at the block row containing row_begin; CBLK: the
 // output (and the epilogue's auxiliary input) too.  Otherwise row-major.
@@ -293,6 +288,12 @@ gemm_bf16_kernel(GemmParams p, int tilesM, int tilesN, int groups) {
   using TB = typename std::conditional<BK_C, TileK<BN, NW, BLK>, TileMN<BN, NW, BLK>>::type;
   constexpr int LPS = TA::NI + TB::NI;           // loads per wave per stage
   static_assert(STAGES >= 2 && LPS * (STAGES - 1) < 64, "vmcnt range");
+  // The one geometry this kernel is tested in.  Sweep builds of other tile
+  // shapes (256 x 128 with six stages, 128 x 256, 256 x 256 with four
+  // stages) gave wrong products or an illegal address on the device; their
+  // register and LDS budgets were never derived, so they are not allowed.
+  static_assert(BM == 128 && BN == 128 && WGM == 2 && WGN == 2 && STAGES == 4 && OCC == 2,
+                "gemm_bf16_kernel supports only 128 x 128 tiles, 2 x 2 waves, 4 stages, 2 blocks per CU");
   static_assert(WTM % EPI_ROWS == 0, "wave tile rows must be a multiple of the staged slice");
   static_assert(NW * EPI_ROWS * EPI_LD * 4 <= STAGES * STAGE * 2, "epilogue staging does not fit");
   extern __shared__ __attribute__((aligned(16))) uint16_t lds[];
@@ -400,7 +401,7 @@ gemm_bf16_kernel(GemmParams p, int tilesM, int tilesN, int groups) {
     // With split reads the fragment reads of tile kt+1 are started before a
     // half of tile kt's MFMAs and completed after it, so their latency hides
     // under those MFMAs.
-    constexpr bool kSplit = LMOE_SPLIT_READS && (A_K ? (FM == 4 || FM == 8) : FM == 4) &&
+    constexpr bool kSplit = (A_K ? (FM == 4 || FM == 8) : FM == 4) &&
                             (BK_C ? (FN == 4 || FN == 8) : FN == 4);
     u32x2 pa[8], pb[8];
     auto step = [&](int kt, u32x4 (&ca)[FM], u32x4 (&cb)[FN], u32x4 (&na)[FM], u32x4 (&nb)[FN]) {
@@ -967,7 +968,7 @@ gemm_wide_kernel(GemmParams p, int tilesM, int tilesN, int groups) {
   const int nx = RAGGED_K ? (total > xcd ? (total - xcd + 7) / 8 : 0) : XR.nf + XR.np;
   auto xtile = [&](int j) __attribute__((always_inline)) { return RAGGED_K ? xcd + 8 * j : XR.tile(j); };
   const int nkU = (p.K + BK - 1) / BK;
-  const WSched W = wide_sched(nx, nslot, SPLIT);
+  const WSched W = wide_sched(nx, nslot, SPLIT && p.ksplit != 0);
   int sq = 0, sfirst = 0, scnt = 0, sk0 = 0, sk1 = 0;
   if (SPLIT && W.split) W.split_part(slot, nslot, nkU, sq, sfirst, scnt, sk0, sk1);
   // (uniform values: keep them in scalar registers)
@@ -1359,7 +1360,7 @@ __global__ __launch_bounds__(NW * 64) void gemm_wide_fixup_kernel(GemmParams p, 
   const int xcd = blockIdx.x % 8, q = (blockIdx.x / 8) / FM, i = (blockIdx.x / 8) % FM;
   const WRange XR = wide_range(P, xcd);
   const int nkU = (p.K + kBKb - 1) / kBKb;
-  const WSched W = wide_sched(XR.nf + XR.np, nslot, true);
+  const WSched W = wide_sched(XR.nf + XR.np, nslot, p.ksplit != 0);
   if (!W.split || q >= W.r) return;
   const WGeo G = wide_geo<false, true>(p, XR.tile(W.R * nslot + q), lane, groups, P, tilesM, tilesN);
   // fragment row i of the wave's rows: nothing to add past the group's rows
@@ -1475,26 +1476,14 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmParams p) {
 }
 
 // --------------------------------------------------------------- launchers
-// Tile shape, LDS stages and resident blocks per CU (OCC) of the bf16 kernel.
-#ifndef LMOE_GEMM_TILE
-#define LMOE_GEMM_TILE 128, 128, 2, 2, 4, 2
-#endif
+// Tile shape, LDS stages and resident blocks per CU (OCC) of the bf16 kernel:
+// the one geometry its loads, fragment reads and epilogue staging are
+// written and tested for (four waves of 64 x 64, two blocks per CU).
 template <int BM_, int BN_, int WGM_, int WGN_, int STAGES_, int OCC_> struct TileCfg {
   static constexpr int BM = BM_, BN = BN_, WGM = WGM_, WGN = WGN_, STAGES = STAGES_, OCC = OCC_;
 };
-using Tile = TileCfg<LMOE_GEMM_TILE>;
+using Tile = TileCfg<128, 128, 2, 2, 4, 2>;
 constexpr int kBM = Tile::BM, kBN = Tile::BN;
-
-static int num_cus() {
-  static int n = 0;
-  if (n == 0) {
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess ||
-        hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
-      n = 256;
-  }
-  return n;
-}
 
 template <bool B_K, bool RAGGED_K, int EPI, int ACT, bool BLK, bool CBLK>
 static void launch_bf16(int groups, const GemmParams& p, int tilesM, int tilesN, hipStream_t s) {
@@ -1502,11 +1491,8 @@ static void launch_bf16(int groups, const GemmParams& p, int tilesM, int tilesN,
   constexpr size_t shmem = Tile::STAGES * (size_t)(Tile::BM + Tile::BN) * kBKb * sizeof(uint16_t);
   auto kern = gemm_bf16_kernel<Tile::BM, Tile::BN, Tile::WGM, Tile::WGN, Tile::STAGES, Tile::OCC, B_K, RAGGED_K, EPI,
                                ACT, BLK, CBLK>;
-  static bool attr_set = false;
-  if (!attr_set) {
-    (void)hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)shmem);
-    attr_set = true;
-  }
+  static std::atomic<uint64_t> lds_ok{0};
+  allow_dyn_lds((const void*)kern, (int)shmem, lds_ok);
   const int64_t max_tiles = (int64_t)tilesM * tilesN * groups;
   int blocks = num_cus() * Tile::OCC;
   if (max_tiles < blocks) blocks = (int)((max_tiles + 7) / 8 * 8);
@@ -1542,20 +1528,14 @@ static void run_gemm(int dtype, int act, int groups, const GemmParams& p, int ti
   }
 }
 
-#ifndef LMOE_WIDE_WAVES
-#define LMOE_WIDE_WAVES 8
-#endif
 constexpr int kSkMaxBlocks = 256;   // most blocks of a stream-K launch (partial slots per block: 2)
 template <bool B_K, bool RAGGED_K, int EPI, int ACT, bool CBLK>
 static void launch_wide(int groups, const GemmParams& p, int tilesM, int tilesN, hipStream_t s) {
-  constexpr int S = B_K ? 4 : 5, NW = LMOE_WIDE_WAVES;
+  constexpr int S = B_K ? 4 : 5, NW = 8;
   constexpr size_t shmem = S * (size_t)(2 * kWB) * kBKb * sizeof(uint16_t);
   auto kern = gemm_wide_kernel<NW, S, B_K, RAGGED_K, EPI, ACT, CBLK>;
-  static bool attr_set = false;
-  if (!attr_set) {
-    (void)hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)shmem);
-    attr_set = true;
-  }
+  static std::atomic<uint64_t> lds_ok{0};
+  allow_dyn_lds((const void*)kern, (int)shmem, lds_ok);
   const int64_t max_tiles = (int64_t)tilesM * tilesN * groups;
   int blocks = num_cus();
   if (!RAGGED_K && blocks > kSkMaxBlocks) blocks = kSkMaxBlocks;   // partial slots in the workspace
@@ -1565,7 +1545,7 @@ static void launch_wide(int groups, const GemmParams& p, int tilesM, int tilesN,
   if constexpr (!RAGGED_K && EPI == EPI_STORE) {
     const int nslot = blocks / 8;   // a K-split last round has at most nslot / 4 tiles per XCD
     constexpr int FM = 128 / 16;
-    if (nslot >= 4)
+    if (nslot >= 4 && p.ksplit)
       hipLaunchKernelGGL((gemm_wide_fixup_kernel<NW, EPI, ACT, CBLK>), dim3((unsigned)(8 * (nslot / 4) * FM)),
                          dim3(NW * 64), 0, s, p, tilesM, tilesN, groups, nslot);
   }
@@ -1612,9 +1592,11 @@ void launch_expert_fwd(const moe_cfg& c, const void* X, const int32_t* rb, const
   const int64_t d = c.d_model, f = c.d_ff, C = c.C, Cp = rows_alloc(c);
   GemmParams p1{X, d, Cp * d, W1, d, f * d, H, f, Cp * f, A, nullptr, rb, re, 0, (int)f, (int)d, c.act, (int)C};
   p1.part = (float*)ws;
+  p1.ksplit = c.ksplit;
   run_expert<true, false, EPI_FWD1, true>(c, p1, C, (int)f, s);
   GemmParams p2{A, f, Cp * f, W2, f, d * f, O, d, Cp * d, nullptr, nullptr, rb, re, 0, (int)d, (int)f, c.act, (int)C};
   p2.part = (float*)ws;
+  p2.ksplit = c.ksplit;
   run_expert<true, false, EPI_STORE, false>(c, p2, C, (int)d, s);   // expert_out row-major
 }
 
@@ -1624,10 +1606,12 @@ void launch_expert_bwd_dx(const moe_cfg& c, const void* dO, const int32_t* rb, c
   // dA = dO W2_e  (B(k=i, n=j) = W2[e][i][j], N contiguous), epilogue dH = dA * act'(H)
   GemmParams p1{dO, d, Cp * d, W2, f, d * f, dH, f, Cp * f, nullptr, H, rb, re, 0, (int)f, (int)d, c.act, (int)C};
   p1.part = (float*)ws;
+  p1.ksplit = c.ksplit;
   run_expert<false, false, EPI_DACT, true>(c, p1, C, (int)f, s);
   // dXe = dH W1_e  (B(k=i, n=j) = W1[e][i][j])
   GemmParams p2{dH, f, Cp * f, W1, d, f * d, dXe, d, Cp * d, nullptr, nullptr, rb, re, 0, (int)d, (int)f, c.act, (int)C};
   p2.part = (float*)ws;
+  p2.ksplit = c.ksplit;
   run_expert<false, false, EPI_STORE, false>(c, p2, C, (int)d, s);   // dXe row-major
 }
 

@@ -2,11 +2,44 @@
 #pragma once
 
 #include <algorithm>
+#include <atomic>
 #include <string>
 
 #include "common.h"
 
 namespace lmoe {
+
+inline int current_device() {
+  int d = 0;
+  if (hipGetDevice(&d) != hipSuccess) d = 0;
+  return d;
+}
+
+// A kernel that uses more dynamic LDS than the default limit must be allowed
+// it once per device.  `mask` (one per kernel, zero-initialised) records the
+// devices 0..63 done so far; two threads racing on a first call both set the
+// attribute, which is harmless.  Devices past 63 set it on every call.
+inline void allow_dyn_lds(const void* kern, int bytes, std::atomic<uint64_t>& mask) {
+  const int dev = current_device();
+  const uint64_t bit = dev < 64 ? (uint64_t)1 << dev : 0;
+  if (bit && (mask.load(std::memory_order_acquire) & bit)) return;
+  if (hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, bytes) == hipSuccess && bit)
+    mask.fetch_or(bit, std::memory_order_release);
+}
+
+// Compute units of the current device (cached per device 0..63).
+inline int num_cus() {
+  static std::atomic<int> cache[64];
+  const int dev = current_device();
+  if (dev < 64) {
+    const int n = cache[dev].load(std::memory_order_relaxed);
+    if (n > 0) return n;
+  }
+  int n = 0;
+  if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+  if (dev < 64) cache[dev].store(n, std::memory_order_relaxed);
+  return n;
+}
 
 constexpr int kMaxK = 8;       // largest supported top-k
 constexpr int kMaxE = 64;      // largest supported expert count (one lane per expert in the gate)

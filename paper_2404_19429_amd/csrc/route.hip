@@ -586,12 +586,8 @@ void launch_dispatch_bpr(const moe_cfg& c, const void* x, const float* logits, c
   int32_t* perm = order ? order : (int32_t*)(w + 2 * eb);
   uint64_t* spl = (uint64_t*)(w + 2 * eb + tb);
   if (c.T > 0) {
-    static bool attr_set = false;
-    if (!attr_set) {
-      (void)hipFuncSetAttribute((const void*)bpr_tile_sort_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                (int)kTileSortLds);
-      attr_set = true;
-    }
+    static std::atomic<uint64_t> lds_ok{0};
+    allow_dyn_lds((const void*)bpr_tile_sort_kernel, (int)kTileSortLds, lds_ok);
     const int64_t ntiles = (c.T + kSortTile - 1) / kSortTile;
     hipLaunchKernelGGL(bpr_key_kernel, dim3((unsigned)((c.T + 3) / 4)), dim3(256), 0, s, logits, idx, e0, c.T, c.E,
                        c.k);

@@ -43,7 +43,7 @@ class moe_cfg(ctypes.Structure):
     _fields_ = [("T", ctypes.c_int64), ("d_model", ctypes.c_int32), ("d_ff", ctypes.c_int32),
                 ("E", ctypes.c_int32), ("k", ctypes.c_int32), ("C", ctypes.c_int32), ("G", ctypes.c_int32),
                 ("dtype", ctypes.c_int32), ("act", ctypes.c_int32), ("renorm", ctypes.c_int32),
-                ("wpacked", ctypes.c_int32)]
+                ("wpacked", ctypes.c_int32), ("ksplit", ctypes.c_int32)]
 
 
 class moe_block_cfg(ctypes.Structure):
@@ -105,10 +105,11 @@ _lib = _load()
 
 
 # ----------------------------------------------------------------------- helpers
-def make_cfg(T, d_model, d_ff, E, k, C, G=1, dtype="bf16", act="gelu_tanh", renorm=1, wpacked=0) -> moe_cfg:
+def make_cfg(T, d_model, d_ff, E, k, C, G=1, dtype="bf16", act="gelu_tanh", renorm=1, wpacked=0,
+             ksplit=1) -> moe_cfg:
     dt = {"bf16": MOE_BF16, "f32": MOE_F32}[dtype] if isinstance(dtype, str) else int(dtype)
     return moe_cfg(int(T), int(d_model), int(d_ff), int(E), int(k), int(C), int(G), dt,
-                   ACTS[act] if isinstance(act, str) else int(act), int(renorm), int(wpacked))
+                   ACTS[act] if isinstance(act, str) else int(act), int(renorm), int(wpacked), int(ksplit))
 
 
 def torch_dtype(cfg: moe_cfg):

@@ -92,11 +92,11 @@ def nan_fill(b):
         getattr(b, name).fill_(float("nan"))
 
 
-def run_layer(L, spec, inp, C, backward=True, dw_stream=None, carry=None, routing="token"):
+def run_layer(L, spec, inp, C, backward=True, dw_stream=None, carry=None, routing="token", ksplit=1):
     """Run gate -> dispatch -> experts -> combine (and the backward) on cuda:0."""
     dt = torch.bfloat16 if spec.dtype == "bf16" else torch.float32
     cfg = L.make_cfg(inp["x"].shape[0], spec.d, spec.f, spec.E, spec.k, C, spec.G, spec.dtype, spec.act,
-                     spec.renorm)
+                     spec.renorm, ksplit=ksplit)
     b = L.alloc_layer(cfg)
     nan_fill(b)
     if carry is not None:
@@ -112,3 +112,43 @@ def run_layer(L, spec, inp, C, backward=True, dw_stream=None, carry=None, routin
 
 def spec_C(spec, T=None):
     return O.capacity(spec.T if T is None else T, spec.E, spec.k, spec.cf_num, spec.cf_den)
+
+
+def ksplit_xcds(lo, hi, C, ncols, cus=256, tile=256):
+    """How many XCDs split the K sums of their last round in a plain-store
+    ragged-M expert product (expert_out, dXe) with ksplit = 1: a mirror of the
+    product's schedule (256 x 256 tiles; full M-tiles of every expert, then
+    its short last M-tile, dealt to 8 XCDs in even contiguous shares; rounds of
+    nslot = blocks / 8 tiles; a last round of r tiles is split when
+    0 < 4 r <= nslot).  Used to check that a test case exercises the split."""
+    tn = -(-ncols // tile)
+    tm = -(-(C + 15) // tile)
+    blocks = min(cus, 256, tm * tn * len(lo))
+    blocks = -(-blocks // 8) * 8
+    nslot = blocks // 8
+    NF = NP = 0
+    for a, b in zip(lo, hi):
+        a, b = int(a), int(b)
+        span = b - a
+        if span <= 0:
+            continue
+        span += a & 15
+        t = -(-span // tile)
+        sh = 1 if span % tile else 0
+        NF += (t - sh) * tn
+        NP += sh * tn
+    perF, perP = -(-NF // 8), -(-NP // 8)
+    n_split = 0
+    for x in range(8):
+        nf = max(min(NF, x * perF + perF) - x * perF, 0)
+        npp = max(min(NP, x * perP + perP) - x * perP, 0)
+        r = (nf + npp) % nslot
+        n_split += int(nslot >= 4 and 0 < r and 4 * r <= nslot)
+    return n_split
+
+
+def bf16_ulp(a):
+    """Spacing of bfloat16 numbers at |a| (the ulp of a bf16 value of that magnitude)."""
+    a = np.abs(np.asarray(a, np.float64))
+    e = np.floor(np.log2(np.maximum(a, np.finfo(np.float32).tiny)))
+    return np.exp2(e - 7)

@@ -212,7 +212,17 @@ def test_wpacked_flag_validation():
     assert _gate(_cfg(wpacked=2)) == L.MOE_EINVAL
     assert "wpacked" in L.moe_last_error()
     assert _gate(_cfg(wpacked=1)) == L.MOE_EDEVICE   # valid; no GPU here
-    assert ctypes.sizeof(L.moe_cfg) == 48
+
+
+def test_ksplit_flag_validation_and_struct_layout():
+    assert _gate(_cfg(ksplit=2)) == L.MOE_EINVAL
+    assert "ksplit" in L.moe_last_error()
+    assert _gate(_cfg(ksplit=-1)) == L.MOE_EINVAL
+    assert _gate(_cfg(ksplit=0)) == L.MOE_EDEVICE     # valid; no GPU here
+    # int64 T, ten int32 fields, ksplit, padded to the int64 alignment
+    assert ctypes.sizeof(L.moe_cfg) == 56
+    assert L.moe_cfg.ksplit.offset == 48
+    assert L.moe_block_cfg.moe.offset == 16
 
 
 def test_dispatch_bpr_validation():

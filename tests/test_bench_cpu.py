@@ -1,6 +1,8 @@
-"""Host-side checks of bench.py's bookkeeping (no GPU): the recorded HBM
-traffic of the expert FFN forward is only used for the GEMM sources it was
-measured on, and then lies between the algorithmic bytes and a few times them."""
+"""Host-side checks of bench.py's bookkeeping (no GPU): recorded HBM traffic
+(profiles/*_pmc_traffic.md) is used only for the workload, call and GEMM
+sources it was measured on, and then lies between the algorithmic bytes it
+states and a few times them."""
+import glob
 import os
 import sys
 
@@ -9,27 +11,39 @@ sys.path.insert(0, ROOT)
 
 import bench  # noqa: E402
 
-WORKLOAD = "layer_bf16_T8192_d1024_f4096_E16"
+KEYS = {"workload", "call", "gemm_source_hash", "traffic_bytes_per_call", "algorithmic_bytes_per_call"}
 
 
-def _algorithmic_bytes():
-    # FWD1 reads X and W1 and writes H and act(H); FWD2 reads act(H) and W2 and writes O (bf16).
-    n, d, f, e = 16384, 1024, 4096, 16
-    return ((n * d + e * f * d) + 2 * n * f + (n * f + e * d * f) + n * d) * 2
+def _records():
+    out = []
+    for path in sorted(glob.glob(os.path.join(bench.PROFILES, "*_pmc_traffic.md"))):
+        kv = {}
+        for line in open(path).read().splitlines():
+            if ":" in line and line.split(":", 1)[0].strip() in KEYS:
+                k, v = line.split(":", 1)
+                kv[k.strip()] = v.strip()
+        out.append((path, kv))
+    return out
 
 
-def test_traffic_record_parses_and_is_plausible():
-    text = open(bench.TRAFFIC_FILE).read()
-    keys = {line.split(":", 1)[0].strip() for line in text.splitlines() if ":" in line}
-    assert {"workload", "gemm_source_hash", "traffic_bytes_per_call"} <= keys
-    t = bench.measured_traffic(WORKLOAD)
-    if t is not None:   # recorded for the current sources
-        alg = _algorithmic_bytes()
-        assert alg <= t <= 3 * alg
+def test_traffic_records_parse_and_are_plausible():
+    recs = _records()
+    assert recs, "no PMC traffic summary committed"
+    for path, kv in recs:
+        assert KEYS <= set(kv), (path, kv)
+        t, alg = float(kv["traffic_bytes_per_call"]), float(kv["algorithmic_bytes_per_call"])
+        assert alg <= t <= 3 * alg, path
+        got = bench.measured_traffic(kv["workload"], kv["call"])
+        if kv["gemm_source_hash"] == bench.gemm_source_hash():
+            assert got == t
+        else:
+            assert got is None
 
 
-def test_traffic_record_ignored_for_other_workloads():
-    assert bench.measured_traffic("layer_bf16_T16384_d2048_f8192_E8") is None
+def test_traffic_record_ignored_for_other_workloads_and_calls():
+    assert bench.measured_traffic("no_such_workload", "expert_ffn_fwd") is None
+    for _, kv in _records():
+        assert bench.measured_traffic(kv["workload"], "no_such_call") is None
 
 
 def test_source_hash_covers_the_gemm_sources():

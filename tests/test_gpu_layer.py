@@ -10,8 +10,8 @@ import pytest
 
 from oracle import moe_oracle as O
 from synth import LayerSpec, layer_inputs, layer_spec
-from tests.gpu_harness import (TOL, assert_close, ebuf, host, kept_rows, log, nan_fill, run_layer, spec_C,
-                               to_dev)
+from tests.gpu_harness import (TOL, assert_close, bf16_ulp, ebuf, host, kept_rows, ksplit_xcds, log, nan_fill,
+                               run_layer, spec_C, to_dev)
 
 pytestmark = pytest.mark.gpu
 
@@ -53,7 +53,9 @@ def _check_layer(L, spec):
     log(f"[layer] {spec.name}: T={spec.T} d={spec.d} f={spec.f} E={spec.E} k={spec.k} C={C} {spec.dtype}")
     fw = O.layer_forward(spec, inp)
     bw = O.layer_backward(spec, inp, fw)
+    log(f"[layer] {spec.name}: oracle done")
     b, _ = run_layer(L, spec, inp, C)
+    log(f"[layer] {spec.name}: GPU step done")
     fill = fw["fill"]
 
     np.testing.assert_array_max_ulp(host(b.logits), fw["logits"], maxulp=1)
@@ -118,23 +120,14 @@ def test_packed_weight_gradients_equal_row_major(L):
     np.testing.assert_array_equal(host(dWg), host(b.dWg))
 
 
-def test_batch_partitions_with_capacity_carry_equal_unpartitioned(L):
-    """Four batch partitions, each continuing from the capacity the previous ones
-    used: routing and drops equal the unpartitioned layer (Sec. 2.3), the
-    dispatched rows are bitwise the unpartitioned ones, and the expert outputs
-    agree with the unpartitioned GPU run to float summation order."""
-    spec = _s("chunks", T=1024, d=128, f=256, E=8, cf_num=1, cf_den=1, zipf_s=0.8, seed=21)
-    inp = layer_inputs(spec)
-    C = spec_C(spec)
-    fw = O.layer_forward(spec, inp)
-    full, dev = run_layer(L, spec, inp, C, backward=False)
-    dt = torch.bfloat16
-    n = 4
+def _partitioned_forward(L, spec, inp, dev, C, n, ksplit):
+    """The layer forward in n batch partitions through the C ABI, each
+    dispatch continuing from the capacity the previous partitions used."""
     Tc = spec.T // n
-    cfg = L.make_cfg(Tc, spec.d, spec.f, spec.E, spec.k, C, 1, spec.dtype, spec.act, spec.renorm)
+    cfg = L.make_cfg(Tc, spec.d, spec.f, spec.E, spec.k, C, 1, spec.dtype, spec.act, spec.renorm, ksplit=ksplit)
     b = L.alloc_layer(L.make_cfg(spec.T, spec.d, spec.f, spec.E, spec.k, C, 1, spec.dtype, spec.act, spec.renorm))
     nan_fill(b)
-    bias = torch.as_tensor(inp["bias"], dtype=torch.float32).cuda()
+    bias = None if inp.get("bias") is None else torch.as_tensor(inp["bias"], dtype=torch.float32).cuda()
     fills = [torch.zeros(spec.E, dtype=torch.int32, device="cuda")]
     ws = torch.empty(max(16, L.moe_workspace_bytes(cfg, L.MOE_CALL_DISPATCH)), dtype=torch.uint8, device="cuda")
     L.moe_pack_weights(cfg, dev["W1"], dev["W2"], b.W1p, b.W2p)
@@ -147,19 +140,99 @@ def test_batch_partitions_with_capacity_carry_equal_unpartitioned(L):
         L.moe_expert_ffn_fwd(cfg, b.send_buf, fills[i], fills[i + 1], b.W1p, b.W2p, b.H, b.A, b.O, b.ws_ffn)
         L.moe_combine(cfg, b.O, b.idx[sl], b.slot[sl], b.w[sl], b.y[sl])
     torch.cuda.synchronize()
+    return b, fills
+
+
+def test_batch_partitions_with_capacity_carry_equal_unpartitioned(L):
+    """Four batch partitions, each continuing from the capacity the previous ones
+    used: routing and drops equal the unpartitioned layer (Sec. 2.3), and with
+    ksplit = 0 (every output element one K sum in order) every kept row of
+    every buffer and the output are bitwise the unpartitioned ones."""
+    spec = _s("chunks", T=1024, d=128, f=256, E=8, cf_num=1, cf_den=1, zipf_s=0.8, seed=21)
+    inp = layer_inputs(spec)
+    C = spec_C(spec)
+    fw = O.layer_forward(spec, inp)
+    full, dev = run_layer(L, spec, inp, C, backward=False, ksplit=0)
+    b, fills = _partitioned_forward(L, spec, inp, dev, C, 4, ksplit=0)
     np.testing.assert_array_equal(host(b.slot), fw["slot"])
     np.testing.assert_array_equal(host(fills[-1]), fw["fill"])
     fill = fw["fill"]
-    np.testing.assert_array_equal(kept_rows(ebuf(b, "send_buf"), fill), kept_rows(ebuf(full, "send_buf"), fill))
-    # The expert products split a tile's K sum where their equal pieces fall,
-    # which depends on the call's tile count: after the experts, partitioned
-    # and unpartitioned runs agree to float summation order.
-    for name in ("H", "A", "O"):
-        assert_close(name, kept_rows(ebuf(b, name), fill), kept_rows(ebuf(full, name), fill), 5e-3)
-    assert_close("y", host(b.y), host(full.y), 5e-3)
+    for name in ("send_buf", "H", "A", "O"):
+        np.testing.assert_array_equal(kept_rows(ebuf(b, name), fill), kept_rows(ebuf(full, name), fill), err_msg=name)
+    np.testing.assert_array_equal(host(b.y), host(full.y))
     # carries are the per-partition fills; every partition filled a contiguous, disjoint row range
     f = np.stack([host(t) for t in fills])
     assert np.all(np.diff(f, axis=0) >= 0)
+
+
+# A shape whose plain-store products (expert_out, dXe: 16 experts x 8 column
+# tiles) leave a short last round on every XCD of the 256-CU device, so with
+# ksplit = 1 their last tiles' K sums are split over several blocks and added
+# by the fix-up kernel.
+KSPLIT_CASE = _s("ksplit", T=4096, d=2048, f=512, E=16, seed=32)
+
+
+def _ksplit_bound(a_rows, b_mat, o1, o2):
+    """Largest allowed |o1 - o2| per element for two float32 evaluations of the
+    same K-term dot products o = a b^T, each rounded once to bf16: each float
+    sum is within gamma_K sum|a||b| of the exact one (gamma_K = K u / (1 - K u),
+    u = 2^-24), so the two sums differ by at most twice that, and each rounding
+    adds at most half a bf16 ulp of its value."""
+    K = a_rows.shape[1]
+    u = 2.0 ** -24
+    gamma = K * u / (1 - K * u)
+    S = np.abs(np.asarray(a_rows, np.float64)) @ np.abs(np.asarray(b_mat, np.float64)).T
+    return 2 * gamma * S + bf16_ulp(np.maximum(np.abs(o1), np.abs(o2)))
+
+
+def test_ksplit_products_match_oracle_and_whole_k_sums(L):
+    """ksplit = 1 on a case that splits the last round's K sums on every XCD:
+    every output against the oracle; expert_out, dXe and y against the run with
+    ksplit = 0 within the derived bound of float summation order; everything
+    before the split products bitwise."""
+    spec = KSPLIT_CASE
+    inp = layer_inputs(spec)
+    C = spec_C(spec)
+    fw = O.layer_forward(spec, inp)
+    fill = fw["fill"]
+    n_split = ksplit_xcds(np.zeros(spec.E), fill, C, spec.d)
+    log(f"[ksplit] XCDs whose last round is K-split: {n_split} of 8")
+    assert n_split >= 4, "the case no longer exercises the K-split schedule"
+    b1 = _check_layer(L, spec)                         # ksplit = 1 (the default)
+    b0, _ = run_layer(L, spec, inp, C, ksplit=0)
+    for name in ("logits", "idx", "w", "slot", "fill"):
+        np.testing.assert_array_equal(host(getattr(b1, name)), host(getattr(b0, name)), err_msg=name)
+    for name in ("send_buf", "H", "A", "dO", "dH"):
+        np.testing.assert_array_equal(kept_rows(ebuf(b1, name), fill), kept_rows(ebuf(b0, name), fill), err_msg=name)
+    W1 = inp["W1"].astype(np.float64)
+    W2 = inp["W2"].astype(np.float64)
+    A1, dH1 = ebuf(b1, "A"), ebuf(b1, "dH")
+    O1, O0 = ebuf(b1, "O"), ebuf(b0, "O")
+    X1, X0 = ebuf(b1, "dXe"), ebuf(b0, "dXe")
+    boundO = np.zeros(O1.shape, np.float64)
+    worst = 0.0
+    for e in range(spec.E):
+        n = int(fill[e])
+        bo = _ksplit_bound(A1[e, :n], W2[e], O1[e, :n], O0[e, :n])
+        assert np.all(np.abs(O1[e, :n] - O0[e, :n]) <= bo), f"expert_out of expert {e}"
+        bx = _ksplit_bound(dH1[e, :n], W1[e].T, X1[e, :n], X0[e, :n])
+        assert np.all(np.abs(X1[e, :n] - X0[e, :n]) <= bx), f"dXe of expert {e}"
+        boundO[e, :n] = bo
+        worst = max(worst, float(np.max(np.abs(O1[e, :n] - O0[e, :n]) / bo)))
+    log(f"[ksplit] largest expert_out difference / bound: {worst:.3f}")
+    # y_t = sum_r w_r O_r in float, rounded once to bf16: the expert_out bounds
+    # carried through the weights, the float sums' own rounding, one bf16 rounding
+    idx, slot, w = fw["idx"], fw["slot"], host(b1.w).astype(np.float64)
+    y1, y0 = host(b1.y), host(b0.y)
+    by = np.zeros(y1.shape, np.float64)
+    mag = np.zeros(y1.shape, np.float64)
+    for r in range(spec.k):
+        kept = slot[:, r] >= 0
+        e, s_ = idx[kept, r], slot[kept, r]
+        by[kept] += w[kept, r][:, None] * boundO[e, s_]
+        mag[kept] += w[kept, r][:, None] * np.maximum(np.abs(O1[e, s_]), np.abs(O0[e, s_]))
+    by += bf16_ulp(np.maximum(np.abs(y1), np.abs(y0))) + 2.0 ** -22 * mag
+    assert np.all(np.abs(y1 - y0) <= by), "y"
 
 
 def test_zero_tokens(L):
@@ -185,82 +258,20 @@ def test_zero_tokens(L):
 
 
 # ------------------------------------------------------------- full-size workloads
-def _sampled_full(L, n, n_tok=40, seed=0):
-    spec = layer_spec(n)
-    tol = TOL[spec.dtype]
-    log(f"[full] config {n}: {spec.name}")
-    inp = layer_inputs(spec)
-    C = spec_C(spec)
-    x, dy = inp["x"], inp["dy"]
-    logits = O.gate_logits(x, inp["Wg"], inp["bias"])
-    idx = O.topk_route(logits, spec.k)
-    p, w = O.gate_weights(logits, idx, spec.renorm)
-    slot, fill = O.assign_slots(idx, spec.E, C)
-    log(f"[full] config {n}: oracle routing done, kept={int((slot >= 0).sum())} of {slot.size}")
-    b, dev = run_layer(L, spec, inp, C)
-    log(f"[full] config {n}: GPU step done")
-
-    np.testing.assert_array_max_ulp(host(b.logits), logits, maxulp=1)
-    np.testing.assert_array_equal(host(b.idx), idx)
-    np.testing.assert_array_equal(host(b.slot), slot)
-    np.testing.assert_array_equal(host(b.fill), fill)
-    assert_close("w", host(b.w), w, 1e-5)
-
-    # dispatch: every kept row bitwise equals its token's row, in slot order
-    send = ebuf(b, "send_buf")
-    for e in range(spec.E):
-        ts = [t for s_, t in sorted((int(slot[t, r]), t) for t in range(spec.T) for r in range(spec.k)
-                                     if idx[t, r] == e and slot[t, r] >= 0)]
-        np.testing.assert_array_equal(send[e, :int(fill[e])], x[ts])
-
-    rng = np.random.default_rng(seed)
-    dropped_tok = np.nonzero((slot < 0).any(1))[0]
-    toks = rng.choice(spec.T, size=n_tok, replace=False)
-    if len(dropped_tok):
-        toks = np.concatenate([toks[: n_tok - 8], rng.choice(dropped_tok, size=min(8, len(dropped_tok)), replace=False)])
-    y_gpu, dx_gpu, dl_gpu = host(b.y), host(b.dx), host(b.dlogits)
-    y_ref, dx_ref, dl_ref = [], [], []
-    for t in toks:
-        yt = np.zeros(spec.d)
-        dxt = np.zeros(spec.d)
-        g = np.zeros(spec.k)
-        for r in range(spec.k):
-            if slot[t, r] < 0:
-                continue
-            e = idx[t, r]
-            _, _, o = O.expert_row_forward(x[t], inp["W1"][e], inp["W2"][e], spec.act)
-            yt += w[t, r] * o
-            g[r] = dy[t] @ o
-            dxt += O.expert_row_backward(x[t], w[t, r] * dy[t], inp["W1"][e], inp["W2"][e], spec.act)[1]
-        dl = O.gate_bwd(g[None], p[t][None], w[t][None], idx[t][None], spec.renorm)[0]
-        y_ref.append(yt)
-        dx_ref.append(dxt + dl @ inp["Wg"].astype(np.float64))
-        dl_ref.append(dl)
-    assert_close("y[sample]", y_gpu[toks], np.array(y_ref), tol)
-    assert_close("dx[sample]", dx_gpu[toks], np.array(dx_ref), tol)
-    assert_close("dlogits[sample]", dl_gpu[toks], np.array(dl_ref), tol)
-
-    # dW: sampled rows of dW1 and columns of dW2 for the fullest and one random expert
-    dW1, dW2 = b.dW1, b.dW2
-    for e in sorted({int(np.argmax(fill)), int(rng.integers(spec.E))}):
-        X, dO = O.expert_rows(x, dy, idx, slot, w, e)
-        for i in rng.choice(spec.f, size=3, replace=False):
-            ref = O.expert_dw1_row(X, dO, inp["W1"][e], inp["W2"][e], spec.act, int(i))
-            assert_close(f"dW1[{e}][{i}]", host(dW1[e, int(i)]), ref, tol)
-        for c in rng.choice(spec.f, size=3, replace=False):
-            ref = O.expert_dw2_col(X, dO, inp["W1"][e], spec.act, int(c))
-            assert_close(f"dW2[{e}][:, {c}]", host(dW2[e, :, int(c)]), ref, tol)
-    # experts that received no rows: exact-zero weight gradients (written by their own fill)
-    for e in [e for e in range(spec.E) if fill[e] == 0][:8]:
-        assert torch.count_nonzero(dW1[e]).item() == 0 and torch.count_nonzero(dW2[e]).item() == 0, e
-    # dWg is the product dlogits^T x of the kernel's own dlogits (checked above on samples)
-    dWg_ref = host(b.dlogits).astype(np.float64).T @ x.astype(np.float64)
-    assert_close("dWg (= dlogits^T x)", host(b.dWg), dWg_ref, 1e-5)
-    return spec, fill
-
-
+@pytest.mark.timeout(600)
 @pytest.mark.parametrize("n", [2, 3, 4])
-def test_full_size_config_sampled(L, n):
-    spec, fill = _sampled_full(L, n)
+def test_full_size_config_matches_oracle(L, n):
+    """The workloads at full size, every element of every output against the
+    oracle: routing bit-exact, every kept row of H, A, expert_out, dO, dH, dXe,
+    the output, dlogits, dx, dW1, dW2 and dWg within the bf16 tolerance."""
+    spec = layer_spec(n)
+    log(f"[full] config {n}: {spec.name}")
+    b = _check_layer(L, spec)
+    fill = host(b.fill)
+    C = spec_C(spec)
+    log(f"[full] config {n}: kept {int(fill.sum())} of {spec.k * spec.T}; K-split XCDs in the plain-store "
+        f"products: {ksplit_xcds(np.zeros(spec.E), fill, C, spec.d)} of 8")
     if n == 4:
         assert int(fill.sum()) < spec.k * spec.T, "the Zipf-skewed workload must drop tokens"
+    for e in [e for e in range(spec.E) if fill[e] == 0][:8]:
+        assert torch.count_nonzero(b.dW1[e]).item() == 0 and torch.count_nonzero(b.dW2[e]).item() == 0, e

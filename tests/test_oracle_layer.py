@@ -258,3 +258,28 @@ def test_sampled_dw_forms_match_layer():
         for c in (0, spec.f - 1, 7):
             np.testing.assert_allclose(O.expert_dw2_col(X, dO, inp["W1"][e], spec.act, c),
                                        bw["dW2"][e, :, c], rtol=1e-11, atol=1e-13)
+
+
+def test_idx_override_follows_the_given_choice():
+    """idx_override replaces only the top-k choice: its own choice given back
+    changes nothing; another choice is followed, with its weights taken from
+    the same softmax and the result still equal to the dense-masked formula."""
+    spec = _spec(T=40, E=5, k=2, num=1, den=1)
+    inp = _inputs(spec, seed=77)
+    fw = O.layer_forward(spec, inp)
+    same = O.layer_forward(spec, inp, idx_override=fw["idx"])
+    for n in ("idx", "w", "slot", "fill", "y"):
+        np.testing.assert_array_equal(same[n], fw[n])
+    idx2 = fw["idx"].copy()
+    idx2[3] = idx2[3][::-1]                       # same experts, other rank order
+    third = [e for e in range(spec.E) if e not in idx2[7]][0]
+    idx2[7, 1] = third                            # another second choice
+    alt = O.layer_forward(spec, inp, idx_override=idx2)
+    np.testing.assert_array_equal(alt["idx"], idx2)
+    p = O.softmax(fw["logits"].astype(np.float64))
+    sel = p[7, idx2[7]]
+    np.testing.assert_allclose(alt["w"][7], sel / sel.sum(), rtol=1e-15)
+    np.testing.assert_allclose(alt["y"], _dense_masked_forward(spec, inp, alt), rtol=1e-12, atol=1e-13)
+    changed = {3, 7}
+    keep = [t for t in range(spec.T) if t not in changed and (fw["slot"][t] == alt["slot"][t]).all()]
+    np.testing.assert_allclose(alt["y"][keep], fw["y"][keep], rtol=1e-13, atol=1e-14)
