@@ -155,6 +155,21 @@ moe_status moe_dispatch(const moe_cfg* cfg, const void* x, const int32_t* idx, c
                         int32_t* fill, int32_t* slot, void* send_buf, void* ws, size_t ws_bytes,
                         moe_stream_t stream);
 
+/* moe_dispatch for callers that cannot allocate device memory (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid hipMalloc): the
+ * same arguments, kernels and results, without the workspace argument.  The
+ * workspace is a fixed 1 MiB array inside the library, one per GPU, held until
+ * the process ends; its device address is looked up on the first call on each
+ * device.  The call allocates nothing.
+ *   Limit: 4 * (2 * ceil(T / 256) * E + T * k) <= 1 MiB (for example T = 65536
+ *   tokens at k = 2 and E = 64); larger calls return MOE_ESHAPE and must use
+ *   moe_dispatch.
+ *   All calls on one GPU share the array: calls that overlap in time on that
+ *   GPU (on different streams, or from different threads) race and must not
+ *   be issued.  Nothing in the array needs to start at zero. */
+moe_status moe_dispatch_noalloc(const moe_cfg* cfg, const void* x, const int32_t* idx, const int32_t* carry,
+                                int32_t* fill, int32_t* slot, void* send_buf, moe_stream_t stream);
+
 /* Capacity-bounded dispatch with Batch-prioritized Routing (Sec. 2.3,
  * "Opportunities and Challenges": the tokens of the batch are sorted by
  * importance, the sum of their top-k gating scores, before they are assigned

@@ -163,6 +163,28 @@ moe_status moe_dispatch(const moe_cfg* cfg, const void* x, const int32_t* idx, c
   return check_launch(fn);
 }
 
+moe_status moe_dispatch_noalloc(const moe_cfg* cfg, const void* x, const int32_t* idx, const int32_t* carry,
+                                int32_t* fill, int32_t* slot, void* send_buf, moe_stream_t stream) {
+  const char* fn = "moe_dispatch_noalloc";
+  CHECK(check_cfg(cfg, fn, false));
+  REQUIRE_TPTR(x); REQUIRE_TPTR(idx); OPTIONAL_PTR(carry); REQUIRE_PTR(fill);
+  REQUIRE_TPTR(slot); REQUIRE_PTR(send_buf);
+  if (carry != nullptr && (const void*)carry == (const void*)fill)
+    return fail(MOE_EINVAL, "%s: carry and fill may not alias", fn);
+  const size_t need = lmoe::dispatch_ws_bytes(*cfg);
+  if (need > lmoe::kNoAllocScratchBytes)
+    return fail(MOE_ESHAPE, "%s: this call needs %zu bytes of workspace, above the library's fixed %zu "
+                "(4 * (2 * ceil(T / 256) * E + T * k) must not exceed it); use moe_dispatch", fn, need,
+                lmoe::kNoAllocScratchBytes);
+  CHECK(check_device(fn));
+  void* ws = nullptr;
+  const hipError_t e = lmoe::noalloc_scratch(&ws);
+  if (e != hipSuccess) return fail(MOE_ELAUNCH, "%s: no device address for the fixed workspace: %s", fn,
+                                   hipGetErrorString(e));
+  lmoe::launch_dispatch(*cfg, x, idx, carry, fill, slot, send_buf, ws, (hipStream_t)stream);
+  return check_launch(fn);
+}
+
 moe_status moe_dispatch_bpr(const moe_cfg* cfg, const void* x, const float* logits, const int32_t* idx,
                             int32_t* fill, int32_t* slot, void* send_buf, int32_t* order, void* ws, size_t ws_bytes,
                             moe_stream_t stream) {

@@ -63,6 +63,10 @@ void launch_gate(const moe_cfg& c, const void* x, const void* Wg, const float* b
 size_t dispatch_ws_bytes(const moe_cfg& c);
 void launch_dispatch(const moe_cfg& c, const void* x, const int32_t* idx, const int32_t* carry, int32_t* fill,
                      int32_t* slot, void* send_buf, void* ws, hipStream_t s);
+// moe_dispatch_noalloc: the device address, on the current device, of the
+// library's fixed dispatch workspace (kNoAllocScratchBytes), looked up once per device.
+constexpr size_t kNoAllocScratchBytes = (size_t)1 << 20;
+hipError_t noalloc_scratch(void** out);
 size_t dispatch_bpr_ws_bytes(const moe_cfg& c);
 void launch_dispatch_bpr(const moe_cfg& c, const void* x, const float* logits, const int32_t* idx, int32_t* fill,
                          int32_t* slot, void* send_buf, int32_t* order, void* ws, hipStream_t s);

@@ -9,6 +9,7 @@
 // makes batch partitions exact), and a final pass that adds the chunk base to
 // each rank, applies the capacity and copies the kept rows with 16-byte
 // vector accesses, one thread per (token, 16-byte column chunk).
+#include <mutex>
 #include <type_traits>
 
 #include "internal.h"
@@ -290,6 +291,35 @@ static void dispatch_walk(const moe_cfg& c, const void* x, const int32_t* idx, c
 void launch_dispatch(const moe_cfg& c, const void* x, const int32_t* idx, const int32_t* carry, int32_t* fill,
                      int32_t* slot, void* send_buf, void* ws, hipStream_t s) {
   dispatch_walk(c, x, idx, nullptr, carry, fill, slot, send_buf, ws, s);
+}
+
+// ------------------------------------------- dispatch without caller workspace
+// The workspace of moe_dispatch_noalloc: one file-scope device array, which
+// every GPU the library runs on holds for the life of the process.  Host code
+// never passes the array's name to a kernel (on the host it only stands in
+// for the symbol); it takes the array's device address on each device once,
+// with that device current, and uses that address from then on.
+static __device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+
+namespace {
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[64];   // device address of `scratch` on device i (null until first use)
+}  // namespace
+
+hipError_t noalloc_scratch(void** out) {
+  *out = nullptr;
+  const int dev = current_device();
+  if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_ptr[dev] == nullptr) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (p == nullptr) return hipErrorInvalidSymbol;
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return hipSuccess;
 }
 
 // ------------------------------------------------------ batch-prioritized routing

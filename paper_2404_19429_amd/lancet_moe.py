@@ -27,7 +27,7 @@ MOE_CALL_DISPATCH, MOE_CALL_BWD_DX, MOE_CALL_BWD_DW, MOE_CALL_FFN_FWD, MOE_CALL_
 
 #: Every symbol include/lancet_moe.h declares.
 EXPORTS = ["moe_capacity", "moe_workspace_bytes", "moe_last_error", "moe_gate_topk", "moe_dispatch",
-           "moe_dispatch_bpr", "moe_pack_weights", "moe_expert_ffn_fwd", "moe_combine", "moe_bwd_dx", "moe_bwd_dw",
+           "moe_dispatch_noalloc", "moe_dispatch_bpr", "moe_pack_weights", "moe_expert_ffn_fwd", "moe_combine", "moe_bwd_dx", "moe_bwd_dw",
            "moe_block_workspace_bytes", "moe_block_chunked", "moe_dw_schedule", "moe_pipeline_plan",
            "moe_pipeline_range_cost"]
 MOE_BLOCK_FWD, MOE_BLOCK_BWD = 1, 2
@@ -81,6 +81,7 @@ def _load():
         "moe_last_error": (ctypes.c_char_p, []),
         "moe_gate_topk": (I32, [CFG, P, P, P, P, P, P, P]),
         "moe_dispatch": (I32, [CFG, P, P, P, P, P, P, P, SZ, P]),
+        "moe_dispatch_noalloc": (I32, [CFG, P, P, P, P, P, P, P]),
         "moe_dispatch_bpr": (I32, [CFG, P, P, P, P, P, P, P, P, SZ, P]),
         "moe_pack_weights": (I32, [CFG, P, P, P, P, P]),
         "moe_expert_ffn_fwd": (I32, [CFG, P, P, P, P, P, P, P, P, P, SZ, P]),
@@ -186,6 +187,15 @@ def moe_dispatch(cfg, x, idx, carry, fill, slot, send_buf, ws, stream=None):
                              _ptr(slot, "slot", torch.int32, T * k), _ptr(send_buf, "send_buf", dt, expert_numel(cfg, d)),
                              _ptr(ws, "ws", torch.uint8, need, nullable=need == 0),
                              ws.numel() if ws is not None else 0, _stream(stream)))
+
+
+def moe_dispatch_noalloc(cfg, x, idx, carry, fill, slot, send_buf, stream=None):
+    dt = torch_dtype(cfg)
+    T, d, E, k = cfg.T, cfg.d_model, cfg.E, cfg.k
+    _check(_lib.moe_dispatch_noalloc(ctypes.byref(cfg), _ptr(x, "x", dt, T * d), _ptr(idx, "idx", torch.int32, T * k),
+                                     _ptr(carry, "carry", torch.int32, E, nullable=True),
+                                     _ptr(fill, "fill", torch.int32, E), _ptr(slot, "slot", torch.int32, T * k),
+                                     _ptr(send_buf, "send_buf", dt, expert_numel(cfg, d)), _stream(stream)))
 
 
 def moe_dispatch_bpr(cfg, x, logits, idx, fill, slot, send_buf, order, ws, stream=None):

@@ -239,3 +239,27 @@ def test_dispatch_bpr_validation():
     assert f(ctypes.byref(c), GOOD, GOOD, GOOD, GOOD, GOOD, GOOD, GOOD + 4, GOOD, need, None) == L.MOE_EALIGN
     assert f(ctypes.byref(c), GOOD, GOOD, GOOD, GOOD, GOOD, GOOD, None, GOOD, need, None) == L.MOE_EDEVICE
     assert f(ctypes.byref(c), GOOD, GOOD, GOOD, GOOD, GOOD, GOOD, GOOD, GOOD, need, None) == L.MOE_EDEVICE
+
+
+def test_dispatch_noalloc_validation():
+    """The fixed-workspace dispatch validates like moe_dispatch and rejects a
+    call whose workspace would exceed the library's fixed 1 MiB, on the host."""
+    lib = L._lib
+    f = lib.moe_dispatch_noalloc
+    c = _cfg()
+    assert f(ctypes.byref(c), GOOD, GOOD, None, GOOD, GOOD, GOOD, None) == L.MOE_EDEVICE   # valid; no GPU here
+    assert f(ctypes.byref(c), GOOD, GOOD, GOOD, GOOD, GOOD, GOOD, None) == L.MOE_EINVAL    # carry aliases fill
+    assert "alias" in L.moe_last_error()
+    assert f(ctypes.byref(c), GOOD, None, None, GOOD, GOOD, GOOD, None) == L.MOE_EINVAL
+    assert f(ctypes.byref(c), GOOD + 8, GOOD, None, GOOD, GOOD, GOOD, None) == L.MOE_EALIGN
+    # 4 * (2 * ceil(T / 256) * E + T * k) bytes: T = 65536, E = 64, k = 2 fits exactly below 1 MiB ...
+    fits = _cfg(T=65536, E=64, k=2, C=4096, d_model=128, d_ff=128)
+    assert 4 * (2 * 256 * 64 + 65536 * 2) <= 1 << 20
+    assert f(ctypes.byref(fits), GOOD, GOOD, None, GOOD, GOOD, GOOD, None) == L.MOE_EDEVICE
+    # ... twice the tokens do not
+    big = _cfg(T=131072, E=64, k=2, C=4096, d_model=128, d_ff=128)
+    assert f(ctypes.byref(big), GOOD, GOOD, None, GOOD, GOOD, GOOD, None) == L.MOE_ESHAPE
+    assert "moe_dispatch" in L.moe_last_error()
+    # T = 0 is a valid no-op with null token arrays
+    z = _cfg(T=0)
+    assert f(ctypes.byref(z), None, None, None, GOOD, None, GOOD, None) == L.MOE_EDEVICE
