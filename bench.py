@@ -474,24 +474,25 @@ def main():
         sink = torch.empty(1, dtype=torch.float32, device="cuda")
         flush = lambda: torch.sum(scratch, dim=0, keepdim=True, out=sink)
         cs = max(3, a.steps // 2)
-        ce = [[torch.cuda.Event(enable_timing=True) for _ in range(len(CALLS) + 1)] for _ in range(cs)]
-        cstep = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(cs)]
+        ev = lambda: torch.cuda.Event(enable_timing=True)
+        cstep = [(ev(), ev()) for _ in range(cs)]
+        ccall = [[(ev(), ev()) for _ in CALLS] for _ in range(cs)]   # own start and end per call
         for i in range(cs):
             flush()
             cstep[i][0].record(stream)
             step()
             cstep[i][1].record(stream)
         for i in range(cs):
-            calls = step_calls()
-            for j, fn in enumerate(calls):
+            for j, fn in enumerate(step_calls()):
                 flush()
-                ce[i][j].record(stream)
+                ccall[i][j][0].record(stream)
                 fn()
-                ce[i][j + 1].record(stream)
+                ccall[i][j][1].record(stream)
         torch.cuda.synchronize()
         del scratch
-        cold = {"ms_per_step": sum(e[0].elapsed_time(e[1]) for e in cstep) / cs,
-                "per_call_ms": {c: sum(e[j].elapsed_time(e[j + 1]) for e in ce) / cs for j, c in enumerate(CALLS)}}
+        cold = {"ms_per_step": sum(e0.elapsed_time(e1) for e0, e1 in cstep) / cs,
+                "per_call_ms": {c: sum(ccall[i][j][0].elapsed_time(ccall[i][j][1]) for i in range(cs)) / cs
+                                for j, c in enumerate(CALLS)}}
 
     # One re-pack of W1, W2 (not part of the step; reported for callers that re-pack every step).
     pe = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
