@@ -110,6 +110,9 @@ def _args():
     ap.add_argument("--pipeline-check", action="store_true",
                     help="block workload: predict the partitioned forward's time for 1, 2, 4, 8 partitions with the "
                          "library's pipeline simulator from measured stage times, and compare with the measured time")
+    ap.add_argument("--block-one-stream", action="store_true",
+                    help="block workload: run the timed steps with all work on one stream and skip the variants "
+                         "(a kernel trace of it shows each kernel's own time, without concurrent kernels)")
     ap.add_argument("--routing", default="token", choices=["token", "bpr"],
                     help="capacity order of the layer step: token order, or batch-prioritized (importance order)")
     return ap.parse_args()
@@ -187,9 +190,17 @@ def main_block(a):
     m = spec.moe
     T = spec.B * spec.S
     C = L.moe_capacity(T, m.E, m.k, m.cf_num, m.cf_den)
-    cfg = L.make_block_cfg(spec.B, spec.S, spec.heads, m.f, m.E, m.k, C, m.G, m.act, m.renorm)
+    # The expert weights are kept packed, as a training loop on this library keeps
+    # them (packed once here; dW1, dW2 come back packed), like the layer step.
+    cfg = L.make_block_cfg(spec.B, spec.S, spec.heads, m.f, m.E, m.k, C, m.G, m.act, m.renorm, wpacked=1)
     bf = torch.bfloat16
     w = {n: torch.from_numpy(inp[n]).cuda().to(bf).reshape(-1) for n in L.BLOCK_WEIGHTS}
+    for n in ("W1", "W2"):
+        packed = torch.empty_like(w[n])
+        w[n + "_rowmajor"] = w[n]
+        w[n] = packed
+    L.moe_pack_weights(cfg.moe, w["W1_rowmajor"], w["W2_rowmajor"], w["W1"], w["W2"])
+    del w["W1_rowmajor"], w["W2_rowmajor"]
     x = torch.from_numpy(inp["x"]).cuda().to(bf).reshape(-1)
     dy = torch.from_numpy(inp["dy"]).cuda().to(bf).reshape(-1)
     out, dx = torch.empty_like(x), torch.empty_like(x)
@@ -199,34 +210,43 @@ def main_block(a):
     three = [main, torch.cuda.Stream(), torch.cuda.Stream()]
     one = [main] * 3
 
-    def run(passes, nc, streams):
+    def run(passes, nc, streams, c=None):
         b = bufs[nc]
-        L.moe_block_chunked(cfg, w, b, x, out, dy, dx, b, passes, nc, streams, b["ws"])
+        L.moe_block_chunked(cfg if c is None else c, w, b, x, out, dy, dx, b, passes, nc, streams, b["ws"])
 
-    def timed(passes, nc, streams, steps, warm):
+    def timed(passes, nc, streams, steps, warm, c=None):
         if passes == L.MOE_BLOCK_BWD:
-            run(L.MOE_BLOCK_FWD, nc, streams)            # activations for the backward
+            run(L.MOE_BLOCK_FWD, nc, streams, c)         # activations for the backward
         for _ in range(warm):
-            run(passes, nc, streams)
+            run(passes, nc, streams, c)
         torch.cuda.synchronize()
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record(main)
         for _ in range(steps):
-            run(passes, nc, streams)
+            run(passes, nc, streams, c)
         e1.record(main)
         torch.cuda.synchronize()
         return e0.elapsed_time(e1) / steps
 
     FB = L.MOE_BLOCK_FWD | L.MOE_BLOCK_BWD
+    main_streams = one if a.block_one_stream else three
     for _ in range(a.warmup):
-        run(FB, n, three)
+        run(FB, n, main_streams)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(a.steps):
-        run(FB, n, three)
+        run(FB, n, main_streams)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     step_s = wall / a.steps
+    if a.block_one_stream:
+        kept = int(bufs[n]["fill"].view(n, m.E)[-1].sum().item())
+        fwd_fl, bwd_fl = block_flops(spec, kept)
+        print(json.dumps({"metric": "MoE block fwd+bwd tokens/s on 1 MI355X (4 partitions, one stream)",
+                          "value": T / step_s, "unit": "tokens/s", "ms_per_step": step_s * 1e3,
+                          "steps": a.steps, "warmup": a.warmup, "step_tflop": (fwd_fl + bwd_fl) / 1e12,
+                          "config": {"workload": spec.name, "streams": 1}}), flush=True)
+        return
     k = max(3, a.steps // 2)
     variants = {
         "fwd_4part_3streams": timed(L.MOE_BLOCK_FWD, n, three, k, 2),
@@ -236,6 +256,32 @@ def main_block(a):
         "bwd_1stream": timed(L.MOE_BLOCK_BWD, n, one, k, 2),
     }
     kept = int(bufs[n]["fill"].view(n, m.E)[-1].sum().item())
+    # Ablation analogue (whole forward + backward steps): batch partitioning with
+    # the dispatch/combine stream, and the deferred weight-gradient stream, each
+    # on and off.
+    sx, sw = three[1], three[2]
+    ablation = {
+        "neither (1 partition, 1 stream)": timed(FB, 1, one, k, 2),
+        "partitioning only (4 partitions, dispatch/combine stream, no weight stream)": timed(FB, n, [main, sx, main],
+                                                                                               k, 2),
+        "weight-gradient deferral only (1 partition, weight stream)": timed(FB, 1, [main, main, sw], k, 2),
+        "both (4 partitions, 3 streams)": timed(FB, n, three, k, 2),
+    }
+    # The weight-gradient schedule pass on this run's own operation times
+    # (one stream, MOE_BLOCK_TIMED), the all-to-alls costed as the slice to
+    # one of 7 peers over one 153 GB/s xGMI link.
+    run(L.MOE_BLOCK_FWD, n, one)
+    run(L.MOE_BLOCK_BWD | L.MOE_BLOCK_TIMED, n, one)
+    torch.cuda.synchronize()
+    op_ms = L.moe_block_op_times()
+    a2a_ms = kept * spec.d * 2 / 8 / 153e9 * 1e3
+    dw_order, dw_assign, dw_ov = L.moe_block_dw_schedule(op_ms, a2a_ms)
+    cfg_planned = L.make_block_cfg(spec.B, spec.S, spec.heads, m.f, m.E, m.k, C, m.G, m.act, m.renorm,
+                                   dw_order=dw_order.tolist(), wpacked=1)
+    variants["bwd_3streams_planned_dw_order"] = timed(L.MOE_BLOCK_BWD, n, three, k, 2, cfg_planned)
+    dw_schedule = {"op_ms": {o: float(t) for o, t in zip(L.BLOCK_OPS, op_ms)}, "a2a_ms_model": a2a_ms,
+                   "planned_order": [L.BLOCK_OPS[i] for i in dw_order],
+                   "default_order": L.BLOCK_OPS[8:], "overlap_ms": dw_ov}
     fwd_fl, bwd_fl = block_flops(spec, kept)
     achieved = (fwd_fl + bwd_fl) / step_s / 1e12
     res = {
@@ -245,6 +291,7 @@ def main_block(a):
         "n_gpus": 1, "steps": a.steps, "warmup": a.warmup, "ms_per_step": step_s * 1e3,
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
         "data": "synthetic (seeded Gaussian hidden states and weights; no dataset)",
+        "weights": "expert weights packed once before the timed steps; dW1/dW2 written packed (moe.wpacked=1)",
         "config": {"workload": spec.name, "B": spec.B, "S": spec.S, "d_model": spec.d, "heads": spec.heads,
                    "E": m.E, "k": m.k, "d_ff": m.f, "C": C, "n_chunks": n, "kept_rows": kept,
                    "parallelism": "single GPU (one GPU's share; all-to-all not run)"},
@@ -255,6 +302,8 @@ def main_block(a):
         "variant_ms": variants,
         "pipelining_gain_fwd_ms": variants["fwd_4part_1stream"] - variants["fwd_4part_3streams"],
         "deferred_dw_gain_bwd_ms": variants["bwd_1stream"] - variants["bwd_3streams"],
+        "ablation_step_ms": ablation,
+        "dw_schedule": dw_schedule,
     }
     if a.pipeline_check:
         del bufs
@@ -267,8 +316,8 @@ def main_block(a):
 def pipeline_check(L, torch, spec, cfg, w, x, out, dy, dx, main, three, one):
     """The block forward split into k = 1, 2, 4, 8 batch partitions: stage times
     of one partition (pre-MoE computation up to the gate; dispatch; experts;
-    combine) measured at T / k tokens, plus the expert weight packing the
-    forward does once, the pipelined time the library's
+    combine) measured at T / k tokens (the expert weights stay packed, so the
+    forward's packing stage is empty), the pipelined time the library's
     simulator predicts from them (moe_pipeline_range_cost: compute stages on
     one resource, dispatch/combine on another), and the measured time of the
     partitioned forward on three streams.  On one GPU the dispatch/combine
@@ -294,7 +343,7 @@ def pipeline_check(L, torch, spec, cfg, w, x, out, dy, dx, main, three, one):
         B1 = spec.B // k
         T1 = B1 * spec.S
         C1 = L.moe_capacity(T1, m.E, m.k, m.cf_num, m.cf_den)
-        c1 = L.make_block_cfg(B1, spec.S, spec.heads, m.f, m.E, m.k, C1, m.G, m.act, m.renorm)
+        c1 = L.make_block_cfg(B1, spec.S, spec.heads, m.f, m.E, m.k, C1, m.G, m.act, m.renorm, wpacked=1)
         b = L.alloc_block(c1, 1)
         n1 = T1 * spec.d
         xs, outs = x[:n1], out[:n1]
@@ -304,10 +353,10 @@ def pipeline_check(L, torch, spec, cfg, w, x, out, dy, dx, main, three, one):
         ws_f = torch.empty(max(16, L.moe_workspace_bytes(mc, L.MOE_CALL_FFN_FWD)), dtype=torch.uint8, device="cuda")
         y = b["dm"][:n1]
         disp = avg_ms(lambda: L.moe_dispatch(mc, b["m"], b["idx"], None, b["fill"], b["slot"], b["send_buf"], ws_d))
-        ffn = avg_ms(lambda: L.moe_expert_ffn_fwd(mc, b["send_buf"], None, b["fill"], b["W1p"], b["W2p"], b["H"],
+        ffn = avg_ms(lambda: L.moe_expert_ffn_fwd(mc, b["send_buf"], None, b["fill"], w["W1"], w["W2"], b["H"],
                                                   b["A"], b["expert_out"], ws_f))
         comb = avg_ms(lambda: L.moe_combine(mc, b["expert_out"], b["idx"], b["slot"], b["w"], y))
-        pack = avg_ms(lambda: L.moe_pack_weights(mc, w["W1"], w["W2"], b["W1p"], b["W2p"]))
+        pack = 0.0   # the weights stay packed (moe.wpacked = 1): the forward packs nothing
         stage[k] = [pack, max(0.0, fwd - pack - disp - ffn - comb), disp, ffn, comb]
         if k == 1:
             kept_rows = int(b["fill"].sum().item())

@@ -269,12 +269,40 @@ moe_status moe_bwd_dw(const moe_cfg* cfg, const void* x, const float* dlogits,
  * scaled by 1/sqrt(128), softmax in float; head j uses columns
  * 128 j .. 128 j + 127 of each of the q, k, v blocks of Wqkv [3d][d].  No
  * projection biases.  bf16 only (moe.dtype = MOE_BF16). */
+/* The block backward's operations, as moe_block_chunked issues them:
+ * streams[0] runs the activation-gradient chain 0..7 in this order; the
+ * weight-gradient groups 8..13 go to streams[2], each after the chain
+ * operation whose output it reads (8 after 1, 9 after 0, 10 and 11 after 3,
+ * 12 after 5, 13 after 7). */
+typedef enum {
+  MOE_BOP_COMBINE_BWD = 0,  /* combine and gate backward: dO, dlogits */
+  MOE_BOP_EXPERT_DX = 1,    /* dH = (dO W2) * act'(H), dXe = dH W1 */
+  MOE_BOP_DISPATCH_BWD = 2, /* dm = gathered dXe + dlogits Wg */
+  MOE_BOP_LN2_BWD = 3,      /* dh = dy + LN2'(dm) (and the gain/bias partials) */
+  MOE_BOP_DATTN = 4,        /* d(attention output) = dh Wo */
+  MOE_BOP_ATTN_BWD = 5,     /* dqkv */
+  MOE_BOP_DA = 6,           /* da = dqkv Wqkv */
+  MOE_BOP_LN1_BWD = 7,      /* dx = dh + LN1'(da) (and partials) */
+  MOE_BOP_DW_EXPERT = 8,    /* dW1, dW2 */
+  MOE_BOP_DWG = 9,          /* dWg */
+  MOE_BOP_DLN2 = 10,        /* LN2 gain and bias gradients */
+  MOE_BOP_DWO = 11,         /* dWo = dh^T o */
+  MOE_BOP_DWQKV = 12,       /* dWqkv = dqkv^T a */
+  MOE_BOP_DLN1 = 13,        /* LN1 gain and bias gradients */
+  MOE_BOP_COUNT = 14
+} moe_block_op;
+
 typedef struct {
   int32_t B;     /* sequences */
   int32_t S;     /* tokens per sequence (any S >= 1) */
   int32_t heads; /* d_model = 128 * heads, d_model <= 4096 */
   moe_cfg moe;   /* the MoE layer: moe.T = B*S, moe.d_model = d_model, moe.C = the
                     capacity of all B*S tokens (batch partitions share it) */
+  int32_t dw_order[6]; /* the order in which streams[2] launches the weight-gradient
+                          groups: a permutation of MOE_BOP_DW_EXPERT .. MOE_BOP_DLN1
+                          (moe_block_dw_schedule computes one); dw_order[0] < 0: the
+                          default order 8, 9, 10, 11, 12, 13.  Any order gives the same
+                          gradients bit for bit; it changes only when each group runs. */
 } moe_block_cfg;
 
 typedef struct {           /* all bf16, caller-owned, read only */
@@ -285,8 +313,8 @@ typedef struct {           /* all bf16, caller-owned, read only */
   const void* ln2_g;       /* [d] */
   const void* ln2_b;       /* [d] */
   const void* Wg;          /* [E][d] */
-  const void* W1;          /* [E][f][d] */
-  const void* W2;          /* [E][d][f] */
+  const void* W1;          /* [E][f][d]; with moe.wpacked = 1 the packed copy (moe_pack_weights) */
+  const void* W2;          /* [E][d][f]; likewise */
 } moe_block_weights;
 
 typedef struct {           /* written by the backward (overwritten, not accumulated) */
@@ -297,8 +325,8 @@ typedef struct {           /* written by the backward (overwritten, not accumula
   float* dln2_g;           /* [d] float */
   float* dln2_b;           /* [d] float */
   float* dWg;              /* [E][d] float */
-  void* dW1;               /* [E][f][d] bf16 */
-  void* dW2;               /* [E][d][f] bf16 */
+  void* dW1;               /* [E][f][d] bf16 (moe.wpacked = 1: in the packed layout) */
+  void* dW2;               /* [E][d][f] bf16 (likewise) */
 } moe_block_grads;
 
 /* Caller-owned activations: the forward writes the first group, the backward
@@ -325,8 +353,9 @@ typedef struct {
   void* H;                 /* [E][C][f] */
   void* A;                 /* [E][C][f] */
   void* expert_out;        /* [E][C][d] */
-  void* W1p;               /* [E][f][d] packed copy of W1 (moe_pack_weights), written by the forward */
-  void* W2p;               /* [E][d][f] packed copy of W2 */
+  void* W1p;               /* [E][f][d] packed copy of W1 (moe_pack_weights), written by the forward;
+                              unused (may be NULL) with moe.wpacked = 1, whose weights come packed */
+  void* W2p;               /* [E][d][f] packed copy of W2 (likewise) */
   /* backward */
   void* dO;                /* [E][C][d] */
   void* dH;                /* [E][C][f] */
@@ -340,14 +369,17 @@ typedef struct {
   void* da;                /* [T][d] gradient at a */
 } moe_block_acts;
 
-typedef enum { MOE_BLOCK_FWD = 1, MOE_BLOCK_BWD = 2 } moe_block_pass;
+/* MOE_BLOCK_TIMED (with MOE_BLOCK_BWD): the backward also records timing
+ * events around each operation on its stream (no host synchronisation);
+ * moe_block_op_times reads them afterwards. */
+typedef enum { MOE_BLOCK_FWD = 1, MOE_BLOCK_BWD = 2, MOE_BLOCK_TIMED = 4 } moe_block_pass;
 
 /* Workspace bytes moe_block_chunked needs (host only; 0 and a message on an
  * invalid cfg or n_chunks). */
 size_t moe_block_workspace_bytes(const moe_block_cfg* cfg, int32_t n_chunks);
 
 /* One forward and/or backward pass of the block (passes = MOE_BLOCK_FWD,
- * MOE_BLOCK_BWD or both).
+ * MOE_BLOCK_BWD or both, optionally | MOE_BLOCK_TIMED).
  *   Forward: the B sequences are split into n_chunks partitions of
  *   B/n_chunks whole sequences.  streams[0] (compute) runs LN1, the QKV
  *   projection, attention, the output projection with the residual, LN2 and
@@ -362,8 +394,8 @@ size_t moe_block_workspace_bytes(const moe_block_cfg* cfg, int32_t n_chunks);
  *   n_chunks.
  *   Backward (unpartitioned; L = sum <dy, out>): the dX chain runs on
  *   streams[0]; every weight gradient (MoE dW1, dW2, dWg, dWo, dWqkv and the
- *   LayerNorm gains and biases) is deferred to streams[2] as soon as its
- *   inputs exist (Sec. 2.3 "Opportunity 1"; Sec. 4).
+ *   LayerNorm gains and biases) is deferred to streams[2], in cfg->dw_order,
+ *   each as soon as its inputs exist (Sec. 2.3 "Opportunity 1"; Sec. 4).
  *   x [T][d], out [T][d], dy [T][d], dx [T][d], bf16.  The backward reads the
  *   forward's acts (a forward with the same n_chunks must precede it).
  *   streams: three hipStream_t (entries may repeat).  When the call returns,
@@ -375,6 +407,39 @@ moe_status moe_block_chunked(const moe_block_cfg* cfg, const moe_block_weights* 
                              const moe_block_grads* grads, const void* x, void* out, const void* dy,
                              void* dx, const moe_block_acts* acts, int32_t passes, int32_t n_chunks,
                              const moe_stream_t* streams, void* ws, size_t ws_bytes);
+
+/* Durations (ms) of the MOE_BOP_COUNT backward operations of this thread's
+ * last moe_block_chunked call with MOE_BLOCK_TIMED, from its timing events
+ * (host: waits for them, so call it off the hot path).  With all three
+ * streams the same, each is that operation's own time.  MOE_EINVAL if no
+ * timed backward was issued on this thread and device. */
+moe_status moe_block_op_times(double* ms);
+
+/* The weight-gradient schedule pass (Sec. 4; Alg. 1; moe_dw_schedule below)
+ * applied to the block backward.  Host only.
+ *   The instance: the block backward as the paper's expert-parallel step
+ *   would run it, in the order reverse-mode differentiation emits it (each
+ *   weight gradient where its layer's backward produces it), 16 instructions:
+ *     0 combine bwd, 1 all-to-all (dO to the experts' GPUs), 2 expert dX,
+ *     3 expert dW, 4 all-to-all (dXe back), 5 dispatch bwd, 6 dWg (the gate's
+ *     backward), 7 LN2 bwd, 8 LN2 gain/bias, 9 dWo, 10 d(attn out),
+ *     11 attention bwd, 12 dWqkv, 13 da, 14 LN1 bwd, 15 LN1 gain/bias,
+ *   with the edges 0-1, 1-2, 1-3, 2-3, 2-4, 4-5, 0-5, 0-6, 5-7, 7-8, 7-9,
+ *   7-10, 10-11, 11-12, 11-13, 13-14, 14-15 (dst reads src's output).
+ *   Without a schedule (no all-to-all time) the weight gradients keep this
+ *   order, which is the default dw_order.
+ *   op_ms [MOE_BOP_COUNT] gives the operations' times (for example from
+ *   moe_block_op_times), a2a_ms each all-to-all's (one GPU runs none; the
+ *   caller models it, e.g. bytes over link bandwidth).
+ *   Out: dw_order [6] = the weight-gradient groups (MOE_BOP_DW_EXPERT ..
+ *   MOE_BOP_DLN1) in the order of the reordered sequence, ready for
+ *   moe_block_cfg.dw_order; assign [16] (nullable) = the all-to-all
+ *   (instruction 1 or 4) each instruction overlaps, -1 if none; *overlap =
+ *   the overlapped time.
+ *   Errors (MOE_EINVAL): NULL op_ms, dw_order or overlap; a negative or
+ *   non-finite time. */
+moe_status moe_block_dw_schedule(const double* op_ms, double a2a_ms, int32_t* dw_order, int32_t* assign,
+                                 double* overlap);
 
 /* ------------------------------------------------------------ host planner */
 

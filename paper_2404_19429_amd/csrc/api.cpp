@@ -11,7 +11,9 @@
 
 // The Python binding and other callers lay these structs out by hand.
 static_assert(sizeof(moe_cfg) == 56 && offsetof(moe_cfg, ksplit) == 48, "moe_cfg layout");
-static_assert(sizeof(moe_block_cfg) == 72 && offsetof(moe_block_cfg, moe) == 16, "moe_block_cfg layout");
+static_assert(sizeof(moe_block_cfg) == 96 && offsetof(moe_block_cfg, moe) == 16 &&
+                  offsetof(moe_block_cfg, dw_order) == 72,
+              "moe_block_cfg layout");
 
 namespace {
 
@@ -203,6 +205,26 @@ moe_status moe_dispatch_bpr(const moe_cfg* cfg, const void* x, const float* logi
   return check_launch(fn);
 }
 
+moe_status moe_block_op_times(double* ms) {
+  const char* fn = "moe_block_op_times";
+  if (ms == nullptr) return fail(MOE_EINVAL, "%s: ms is NULL", fn);
+  const hipError_t e = lmoe::block_op_times(ms);
+  if (e == hipErrorNotReady)
+    return fail(MOE_EINVAL, "%s: no timed backward (MOE_BLOCK_TIMED) was issued on this thread and device", fn);
+  if (e != hipSuccess) return fail(MOE_ELAUNCH, "%s: %s", fn, hipGetErrorString(e));
+  return ok();
+}
+
+moe_status moe_block_dw_schedule(const double* op_ms, double a2a_ms, int32_t* dw_order, int32_t* assign,
+                                 double* overlap) {
+  const char* fn = "moe_block_dw_schedule";
+  if (op_ms == nullptr || dw_order == nullptr || overlap == nullptr)
+    return fail(MOE_EINVAL, "%s: op_ms, dw_order and overlap are required", fn);
+  const std::string err = lmoe::block_dw_schedule(op_ms, a2a_ms, dw_order, assign, overlap);
+  if (!err.empty()) return fail(MOE_EINVAL, "%s: %s", fn, err.c_str());
+  return ok();
+}
+
 moe_status moe_dw_schedule(int32_t n, const int32_t* kind, const double* time, int32_t n_edges, const int32_t* src,
                            const int32_t* dst, int32_t* assign, int32_t* order, double* overlap) {
   const char* fn = "moe_dw_schedule";
@@ -336,6 +358,15 @@ moe_status check_block(const moe_block_cfg* c, int32_t n_chunks, const char* fn)
   if (c->moe.T != (int64_t)c->B * c->S) return fail(MOE_EINVAL, "%s: moe.T must equal B*S", fn);
   if (n_chunks < 1 || n_chunks > 64 || c->B % n_chunks != 0)
     return fail(MOE_EINVAL, "%s: n_chunks=%d must divide B=%d (1..64)", fn, n_chunks, c->B);
+  if (c->dw_order[0] >= 0) {
+    int seen = 0;
+    for (int q = 0; q < 6; ++q) {
+      const int op = c->dw_order[q];
+      if (op < MOE_BOP_DW_EXPERT || op > MOE_BOP_DLN1 || (seen >> op) & 1)
+        return fail(MOE_EINVAL, "%s: dw_order is not a permutation of MOE_BOP_DW_EXPERT..MOE_BOP_DLN1", fn);
+      seen |= 1 << op;
+    }
+  }
   return MOE_OK;
 }
 
@@ -352,7 +383,8 @@ moe_status moe_block_chunked(const moe_block_cfg* cfg, const moe_block_weights* 
                              size_t ws_bytes) {
   const char* fn = "moe_block_chunked";
   CHECK(check_block(cfg, n_chunks, fn));
-  if (passes < 1 || passes > 3) return fail(MOE_EINVAL, "%s: passes=%d (1 forward, 2 backward, 3 both)", fn, passes);
+  if (passes < 1 || passes > 7 || passes == MOE_BLOCK_TIMED || passes == (MOE_BLOCK_TIMED | MOE_BLOCK_FWD))
+    return fail(MOE_EINVAL, "%s: passes=%d (1 forward, 2 backward, 3 both; | 4 timed, with a backward)", fn, passes);
   if (!wts || !acts || !streams) return fail(MOE_EINVAL, "%s: weights, acts and streams are required", fn);
   REQUIRE_PTR(x);
   REQUIRE_PTR(wts->ln1_g); REQUIRE_PTR(wts->ln1_b); REQUIRE_PTR(wts->Wqkv); REQUIRE_PTR(wts->Wo);
@@ -361,8 +393,12 @@ moe_status moe_block_chunked(const moe_block_cfg* cfg, const moe_block_weights* 
   REQUIRE_PTR(acts->attn); REQUIRE_PTR(acts->lse); REQUIRE_PTR(acts->h); REQUIRE_PTR(acts->ln2_mean);
   REQUIRE_PTR(acts->ln2_rstd); REQUIRE_PTR(acts->m); REQUIRE_PTR(acts->logits); REQUIRE_PTR(acts->idx);
   REQUIRE_PTR(acts->w); REQUIRE_PTR(acts->slot); REQUIRE_PTR(acts->fill); REQUIRE_PTR(acts->send_buf);
-  REQUIRE_PTR(acts->H); REQUIRE_PTR(acts->A); REQUIRE_PTR(acts->expert_out); REQUIRE_PTR(acts->W1p);
-  REQUIRE_PTR(acts->W2p);
+  REQUIRE_PTR(acts->H); REQUIRE_PTR(acts->A); REQUIRE_PTR(acts->expert_out);
+  if (cfg->moe.wpacked) {
+    OPTIONAL_PTR(acts->W1p); OPTIONAL_PTR(acts->W2p);
+  } else {
+    REQUIRE_PTR(acts->W1p); REQUIRE_PTR(acts->W2p);
+  }
   if (passes & MOE_BLOCK_FWD) REQUIRE_PTR(out);
   if (passes & MOE_BLOCK_BWD) {
     REQUIRE_PTR(dy); REQUIRE_PTR(dx);

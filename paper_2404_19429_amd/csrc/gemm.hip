@@ -851,7 +851,7 @@ __device__ __forceinline__ void wide_epilogue(const GemmParams& p, const WGeo& G
   __amdgpu_buffer_rsrc_t rC2 = rC, rAux = rC;
   if constexpr (EPI == EPI_FWD1)
     rC2 = __builtin_amdgcn_make_buffer_rsrc((uint16_t*)p.C2 + cofs, (short)0, 0x7fffffff, kBufCfg);
-  if constexpr (EPI == EPI_DACT)
+  if constexpr (EPI == EPI_DACT || EPI == EPI_RES)
     rAux = __builtin_amdgcn_make_buffer_rsrc((uint16_t*)p.Aux + cofs, (short)0, 0x7fffffff, kBufCfg);
   const int rl = lane & 15, cq = 4 * (lane >> 4);
   auto voff = [&](bool ok, int row, int col) __attribute__((always_inline)) -> uint32_t {
@@ -861,7 +861,7 @@ __device__ __forceinline__ void wide_epilogue(const GemmParams& p, const WGeo& G
 #pragma unroll
   for (int h = 0; h < 2; ++h) {          // two halves of four fragment rows
     u32x2 aux[4][FN];
-    if constexpr (EPI == EPI_DACT) {     // all loads of the half first, then the math
+    if constexpr (EPI == EPI_DACT || EPI == EPI_RES) {   // all loads of the half first, then the math
 #pragma unroll
       for (int ii = 0; ii < 4; ++ii) {
         const int row = G.m0 + wm * WTM + 16 * (4 * h + ii) + rl;
@@ -895,6 +895,13 @@ __device__ __forceinline__ void wide_epilogue(const GemmParams& p, const WGeo& G
                                __uint_as_float(hv[1] << 16), __uint_as_float(hv[1] & 0xffff0000u)};
 #pragma unroll
           for (int u = 0; u < 4; ++u) v[u] *= act_bwd_t<ACT>(hh[u]);
+          __builtin_amdgcn_raw_buffer_store_b64(pack4_bf16(v), rC, vo, 0, 0);
+        } else if constexpr (EPI == EPI_RES) {
+          const u32x2 rv = aux[ii][j];
+          v[0] += __uint_as_float(rv[0] << 16);
+          v[1] += __uint_as_float(rv[0] & 0xffff0000u);
+          v[2] += __uint_as_float(rv[1] << 16);
+          v[3] += __uint_as_float(rv[1] & 0xffff0000u);
           __builtin_amdgcn_raw_buffer_store_b64(pack4_bf16(v), rC, vo, 0, 0);
         } else {
           __builtin_amdgcn_raw_buffer_store_b64(pack4_bf16(v), rC, vo, 0, 0);
@@ -1650,6 +1657,52 @@ void launch_dense_wgrad(int M, int N, int64_t K, const void* A, int64_t lda, con
                         int64_t ldc, hipStream_t s) {
   GemmParams p{A, lda, 0, B, ldb, 0, C, ldc, 0, nullptr, nullptr, nullptr, nullptr, M, N, 0, 0, (int)K};
   run_gemm<false, true, EPI_STORE>(MOE_BF16, 0, 1, p, cdiv(M, kBM), cdiv(N, kBN), s);
+}
+
+// Row-major [M][K] bf16 -> the blocked layout with pad16(M) rows (rows past M
+// zero).  One wave per 16 x 32 block: each lane reads 16 bytes of one row and
+// the wave writes the block's 1 KiB as one contiguous run.
+__global__ __launch_bounds__(256) void pack_rows_kernel(const uint16_t* __restrict__ src, uint16_t* __restrict__ dst,
+                                                        int64_t M, int K) {
+  const int64_t b = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
+  const int lane = threadIdx.x & 63;
+  const int kb = K >> 5;
+  const int64_t rb = b / kb;
+  if (rb * 16 >= pad16(M)) return;
+  const int cb = (int)(b - rb * kb);
+  const int64_t row = rb * 16 + (lane >> 2);
+  const int col = cb * 32 + (lane & 3) * 8;
+  u32x4 v = u32x4{0u, 0u, 0u, 0u};
+  if (row < M) v = *reinterpret_cast<const u32x4*>(src + row * K + col);
+  *reinterpret_cast<u32x4*>(dst + b * 512 + lane * 8) = v;
+}
+
+void launch_pack_rows(const void* src, void* dst, int64_t M, int K, hipStream_t s) {
+  if (M <= 0 || K <= 0) return;
+  const int64_t blocks = pad16(M) / 16 * (K / 32);
+  hipLaunchKernelGGL(pack_rows_kernel, dim3((unsigned)((blocks * 64 + 255) / 256)), dim3(256), 0, s,
+                     (const uint16_t*)src, (uint16_t*)dst, M, K);
+}
+
+// Dense products on the wide MFMA kernel: one group of M rows, both operands
+// blocked (A [pad16(M)][K]; B [N][K] if b_nk else [K][N]), output row-major,
+// + resid (row-major like C) if given.  Every output element is one in-order
+// K sum (no K-split), so a product over a batch partition's rows gives the
+// same bits as over the whole batch.
+void launch_dense_wide(int64_t M, int N, int K, const void* A, const void* B, bool b_nk, void* C, int64_t ldc,
+                       const void* resid, hipStream_t s) {
+  if (M <= 0 || N <= 0 || K <= 0) return;
+  GemmParams p{A, K, pad16(M) * K, B, b_nk ? K : N, (int64_t)N * K, C, ldc, M * ldc, nullptr, resid, nullptr, nullptr,
+               0, N, K, 0, (int)M};
+  p.ksplit = 0;
+  const int tm = (int)((M + 15 + kWB - 1) / kWB), tn = (N + kWB - 1) / kWB;
+  if (b_nk) {
+    if (resid) launch_wide<true, false, EPI_RES, MOE_ACT_IDENTITY, false>(1, p, tm, tn, s);
+    else launch_wide<true, false, EPI_STORE, MOE_ACT_IDENTITY, false>(1, p, tm, tn, s);
+  } else {
+    if (resid) launch_wide<false, false, EPI_RES, MOE_ACT_IDENTITY, false>(1, p, tm, tn, s);
+    else launch_wide<false, false, EPI_STORE, MOE_ACT_IDENTITY, false>(1, p, tm, tn, s);
+  }
 }
 
 }  // namespace lmoe

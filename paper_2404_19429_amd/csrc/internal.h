@@ -52,6 +52,10 @@ std::string dw_schedule(int n, const int32_t* kind, const double* time, int n_ed
 
 double pipeline_range_cost(int N, int K, const int32_t* kind, const double* times, const double* join, int i, int n,
                            int k);
+// The block backward's weight-gradient schedule (the instance is described
+// with moe_block_dw_schedule in lancet_moe.h).
+std::string block_dw_schedule(const double* op_ms, double a2a_ms, int32_t* dw_order, int32_t* assign,
+                              double* overlap);
 std::string pipeline_plan(int N, int K, const int32_t* kind, const double* times, const double* join, int G,
                           int32_t* seg_begin, int32_t* seg_end, int32_t* seg_k, int32_t* n_seg, double* total);
 
@@ -101,6 +105,11 @@ void launch_dense(int64_t M, int N, int K, const void* A, int64_t lda, const voi
                   void* C, int64_t ldc, const void* resid, hipStream_t s);
 void launch_dense_wgrad(int M, int N, int64_t K, const void* A, int64_t lda, const void* B, int64_t ldb, void* C,
                         int64_t ldc, hipStream_t s);
+// Row-major [M][K] -> blocked [pad16(M)][K] (K a multiple of 32), and dense
+// products on the wide kernel over blocked operands (see gemm.hip).
+void launch_pack_rows(const void* src, void* dst, int64_t M, int K, hipStream_t s);
+void launch_dense_wide(int64_t M, int N, int K, const void* A, const void* B, bool b_nk, void* C, int64_t ldc,
+                       const void* resid, hipStream_t s);
 
 // attn.hip: causal attention of the block (head dim 128).  Pointers are at
 // the first token of nseq whole sequences of S tokens; lse and delta rows have
@@ -112,16 +121,19 @@ void launch_attn_bwd(const void* qkv, const void* o, const void* dout, const flo
 
 // norm.hip: LayerNorm (eps 1e-5) of bf16 rows of width d (multiple of 8, <= 4096).
 // The backward writes ln_bwd_blocks(T) x 2 x d float partials, reduced by
-// launch_ln_gain_reduce into the gain and bias gradients.
+// launch_ln_gain_reduce into the gain and bias gradients (the reduction
+// overwrites some partials: run it once per backward).
 int ln_bwd_blocks(int64_t T);
 void launch_ln_fwd(const void* x, const void* g, const void* b, void* y, float* mean, float* rstd, int64_t T, int d,
                    hipStream_t s);
 void launch_ln_bwd(const void* dyl, const void* x, const float* mean, const float* rstd, const void* g,
                    const void* dres, void* dx, float* part, int64_t T, int d, hipStream_t s);
-void launch_ln_gain_reduce(const float* part, int64_t T, int d, float* dg, float* db, hipStream_t s);
+void launch_ln_gain_reduce(float* part, int64_t T, int d, float* dg, float* db, hipStream_t s);
 
 // block.cpp: the partitioned block (arguments validated by the C ABI layer).
 size_t block_ws_bytes(const moe_block_cfg& c, int n_chunks);
+void dw_launch_order(const moe_block_cfg& c, int32_t out[6]);
+hipError_t block_op_times(double* ms);   // hipErrorNotReady: no timed backward on this thread and device
 hipError_t run_block(const moe_block_cfg& c, const moe_block_weights& W, const moe_block_grads* G, const void* x,
                      void* out, const void* dy, void* dx, const moe_block_acts& A, int passes, int n,
                      const hipStream_t st[3], void* ws);

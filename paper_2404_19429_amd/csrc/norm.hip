@@ -186,14 +186,28 @@ __global__ __launch_bounds__(256) void ln_bwd_kernel(const uint16_t* __restrict_
   }
 }
 
-// dg[j] = sum over blocks of part[blk][0][j], db likewise, in block order.
+// dg[j] = sum over blocks of part[blk][0][j], db likewise, in a fixed order:
+// runs of kGainRun consecutive block partials are summed first (in block
+// order, the sum left in the run's first partial row), then the run sums in
+// run order.  Two launches spread the reads of the partials over the GPU.
+constexpr int kGainRun = 32;
+__global__ __launch_bounds__(256) void ln_gain_run_kernel(float* __restrict__ part, int nblk, int d) {
+  const int j = blockIdx.x * blockDim.x + threadIdx.x;
+  if (j >= 2 * d) return;
+  const int b0 = blockIdx.y * kGainRun, b1 = min(nblk, b0 + kGainRun);
+  float acc = 0.f;
+#pragma unroll 8
+  for (int b = b0; b < b1; ++b) acc += part[(int64_t)b * 2 * d + j];
+  part[(int64_t)b0 * 2 * d + j] = acc;
+}
+
 __global__ __launch_bounds__(256) void ln_gain_reduce_kernel(const float* __restrict__ part, int nblk, int d,
                                                              float* __restrict__ dg, float* __restrict__ db) {
   const int j = blockIdx.x * blockDim.x + threadIdx.x;
   if (j >= 2 * d) return;
   const int which = j / d, col = j % d;
   float acc = 0.f;
-  for (int k = 0; k < nblk; ++k) acc += part[(int64_t)k * 2 * d + which * d + col];
+  for (int b = 0; b < nblk; b += kGainRun) acc += part[(int64_t)b * 2 * d + j];
   (which == 0 ? dg : db)[col] = acc;
 }
 
@@ -228,10 +242,13 @@ void launch_ln_bwd(const void* dyl, const void* x, const float* mean, const floa
 #undef LMOE_LN_BWD
 }
 
-void launch_ln_gain_reduce(const float* part, int64_t T, int d, float* dg, float* db, hipStream_t s) {
+void launch_ln_gain_reduce(float* part, int64_t T, int d, float* dg, float* db, hipStream_t s) {
   const int nblk = T > 0 ? ln_bwd_blocks(T) : 0;
-  hipLaunchKernelGGL(ln_gain_reduce_kernel, dim3((unsigned)((2 * d + 255) / 256)), dim3(256), 0, s, part, nblk, d,
-                     dg, db);
+  const unsigned cols = (unsigned)((2 * d + 255) / 256);
+  if (nblk > 0)
+    hipLaunchKernelGGL(ln_gain_run_kernel, dim3(cols, (unsigned)((nblk + kGainRun - 1) / kGainRun)), dim3(256), 0, s,
+                       part, nblk, d);
+  hipLaunchKernelGGL(ln_gain_reduce_kernel, dim3(cols), dim3(256), 0, s, (const float*)part, nblk, d, dg, db);
 }
 
 }  // namespace lmoe

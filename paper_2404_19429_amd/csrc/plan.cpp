@@ -157,6 +157,45 @@ std::string dw_schedule(int n, const int32_t* kind, const double* time, int n_ed
   return "";
 }
 
+// ------------------------------------------------- the block backward's schedule
+// The block backward as the paper's expert-parallel step runs it, in the
+// order reverse-mode differentiation emits it (the instance is spelled out
+// with moe_block_dw_schedule in lancet_moe.h): the chain, each weight
+// gradient where the backward of its layer produces it, and the two
+// all-to-alls of the MoE layer around its experts.
+std::string block_dw_schedule(const double* op_ms, double a2a_ms, int32_t* dw_order, int32_t* assign,
+                              double* overlap) {
+  if (!std::isfinite(a2a_ms) || a2a_ms < 0) return "a2a_ms not a finite value >= 0";
+  constexpr int A2A = -1;   // stand-in for an all-to-all in the op list below
+  static const int ops[16] = {MOE_BOP_COMBINE_BWD, A2A,           MOE_BOP_EXPERT_DX, MOE_BOP_DW_EXPERT,
+                              A2A,                 MOE_BOP_DISPATCH_BWD, MOE_BOP_DWG,   MOE_BOP_LN2_BWD,
+                              MOE_BOP_DLN2,        MOE_BOP_DWO,   MOE_BOP_DATTN,     MOE_BOP_ATTN_BWD,
+                              MOE_BOP_DWQKV,       MOE_BOP_DA,    MOE_BOP_LN1_BWD,   MOE_BOP_DLN1};
+  static const int32_t src[] = {0, 1, 1, 2, 2, 4, 0, 0, 5, 7, 7, 7, 10, 11, 11, 13, 14};
+  static const int32_t dst[] = {1, 2, 3, 3, 4, 5, 5, 6, 7, 8, 9, 10, 11, 12, 13, 14, 15};
+  int32_t kind[16];
+  double time[16];
+  for (int i = 0; i < 16; ++i) {
+    const int op = ops[i];
+    if (op == A2A) {
+      kind[i] = kA2A;
+      time[i] = a2a_ms;
+    } else {
+      kind[i] = op >= MOE_BOP_DW_EXPERT ? kDW : kOther;
+      time[i] = op_ms[op];
+    }
+  }
+  int32_t asg[16], ord[16];
+  const std::string err = dw_schedule(16, kind, time, (int)(sizeof src / sizeof src[0]), src, dst, asg, ord, overlap);
+  if (!err.empty()) return err;
+  int q = 0;
+  for (int i = 0; i < 16; ++i)
+    if (kind[ord[i]] == kDW) dw_order[q++] = ops[ord[i]];
+  if (assign)
+    for (int i = 0; i < 16; ++i) assign[i] = asg[i];
+  return "";
+}
+
 // ----------------------------------------------------------- partition ranges
 
 namespace {

@@ -28,9 +28,13 @@ MOE_CALL_DISPATCH, MOE_CALL_BWD_DX, MOE_CALL_BWD_DW, MOE_CALL_FFN_FWD, MOE_CALL_
 #: Every symbol include/lancet_moe.h declares.
 EXPORTS = ["moe_capacity", "moe_workspace_bytes", "moe_last_error", "moe_gate_topk", "moe_dispatch",
            "moe_dispatch_noalloc", "moe_dispatch_bpr", "moe_pack_weights", "moe_expert_ffn_fwd", "moe_combine", "moe_bwd_dx", "moe_bwd_dw",
-           "moe_block_workspace_bytes", "moe_block_chunked", "moe_dw_schedule", "moe_pipeline_plan",
-           "moe_pipeline_range_cost"]
-MOE_BLOCK_FWD, MOE_BLOCK_BWD = 1, 2
+           "moe_block_workspace_bytes", "moe_block_chunked", "moe_block_op_times", "moe_block_dw_schedule",
+           "moe_dw_schedule", "moe_pipeline_plan", "moe_pipeline_range_cost"]
+MOE_BLOCK_FWD, MOE_BLOCK_BWD, MOE_BLOCK_TIMED = 1, 2, 4
+#: The block backward's operations (moe_block_op): the chain 0..7, the weight-gradient groups 8..13.
+BLOCK_OPS = ["combine_bwd", "expert_dx", "dispatch_bwd", "ln2_bwd", "dattn", "attn_bwd", "da", "ln1_bwd",
+             "dw_expert", "dwg", "dln2", "dwo", "dwqkv", "dln1"]
+MOE_BOP_DW_EXPERT = 8
 
 
 class MoeError(RuntimeError):
@@ -47,7 +51,8 @@ class moe_cfg(ctypes.Structure):
 
 
 class moe_block_cfg(ctypes.Structure):
-    _fields_ = [("B", ctypes.c_int32), ("S", ctypes.c_int32), ("heads", ctypes.c_int32), ("moe", moe_cfg)]
+    _fields_ = [("B", ctypes.c_int32), ("S", ctypes.c_int32), ("heads", ctypes.c_int32), ("moe", moe_cfg),
+                ("dw_order", ctypes.c_int32 * 6)]
 
 
 BLOCK_WEIGHTS = ["ln1_g", "ln1_b", "Wqkv", "Wo", "ln2_g", "ln2_b", "Wg", "W1", "W2"]
@@ -89,6 +94,8 @@ def _load():
         "moe_bwd_dx": (I32, [CFG] + [P] * 18 + [SZ, P]),
         "moe_bwd_dw": (I32, [CFG] + [P] * 12 + [SZ, P]),
         "moe_dw_schedule": (I32, [I32, P, P, I32, P, P, P, P, P]),
+        "moe_block_op_times": (I32, [P]),
+        "moe_block_dw_schedule": (I32, [P, ctypes.c_double, P, P, P]),
         "moe_pipeline_plan": (I32, [I32, I32, P, P, P, I32, P, P, P, P, P]),
         "moe_pipeline_range_cost": (I32, [I32, I32, P, P, P, I32, I32, I32, P]),
         "moe_block_workspace_bytes": (SZ, [ctypes.POINTER(moe_block_cfg), I32]),
@@ -409,9 +416,35 @@ def layer_backward(b: LayerBuffers, x, Wg, dy, stream=None, dw_stream=None):
 
 
 # ------------------------------------------------------------------------ block
-def make_block_cfg(B, S, heads, d_ff, E, k, C, G=1, act="gelu_tanh", renorm=1) -> moe_block_cfg:
+def make_block_cfg(B, S, heads, d_ff, E, k, C, G=1, act="gelu_tanh", renorm=1, dw_order=None,
+                   wpacked=0) -> moe_block_cfg:
+    """dw_order: the weight-gradient groups (8..13) in launch order; None = the default order.
+    wpacked: 1 = the block's W1, W2 are the packed copies and dW1, dW2 come packed."""
     d = 128 * heads
-    return moe_block_cfg(int(B), int(S), int(heads), make_cfg(B * S, d, d_ff, E, k, C, G, "bf16", act, renorm))
+    order = (ctypes.c_int32 * 6)(*([-1] * 6 if dw_order is None else [int(v) for v in dw_order]))
+    return moe_block_cfg(int(B), int(S), int(heads),
+                         make_cfg(B * S, d, d_ff, E, k, C, G, "bf16", act, renorm, wpacked=wpacked), order)
+
+
+def moe_block_op_times():
+    """Durations (ms) of the backward operations of this thread's last timed block call (BLOCK_OPS order)."""
+    import numpy as np
+    ms = np.zeros(len(BLOCK_OPS), np.float64)
+    _check(_lib.moe_block_op_times(ms.ctypes.data))
+    return ms
+
+
+def moe_block_dw_schedule(op_ms, a2a_ms):
+    """The block backward's weight-gradient schedule: (dw_order [6], assign [16], overlap)."""
+    import numpy as np
+    t = np.ascontiguousarray(op_ms, np.float64)
+    assert t.size == len(BLOCK_OPS)
+    order = np.empty(6, np.int32)
+    assign = np.empty(16, np.int32)
+    ov = ctypes.c_double(0.0)
+    _check(_lib.moe_block_dw_schedule(t.ctypes.data, float(a2a_ms), order.ctypes.data, assign.ctypes.data,
+                                      ctypes.byref(ov)))
+    return order, assign, ov.value
 
 
 def block_shapes(cfg: moe_block_cfg, n_chunks: int):

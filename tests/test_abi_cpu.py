@@ -263,3 +263,20 @@ def test_dispatch_noalloc_validation():
     # T = 0 is a valid no-op with null token arrays
     z = _cfg(T=0)
     assert f(ctypes.byref(z), None, None, None, GOOD, None, GOOD, None) == L.MOE_EDEVICE
+
+
+def test_block_cfg_layout_and_dw_order_validation():
+    assert ctypes.sizeof(L.moe_block_cfg) == 96 and L.moe_block_cfg.dw_order.offset == 72
+    bad = L.make_block_cfg(2, 64, 2, 512, 8, 2, 40, dw_order=[8, 9, 10, 11, 12, 12])
+    assert L.moe_block_workspace_bytes(bad, 1) == 0
+    assert "dw_order" in L.moe_last_error()
+    bad2 = L.make_block_cfg(2, 64, 2, 512, 8, 2, 40, dw_order=[7, 9, 10, 11, 12, 13])
+    assert L.moe_block_workspace_bytes(bad2, 1) == 0
+    good = L.make_block_cfg(2, 64, 2, 512, 8, 2, 40, dw_order=[13, 12, 11, 10, 9, 8])
+    assert L.moe_block_workspace_bytes(good, 1) > 0
+    assert L.moe_block_workspace_bytes(L.make_block_cfg(2, 64, 2, 512, 8, 2, 40), 1) > 0
+
+
+def test_block_op_times_without_a_timed_call():
+    ms = (ctypes.c_double * 14)()
+    assert L._lib.moe_block_op_times(ms) in (L.MOE_EINVAL, L.MOE_ELAUNCH)

@@ -177,3 +177,58 @@ def test_planner_large_instance_is_fast():
     pos[o] = np.arange(n)
     assert all(pos[s] < pos[d] for s, d in edges)          # a valid execution order
     assert sorted(o.tolist()) == list(range(n))
+
+
+# --------------------------------------------- the library's block schedule
+# moe_block_dw_schedule's instance, written here from its description in
+# include/lancet_moe.h: instruction i runs block op OPS[i] (None = an
+# all-to-all), in reverse-mode emission order.
+_BOP = {n: i for i, n in enumerate(L.BLOCK_OPS)}
+_LIB_OPS = ["combine_bwd", None, "expert_dx", "dw_expert", None, "dispatch_bwd", "dwg", "ln2_bwd", "dln2", "dwo",
+            "dattn", "attn_bwd", "dwqkv", "da", "ln1_bwd", "dln1"]
+_LIB_EDGES = [(0, 1), (1, 2), (1, 3), (2, 3), (2, 4), (4, 5), (0, 5), (0, 6), (5, 7), (7, 8), (7, 9), (7, 10),
+              (10, 11), (11, 12), (11, 13), (13, 14), (14, 15)]
+
+
+def _lib_instance(op_ms, a2a_ms):
+    kinds = [A2A if o is None else (DW if _BOP[o] >= L.MOE_BOP_DW_EXPERT else OTHER) for o in _LIB_OPS]
+    times = [a2a_ms if o is None else float(op_ms[_BOP[o]]) for o in _LIB_OPS]
+    return kinds, times
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_block_schedule_matches_oracle(seed):
+    rng = np.random.default_rng(100 + seed)
+    op_ms = rng.random(len(L.BLOCK_OPS)) * rng.choice([0.05, 1.0, 3.0])
+    a2a_ms = float(rng.choice([0.0, 0.02, 0.11, 1.0, 9.4]))
+    order, assign, ov = L.moe_block_dw_schedule(op_ms, a2a_ms)
+    kinds, times = _lib_instance(op_ms, a2a_ms)
+    asg, seq, ov_o = D.schedule(16, kinds, times, _LIB_EDGES)
+    want_assign = np.full(16, -1, np.int32)
+    for j, a in asg.items():
+        want_assign[j] = a
+    np.testing.assert_array_equal(assign, want_assign)
+    np.testing.assert_array_equal(order, [_BOP[_LIB_OPS[i]] for i in seq if kinds[i] == DW])
+    assert ov == pytest.approx(ov_o, rel=1e-12, abs=1e-15)
+    assert sorted(order.tolist()) == list(range(L.MOE_BOP_DW_EXPERT, L.MOE_BOP_DW_EXPERT + 6))
+
+
+def test_block_schedule_moves_the_gate_gradient_under_the_first_all_to_all():
+    """With all-to-all time, dWg (which reads only the gate's gradient) is the
+    one candidate of the exchange of dO and goes right after it; the expert dW
+    overlaps the exchange of dXe; without all-to-all time the emission order
+    (the default dw_order) stays."""
+    op_ms = np.array([0.07, 2.2, 0.09, 0.2, 0.24, 1.9, 0.77, 0.2, 2.4, 0.05, 0.15, 0.6, 0.6, 0.15])
+    order, assign, ov = L.moe_block_dw_schedule(op_ms, 0.11)
+    assert order.tolist() == [L.MOE_BOP_DW_EXPERT + 1, L.MOE_BOP_DW_EXPERT, 10, 11, 12, 13]
+    assert assign[6] == 1 and assign[3] == 4
+    assert ov == pytest.approx(0.05 + 0.11)
+    order0, assign0, ov0 = L.moe_block_dw_schedule(op_ms, 0.0)
+    assert order0.tolist() == [8, 9, 10, 11, 12, 13] and (assign0 == -1).all() and ov0 == 0.0
+
+
+def test_block_schedule_validation():
+    with pytest.raises(L.MoeError):
+        L.moe_block_dw_schedule(np.full(len(L.BLOCK_OPS), -1.0), 0.1)
+    with pytest.raises(L.MoeError):
+        L.moe_block_dw_schedule(np.ones(len(L.BLOCK_OPS)), float("nan"))

@@ -332,3 +332,77 @@ def test_full_size_whole_sequences_match_block_oracle(L, full):
                           ("out", fw["out"]), ("dm", bw["dm"]), ("dh", bw["dh"]), ("dattn", bw["do"]),
                           ("dqkv", bw["dqkv"]), ("da", bw["da"]), ("dx", bw["dx"])):
             assert_close(f"sequence {seq}: {name}", gpu[name][rows], ref, TOLB)
+
+
+def test_dw_schedule_from_measured_times_orders_the_weight_stream(L):
+    """The weight-gradient schedule pass applied to the block backward (Sec. 4,
+    Alg. 1): the operations' times measured in this run (one stream,
+    MOE_BLOCK_TIMED), the all-to-alls costed by an xGMI model, the planner's
+    order given to the weight stream.  Every gradient is bitwise the same as
+    with the default order and with the reverse order."""
+    spec = SMALL["B4_S64_d256_f192_E8_drops_4chunks"]
+    inp = block_inputs(spec)
+    w, x, dy = _upload(L, inp)
+    m = spec.moe
+    C = O.capacity(spec.B * spec.S, m.E, m.k, m.cf_num, m.cf_den)
+
+    def backward(order, passes=L.MOE_BLOCK_BWD, one_stream=False):
+        cfg = L.make_block_cfg(spec.B, spec.S, spec.heads, m.f, m.E, m.k, C, m.G, m.act, m.renorm, dw_order=order)
+        b = L.alloc_block(cfg, 4)
+        out, dx = torch.empty_like(x), torch.empty_like(x)
+        streams = [torch.cuda.current_stream()] * 3 if one_stream else [torch.cuda.Stream() for _ in range(3)]
+        streams[0].wait_stream(torch.cuda.current_stream())
+        L.moe_block_chunked(cfg, w, b, x, out, dy, dx, b, L.MOE_BLOCK_FWD, 4, streams, b["ws"])
+        L.moe_block_chunked(cfg, w, b, x, out, dy, dx, b, passes, 4, streams, b["ws"])
+        torch.cuda.synchronize()
+        b["out"], b["dx"] = out, dx
+        return b
+
+    timed = backward(None, L.MOE_BLOCK_BWD | L.MOE_BLOCK_TIMED, one_stream=True)
+    op_ms = L.moe_block_op_times()
+    log("  op times (ms): " + ", ".join(f"{n} {t:.3f}" for n, t in zip(L.BLOCK_OPS, op_ms)))
+    assert np.all(op_ms > 0) and np.all(np.isfinite(op_ms))
+    kept = int(host(timed["fill"]).reshape(4, m.E)[-1].sum())
+    a2a_ms = kept * spec.d * 2 / 8 / 153e9 * 1e3     # the slice to one of 7 peers over one xGMI link
+    order, assign, ov = L.moe_block_dw_schedule(op_ms, a2a_ms)
+    log(f"  all-to-all {a2a_ms:.4f} ms each; planner order {order.tolist()}, overlap {ov:.4f} ms")
+    assert assign[6] == 1, "dWg should overlap the first all-to-all"
+    base = backward(None)
+    planned = backward(order.tolist())
+    reverse = backward(list(range(13, 7, -1)))
+    grads = ("dx", "dWqkv", "dWo", "dln1_g", "dln1_b", "dln2_g", "dln2_b", "dWg", "dW1", "dW2", "dm", "dh", "dqkv")
+    _assert_bitwise(base, timed, m.E, "timed single stream vs default", grads)
+    _assert_bitwise(base, planned, m.E, "planner order vs default", grads)
+    _assert_bitwise(base, reverse, m.E, "reverse order vs default", grads)
+
+
+def test_prepacked_expert_weights_give_the_same_block(L):
+    """moe.wpacked = 1: the block takes W1, W2 already packed (moe_pack_weights)
+    and writes dW1, dW2 packed; every output and gradient is bitwise the one
+    of the block that packs the row-major weights itself."""
+    spec = SMALL["B2_S200_d256_f256_E8_2chunks"]
+    inp = block_inputs(spec)
+    w, x, dy = _upload(L, inp)
+    m = spec.moe
+    C = O.capacity(spec.B * spec.S, m.E, m.k, m.cf_num, m.cf_den)
+    cfg0 = L.make_block_cfg(spec.B, spec.S, spec.heads, m.f, m.E, m.k, C, m.G, m.act, m.renorm)
+    cfg1 = L.make_block_cfg(spec.B, spec.S, spec.heads, m.f, m.E, m.k, C, m.G, m.act, m.renorm, wpacked=1)
+    wp = dict(w)
+    wp["W1"], wp["W2"] = torch.empty_like(w["W1"]), torch.empty_like(w["W2"])
+    L.moe_pack_weights(cfg1.moe, w["W1"], w["W2"], wp["W1"], wp["W2"])
+    res = []
+    for cfg, weights in ((cfg0, w), (cfg1, wp)):
+        b = L.alloc_block(cfg, 2)
+        out, dx = torch.empty_like(x), torch.empty_like(x)
+        s = torch.cuda.current_stream()
+        L.moe_block_chunked(cfg, weights, b, x, out, dy, dx, b, L.MOE_BLOCK_FWD | L.MOE_BLOCK_BWD, 2, [s] * 3,
+                            b["ws"])
+        torch.cuda.synchronize()
+        b["out"], b["dx"] = out, dx
+        res.append(b)
+    b0, b1 = res
+    _assert_bitwise(b0, b1, m.E, "prepacked vs row-major weights", tuple(n for n in _COMPARED if n not in ("dW1", "dW2")))
+    E, f, d = m.E, m.f, spec.d
+    unpack = lambda t, R, X: host(t).reshape(E, R // 16, X // 32, 16, 32).transpose(0, 1, 3, 2, 4).reshape(E, R, X)
+    np.testing.assert_array_equal(unpack(b1["dW1"], f, d), host(b0["dW1"]).reshape(E, f, d))
+    np.testing.assert_array_equal(unpack(b1["dW2"], d, f), host(b0["dW2"]).reshape(E, d, f))
