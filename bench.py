@@ -74,20 +74,31 @@ def gemm_source_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def measured_traffic(workload: str, call: str):
-    """HBM bytes per call of `call` recorded in a committed PMC summary, or None
-    if none was taken on this workload with the current GEMM sources."""
+def traffic_records():
+    """Every `traffic_record:` line of the committed PMC summaries, as dicts
+    (workload, call, gemm_source_hash, traffic_bytes_per_call,
+    algorithmic_bytes_per_call) with the file they came from."""
     import glob
-    h = gemm_source_hash()
-    for path in sorted(glob.glob(os.path.join(PROFILES, "*_pmc_traffic.md"))):
-        kv = {}
+    out = []
+    for path in sorted(glob.glob(os.path.join(PROFILES, "*_pmc*.md"))):
         for line in open(path).read().splitlines():
-            if line.startswith(("traffic_", "gemm_", "workload", "call")) and ":" in line:
-                k, v = line.split(":", 1)
-                kv[k.strip()] = v.strip()
+            if line.startswith("traffic_record:"):
+                kv = dict(f.split("=", 1) for f in line.split(":", 1)[1].split())
+                kv["file"] = path
+                out.append(kv)
+    return out
+
+
+def measured_traffic(workload: str, call: str):
+    """HBM-side bytes per call of `call` recorded in a committed PMC summary, or
+    None if none was taken on this workload with the current GEMM sources."""
+    h = gemm_source_hash()
+    for kv in traffic_records():
         if kv.get("workload") == workload and kv.get("call") == call and kv.get("gemm_source_hash") == h:
             return float(kv["traffic_bytes_per_call"])
     return None
+
+
 METRIC = "MoE layer fwd+bwd tokens/s on 1 MI355X; expert GEMM MFMA util; dispatch GB/s"
 CALLS = ["gate", "dispatch", "expert_ffn_fwd", "combine", "bwd_dx", "bwd_dw"]
 
