@@ -86,6 +86,56 @@ def build(verbose: bool = False) -> str:
     return LIB
 
 
+# Host sources checked under AddressSanitizer and UndefinedBehaviorSanitizer
+# (the C-ABI validation, the planners and the block's host orchestration).
+# Their device-free objects are rebuilt with the sanitizers on the host side
+# only and linked with the regular objects of the kernel sources.
+SANITIZED_SOURCES = ["api.cpp", "plan.cpp", "block.cpp"]
+SANITIZE_HOST = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
+                 "-Xarch_host", "-fno-sanitize-recover=undefined", "-Xarch_host", "-fno-omit-frame-pointer"]
+
+
+def asan_runtime() -> str:
+    """The compiler's AddressSanitizer runtime (to preload into a host process that loads the sanitized library)."""
+    clang = os.path.join(os.path.dirname(os.path.realpath(_hipcc())), "..", "llvm", "bin", "clang")
+    if not os.path.exists(clang):
+        clang = "/opt/rocm/llvm/bin/clang"
+    r = subprocess.run([clang, "--print-file-name=libclang_rt.asan-x86_64.so"], capture_output=True, text=True)
+    return r.stdout.strip()
+
+
+def build_host_sanitized(verbose: bool = False) -> str:
+    """_build/san/liblancet_moe_san.so: SANITIZED_SOURCES with host-side ASan/UBSan,
+    the kernel sources' objects from the last regular build (which must exist)."""
+    san = os.path.join(BUILD, "san")
+    os.makedirs(san, exist_ok=True)
+    others = [os.path.join(BUILD, os.path.splitext(s)[0] + ".o") for s in SOURCES if s not in SANITIZED_SOURCES]
+    missing = [o for o in others if not os.path.exists(o)]
+    if missing:
+        raise FileNotFoundError("run the regular build first; missing " + ", ".join(missing))
+
+    def one(src):
+        obj = os.path.join(san, os.path.splitext(src)[0] + ".o")
+        flags = [f for f in HIPCC_FLAGS if f != "-O3"] + ["-O1", "-g"] + SANITIZE_HOST
+        cmd = [_hipcc(), "-x", "hip", "-c", os.path.join(CSRC, src), "-o", obj] + flags
+        r = subprocess.run(cmd, capture_output=True, text=True)
+        if r.returncode != 0:
+            raise RuntimeError(f"hipcc (sanitized) failed on {src}:\n{r.stderr}")
+        return obj
+
+    with cf.ThreadPoolExecutor(max_workers=len(SANITIZED_SOURCES)) as ex:
+        objs = list(ex.map(one, SANITIZED_SOURCES))
+    lib = os.path.join(san, "liblancet_moe_san.so")
+    cmd = ([_hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", lib] + objs + others +
+           ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined", "-Xarch_host", "-shared-libsan"])
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError("sanitized link failed:\n" + r.stdout + r.stderr)
+    return lib
+
+
 if __name__ == "__main__":
     if ROOT not in sys.path:
         sys.path.insert(0, ROOT)
