@@ -742,20 +742,23 @@ struct WPrefix {
   int incl, excl;     // full tiles (ragged-K: all tiles), lane = group
   int inclP, exclP;   // ragged-M short tiles, lane = group
   int NF, NP;         // totals (uniform)
+  int lo, span;       // the group's clamped row range (group_rows), lane = group: read once, so a
+                      // tile change never waits on a memory load (which would drain the wave's
+                      // in-flight operand loads and epilogue stores)
 };
 template <bool RAGGED_K, bool SEP>
 __device__ __forceinline__ WPrefix wide_tile_prefix(const GemmParams& p, int lane, int groups, int tilesM,
                                                     int tilesN) {
   int cnt = 0, cntP = 0;
+  int lo = 0, span = 0;
   if (lane < groups) {
-    int lo, span;
     group_rows(p, lane, lo, span);
     if constexpr (RAGGED_K) {
       cnt = span > 0 ? tilesM * tilesN : 0;   // an empty group's output is zeroed in the prologue
     } else {
-      if (span > 0) span += lo & 15;
-      const int tm = (span + kWB - 1) / kWB;
-      const int sh = (SEP && (span % kWB) != 0) ? 1 : 0;
+      const int rows = span > 0 ? span + (lo & 15) : 0;   // from the 16-row block holding the first row
+      const int tm = (rows + kWB - 1) / kWB;
+      const int sh = (SEP && (rows % kWB) != 0) ? 1 : 0;
       cnt = (tm - sh) * tilesN;
       cntP = sh * tilesN;
     }
@@ -763,6 +766,8 @@ __device__ __forceinline__ WPrefix wide_tile_prefix(const GemmParams& p, int lan
   WPrefix P;
   P.incl = cnt;
   P.inclP = cntP;
+  P.lo = lo;
+  P.span = span;
 #pragma unroll
   for (int o = 1; o < 64; o <<= 1) {
     const int u = __shfl_up(P.incl, o, 64);
@@ -793,9 +798,9 @@ __device__ __forceinline__ WGeo wide_geo(const GemmParams& p, int t, int lane, i
   const int inc = shrt ? P.inclP : P.incl;
   const int exc = shrt ? P.exclP : P.excl;
   G.g = __builtin_amdgcn_readfirstlane(__popcll(__ballot(lane < groups && inc <= tt)));
-  const int local = tt - __builtin_amdgcn_readfirstlane(__shfl(exc, G.g, 64));
-  int lo, span;
-  group_rows(p, G.g, lo, span);
+  const int local = tt - __builtin_amdgcn_readlane(exc, G.g);
+  const int lo = __builtin_amdgcn_readlane(P.lo, G.g);
+  int span = __builtin_amdgcn_readlane(P.span, G.g);
   G.lo = lo;
   G.hi = lo + span;
   G.lo_al = lo & ~15;
