@@ -1151,11 +1151,17 @@ gemm_wide_kernel(GemmParams p, int tilesM, int tilesN, int groups) {
   constexpr int NRA = AK ? FM : 2 * FM, NRB = BKK ? FN : 2 * FN, NRD = NRA + NRB;
   constexpr int NMF = FM * FN, NDMA = 2 * kWNI;
   // PRE: MFMAs of a step issued before its wait and barrier (they use the
-  // fragments read in the previous step); the reads and refills follow the
-  // barrier.  Measured on the ragged-M plain-store product with a transposed
-  // B (dXe): -7 % with 8 (8192-token layer), -4 % at d_model 2048; neutral or
-  // slower on the others, which keep 0.
-  constexpr int PRE = (!B_K && !RAGGED_K && EPI == EPI_STORE) ? 8 : 0;
+  // fragments read in the previous step), at the low wave priority; the rest
+  // of the step, with the reads and refills, follows the barrier at the raised
+  // priority.  Of the two waves on a SIMD the older one wins every tie for the
+  // matrix core, so it finishes its MFMAs first and then waits at the barrier
+  // while the other still issues; the early wave's PRE MFMAs of the next step
+  // fill the matrix core while the late wave finishes its step, waits and
+  // passes the barrier.  Measured (16384-token layer, one MI355X, per-wave
+  // cycle counters): FWD2 1750 -> 1564 cycles per K-step, dXe 1773 -> 1505;
+  // the layer's ragged-M calls -4 to -7 %, 12 and 16 equal, 20 and 24 slower.
+  // The ragged-K (dW) products were measured slower with it (+2 %) and keep 0.
+  constexpr int PRE = RAGGED_K ? 0 : 16;
   constexpr int RSPAN = (NMF - PRE) * 3 / 4;  // reads issued within the first 3/4 of the MFMAs after PRE
   u32x2 qa[2 * FM], qb[2 * FN];               // pending halves of MN-contiguous fragments
   // LDS byte address of read r of an operand = base(par) + imm(r), with a
@@ -1234,15 +1240,17 @@ gemm_wide_kernel(GemmParams p, int tilesM, int tilesN, int groups) {
     const uint32_t rb0 = read_base(TB{}, st + kWB * BK, wn * WTN, 0);
     const uint32_t rb1 = BKK ? rb0 : read_base(TB{}, st + kWB * BK, wn * WTN, 1);
     __builtin_amdgcn_sched_barrier(0);
-    // Raised wave priority while this step's MFMAs and reads issue: of the two
-    // waves on a SIMD, the one past the barrier keeps the matrix core fed
-    // while the other waits (measured: FWD2 -3 %, the layer step -1 %).
-    __builtin_amdgcn_s_setprio(1);
+    // Raised wave priority while this step's MFMAs after the barrier and the
+    // reads issue: of the two waves on a SIMD, the one past the barrier keeps
+    // the matrix core fed while the other waits (measured: FWD2 -3 %, the
+    // layer step -1 %).  PRE MFMAs before the barrier issue at the low priority.
+    if constexpr (PRE == 0) __builtin_amdgcn_s_setprio(1);
     static_for<0, NMF>([&](auto mc) __attribute__((always_inline)) {
       constexpr int m = decltype(mc)::value;
       if constexpr (PRE > 0 && m == PRE) {
         __builtin_amdgcn_sched_barrier(0);
         sync();
+        __builtin_amdgcn_s_setprio(1);
         __builtin_amdgcn_sched_barrier(0);
       }
       if constexpr (MMA) mfma_acc(acc[m / FN][m % FN], cb[m % FN], ca[m / FN]);
