@@ -107,7 +107,7 @@ int dw_producer(int op) {
 }
 
 struct WsLayout {
-  size_t disp, dw, ln2, ln1, sk, wqkv, wo, act, total;
+  size_t disp, dw, ln2, ln1, sk, wqkv, wo, act, wgp, total;
 };
 
 WsLayout ws_layout(const moe_block_cfg& c, int n) {
@@ -127,6 +127,9 @@ WsLayout ws_layout(const moe_block_cfg& c, int n) {
   L.wqkv = off; off += align256((size_t)3 * d * d * 2);
   L.wo = off;   off += align256((size_t)d * d * 2);
   L.act = off;  off += align256((size_t)pad16(T) * 3 * d * 2);
+  // Float partials of the dense weight gradients (dWo, then dWqkv, on the
+  // weight stream).
+  L.wgp = off;  off += align256(wgrad_ws_bytes(3 * d, d));
   L.total = off;
   return L;
 }
@@ -288,9 +291,9 @@ hipError_t run_block(const moe_block_cfg& c, const moe_block_weights& W, const m
         case MOE_BOP_DLN2:
           launch_ln_gain_reduce((float*)(wsb + L.ln2), T, d, G->dln2_g, G->dln2_b, Sw);
           break;
-        case MOE_BOP_DWO: launch_dense_wgrad(d, d, T, A.dh, d, A.attn, d, G->dWo, d, Sw); break;  // dWo = dh^T o
+        case MOE_BOP_DWO: launch_dense_wgrad(d, d, T, A.dh, A.attn, G->dWo, wsb + L.wgp, Sw); break;  // dh^T o
         case MOE_BOP_DWQKV:
-          launch_dense_wgrad((int)d3, d, T, A.dqkv, d3, A.a, d, G->dWqkv, d, Sw);  // dWqkv = dqkv^T a
+          launch_dense_wgrad((int)d3, d, T, A.dqkv, A.a, G->dWqkv, wsb + L.wgp, Sw);  // dWqkv = dqkv^T a
           break;
         default:
           launch_ln_gain_reduce((float*)(wsb + L.ln1), T, d, G->dln1_g, G->dln1_b, Sw);

@@ -12,16 +12,22 @@
 // bf16 path: a persistent kernel with v_mfma_f32_16x16x32_bf16 and float
 // accumulation; operand tiles stream global -> LDS asynchronously through a
 // multi-stage ring (details below).  Epilogues: plain store, (H, act(H))
-// store, dA * act'(H) for the backward, and a residual add.
+// store, dA * act'(H) for the backward, a residual add, and float partials of
+// a K-split dense weight gradient.
 // The same kernel serves dense products (one group, no row ranges): the
-// block's projections and their weight gradients.
+// block's projections and, with row-major operands split into token ranges,
+// their weight gradients.
 // f32 path: a plain LDS-tiled FMA GEMM with the same addressing.
 #include "internal.h"
 #include "lds_ops.h"
 
 namespace lmoe {
 
-enum { EPI_STORE = 0, EPI_FWD1 = 1, EPI_DACT = 2, EPI_RES = 3 };
+// EPI_WGF32: the dense weight-gradient product C = A^T B of the block, both
+// operands row-major [K][*] (not blocked), K split into groups of kchunk rows
+// (group g: rows [g kchunk, (g + 1) kchunk)), each group's float partial C at
+// C + g sC; gemm_wgrad_reduce_kernel adds the partials in group order.
+enum { EPI_STORE = 0, EPI_FWD1 = 1, EPI_DACT = 2, EPI_RES = 3, EPI_WGF32 = 4 };
 
 struct GemmParams {
   const void* A;
@@ -39,12 +45,13 @@ struct GemmParams {
   int cap;          // rows per expert block (C): row ranges are clamped to [0, cap]; re == NULL means [0, cap)
   float* part;      // wide ragged-M products: partial tiles of the K-split (stream-K) schedule
   int ksplit;       // wide plain-store ragged-M products: 1 = a short last round may be K-split
+  int kchunk;       // rb == re == NULL and kchunk > 0: group g's rows are [g kchunk, (g + 1) kchunk)
 };
 
 // Row range of group g, clamped to the buffer so bad ranges cannot reach outside it.
 __device__ __forceinline__ void group_rows(const GemmParams& p, int g, int& lo, int& span) {
-  int a = p.rb ? p.rb[g] : 0;
-  int b = p.re ? p.re[g] : p.cap;
+  int a = p.rb ? p.rb[g] : (p.kchunk > 0 ? g * p.kchunk : 0);
+  int b = p.re ? p.re[g] : (p.kchunk > 0 ? (g + 1) * p.kchunk : p.cap);
   a = a < 0 ? 0 : (a > p.cap ? p.cap : a);
   b = b < a ? a : (b > p.cap ? p.cap : b);
   lo = a;
@@ -258,262 +265,11 @@ struct TileMN {
   }
 };
 
-// Persistent grouped GEMM: resident blocks walk the list of real tiles of all
-// groups.  Within a group, tiles are numbered panel by panel (kPanelN tile
-// columns wide), m-tile by m-tile inside a panel, n fastest.  The list is cut
-// into 8 contiguous ranges, one per XCD (workgroups are dealt to XCDs
-// round-robin by block index), so the ~64 tiles an XCD has in flight form an
-// 8 x 8 patch: each A row-slice and B column-slice it streams is shared by 8
-// tiles through that XCD's L2, instead of one A slice shared by a whole row of
-// tiles while every B slice of the row is fetched afresh.
+// Tiles of a group are numbered panel by panel (kPanelN tile columns wide),
+// m-tile by m-tile inside a panel, n fastest, so the tiles an XCD has in
+// flight form a square-ish patch whose operand slices are shared through that
+// XCD's L2.
 constexpr int kPanelN = 8;
-// BLK: both operands in 16 x 32 blocks (expert buffers and packed weights),
-// ragged row ranges start at the block row containing row_begin; CBLK: the
-// output (and the epilogue's auxiliary input) too.  Otherwise row-major.
-template <int BM, int BN, int WGM, int WGN, int STAGES, int OCC, bool B_K, bool RAGGED_K, int EPI, int ACT, bool BLK,
-          bool CBLK>
-__global__ __attribute__((amdgpu_flat_work_group_size(WGM * WGN * 64, WGM * WGN * 64),
-                          amdgpu_waves_per_eu(OCC, OCC))) void
-gemm_bf16_kernel(GemmParams p, int tilesM, int tilesN, int groups) {
-  constexpr int NW = WGM * WGN;
-  constexpr int WTM = BM / WGM, WTN = BN / WGN;
-  constexpr int FM = WTM / 16, FN = WTN / 16;
-  constexpr int BK = kBKb;
-  constexpr int STAGE = (BM + BN) * BK;          // elements per pipeline stage
-  constexpr int EPI_LD = WTN + 4;                // fp32 staging row stride
-  constexpr int EPI_ROWS = (NW * 32 * EPI_LD * 4 <= STAGES * STAGE * 2) ? 32 : 16;  // rows staged at once
-  constexpr bool A_K = !RAGGED_K;
-  constexpr bool BK_C = B_K && !RAGGED_K;
-  using TA = typename std::conditional<A_K, TileK<BM, NW, BLK>, TileMN<BM, NW, BLK>>::type;
-  using TB = typename std::conditional<BK_C, TileK<BN, NW, BLK>, TileMN<BN, NW, BLK>>::type;
-  constexpr int LPS = TA::NI + TB::NI;           // loads per wave per stage
-  static_assert(STAGES >= 2 && LPS * (STAGES - 1) < 64, "vmcnt range");
-  // The one geometry this kernel is tested in.  Sweep builds of other tile
-  // shapes (256 x 128 with six stages, 128 x 256, 256 x 256 with four
-  // stages) gave wrong products or an illegal address on the device; their
-  // register and LDS budgets were never derived, so they are not allowed.
-  static_assert(BM == 128 && BN == 128 && WGM == 2 && WGN == 2 && STAGES == 4 && OCC == 2,
-                "gemm_bf16_kernel supports only 128 x 128 tiles, 2 x 2 waves, 4 stages, 2 blocks per CU");
-  static_assert(WTM % EPI_ROWS == 0, "wave tile rows must be a multiple of the staged slice");
-  static_assert(NW * EPI_ROWS * EPI_LD * 4 <= STAGES * STAGE * 2, "epilogue staging does not fit");
-  extern __shared__ __attribute__((aligned(16))) uint16_t lds[];
-  __shared__ int s_prefix[kMaxE + 1];
-
-  const int tid = threadIdx.x;
-  const int lane = tid & 63;
-  const int wid = tid >> 6;
-  const int wm = wid / WGN, wn = wid % WGN;
-
-  // Tile counts per group -> exclusive prefix (one wave, groups <= 64).
-  if (wid == 0) {
-    int cnt = 0;
-    if (lane < groups) {
-      if constexpr (RAGGED_K) {
-        cnt = tilesM * tilesN;
-      } else {
-        int lo, span;
-        group_rows(p, lane, lo, span);
-        if (BLK && span > 0) span += lo & 15;  // tiles start at the block row holding row_begin
-        cnt = ((span + BM - 1) / BM) * tilesN;
-      }
-    }
-    int incl = cnt;
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-      const int u = __shfl_up(incl, o, 64);
-      if (lane >= o) incl += u;
-    }
-    if (lane < groups) s_prefix[lane + 1] = incl;
-    if (lane == 0) s_prefix[0] = 0;
-  }
-  __syncthreads();
-  const int total = s_prefix[groups];
-  const int nslot = gridDim.x / 8;
-  const int xcd = blockIdx.x % 8, slot = blockIdx.x / 8;
-  const int per = (total + 7) / 8;
-  const int t_begin = xcd * per + slot;
-  const int t_end = min(total, (xcd + 1) * per);
-
-  for (int t = t_begin; t < t_end; t += nslot) {
-    int g = 0;
-    while (g + 1 < groups && s_prefix[g + 1] <= t) ++g;
-    const int local = t - s_prefix[g];
-    int lo, span;
-    group_rows(p, g, lo, span);
-    const int hi = lo + span;
-    const int lo_al = BLK ? (lo & ~15) : lo;   // row (or K) origin of this group's tiles
-    if (BLK && span > 0) span += lo - lo_al;
-    // Panel order: n-panels of kPanelN tile columns, m-tiles within a panel,
-    // n fastest, so the tiles in flight on one XCD form a square-ish patch.
-    const int tmg = RAGGED_K ? tilesM : (span + BM - 1) / BM;
-    const int pnl = local / (tmg * kPanelN);
-    const int rem = local - pnl * tmg * kPanelN;
-    const int pw = min(kPanelN, tilesN - pnl * kPanelN);
-    const int m0 = (rem / pw) * BM;
-    const int n0 = (pnl * kPanelN + rem % pw) * BN;
-    const int Mlim = RAGGED_K ? p.M : span;
-    const int Klim = RAGGED_K ? span : p.K;
-    const uint16_t* Ab = (const uint16_t*)p.A + g * p.sA + (BLK ? 0 : (int64_t)lo * p.lda);
-    const uint16_t* Bb = (const uint16_t*)p.B + g * p.sB + (RAGGED_K && !BLK ? (int64_t)lo * p.ldb : 0);
-
-    f32x4 acc[FM][FN];
-#pragma unroll
-    for (int i = 0; i < FM; ++i)
-#pragma unroll
-      for (int j = 0; j < FN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-    const int nk = (Klim + BK - 1) / BK;
-    auto issue = [&](int kt) {
-      uint16_t* st = lds + (kt % STAGES) * STAGE;
-      if constexpr (!BLK) {
-        TA::issue(Ab, p.lda, m0, Mlim, kt * BK, Klim, st, wid, lane);
-        TB::issue(Bb, p.ldb, n0, p.N, kt * BK, Klim, st + BM * BK, wid, lane);
-      } else {
-        if constexpr (A_K) TA::issue_blk(Ab, p.lda, lo_al + m0, (int)pad16(p.cap), kt * BK, Klim, st, wid, lane);
-        else TA::issue_blk(Ab, p.lda, m0, p.M, lo_al + kt * BK, lo, hi, st, wid, lane);
-        if constexpr (BK_C) TB::issue_blk(Bb, p.ldb, n0, p.N, kt * BK, Klim, st + BM * BK, wid, lane);
-        else if constexpr (RAGGED_K) TB::issue_blk(Bb, p.ldb, n0, p.N, lo_al + kt * BK, lo, hi, st + BM * BK, wid, lane);
-        else TB::issue_blk(Bb, p.ldb, n0, p.N, kt * BK, 0, p.K, st + BM * BK, wid, lane);
-      }
-    };
-    // Fragment reads of one tile: the A fragments, then the B fragments, each in
-    // asm blocks of at most kReadChunk reads that complete before they return.
-    auto read_a = [&](int kt, u32x4 (&fa)[FM]) {
-      TA::template read<FM>(fa, lds + (kt % STAGES) * STAGE, wm * WTM, lane);
-    };
-    auto read_b = [&](int kt, u32x4 (&fb)[FN]) {
-      TB::template read<FN>(fb, lds + (kt % STAGES) * STAGE + BM * BK, wn * WTN, lane);
-    };
-    auto mfma_rows = [&](int i0, int i1, u32x4 (&ca)[FM], u32x4 (&cb)[FN]) {
-#pragma unroll
-      for (int i = 0; i < FM; ++i) {
-        if (i < i0 || i >= i1) continue;
-#pragma unroll
-        for (int j = 0; j < FN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, ca[i]),
-                                                              __builtin_bit_cast(bf16x8, cb[j]), acc[i][j], 0, 0, 0);
-      }
-    };
-    // One K step: multiply tile kt (fragments in ca/cb) in two halves; the
-    // fragments of tile kt+1 are read into na/nb before each half, so the read
-    // latency overlaps the MFMAs already in the pipe.  Called with the two
-    // register sets in alternating roles (static indexing).
-    // With split reads the fragment reads of tile kt+1 are started before a
-    // half of tile kt's MFMAs and completed after it, so their latency hides
-    // under those MFMAs.
-    constexpr bool kSplit = (A_K ? (FM == 4 || FM == 8) : FM == 4) &&
-                            (BK_C ? (FN == 4 || FN == 8) : FN == 4);
-    u32x2 pa[8], pb[8];
-    auto step = [&](int kt, u32x4 (&ca)[FM], u32x4 (&cb)[FN], u32x4 (&na)[FM], u32x4 (&nb)[FN]) {
-      const bool more = kt + 1 < nk;
-      const uint16_t* st = lds + ((kt + 1) % STAGES) * STAGE;
-      if (more) {
-        // tile kt+1 has landed once only tiles kt+2 .. min(kt+STAGES-1, nk-1) are pending
-        wait_vm_tiles<LPS, STAGES - 2>(min(STAGES - 2, nk - 2 - kt));
-        lds_barrier();  // tile kt+1 is in LDS for every wave; no wave reads tile kt's stage any more
-        if (kt + STAGES < nk) issue(kt + STAGES);
-      }
-      // Split reads are unconditional (branch-free, so the pending registers
-      // are never copied): after the last tile they read a stale stage that
-      // no load is writing, and the values are discarded.
-      if constexpr (kSplit) TA::template read_issue<FM>(na, pa, st, wm * WTM, lane);
-      else if (more) read_a(kt + 1, na);
-      __builtin_amdgcn_sched_barrier(0);
-      mfma_rows(0, FM / 2, ca, cb);
-      __builtin_amdgcn_sched_barrier(0);
-      if constexpr (kSplit) {
-        TA::template read_finish<FM>(na, pa);
-        TB::template read_issue<FN>(nb, pb, st + BM * BK, wn * WTN, lane);
-      } else if (more) {
-        read_b(kt + 1, nb);
-      }
-      __builtin_amdgcn_sched_barrier(0);
-      mfma_rows(FM / 2, FM, ca, cb);
-      __builtin_amdgcn_sched_barrier(0);
-      if constexpr (kSplit) {
-        TB::template read_finish<FN>(nb, pb);
-        __builtin_amdgcn_sched_barrier(0);
-      }
-    };
-
-    u32x4 fa0[FM], fb0[FN], fa1[FM], fb1[FN];
-    if (nk > 0) {
-#pragma unroll
-      for (int s = 0; s < STAGES; ++s)
-        if (s < nk) issue(s);
-      wait_vm_tiles<LPS, STAGES - 1>(min(STAGES - 1, nk - 1));  // tile 0 has landed
-      lds_barrier();
-      read_a(0, fa0);
-      read_b(0, fb0);
-    }
-    for (int kt = 0; kt < nk; kt += 2) {
-      step(kt, fa0, fb0, fa1, fb1);
-      if (kt + 1 < nk) step(kt + 1, fa1, fb1, fa0, fb0);
-    }
-    wait_vm<0>();
-    lds_barrier();  // all waves are done reading the operand stages
-
-    // Epilogue: stage 32-row slices of the wave tile through LDS as float,
-    // then write 16-byte vectors (8 bf16) with the epilogue applied.
-    float* st = reinterpret_cast<float*>(lds) + wid * (EPI_ROWS * EPI_LD);
-    // Output rows are relative to lo_al; a row-major output starts at row lo_al.
-    const int64_t cofs = (int64_t)g * p.sC + (RAGGED_K || CBLK ? 0 : (int64_t)lo_al * p.ldc);
-    uint16_t* C = (uint16_t*)p.C + cofs;
-    uint16_t* C2 = EPI == EPI_FWD1 ? (uint16_t*)p.C2 + cofs : nullptr;
-    const uint16_t* Aux = (EPI == EPI_DACT || EPI == EPI_RES) ? (const uint16_t*)p.Aux + cofs : nullptr;
-    const int g4 = lane >> 4;
-#pragma unroll
-    for (int pass = 0; pass < WTM / EPI_ROWS; ++pass) {
-#pragma unroll
-      for (int ii = 0; ii < EPI_ROWS / 16; ++ii) {
-        const int i = pass * (EPI_ROWS / 16) + ii;
-#pragma unroll
-        for (int j = 0; j < FN; ++j)
-#pragma unroll
-          for (int v = 0; v < 4; ++v) st[(ii * 16 + 4 * g4 + v) * EPI_LD + j * 16 + (lane & 15)] = acc[i][j][v];
-      }
-      // The staging slice is private to this wave and LDS executes a wave's
-      // accesses in order, so no barrier is needed between writes and reads.
-      constexpr int CPR = WTN / 8;          // 8-column chunks per row
-#pragma unroll
-      for (int q = lane; q < EPI_ROWS * CPR; q += 64) {
-        const int rr = q / CPR, cc = q % CPR;
-        const int row = m0 + wm * WTM + pass * EPI_ROWS + rr;
-        const int col = n0 + wn * WTN + cc * 8;
-        if (row < Mlim && col < p.N && (RAGGED_K || lo_al + row >= lo)) {
-          float v[8];
-          const f32x4 a = *reinterpret_cast<const f32x4*>(st + rr * EPI_LD + cc * 8);
-          const f32x4 b = *reinterpret_cast<const f32x4*>(st + rr * EPI_LD + cc * 8 + 4);
-#pragma unroll
-          for (int u = 0; u < 4; ++u) { v[u] = a[u]; v[4 + u] = b[u]; }
-          const int64_t off = CBLK ? blk_off(lo_al + row, col, p.ldc) : (int64_t)row * p.ldc + col;
-          if constexpr (EPI == EPI_FWD1) {
-            Vec<uint16_t>::store(C + off, v);
-#pragma unroll
-            for (int u = 0; u < 8; ++u) v[u] = act_fwd_t<ACT>(v[u]);
-            Vec<uint16_t>::store(C2 + off, v);
-          } else if constexpr (EPI == EPI_DACT) {
-            float h[8];
-            Vec<uint16_t>::load(Aux + off, h);
-#pragma unroll
-            for (int u = 0; u < 8; ++u) v[u] *= act_bwd_t<ACT>(h[u]);
-            Vec<uint16_t>::store(C + off, v);
-          } else if constexpr (EPI == EPI_RES) {
-            float r[8];
-            Vec<uint16_t>::load(Aux + off, r);
-#pragma unroll
-            for (int u = 0; u < 8; ++u) v[u] += r[u];
-            Vec<uint16_t>::store(C + off, v);
-          } else {
-            Vec<uint16_t>::store(C + off, v);
-          }
-        }
-      }
-    }
-    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-    lds_barrier();  // every wave is done with its staging slice before the next tile's loads land
-  }
-}
 
 // ------------------------------------------------------ wide bf16 MFMA tiles
 // The expert products at full size.  256 x 256 block tiles, one block per CU,
@@ -630,7 +386,10 @@ __device__ __forceinline__ void acc_pin_mem(f32x4 (&a)[4]) {
 // columns past `lim` and, with KCHK, K rows outside [klo, khi) read zeros.
 constexpr int kBufCfg = 0x00020000;   // buffer descriptor word 3: raw 32-bit data, gfx9 family
 constexpr uint32_t kOob = 0x80000000u;
-template <bool KC, bool KCHK, int NW>
+// RM (MN-contiguous only): the operand is row-major [K][ld] instead of blocked;
+// a lane loads the same 16-byte chunk (K row, 8 columns) that it would take
+// from the blocked layout, so the stage's LDS layout is the same.
+template <bool KC, bool KCHK, int NW, bool RM = false>
 struct WOp {
   static constexpr int kWNI = 16 / NW;   // loads per wave per stage (16 blocks of 1 KB)
   const char* base;      // the group's operand (uniform)
@@ -659,7 +418,7 @@ struct WOp {
       }
     } else {
       const int nb = (int)(ld >> 5);
-      stride = (uint32_t)nb * 2048u;
+      stride = RM ? (uint32_t)(32 * ld * 2) : (uint32_t)nb * 2048u;
       const int r = lane >> 2;
       const int c = (lane & 3) ^ bsw(r);
 #pragma unroll
@@ -667,7 +426,9 @@ struct WOp {
         const int b2 = i * NW + wid;
         const int kb = b2 / 8, cb = b2 % 8;
         const int col = row0 + 32 * cb;
-        const uint32_t off = (uint32_t)((((korg >> 4) + kb) * nb + (col >> 5)) * 512 + r * 32 + c * 8) * 2u;
+        const uint32_t off =
+            RM ? (uint32_t)(((int64_t)(korg + 16 * kb + r) * ld + col + c * 8) * 2)
+               : (uint32_t)((((korg >> 4) + kb) * nb + (col >> 5)) * 512 + r * 32 + c * 8) * 2u;
         voff[i] = col < lim ? off : (off | kOob);
         kr[i] = korg + 16 * kb + r;
       }
@@ -852,7 +613,9 @@ __device__ __forceinline__ void wide_epilogue(const GemmParams& p, const WGeo& G
   // the epilogue is branch-free and dA * act'(H) issues all of a half's H
   // loads together.  Group offsets fit 31 bits (validated on the host).
   const int64_t cofs = (int64_t)G.g * p.sC + (RAGGED_K || CBLK ? 0 : (int64_t)G.lo_al * p.ldc);
-  const __amdgpu_buffer_rsrc_t rC = __builtin_amdgcn_make_buffer_rsrc((uint16_t*)p.C + cofs, (short)0, 0x7fffffff, kBufCfg);
+  constexpr int ESZ = EPI == EPI_WGF32 ? 4 : 2;   // bytes per output element
+  void* const cbase = EPI == EPI_WGF32 ? (void*)((float*)p.C + cofs) : (void*)((uint16_t*)p.C + cofs);
+  const __amdgpu_buffer_rsrc_t rC = __builtin_amdgcn_make_buffer_rsrc(cbase, (short)0, 0x7fffffff, kBufCfg);
   __amdgpu_buffer_rsrc_t rC2 = rC, rAux = rC;
   if constexpr (EPI == EPI_FWD1)
     rC2 = __builtin_amdgcn_make_buffer_rsrc((uint16_t*)p.C2 + cofs, (short)0, 0x7fffffff, kBufCfg);
@@ -861,7 +624,7 @@ __device__ __forceinline__ void wide_epilogue(const GemmParams& p, const WGeo& G
   const int rl = lane & 15, cq = 4 * (lane >> 4);
   auto voff = [&](bool ok, int row, int col) __attribute__((always_inline)) -> uint32_t {
     const int64_t e = CBLK ? blk_off((RAGGED_K ? 0 : G.lo_al) + row, col, p.ldc) : (int64_t)row * p.ldc + col;
-    return ok ? (uint32_t)(e * 2) : kOob;
+    return ok ? (uint32_t)(e * ESZ) : kOob;
   };
 #pragma unroll
   for (int h = 0; h < 2; ++h) {          // two halves of four fragment rows
@@ -901,6 +664,10 @@ __device__ __forceinline__ void wide_epilogue(const GemmParams& p, const WGeo& G
 #pragma unroll
           for (int u = 0; u < 4; ++u) v[u] *= act_bwd_t<ACT>(hh[u]);
           __builtin_amdgcn_raw_buffer_store_b64(pack4_bf16(v), rC, vo, 0, 0);
+        } else if constexpr (EPI == EPI_WGF32) {
+          __builtin_amdgcn_raw_buffer_store_b128(
+              u32x4{__float_as_uint(v[0]), __float_as_uint(v[1]), __float_as_uint(v[2]), __float_as_uint(v[3])}, rC, vo,
+              0, 0);
         } else if constexpr (EPI == EPI_RES) {
           const u32x2 rv = aux[ii][j];
           v[0] += __uint_as_float(rv[0] << 16);
@@ -955,12 +722,13 @@ gemm_wide_kernel(GemmParams p, int tilesM, int tilesN, int groups) {
     // Groups without rows have no tiles: their [M][N] outputs are zeroed here,
     // spread over the whole grid (16-byte stores; no tile writes them).
     uint64_t empty = __ballot(lane < groups && P.incl == P.excl);
-    const int64_t chunks = (int64_t)p.M * p.N / 8;
+    const int64_t chunks = (int64_t)p.M * p.N / (EPI == EPI_WGF32 ? 4 : 8);
     const int64_t gtid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x, gstride = (int64_t)gridDim.x * blockDim.x;
     while (empty) {
       const int g = __builtin_ctzll(empty);
       empty &= empty - 1;
-      u32x4* o = reinterpret_cast<u32x4*>((uint16_t*)p.C + (int64_t)g * p.sC);
+      u32x4* o = EPI == EPI_WGF32 ? reinterpret_cast<u32x4*>((float*)p.C + (int64_t)g * p.sC)
+                                  : reinterpret_cast<u32x4*>((uint16_t*)p.C + (int64_t)g * p.sC);
       for (int64_t i = gtid; i < chunks; i += gstride) o[i] = u32x4{0u, 0u, 0u, 0u};
     }
   }
@@ -1010,17 +778,22 @@ gemm_wide_kernel(GemmParams p, int tilesM, int tilesN, int groups) {
   };
   // Load cursor: segment le, its tile lt, K-step lk, end lkend; ls = stages
   // issued so far.
-  WOp<A_K, RAGGED_K, NW> opA;
-  WOp<BK_C, RAGGED_K, NW> opB;
+  // EPI_WGF32: both operands row-major and shared by every group (each group
+  // a K range of them), so the extent is the whole operand.
+  constexpr bool RMO = EPI == EPI_WGF32;
+  static_assert(!RMO || RAGGED_K, "row-major operands: ragged-K products only");
+  WOp<A_K, RAGGED_K, NW, RMO> opA;
+  WOp<BK_C, RAGGED_K, NW, RMO> opB;
   int le = 0, lt = 0, lk = 0, lkend = 0, ls = 0;
   auto plan = [&](int t) __attribute__((always_inline)) {
     const WGeo G = geo(t);
-    const uint16_t* Ab = (const uint16_t*)p.A + G.g * p.sA;
-    const uint16_t* Bb = (const uint16_t*)p.B + G.g * p.sB;
+    const uint16_t* Ab = (const uint16_t*)p.A + (RMO ? 0 : G.g * p.sA);
+    const uint16_t* Bb = (const uint16_t*)p.B + (RMO ? 0 : G.g * p.sB);
+    const int64_t extA = RMO ? (int64_t)p.cap * p.lda : p.sA, extB = RMO ? (int64_t)p.cap * p.ldb : p.sB;
     if constexpr (A_K) opA.plan(Ab, p.sA, p.lda, G.lo_al + G.m0, (int)pad16(p.cap), 0, 0, 0, wid, lane);
-    else opA.plan(Ab, p.sA, p.lda, G.m0, p.M, G.lo_al, G.lo, G.hi, wid, lane);
+    else opA.plan(Ab, extA, p.lda, G.m0, p.M, G.lo_al, G.lo, G.hi, wid, lane);
     if constexpr (BK_C) opB.plan(Bb, p.sB, p.ldb, G.n0, p.N, 0, 0, 0, wid, lane);
-    else if constexpr (RAGGED_K) opB.plan(Bb, p.sB, p.ldb, G.n0, p.N, G.lo_al, G.lo, G.hi, wid, lane);
+    else if constexpr (RAGGED_K) opB.plan(Bb, extB, p.ldb, G.n0, p.N, G.lo_al, G.lo, G.hi, wid, lane);
     else opB.plan(Bb, p.sB, p.ldb, G.n0, p.N, 0, 0, p.K, wid, lane);
     if (lkend == 0) lkend = G.nk;
   };
@@ -1496,58 +1269,6 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmParams p) {
 }
 
 // --------------------------------------------------------------- launchers
-// Tile shape, LDS stages and resident blocks per CU (OCC) of the bf16 kernel:
-// the one geometry its loads, fragment reads and epilogue staging are
-// written and tested for (four waves of 64 x 64, two blocks per CU).
-template <int BM_, int BN_, int WGM_, int WGN_, int STAGES_, int OCC_> struct TileCfg {
-  static constexpr int BM = BM_, BN = BN_, WGM = WGM_, WGN = WGN_, STAGES = STAGES_, OCC = OCC_;
-};
-using Tile = TileCfg<128, 128, 2, 2, 4, 2>;
-constexpr int kBM = Tile::BM, kBN = Tile::BN;
-
-template <bool B_K, bool RAGGED_K, int EPI, int ACT, bool BLK, bool CBLK>
-static void launch_bf16(int groups, const GemmParams& p, int tilesM, int tilesN, hipStream_t s) {
-  constexpr int NT = Tile::WGM * Tile::WGN * 64;
-  constexpr size_t shmem = Tile::STAGES * (size_t)(Tile::BM + Tile::BN) * kBKb * sizeof(uint16_t);
-  auto kern = gemm_bf16_kernel<Tile::BM, Tile::BN, Tile::WGM, Tile::WGN, Tile::STAGES, Tile::OCC, B_K, RAGGED_K, EPI,
-                               ACT, BLK, CBLK>;
-  static std::atomic<uint64_t> lds_ok{0};
-  allow_dyn_lds((const void*)kern, (int)shmem, lds_ok);
-  const int64_t max_tiles = (int64_t)tilesM * tilesN * groups;
-  int blocks = num_cus() * Tile::OCC;
-  if (max_tiles < blocks) blocks = (int)((max_tiles + 7) / 8 * 8);
-  blocks = (blocks + 7) / 8 * 8;
-  hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(NT), shmem, s, p, tilesM, tilesN, groups);
-}
-
-// groups: experts (or 1 for a dense product); dtype/act as in moe_cfg.  BLK,
-// CBLK (bf16 only): operands / output in the blocked layout.
-template <bool B_K, bool RAGGED_K, int EPI, bool BLK = false, bool CBLK = false>
-static void run_gemm(int dtype, int act, int groups, const GemmParams& p, int tilesM, int tilesN, hipStream_t s) {
-  if (tilesM <= 0 || tilesN <= 0 || groups <= 0) return;
-  if (dtype == MOE_BF16) {
-    if constexpr (EPI == EPI_STORE || EPI == EPI_RES) {
-      launch_bf16<B_K, RAGGED_K, EPI, MOE_ACT_IDENTITY, BLK, CBLK>(groups, p, tilesM, tilesN, s);
-    } else {
-      switch (act) {
-        case MOE_ACT_RELU: launch_bf16<B_K, RAGGED_K, EPI, MOE_ACT_RELU, BLK, CBLK>(groups, p, tilesM, tilesN, s); break;
-        case MOE_ACT_GELU_TANH:
-          launch_bf16<B_K, RAGGED_K, EPI, MOE_ACT_GELU_TANH, BLK, CBLK>(groups, p, tilesM, tilesN, s);
-          break;
-        case MOE_ACT_GELU_ERF:
-          launch_bf16<B_K, RAGGED_K, EPI, MOE_ACT_GELU_ERF, BLK, CBLK>(groups, p, tilesM, tilesN, s);
-          break;
-        default: launch_bf16<B_K, RAGGED_K, EPI, MOE_ACT_IDENTITY, BLK, CBLK>(groups, p, tilesM, tilesN, s); break;
-      }
-    }
-  } else {
-    if constexpr (EPI != EPI_RES) {
-      dim3 grid((unsigned)tilesN, (unsigned)tilesM, (unsigned)groups);
-      hipLaunchKernelGGL((gemm_f32_kernel<B_K, RAGGED_K, EPI>), grid, dim3(256), 0, s, p);
-    }
-  }
-}
-
 constexpr int kSkMaxBlocks = 256;   // most blocks of a stream-K launch (partial slots per block: 2)
 template <bool B_K, bool RAGGED_K, int EPI, int ACT, bool CBLK>
 static void launch_wide(int groups, const GemmParams& p, int tilesM, int tilesN, hipStream_t s) {
@@ -1603,7 +1324,6 @@ static void run_expert(const moe_cfg& c, const GemmParams& p, int64_t rows, int 
   }
 }
 
-static int cdiv(int64_t a, int b) { return (int)((a + b - 1) / b); }
 // Rows per expert block of an [E][C][*] buffer (C rounded up to 16 for bf16).
 static int64_t rows_alloc(const moe_cfg& c) { return c.dtype == MOE_BF16 ? pad16(c.C) : c.C; }
 
@@ -1652,24 +1372,42 @@ void launch_expert_bwd_dw(const moe_cfg& c, const void* X, const void* A, const 
   }
 }
 
-// Dense bf16 products of the transformer block (one group, every row, row-major).
-void launch_dense(int64_t M, int N, int K, const void* A, int64_t lda, const void* B, int64_t ldb, bool b_nk,
-                  void* C, int64_t ldc, const void* resid, hipStream_t s) {
-  GemmParams p{A, lda, 0, B, ldb, 0, C, ldc, 0, nullptr, resid, nullptr, nullptr, 0, N, K, 0, (int)M};
-  const int tm = cdiv(M, kBM), tn = cdiv(N, kBN);
-  if (b_nk) {
-    if (resid) run_gemm<true, false, EPI_RES>(MOE_BF16, 0, 1, p, tm, tn, s);
-    else run_gemm<true, false, EPI_STORE>(MOE_BF16, 0, 1, p, tm, tn, s);
-  } else {
-    if (resid) run_gemm<false, false, EPI_RES>(MOE_BF16, 0, 1, p, tm, tn, s);
-    else run_gemm<false, false, EPI_STORE>(MOE_BF16, 0, 1, p, tm, tn, s);
+// Sum of the S float partials of a K-split weight gradient, in group order,
+// rounded once to bf16: 8 consecutive elements per thread.
+__global__ __launch_bounds__(256) void gemm_wgrad_reduce_kernel(const float* __restrict__ part, int S, int64_t MN,
+                                                                 uint16_t* __restrict__ C) {
+  const int64_t i = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * 8;
+  if (i >= MN) return;
+  f32x4 a0 = *reinterpret_cast<const f32x4*>(part + i), a1 = *reinterpret_cast<const f32x4*>(part + i + 4);
+  for (int g = 1; g < S; ++g) {
+    a0 += *reinterpret_cast<const f32x4*>(part + (int64_t)g * MN + i);
+    a1 += *reinterpret_cast<const f32x4*>(part + (int64_t)g * MN + i + 4);
   }
+  const float v0[4] = {a0[0], a0[1], a0[2], a0[3]}, v1[4] = {a1[0], a1[1], a1[2], a1[3]};
+  const u32x2 lo = pack4_bf16(v0), hi = pack4_bf16(v1);
+  *reinterpret_cast<u32x4*>(C + i) = u32x4{lo[0], lo[1], hi[0], hi[1]};
 }
 
-void launch_dense_wgrad(int M, int N, int64_t K, const void* A, int64_t lda, const void* B, int64_t ldb, void* C,
-                        int64_t ldc, hipStream_t s) {
-  GemmParams p{A, lda, 0, B, ldb, 0, C, ldc, 0, nullptr, nullptr, nullptr, nullptr, M, N, 0, 0, (int)K};
-  run_gemm<false, true, EPI_STORE>(MOE_BF16, 0, 1, p, cdiv(M, kBM), cdiv(N, kBN), s);
+// Token ranges of the dense weight gradients: the block's 2048 x 2048 and
+// 6144 x 2048 products have 64 and 192 tiles of 256 x 256, so four ranges give
+// every CU work (256 and 768 tile-ranges).
+constexpr int kWgradSplit = 4;
+size_t wgrad_ws_bytes(int M, int N) { return (size_t)kWgradSplit * M * N * sizeof(float); }
+
+// Weight gradient C[M][N] = A^T B of the block's dense projections, A [K][M]
+// and B [K][N] row-major bf16 (K = tokens), C bf16: the wide kernel's ragged-K
+// product with K split into wgrad_ksplit(M, N) token ranges of equal length
+// (multiples of 32), one float partial per range in `part`
+// (wgrad_ws_bytes(M, N) bytes), then their sum in range order.
+void launch_dense_wgrad(int M, int N, int64_t K, const void* A, const void* B, void* C, void* part, hipStream_t s) {
+  if (M <= 0 || N <= 0) return;
+  const int S = kWgradSplit;
+  const int64_t MN = (int64_t)M * N;
+  GemmParams p{A, M, 0, B, N, 0, part, N, MN, nullptr, nullptr, nullptr, nullptr, M, N, 0, 0, (int)K};
+  p.kchunk = (int)(((K + S - 1) / S + 31) / 32 * 32);
+  launch_wide<false, true, EPI_WGF32, MOE_ACT_IDENTITY, false>(S, p, (M + kWB - 1) / kWB, (N + kWB - 1) / kWB, s);
+  hipLaunchKernelGGL(gemm_wgrad_reduce_kernel, dim3((unsigned)((MN / 8 + 255) / 256)), dim3(256), 0, s,
+                     (const float*)part, S, MN, (uint16_t*)C);
 }
 
 // Row-major [M][K] bf16 -> the blocked layout with pad16(M) rows (rows past M

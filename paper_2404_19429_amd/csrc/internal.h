@@ -98,13 +98,12 @@ void launch_expert_bwd_dx(const moe_cfg& c, const void* dO, const int32_t* rb, c
 void launch_expert_bwd_dw(const moe_cfg& c, const void* X, const void* A, const void* dO, const void* dH,
                           const int32_t* rb, const int32_t* re, void* dW1, void* dW2, hipStream_t s);
 
-// Dense bf16 products (gemm.hip).  launch_dense: C[M][N] = A[M][K] op(B)
-// (+ resid, same layout as C), B is [N][K] if b_nk else [K][N].
-// launch_dense_wgrad: C[M][N] = A^T B with A [K][M], B [K][N] (sum over K rows).
-void launch_dense(int64_t M, int N, int K, const void* A, int64_t lda, const void* B, int64_t ldb, bool b_nk,
-                  void* C, int64_t ldc, const void* resid, hipStream_t s);
-void launch_dense_wgrad(int M, int N, int64_t K, const void* A, int64_t lda, const void* B, int64_t ldb, void* C,
-                        int64_t ldc, hipStream_t s);
+// Dense bf16 products of the block (gemm.hip).
+// launch_dense_wgrad: C[M][N] = A^T B with A [K][M], B [K][N] row-major bf16
+// (sum over K rows), on the wide kernel with K split into token ranges whose
+// float partials go to `part` (wgrad_ws_bytes(M, N) bytes).
+size_t wgrad_ws_bytes(int M, int N);
+void launch_dense_wgrad(int M, int N, int64_t K, const void* A, const void* B, void* C, void* part, hipStream_t s);
 // Row-major [M][K] -> blocked [pad16(M)][K] (K a multiple of 32), and dense
 // products on the wide kernel over blocked operands (see gemm.hip).
 void launch_pack_rows(const void* src, void* dst, int64_t M, int K, hipStream_t s);
