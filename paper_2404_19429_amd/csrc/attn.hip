@@ -92,6 +92,36 @@ __device__ __forceinline__ void read_cols(u32x4 (&f)[4], const uint16_t* st, int
   for (int u = 0; u < 4; ++u) f[u] = u32x4{o[2 * u][0], o[2 * u][1], o[2 * u + 1][0], o[2 * u + 1][1]};
 }
 
+// Split forms of read_rows<4> and read_cols: the *_issue calls start the 8
+// reads and return; the registers are pending until the matching wait (an
+// s_waitcnt lgkmcnt(0) that names them), so MFMAs on other registers overlap
+// the reads.  At most 8 reads are in flight (the counter holds 15).
+__device__ __forceinline__ void rows_issue(u32x4 (&f)[8], const uint16_t* st, int kk0, int lane) {
+  uint32_t a[8];
+#pragma unroll
+  for (int u = 0; u < 8; ++u) a[u] = lds_addr(st + toff(16 * (u % 4) + (lane & 15), 32 * (kk0 + u / 4) + 8 * (lane >> 4)));
+  Rd128Issue<8>::run(f, a);
+}
+__device__ __forceinline__ void cols_issue(u32x2 (&o)[8], const uint16_t* st, int cf0, int lane) {
+  const int g = lane >> 4, j = lane & 15;
+  uint32_t a[8];
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    const int cf = cf0 + (u >> 1), ks = u & 1;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int r = 16 * (2 * ks + h) + 4 * g + (j >> 2);
+      a[2 * u + h] = lds_addr(st + toff(r, 16 * cf + 4 * (j & 3)));
+    }
+  }
+  RdTrIssue8::run(o, a);
+}
+__device__ __forceinline__ void cols_finish(u32x4 (&f)[4], u32x2 (&o)[8]) {
+  lds_wait(o);
+#pragma unroll
+  for (int u = 0; u < 4; ++u) f[u] = u32x4{o[2 * u][0], o[2 * u][1], o[2 * u + 1][0], o[2 * u + 1][1]};
+}
+
 __device__ __forceinline__ f32x4 mfma(const u32x4& a, const u32x4& b, const f32x4& c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
 }
@@ -110,13 +140,22 @@ __device__ __forceinline__ u32x4 load_row16(const uint16_t* base, int64_t ld, in
 }
 
 
+// Max / sum over the four 16-lane groups (lanes l, l^16, l^32, l^48) with
+// gfx950's lane-swap instructions: swapping v with itself, permlane16_swap
+// returns (v, partner at l^16) in one order or the other, and permlane32_swap
+// likewise for l^32, so combining the two results needs no lane select and no
+// trip through the LDS crossbar.
 __device__ __forceinline__ float group_max(float v) {
-  v = fmaxf(v, __shfl_xor(v, 16, 64));
-  return fmaxf(v, __shfl_xor(v, 32, 64));
+  const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  v = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
 }
 __device__ __forceinline__ float group_sum(float v) {
-  v += __shfl_xor(v, 16, 64);
-  return v + __shfl_xor(v, 32, 64);
+  const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  v = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+  const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(b[0]) + __uint_as_float(b[1]);
 }
 
 // Store 4 consecutive columns (c0 .. c0+3) of one row as bf16.
@@ -178,19 +217,28 @@ attn_fwd_kernel(const uint16_t* __restrict__ qkv, uint16_t* __restrict__ o, floa
     f32x4 s[4][2];
 #pragma unroll
     for (int i = 0; i < 4; ++i) s[i][0] = s[i][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+    // Reads one batch ahead of the MFMAs: K columns 0..63 (wait), then K
+    // columns 64..127 in flight under the first half's MFMAs, then the first V
+    // batch in flight under the second half's MFMAs and the softmax.
+    u32x4 kf0[8], kf1[8];
+    u32x2 vp[8];
+    rows_issue(kf0, Ks, 0, lane);
+    lds_wait(kf0);
+    rows_issue(kf1, Ks, 2, lane);
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-    for (int half = 0; half < 2; ++half) {
-      u32x4 kf[8];
-      read_rows<4>(kf, Ks, 0, 2 * half, lane);
-      __builtin_amdgcn_sched_barrier(0);
+    for (int u = 0; u < 8; ++u)
 #pragma unroll
-      for (int u = 0; u < 8; ++u)
+      for (int f = 0; f < 2; ++f) s[u % 4][f] = mfma(kf0[u], qf[f][u / 4], s[u % 4][f]);
+    __builtin_amdgcn_sched_barrier(0);
+    lds_wait(kf1);
+    cols_issue(vp, Vs, 0, lane);
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-        for (int f = 0; f < 2; ++f) s[u % 4][f] = mfma(kf[u], qf[f][2 * half + u / 4], s[u % 4][f]);
-      __builtin_amdgcn_sched_barrier(0);
-    }
-    u32x4 vf[4];
-    read_cols(vf, Vs, 0, lane);  // overlaps the tail of the score MFMAs
+    for (int u = 0; u < 8; ++u)
+#pragma unroll
+      for (int f = 0; f < 2; ++f) s[u % 4][f] = mfma(kf1[u], qf[f][2 + u / 4], s[u % 4][f]);
+    __builtin_amdgcn_sched_barrier(0);
     // Online softmax per query (lane column); keys 16 i + 4 g + v.
     u32x4 pb[2][2];
 #pragma unroll
@@ -225,10 +273,13 @@ attn_fwd_kernel(const uint16_t* __restrict__ qkv, uint16_t* __restrict__ o, floa
       pb[f][0] = pack_b(s[0][f], s[1][f]);
       pb[f][1] = pack_b(s[2][f], s[3][f]);
     }
-    // O^T += V^T P^T, two head-dim fragments per transposed read batch.
+    // O^T += V^T P^T, two head-dim fragments per transposed read batch, the
+    // next batch in flight under the current batch's MFMAs.
+    u32x4 vf[4];
+    cols_finish(vf, vp);
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
-      if (c > 0) read_cols(vf, Vs, 2 * c, lane);
+      if (c + 1 < 4) cols_issue(vp, Vs, 2 * (c + 1), lane);
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int u = 0; u < 4; ++u)
@@ -236,6 +287,7 @@ attn_fwd_kernel(const uint16_t* __restrict__ qkv, uint16_t* __restrict__ o, floa
         for (int f = 0; f < 2; ++f)
           acc_o[2 * c + (u >> 1)][f] = mfma(vf[u], pb[f][u & 1], acc_o[2 * c + (u >> 1)][f]);
       __builtin_amdgcn_sched_barrier(0);
+      if (c + 1 < 4) cols_finish(vf, vp);
     }
   }
 
