@@ -122,6 +122,12 @@ __device__ __forceinline__ void cols_finish(u32x4 (&f)[4], u32x2 (&o)[8]) {
   for (int u = 0; u < 4; ++u) f[u] = u32x4{o[2 * u][0], o[2 * u][1], o[2 * u + 1][0], o[2 * u + 1][1]};
 }
 
+// 2^x with the hardware instruction (v_exp_f32, about 1 ulp; results below
+// the float normal range flush to 0, which only a probability too small to
+// change a bf16-rounded product can be).  The library exp2f adds a range
+// fix-up around it (five more instructions per value).
+__device__ __forceinline__ float exp2_hw(float x) { return __builtin_amdgcn_exp2f(x); }
+
 __device__ __forceinline__ f32x4 mfma(const u32x4& a, const u32x4& b, const f32x4& c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
 }
@@ -256,14 +262,14 @@ attn_fwd_kernel(const uint16_t* __restrict__ qkv, uint16_t* __restrict__ o, floa
         }
       tmax = group_max(tmax);
       const float mnew = fmaxf(mrow[f], tmax);
-      const float alpha = exp2f(mrow[f] - mnew);
+      const float alpha = exp2_hw(mrow[f] - mnew);
       mrow[f] = mnew;
       float ps = 0.f;
 #pragma unroll
       for (int i = 0; i < 4; ++i)
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
-          const float p = exp2f(s[i][f][v] - mnew);
+          const float p = exp2_hw(s[i][f][v] - mnew);
           s[i][f][v] = p;
           ps += p;
         }
@@ -417,7 +423,7 @@ attn_dq_kernel(const uint16_t* __restrict__ qkv, const uint16_t* __restrict__ do
 #pragma unroll
       for (int v = 0; v < 4; ++v) {
         const int key = k0 + 16 * i + 4 * g + v;
-        s[i][v] = (key > q || q >= S) ? 0.f : exp2f(s[i][v] * c2 - lq) * (dp[i][v] - dq_delta);
+        s[i][v] = (key > q || q >= S) ? 0.f : exp2_hw(s[i][v] * c2 - lq) * (dp[i][v] - dq_delta);
       }
     const u32x4 ds0 = pack_b(s[0], s[1]), ds1 = pack_b(s[2], s[3]);
 #pragma unroll
@@ -544,7 +550,7 @@ attn_dkdv_kernel(const uint16_t* __restrict__ qkv, const uint16_t* __restrict__ 
       for (int v = 0; v < 4; ++v) {
         const int q = qbase + 16 * i + 4 * g + v;
         const bool live = key <= q && q < S;  // statistics past S are unspecified
-        const float p = live ? exp2f(s[i][v] * c2 - L4[v]) : 0.f;
+        const float p = live ? exp2_hw(s[i][v] * c2 - L4[v]) : 0.f;
         s[i][v] = p;
         dp[i][v] = live ? p * (dp[i][v] - D4[v]) : 0.f;
       }
