@@ -57,45 +57,17 @@ __device__ __forceinline__ void load_tile(const uint16_t* base, int64_t ld, int 
   }
 }
 
-// A operand with K = the 128 columns: fragment (rf, kk) = rows 16 rf + l%16,
-// columns 32 kk + 8*(l/16) .. +7.  Reads 8 fragments (rf0..rf0+NR-1) x (kk0..kk0+8/NR-1).
-template <int NR>
-__device__ __forceinline__ void read_rows(u32x4 (&f)[8], const uint16_t* st, int rf0, int kk0, int lane) {
-  uint32_t a[8];
-#pragma unroll
-  for (int u = 0; u < 8; ++u) {
-    const int rf = rf0 + u % NR, kk = kk0 + u / NR;
-    a[u] = lds_addr(st + toff(16 * rf + (lane & 15), 32 * kk + 8 * (lane >> 4)));
-  }
-  Rd128<8>::run(f, a);
-}
-
-// A operand with K = rows (transposed read): fragment (cf, ks) = columns
-// 16 cf + l%16; K index 8*(l/16) + j reads row 16*(2ks) + 4*(l/16) + j for
-// j < 4 and row 16*(2ks+1) + 4*(l/16) + j-4 for j >= 4.  Reads 4 fragments:
-// cf in {cf0, cf0+1} x ks in {0, 1}, stored f[2*(cf-cf0) + ks].
-__device__ __forceinline__ void read_cols(u32x4 (&f)[4], const uint16_t* st, int cf0, int lane) {
-  const int g = lane >> 4, j = lane & 15;
-  uint32_t a[8];
-#pragma unroll
-  for (int u = 0; u < 4; ++u) {
-    const int cf = cf0 + (u >> 1), ks = u & 1;
-#pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      const int r = 16 * (2 * ks + h) + 4 * g + (j >> 2);
-      a[2 * u + h] = lds_addr(st + toff(r, 16 * cf + 4 * (j & 3)));
-    }
-  }
-  u32x2 o[8];
-  RdTr<8>::run(o, a);
-#pragma unroll
-  for (int u = 0; u < 4; ++u) f[u] = u32x4{o[2 * u][0], o[2 * u][1], o[2 * u + 1][0], o[2 * u + 1][1]};
-}
-
-// Split forms of read_rows<4> and read_cols: the *_issue calls start the 8
-// reads and return; the registers are pending until the matching wait (an
+// Fragment reads, split into issue and wait: the *_issue calls start 8 reads
+// and return; the registers are pending until the matching wait (an
 // s_waitcnt lgkmcnt(0) that names them), so MFMAs on other registers overlap
 // the reads.  At most 8 reads are in flight (the counter holds 15).
+// rows_issue: A operand with K = the 128 columns, fragments (rf = u % 4,
+// kk = kk0 + u / 4): rows 16 rf + l%16, columns 32 kk + 8 (l/16) .. +7.
+// cols_issue / cols_finish: A operand with K = rows (transposed reads),
+// fragments (cf, ks) for cf in {cf0, cf0 + 1}, ks in {0, 1}: columns
+// 16 cf + l%16; K index 8 (l/16) + j reads row 16 (2 ks) + 4 (l/16) + j for
+// j < 4 and row 16 (2 ks + 1) + 4 (l/16) + j - 4 for j >= 4; stored
+// f[2 (cf - cf0) + ks].
 __device__ __forceinline__ void rows_issue(u32x4 (&f)[8], const uint16_t* st, int kk0, int lane) {
   uint32_t a[8];
 #pragma unroll
@@ -116,6 +88,10 @@ __device__ __forceinline__ void cols_issue(u32x2 (&o)[8], const uint16_t* st, in
   }
   RdTrIssue8::run(o, a);
 }
+// Wait states before LDS reads land in registers that MFMAs issued just
+// before still read as sources.
+__device__ __forceinline__ void mfma_src_gap() { asm volatile("s_nop 7" ::: "memory"); }
+
 __device__ __forceinline__ void cols_finish(u32x4 (&f)[4], u32x2 (&o)[8]) {
   lds_wait(o);
 #pragma unroll
@@ -398,26 +374,37 @@ attn_dq_kernel(const uint16_t* __restrict__ qkv, const uint16_t* __restrict__ do
     f32x4 s[4], dp[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) s[i] = dp[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+    // Each batch of fragment reads is in flight under the previous batch's MFMAs.
+    u32x4 fr0[8], fr1[8];
+    u32x2 cp[8];
+    rows_issue(fr0, Ks, 0, lane);
+    lds_wait(fr0);
+    rows_issue(fr1, Ks, 2, lane);
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-    for (int half = 0; half < 2; ++half) {
-      u32x4 kf[8];
-      read_rows<4>(kf, Ks, 0, 2 * half, lane);
-      __builtin_amdgcn_sched_barrier(0);
+    for (int u = 0; u < 8; ++u) s[u % 4] = mfma(fr0[u], qf[u / 4], s[u % 4]);
+    __builtin_amdgcn_sched_barrier(0);
+    lds_wait(fr1);
+    mfma_src_gap();
+    rows_issue(fr0, Vs, 0, lane);
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-      for (int u = 0; u < 8; ++u) s[u % 4] = mfma(kf[u], qf[2 * half + u / 4], s[u % 4]);
-      __builtin_amdgcn_sched_barrier(0);
-    }
+    for (int u = 0; u < 8; ++u) s[u % 4] = mfma(fr1[u], qf[2 + u / 4], s[u % 4]);
+    __builtin_amdgcn_sched_barrier(0);
+    lds_wait(fr0);
+    mfma_src_gap();
+    rows_issue(fr1, Vs, 2, lane);
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-    for (int half = 0; half < 2; ++half) {
-      u32x4 vf[8];
-      read_rows<4>(vf, Vs, 0, 2 * half, lane);
-      __builtin_amdgcn_sched_barrier(0);
+    for (int u = 0; u < 8; ++u) dp[u % 4] = mfma(fr0[u], dof[u / 4], dp[u % 4]);
+    __builtin_amdgcn_sched_barrier(0);
+    lds_wait(fr1);
+    cols_issue(cp, Ks, 0, lane);
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-      for (int u = 0; u < 8; ++u) dp[u % 4] = mfma(vf[u], dof[2 * half + u / 4], dp[u % 4]);
-      __builtin_amdgcn_sched_barrier(0);
-    }
+    for (int u = 0; u < 8; ++u) dp[u % 4] = mfma(fr1[u], dof[2 + u / 4], dp[u % 4]);
+    __builtin_amdgcn_sched_barrier(0);
     u32x4 kt_f[4];
-    read_cols(kt_f, Ks, 0, lane);
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -426,13 +413,15 @@ attn_dq_kernel(const uint16_t* __restrict__ qkv, const uint16_t* __restrict__ do
         s[i][v] = (key > q || q >= S) ? 0.f : exp2_hw(s[i][v] * c2 - lq) * (dp[i][v] - dq_delta);
       }
     const u32x4 ds0 = pack_b(s[0], s[1]), ds1 = pack_b(s[2], s[3]);
+    cols_finish(kt_f, cp);
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
-      if (c > 0) read_cols(kt_f, Ks, 2 * c, lane);
+      if (c + 1 < 4) cols_issue(cp, Ks, 2 * (c + 1), lane);
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int u = 0; u < 4; ++u) acc[2 * c + (u >> 1)] = mfma(kt_f[u], (u & 1) ? ds1 : ds0, acc[2 * c + (u >> 1)]);
       __builtin_amdgcn_sched_barrier(0);
+      if (c + 1 < 4) cols_finish(kt_f, cp);
     }
   }
   if (q < S) {
@@ -513,24 +502,36 @@ attn_dkdv_kernel(const uint16_t* __restrict__ qkv, const uint16_t* __restrict__ 
     f32x4 s[4], dp[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) s[i] = dp[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+    // Each batch of fragment reads is in flight under the previous batch's MFMAs.
+    u32x4 fr0[8], fr1[8];
+    u32x2 cp[8];
+    rows_issue(fr0, Qs, 0, lane);
+    lds_wait(fr0);
+    rows_issue(fr1, Qs, 2, lane);
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-    for (int half = 0; half < 2; ++half) {
-      u32x4 af[8];
-      read_rows<4>(af, Qs, 0, 2 * half, lane);
-      __builtin_amdgcn_sched_barrier(0);
+    for (int u = 0; u < 8; ++u) s[u % 4] = mfma(fr0[u], kf[u / 4], s[u % 4]);
+    __builtin_amdgcn_sched_barrier(0);
+    lds_wait(fr1);
+    mfma_src_gap();
+    rows_issue(fr0, dOs, 0, lane);
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-      for (int u = 0; u < 8; ++u) s[u % 4] = mfma(af[u], kf[2 * half + u / 4], s[u % 4]);
-      __builtin_amdgcn_sched_barrier(0);
-    }
+    for (int u = 0; u < 8; ++u) s[u % 4] = mfma(fr1[u], kf[2 + u / 4], s[u % 4]);
+    __builtin_amdgcn_sched_barrier(0);
+    lds_wait(fr0);
+    mfma_src_gap();
+    rows_issue(fr1, dOs, 2, lane);
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-    for (int half = 0; half < 2; ++half) {
-      u32x4 af[8];
-      read_rows<4>(af, dOs, 0, 2 * half, lane);
-      __builtin_amdgcn_sched_barrier(0);
+    for (int u = 0; u < 8; ++u) dp[u % 4] = mfma(fr0[u], vf[u / 4], dp[u % 4]);
+    __builtin_amdgcn_sched_barrier(0);
+    lds_wait(fr1);
+    cols_issue(cp, dOs, 0, lane);
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-      for (int u = 0; u < 8; ++u) dp[u % 4] = mfma(af[u], vf[2 * half + u / 4], dp[u % 4]);
-      __builtin_amdgcn_sched_barrier(0);
-    }
+    for (int u = 0; u < 8; ++u) dp[u % 4] = mfma(fr1[u], vf[2 + u / 4], dp[u % 4]);
+    __builtin_amdgcn_sched_barrier(0);
     // Statistics of queries qbase + 16 i + 4 g .. +3 (asm reads: see lds_ops.h).
     u32x4 st8[8];
     {
@@ -557,19 +558,22 @@ attn_dkdv_kernel(const uint16_t* __restrict__ qkv, const uint16_t* __restrict__ 
     }
     const u32x4 p0 = pack_b(s[0], s[1]), p1 = pack_b(s[2], s[3]);
     const u32x4 ds0 = pack_b(dp[0], dp[1]), ds1 = pack_b(dp[2], dp[3]);
+    u32x4 tf[4];
+    cols_finish(tf, cp);   // dO columns 0..31
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
-      u32x4 tf[4];
-      read_cols(tf, dOs, 2 * c, lane);
+      cols_issue(cp, Qs, 2 * c, lane);
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int u = 0; u < 4; ++u) dv[2 * c + (u >> 1)] = mfma(tf[u], (u & 1) ? p1 : p0, dv[2 * c + (u >> 1)]);
       __builtin_amdgcn_sched_barrier(0);
-      read_cols(tf, Qs, 2 * c, lane);
+      cols_finish(tf, cp);
+      if (c + 1 < 4) cols_issue(cp, dOs, 2 * (c + 1), lane);
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int u = 0; u < 4; ++u) dk[2 * c + (u >> 1)] = mfma(tf[u], (u & 1) ? ds1 : ds0, dk[2 * c + (u >> 1)]);
       __builtin_amdgcn_sched_barrier(0);
+      if (c + 1 < 4) cols_finish(tf, cp);
     }
   }
   if (key < S) {
