@@ -80,81 +80,31 @@ __device__ __forceinline__ void epilogue_store(const GemmParams& p, int64_t off,
 }
 
 // ----------------------------------------------------------------- bf16 MFMA
-// Operand tiles (BK = 32, one MFMA K step) move global -> LDS with
-// global_load_lds_dwordx4 (each lane's 16 bytes land at LDS base + 16 * lane)
-// into a STAGES-deep ring.  A lane whose element lies outside the operand
-// reads a 16-byte zero page instead, so every wave issues the same number of
-// loads per tile and the vmcnt arithmetic below is exact.  Barriers inside the
-// K loop are plain s_barrier (with a compiler memory clobber) preceded by an
-// explicit s_waitcnt: a full __syncthreads() fence would also drain the loads
-// that are meant to stay in flight.
+// Operand tiles (BK = 32, one MFMA K step) move global -> LDS with buffer
+// loads into LDS (each lane's 16 bytes land at LDS base + 16 * lane) into a
+// multi-stage ring; a lane whose element lies outside the operand reads zeros.
 //
-// Schedule of iteration kt: wait until tile kt+1 has landed, barrier, refill
-// the stage of tile kt (its fragments are already in registers) with tile
-// kt+STAGES, read the fragments of tile kt+1, and multiply tile kt.  Loads get
-// STAGES-1 iterations to land and fragment reads overlap the MFMAs.
-//
-// LDS layouts:
+// LDS layouts of a stage:
 //  * K-contiguous operand, ROWS x 32: fragment-linear.  The 16 x 32 MFMA
 //    fragment of rows 16f..16f+15 is 1 KB at offset 1 KB * f, lane L's 16
 //    bytes (row 16f + L%16, k = 8*(L/16) .. +7) at 16 * L: one DMA instruction
 //    fills one fragment and one ds_read_b128 reads it, both linear.
-//  * MN-contiguous operand, 32 x COLS (row = k, as in memory): 16-byte chunk c
-//    of row k stored at chunk c ^ hsw(k), hsw(k) = 2 * ((k & 3) | ((k >> 3) & 1) << 2).
+//  * MN-contiguous operand, 32 x COLS (row = k): [2][COLS/32] blocks of 16
+//    rows x 4 chunks of 16 bytes, chunk c of block row r at c ^ bsw(r): the 16
+//    lanes of a transposed read cover rows r..r+3 and the next lane group rows
+//    r+8..r+11, and this swizzle puts those 8 x 32 bytes on distinct banks.
 //    Fragments are read with ds_read_b64_tr_b16: within each 16-lane group,
 //    lane j addresses row k0 + j/4, columns n0 + 4*(j%4) .. +3, and receives
 //    column n0 + j of rows k0 .. k0+3 -- two such reads give the 8-element K
 //    run of the MFMA operand.
 constexpr int kBKb = 32;
-__device__ __forceinline__ int hsw(int k) { return 2 * ((k & 3) | (((k >> 3) & 1) << 2)); }
 
 // K-contiguous operand: ROWS x 32 tile, one wave instruction fills one fragment.
-// BLK: the operand is stored in 16 x 32 blocks; a fragment is one block.
-template <int ROWS, int NW, bool BLK>
+template <int ROWS, int NW>
 struct TileK {
   static constexpr int NI = ROWS / 16 / NW;     // loads per wave per tile
   static_assert(NI >= 1 && ROWS % (16 * NW) == 0, "tile/waves mismatch");
-  __device__ static void issue(const uint16_t* base, int64_t ld, int row0, int rowlim, int k0, int klim,
-                               uint16_t* stage, int wid, int lane) {
-#pragma unroll
-    for (int i = 0; i < NI; ++i) {
-      const int q = i * NW + wid;
-      const int row = row0 + 16 * q + (lane & 15), k = k0 + 8 * (lane >> 4);
-      const void* src = (row < rowlim && k < klim) ? (const void*)(base + (int64_t)row * ld + k) : (const void*)g_zero16;
-      dma16(src, stage + q * 512);
-    }
-  }
-  // Blocked source: row0 (a multiple of 16) is the fragment's first row in
-  // the operand, rows at or past rowlim read zeros.  Lane l takes (row l%16,
-  // k chunk l/16) of the block, which is its fragment-linear LDS position.
-  __device__ static void issue_blk(const uint16_t* base, int64_t ld, int row0, int rowlim, int k0, int klim,
-                                   uint16_t* stage, int wid, int lane) {
-#pragma unroll
-    for (int i = 0; i < NI; ++i) {
-      const int q = i * NW + wid;
-      const int rb = (row0 >> 4) + q;
-      const int row = 16 * rb + (lane & 15);
-      const void* src = (row < rowlim && k0 < klim)
-                            ? (const void*)(base + ((int64_t)rb * (ld >> 5) + (k0 >> 5)) * 512 + (lane & 15) * 32 +
-                                            (lane >> 4) * 8)
-                            : (const void*)g_zero16;
-      dma16(src, stage + q * 512);
-    }
-  }
-  // Reads FN fragments (rows r0 + 16 j) of one stage, kReadChunk per asm block.
-  template <int NF>
-  __device__ static void read(u32x4 (&f)[NF], const uint16_t* stage, int r0, int lane) {
-    static_assert(NF % 4 == 0, "fragment count");
-#pragma unroll
-    for (int c = 0; c < NF; c += (NF >= 8 ? 8 : 4)) {
-      constexpr int N = NF >= 8 ? 8 : 4;
-      uint32_t a[N];
-#pragma unroll
-      for (int u = 0; u < N; ++u) a[u] = lds_addr(stage + ((r0 >> 4) + c + u) * 512 + lane * 8);
-      Rd128<N>::run(&f[c], a);
-    }
-  }
-  // Split form (NF = 4 or 8): start the reads, later complete them in place.
+  // Split reads (NF = 4 or 8): start the reads, later complete them in place.
   template <int NF>
   __device__ static void read_issue(u32x4 (&f)[NF], u32x2 (&)[8], const uint16_t* stage, int r0, int lane) {
     static_assert(NF == 4 || NF == 8, "split reads: 4 or 8 fragments");
@@ -163,107 +113,23 @@ struct TileK {
     for (int u = 0; u < NF; ++u) a[u] = lds_addr(stage + ((r0 >> 4) + u) * 512 + lane * 8);
     Rd128Issue<NF>::run(f, a);
   }
-  template <int NF>
-  __device__ static void read_finish(u32x4 (&f)[NF], u32x2 (&)[8]) { lds_wait(f); }
 };
 
 // MN-contiguous operand: 32 x COLS tile (row = k), one wave instruction fills 64 chunks.
-// BLK: the operand is stored in 16 x 32 blocks and the stage keeps them as
-// [2][COLS/32] blocks of 16 rows x 4 chunks, chunk c of block row r at c ^ bsw(r):
-// the 16 lanes of a transposed read cover rows r..r+3 and the next lane group
-// rows r+8..r+11, and this swizzle puts those 8 x 32 bytes on distinct banks.
 __device__ __forceinline__ int bsw(int r) { return 2 * (((r >> 1) ^ (r >> 3)) & 1); }
-template <int COLS, int NW, bool BLK>
+template <int COLS, int NW>
 struct TileMN {
   static constexpr int CB = COLS / 32;          // column blocks per stage
   static constexpr int CPR = COLS / 8;          // 16-byte chunks per row
   static constexpr int NI = kBKb * CPR / 64 / NW;
   static_assert(NI >= 1 && (kBKb * CPR) % (64 * NW) == 0 && CPR >= 16, "tile/waves mismatch");
-  __device__ static void issue(const uint16_t* base, int64_t ld, int col0, int collim, int k0, int klim,
-                               uint16_t* stage, int wid, int lane) {
-#pragma unroll
-    for (int i = 0; i < NI; ++i) {
-      const int q = i * NW + wid;
-      const int L = q * 64 + lane;
-      const int k = L / CPR;
-      const int lc = (L % CPR) ^ hsw(k);
-      const int col = col0 + 8 * lc, kk = k0 + k;
-      const void* src = (col < collim && kk < klim) ? (const void*)(base + (int64_t)kk * ld + col) : (const void*)g_zero16;
-      dma16(src, stage + q * 512);
-    }
-  }
-  // Blocked source: k0 (a multiple of 16) is the stage's first row in the
-  // operand; rows outside [klo, khi) and column blocks at or past collim read zeros.
-  __device__ static void issue_blk(const uint16_t* base, int64_t ld, int col0, int collim, int k0, int klo, int khi,
-                                   uint16_t* stage, int wid, int lane) {
-    const int r = lane >> 2;
-    const int c = (lane & 3) ^ bsw(r);
-#pragma unroll
-    for (int i = 0; i < NI; ++i) {
-      const int b = i * NW + wid;
-      const int kb = b / CB, cb = b % CB;
-      const int krow = k0 + 16 * kb + r;
-      const int col = col0 + 32 * cb;
-      const void* src = (krow >= klo && krow < khi && col < collim)
-                            ? (const void*)(base + ((int64_t)((k0 >> 4) + kb) * (ld >> 5) + (col >> 5)) * 512 +
-                                            r * 32 + c * 8)
-                            : (const void*)g_zero16;
-      dma16(src, stage + b * 512);
-    }
-  }
   // LDS element offset of (k, col) in a stage.
   __device__ static int lds_off(int k, int col) {
-    if constexpr (BLK) {
-      const int r = k & 15;
-      return ((k >> 4) * CB + (col >> 5)) * 512 + r * 32 + ((((col & 31) >> 3) ^ bsw(r)) << 3) + (col & 7);
-    } else {
-      return k * COLS + (((col >> 3) ^ hsw(k)) << 3) + (col & 7);
-    }
-  }
-  // Reads NF 16 (m or n) x 32 k fragments at columns c0 + 16 j: lane gets column
-  // c0 + 16 j + lane%16, k = 8*(lane/16) .. +7 (two transposed reads: k .. k+3, k+4 .. k+7).
-  template <int NF>
-  __device__ static void read(u32x4 (&f)[NF], const uint16_t* stage, int c0, int lane) {
-    static_assert(NF % 4 == 0, "fragment count");
-    const int j = lane & 15;
-    const int k = 8 * (lane >> 4) + (j >> 2);
-#pragma unroll
-    for (int c = 0; c < NF; c += 4) {
-      uint32_t a[8];
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const int col = c0 + 16 * (c + u) + 4 * (j & 3);
-        a[2 * u] = lds_addr(stage + lds_off(k, col));
-        a[2 * u + 1] = lds_addr(stage + lds_off(k + 4, col));
-      }
-      u32x2 o[8];
-      RdTr<8>::run(o, a);
-#pragma unroll
-      for (int u = 0; u < 4; ++u) f[c + u] = u32x4{o[2 * u][0], o[2 * u][1], o[2 * u + 1][0], o[2 * u + 1][1]};
-    }
-  }
-  // Split form (NF = 4): the 8 transposed reads land in p; read_finish waits and assembles.
-  template <int NF>
-  __device__ static void read_issue(u32x4 (&)[NF], u32x2 (&p)[8], const uint16_t* stage, int c0, int lane) {
-    static_assert(NF == 4, "split transposed reads: 4 fragments");
-    const int j = lane & 15;
-    const int k = 8 * (lane >> 4) + (j >> 2);
-    uint32_t a[8];
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int col = c0 + 16 * u + 4 * (j & 3);
-      a[2 * u] = lds_addr(stage + lds_off(k, col));
-      a[2 * u + 1] = lds_addr(stage + lds_off(k + 4, col));
-    }
-    RdTrIssue8::run(p, a);
-  }
-  template <int NF>
-  __device__ static void read_finish(u32x4 (&f)[NF], u32x2 (&p)[8]) {
-    lds_wait(p);
-#pragma unroll
-    for (int u = 0; u < 4; ++u) f[u] = u32x4{p[2 * u][0], p[2 * u][1], p[2 * u + 1][0], p[2 * u + 1][1]};
+    const int r = k & 15;
+    return ((k >> 4) * CB + (col >> 5)) * 512 + r * 32 + ((((col & 31) >> 3) ^ bsw(r)) << 3) + (col & 7);
   }
 };
+
 
 // Tiles of a group are numbered panel by panel (kPanelN tile columns wide),
 // m-tile by m-tile inside a panel, n fastest, so the tiles an XCD has in
@@ -697,8 +563,8 @@ gemm_wide_kernel(GemmParams p, int tilesM, int tilesN, int groups) {
   constexpr int STAGE = (kWB + kWB) * BK;       // elements per pipeline stage
   constexpr bool A_K = !RAGGED_K;
   constexpr bool BK_C = B_K && !RAGGED_K;
-  using TA = typename std::conditional<A_K, TileK<kWB, NW, true>, TileMN<kWB, NW, true>>::type;
-  using TB = typename std::conditional<BK_C, TileK<kWB, NW, true>, TileMN<kWB, NW, true>>::type;
+  using TA = typename std::conditional<A_K, TileK<kWB, NW>, TileMN<kWB, NW>>::type;
+  using TB = typename std::conditional<BK_C, TileK<kWB, NW>, TileMN<kWB, NW>>::type;
   static_assert(TA::NI == kWNI && TB::NI == kWNI, "load plan");
   constexpr int LPS = 2 * kWNI;                  // loads per wave per stage
   static_assert(STAGES >= 2 && LPS * (STAGES - 1) < 64, "vmcnt range");
@@ -827,7 +693,7 @@ gemm_wide_kernel(GemmParams p, int tilesM, int tilesN, int groups) {
                         __attribute__((always_inline)) {
     using T = decltype(tile);
     constexpr int NF = sizeof(f) / sizeof(u32x4);
-    if constexpr (std::is_same<T, TileK<kWB, NW, true>>::value) {
+    if constexpr (std::is_same<T, TileK<kWB, NW>>::value) {
       T::template read_issue<NF>(f, p0, st, c0, lane);
     } else {
       const int j = lane & 15;
@@ -848,7 +714,7 @@ gemm_wide_kernel(GemmParams p, int tilesM, int tilesN, int groups) {
   auto read_finish = [&](auto tile, auto& f, Pend& p0, Pend& p1) __attribute__((always_inline)) {
     using T = decltype(tile);
     constexpr int NF = sizeof(f) / sizeof(u32x4);
-    if constexpr (std::is_same<T, TileK<kWB, NW, true>>::value) {
+    if constexpr (std::is_same<T, TileK<kWB, NW>>::value) {
       lds_wait(f);
     } else {
       lds_wait(p0);
@@ -919,8 +785,8 @@ gemm_wide_kernel(GemmParams p, int tilesM, int tilesN, int groups) {
   // ds_read_b128 per K-contiguous fragment, two ds_read_b64_tr_b16 per
   // MN-contiguous one), each landing in its fragment or in a half-fragment
   // pending register.
-  constexpr bool AK = std::is_same<TA, TileK<kWB, NW, true>>::value;
-  constexpr bool BKK = std::is_same<TB, TileK<kWB, NW, true>>::value;
+  constexpr bool AK = std::is_same<TA, TileK<kWB, NW>>::value;
+  constexpr bool BKK = std::is_same<TB, TileK<kWB, NW>>::value;
   constexpr int NRA = AK ? FM : 2 * FM, NRB = BKK ? FN : 2 * FN, NRD = NRA + NRB;
   constexpr int NMF = FM * FN, NDMA = 2 * kWNI;
   // PRE: MFMAs of a step issued before its wait and barrier (they use the
@@ -946,7 +812,7 @@ gemm_wide_kernel(GemmParams p, int tilesM, int tilesN, int groups) {
   // offsets (rows k and k + 4 share their swizzle).
   auto read_base = [&](auto tile, const uint16_t* st, int c0, int par) __attribute__((always_inline)) -> uint32_t {
     using T = decltype(tile);
-    if constexpr (std::is_same<T, TileK<kWB, NW, true>>::value) {
+    if constexpr (std::is_same<T, TileK<kWB, NW>>::value) {
       return lds_addr(st + (c0 >> 4) * 512 + lane * 8);
     } else {
       const int j = lane & 15;
