@@ -912,11 +912,11 @@ void launch_dispatch_bwd(const moe_cfg& c, const void* Wg, const float* dlogits,
 // -------------------------------------------------------------------- dWg
 // dWg[e][:] = sum_t dlogits[t][e] x[t][:].  Stage 1: a block owns a slab of
 // 256 columns (each lane 4 consecutive columns), a chunk of tokens and a
-// group of up to kDwgEG experts; its eight waves take every eighth token of
+// group of 8, 16 or 32 experts; its eight waves take every eighth token of
 // the chunk, and their sums meet in LDS in wave order.  A dlogits entry that
 // is zero (every unselected expert under renormalised top-k) skips its
 // products: the branch is uniform, since a wave works on one token at a time.
-// Stage 2 adds the chunk partials in chunk order.  Deterministic.
+// Stage 2 adds the chunk partials in a fixed order.  Deterministic.
 constexpr int kDwgCPL = 4;                 // columns per lane
 constexpr int kDwgSlab = 64 * kDwgCPL;     // columns per block
 constexpr int kDwgWaves = 8;
@@ -928,11 +928,15 @@ struct DwgPlan {
 };
 static DwgPlan dwg_plan(const moe_cfg& c) {
   DwgPlan q;
-  q.eg = c.E <= 16 ? 16 : 32;
+  q.eg = c.E <= 8 ? 8 : (c.E <= 16 ? 16 : 32);
   q.slabs = (c.d_model + kDwgSlab - 1) / kDwgSlab;
   q.egroups = (c.E + q.eg - 1) / q.eg;
-  // about 256 blocks (two waves per SIMD) over the chunks, at least 64 tokens per chunk
-  int64_t want = 256 / (q.slabs * q.egroups);
+  // About 512 blocks over the chunks (a wave's few tokens per chunk are
+  // latency-bound, so more blocks in flight read x faster), at least 64
+  // tokens per chunk, at most 16 MiB of partials.
+  int64_t want = 512 / (q.slabs * q.egroups);
+  const int64_t cap = ((int64_t)16 << 20) / ((int64_t)c.E * c.d_model * 4);
+  if (want > cap) want = cap;
   if (want < 1) want = 1;
   int64_t tch = (c.T + want - 1) / want;
   if (tch < 64) tch = 64;
@@ -1061,14 +1065,21 @@ __global__ __launch_bounds__(64 * kDwgWaves) void dwg_partial_kernel(const T* __
   }
 }
 
-// dWg[i] = sum over chunks of part[c][i], in chunk order; 4 consecutive outputs per thread.
-__global__ __launch_bounds__(256) void dwg_reduce_kernel(const float* __restrict__ part, float* __restrict__ dWg,
-                                                         int nch, int64_t ed) {
-  const int64_t i = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * 4;
-  if (i >= ed) return;
+// dWg[i] = sum over chunks of part[c][i]: the chunks fall into kDwgRuns
+// contiguous runs, each summed in chunk order by its own thread, and the run
+// sums are added in run order.  A block covers 32 x 4 consecutive outputs.
+constexpr int kDwgRuns = 8;
+__global__ __launch_bounds__(32 * kDwgRuns) void dwg_reduce_kernel(const float* __restrict__ part,
+                                                                   float* __restrict__ dWg, int nch, int64_t ed) {
+  __shared__ float red[kDwgRuns][32][4];
+  const int q = threadIdx.x & 31, g = threadIdx.x >> 5;
+  const int64_t i = ((int64_t)blockIdx.x * 32 + q) * 4;
+  const int per = (nch + kDwgRuns - 1) / kDwgRuns;
+  const int c_begin = min(nch, g * per), c_end = min(nch, c_begin + per);
   float s[4] = {0.f, 0.f, 0.f, 0.f};
-  int c = 0;
-  for (; c + 4 <= nch; c += 4) {
+  int c = c_begin;
+  if (i >= ed) c = c_end;
+  for (; c + 4 <= c_end; c += 4) {
     float v[4][4];
 #pragma unroll
     for (int u = 0; u < 4; ++u) Vec<float>::load(part + (int64_t)(c + u) * ed + i, v[u]);
@@ -1077,13 +1088,22 @@ __global__ __launch_bounds__(256) void dwg_reduce_kernel(const float* __restrict
 #pragma unroll
       for (int j = 0; j < 4; ++j) s[j] += v[u][j];
   }
-  for (; c < nch; ++c) {
+  for (; c < c_end; ++c) {
     float v[4];
     Vec<float>::load(part + (int64_t)c * ed + i, v);
 #pragma unroll
     for (int j = 0; j < 4; ++j) s[j] += v[j];
   }
-  Vec<float>::store(dWg + i, s);
+#pragma unroll
+  for (int j = 0; j < 4; ++j) red[g][q][j] = s[j];
+  __syncthreads();
+  if (g == 0 && i < ed) {
+#pragma unroll
+    for (int r = 1; r < kDwgRuns; ++r)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) s[j] += red[r][q][j];
+    Vec<float>::store(dWg + i, s);
+  }
 }
 
 size_t bwd_dw_ws_bytes(const moe_cfg& c) {
@@ -1105,7 +1125,8 @@ static void launch_dwg_eg(const moe_cfg& c, const void* x, const float* dl, floa
 template <typename T>
 static void launch_dwg_t(const moe_cfg& c, const void* x, const float* dl, float* part, const DwgPlan& q,
                          hipStream_t s) {
-  if (q.eg == 16) launch_dwg_eg<T, 16>(c, x, dl, part, q, s);
+  if (q.eg == 8) launch_dwg_eg<T, 8>(c, x, dl, part, q, s);
+  else if (q.eg == 16) launch_dwg_eg<T, 16>(c, x, dl, part, q, s);
   else launch_dwg_eg<T, 32>(c, x, dl, part, q, s);
 }
 
@@ -1117,8 +1138,8 @@ void launch_dwg(const moe_cfg& c, const void* x, const float* dlogits, float* dW
     if (c.dtype == MOE_BF16) launch_dwg_t<uint16_t>(c, x, dlogits, part, q, s);
     else launch_dwg_t<float>(c, x, dlogits, part, q, s);
   }
-  hipLaunchKernelGGL(dwg_reduce_kernel, dim3((unsigned)((ed / 4 + 255) / 256)), dim3(256), 0, s, part, dWg,
-                     (int)q.nch, ed);
+  hipLaunchKernelGGL(dwg_reduce_kernel, dim3((unsigned)((ed / 4 + 31) / 32)), dim3(32 * kDwgRuns), 0, s, part,
+                     dWg, (int)q.nch, ed);
 }
 
 }  // namespace lmoe
