@@ -131,18 +131,22 @@ __device__ __forceinline__ float act_bwd(float h, int act) {
 }
 
 // Compile-time activation for the bf16 GEMM epilogues, whose outputs are
-// rounded to bf16: GELU-tanh is evaluated as h * sigmoid(2u), the same function
-// as 0.5 h (1 + tanh u), with the hardware exponential and reciprocal
-// (v_exp_f32, v_rcp_f32: about 1 ulp each, far below the bf16 rounding of the
-// result; an IEEE division would cost about ten instructions per element).
-__device__ __forceinline__ float sigmoid_fast(float z) { return __builtin_amdgcn_rcpf(1.f + __expf(-z)); }
+// rounded to bf16: GELU-tanh is evaluated as h * s, s = sigmoid(2u), the same
+// function as 0.5 h (1 + tanh u), u = sqrt(2/pi) (h + 0.044715 h^3), with the
+// hardware base-2 exponential and reciprocal (v_exp_f32, v_rcp_f32: about 1 ulp
+// each, far below the bf16 rounding of the result; an IEEE division would cost
+// about ten instructions per element).  The constants are folded so that
+// exp(-2u) = 2^(h (c1 + c2 h^2)), c1 = -2 sqrt(2/pi) log2(e),
+// c2 = 0.044715 c1: one multiply-add and one multiply ahead of the exponential.
+__device__ __forceinline__ float gelu_tanh_sig(float h, float h2) {
+  return __builtin_amdgcn_rcpf(1.f + __builtin_amdgcn_exp2f(h * fmaf(-0.10294324f, h2, -2.3022082f)));
+}
 
 template <int ACT>
 __device__ __forceinline__ float act_fwd_t(float h) {
   if constexpr (ACT == MOE_ACT_RELU) return h > 0.f ? h : 0.f;
   else if constexpr (ACT == MOE_ACT_GELU_TANH) {
-    const float u2 = 1.5957691216057308f * (h + 0.044715f * h * h * h);  // 2u
-    return h * sigmoid_fast(u2);
+    return h * gelu_tanh_sig(h, h * h);
   } else if constexpr (ACT == MOE_ACT_GELU_ERF) return 0.5f * h * (1.f + erff(h * 0.7071067811865476f));
   else return h;
 }
@@ -151,11 +155,11 @@ template <int ACT>
 __device__ __forceinline__ float act_bwd_t(float h) {
   if constexpr (ACT == MOE_ACT_RELU) return h > 0.f ? 1.f : 0.f;
   else if constexpr (ACT == MOE_ACT_GELU_TANH) {
-    // d/dh [h s(2u)] = s + 2 h s (1 - s) u',  u' = sqrt(2/pi) (1 + 3 * 0.044715 h^2)
-    const float u2 = 1.5957691216057308f * (h + 0.044715f * h * h * h);
-    const float sg = sigmoid_fast(u2);
-    const float du2 = 1.5957691216057308f * (1.f + 0.134145f * h * h);
-    return sg + h * sg * (1.f - sg) * du2;
+    // d/dh [h s] = s + h s (1 - s) (2u)' = s (1 + h (1 - s) (2u)'),
+    // (2u)' = 2 sqrt(2/pi) (1 + 3 * 0.044715 h^2)
+    const float h2 = h * h;
+    const float sg = gelu_tanh_sig(h, h2);
+    return sg * fmaf(h * (1.f - sg), fmaf(0.21406445f, h2, 1.5957691f), 1.f);
   } else if constexpr (ACT == MOE_ACT_GELU_ERF)
     return 0.5f * (1.f + erff(h * 0.7071067811865476f)) + h * expf(-0.5f * h * h) * 0.3989422804014327f;
   else return 1.f;
