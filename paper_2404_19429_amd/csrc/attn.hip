@@ -221,23 +221,30 @@ attn_fwd_kernel(const uint16_t* __restrict__ qkv, uint16_t* __restrict__ o, floa
 #pragma unroll
       for (int f = 0; f < 2; ++f) s[u % 4][f] = mfma(kf1[u], qf[f][2 + u / 4], s[u % 4][f]);
     __builtin_amdgcn_sched_barrier(0);
-    // Online softmax per query (lane column); keys 16 i + 4 g + v.
+    // Online softmax per query (lane column); keys 16 i + 4 g + v.  The
+    // running max is kept in the base-2 units of s c2 (c2 > 0, and rounding is
+    // monotonic, so the max of the products is the product of the max), and
+    // p = 2^(s c2 - m) is one fused multiply-add ahead of the exponential.
+    // Only a tile reaching past the wave's first query has keys to mask.
     u32x4 pb[2][2];
+    const bool diag = k0 + kTR - 1 > qw;
 #pragma unroll
     for (int f = 0; f < 2; ++f) {
       const int q = qw + 16 * f + jq;
+      if (diag) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int v = 0; v < 4; ++v)
+            if (k0 + 16 * i + 4 * g + v > q) s[i][f][v] = -INFINITY;
+      }
       float tmax = -INFINITY;
 #pragma unroll
       for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int v = 0; v < 4; ++v) {
-          const int key = k0 + 16 * i + 4 * g + v;
-          const float x = key > q ? -INFINITY : s[i][f][v] * c2;
-          s[i][f][v] = x;
-          tmax = fmaxf(tmax, x);
-        }
+        for (int v = 0; v < 4; ++v) tmax = fmaxf(tmax, s[i][f][v]);
       tmax = group_max(tmax);
-      const float mnew = fmaxf(mrow[f], tmax);
+      const float mnew = fmaxf(mrow[f], tmax * c2);
       const float alpha = exp2_hw(mrow[f] - mnew);
       mrow[f] = mnew;
       float ps = 0.f;
@@ -245,7 +252,7 @@ attn_fwd_kernel(const uint16_t* __restrict__ qkv, uint16_t* __restrict__ o, floa
       for (int i = 0; i < 4; ++i)
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
-          const float p = exp2_hw(s[i][f][v] - mnew);
+          const float p = exp2_hw(fmaf(s[i][f][v], c2, -mnew));
           s[i][f][v] = p;
           ps += p;
         }
@@ -405,13 +412,23 @@ attn_dq_kernel(const uint16_t* __restrict__ qkv, const uint16_t* __restrict__ do
     for (int u = 0; u < 8; ++u) dp[u % 4] = mfma(fr1[u], dof[2 + u / 4], dp[u % 4]);
     __builtin_amdgcn_sched_barrier(0);
     u32x4 kt_f[4];
+    // dS = P (dP - delta), P = 2^(s c2 - lse); masked entries (a key after
+    // the query, or a query past S) only in a tile reaching past the wave's
+    // first query or holding the end of the sequence.
+    if (k0 + kTR - 1 > qw || qw + 15 >= S) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+      for (int i = 0; i < 4; ++i)
 #pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const int key = k0 + 16 * i + 4 * g + v;
-        s[i][v] = (key > q || q >= S) ? 0.f : exp2_hw(s[i][v] * c2 - lq) * (dp[i][v] - dq_delta);
-      }
+        for (int v = 0; v < 4; ++v) {
+          const int key = k0 + 16 * i + 4 * g + v;
+          s[i][v] = (key > q || q >= S) ? 0.f : exp2_hw(fmaf(s[i][v], c2, -lq)) * (dp[i][v] - dq_delta);
+        }
+    } else {
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) s[i][v] = exp2_hw(fmaf(s[i][v], c2, -lq)) * (dp[i][v] - dq_delta);
+    }
     const u32x4 ds0 = pack_b(s[0], s[1]), ds1 = pack_b(s[2], s[3]);
     cols_finish(kt_f, cp);
 #pragma unroll
@@ -543,17 +560,34 @@ attn_dkdv_kernel(const uint16_t* __restrict__ qkv, const uint16_t* __restrict__ 
       }
       Rd128<8>::run(st8, a);
     }
+    // Masked entries (a query before the key, or past S, whose statistics
+    // are unspecified) only in a tile starting before the wave's last key or
+    // holding the end of the sequence.
+    if (k0 + 16 * wid + 15 > qbase || qbase + kTR > S) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const f32x4 L4 = __builtin_bit_cast(f32x4, st8[i]);
-      const f32x4 D4 = __builtin_bit_cast(f32x4, st8[4 + i]);
+      for (int i = 0; i < 4; ++i) {
+        const f32x4 L4 = __builtin_bit_cast(f32x4, st8[i]);
+        const f32x4 D4 = __builtin_bit_cast(f32x4, st8[4 + i]);
 #pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const int q = qbase + 16 * i + 4 * g + v;
-        const bool live = key <= q && q < S;  // statistics past S are unspecified
-        const float p = live ? exp2_hw(s[i][v] * c2 - L4[v]) : 0.f;
-        s[i][v] = p;
-        dp[i][v] = live ? p * (dp[i][v] - D4[v]) : 0.f;
+        for (int v = 0; v < 4; ++v) {
+          const int q = qbase + 16 * i + 4 * g + v;
+          const bool live = key <= q && q < S;
+          const float p = live ? exp2_hw(fmaf(s[i][v], c2, -L4[v])) : 0.f;
+          s[i][v] = p;
+          dp[i][v] = live ? p * (dp[i][v] - D4[v]) : 0.f;
+        }
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const f32x4 L4 = __builtin_bit_cast(f32x4, st8[i]);
+        const f32x4 D4 = __builtin_bit_cast(f32x4, st8[4 + i]);
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const float p = exp2_hw(fmaf(s[i][v], c2, -L4[v]));
+          s[i][v] = p;
+          dp[i][v] = p * (dp[i][v] - D4[v]);
+        }
       }
     }
     const u32x4 p0 = pack_b(s[0], s[1]), p1 = pack_b(s[2], s[3]);
