@@ -121,7 +121,9 @@ __global__ __launch_bounds__(256) void ln_bwd_kernel(const uint16_t* __restrict_
     const int64_t row = (int64_t)blockIdx.x * kLnBwdRows + wid * (kLnBwdRows / 4) + rr;
     if (row >= T) break;
     const float mu = mean[row], rs = rstd[row];
-    u32x4 xr[NC], dr[NC];  // the row's bf16 values, kept packed between the two passes
+    // The row's bf16 values, kept packed between the two passes; dres is
+    // loaded with x and dy so that its latency hides under the reduction.
+    u32x4 xr[NC], dr[NC], rv[NC];
     float s1 = 0.f, s2 = 0.f;
 #pragma unroll
     for (int c = 0; c < NC; ++c) {
@@ -129,6 +131,7 @@ __global__ __launch_bounds__(256) void ln_bwd_kernel(const uint16_t* __restrict_
       if (ch < nch) {
         xr[c] = *reinterpret_cast<const u32x4*>(x + row * d + 8 * ch);
         dr[c] = *reinterpret_cast<const u32x4*>(dyl + row * d + 8 * ch);
+        rv[c] = *reinterpret_cast<const u32x4*>(dres + row * d + 8 * ch);
         float xv[8], dv[8];
         unpack8(xr[c], xv);
         unpack8(dr[c], dv);
@@ -152,7 +155,7 @@ __global__ __launch_bounds__(256) void ln_bwd_kernel(const uint16_t* __restrict_
         float xv[8], dv[8], r[8], o[8];
         unpack8(xr[c], xv);
         unpack8(dr[c], dv);
-        Vec<uint16_t>::load(dres + row * d + 8 * ch, r);
+        unpack8(rv[c], r);
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
           const float xh = (xv[i] - mu) * rs;
