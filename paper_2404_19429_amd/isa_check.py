@@ -22,7 +22,7 @@ def _regs(tok: str):
     return {(m.group(1), int(m.group(2)))} if m else set()
 
 
-def check_text(asm: str, kernel_prefix: str = "_ZN4lmoe16gemm_bf16_kernel"):
+def check_text(asm: str, kernel_prefix: str = "_ZN4lmoe"):
     """Return {kernel: [offending instructions]} for kernels with hazards."""
     lines = asm.split("\n")
     starts = [i for i, l in enumerate(lines) if re.match(rf"^{kernel_prefix}\w*:", l)]

@@ -113,7 +113,7 @@ def test_binding_rejects_host_tensors_and_short_buffers():
 
 def test_isa_check_flags_use_before_wait():
     from paper_2404_19429_amd.isa_check import check_text
-    clean = """_ZN4lmoe16gemm_bf16_kernelX:
+    clean = """_ZN4lmoe16gemm_wide_kernelX:
 \t;;#ASMSTART
 \tds_read_b128 v[4:7], v1
 \ts_waitcnt lgkmcnt(0)
@@ -123,7 +123,7 @@ def test_isa_check_flags_use_before_wait():
     bad = clean.replace("\ts_waitcnt lgkmcnt(0)\n", "").replace(";;#ASMEND\n", ";;#ASMEND\n\tv_mov_b32 v20, v5\n")
     assert check_text(clean) == {}
     hits = check_text(bad)
-    assert list(hits) == ["_ZN4lmoe16gemm_bf16_kernelX"] and any("v_mov_b32" in h for h in hits["_ZN4lmoe16gemm_bf16_kernelX"])
+    assert list(hits) == ["_ZN4lmoe16gemm_wide_kernelX"] and any("v_mov_b32" in h for h in hits["_ZN4lmoe16gemm_wide_kernelX"])
 
 
 def _block_call(cfg, n_chunks=2, passes=3, grads=True, ws_bytes=None, **acts_over):
