@@ -152,8 +152,8 @@ __device__ __forceinline__ void store4(uint16_t* p, float a, float b, float c, f
 constexpr int kFwdQ = 128;
 
 __global__ __attribute__((amdgpu_flat_work_group_size(256, 256), amdgpu_waves_per_eu(2, 2))) void
-attn_fwd_kernel(const uint16_t* __restrict__ qkv, uint16_t* __restrict__ o, float* __restrict__ lse, int S, int Sp,
-                int H, int nbh, float c2) {
+attn_fwd_kernel(const uint16_t* __restrict__ qkv, uint16_t* __restrict__ o, uint16_t* __restrict__ o_blk,
+                float* __restrict__ lse, int S, int Sp, int H, int nbh, float c2) {
   __shared__ __attribute__((aligned(16))) uint16_t lds[2][2][kTileElems];  // [stage][K, V]
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
   const int g = lane >> 4, jq = lane & 15;
@@ -289,9 +289,12 @@ attn_fwd_kernel(const uint16_t* __restrict__ qkv, uint16_t* __restrict__ o, floa
     if (q < S) {
       const float inv = 1.f / l;
 #pragma unroll
-      for (int i = 0; i < 8; ++i)
-        store4(Ob + (int64_t)q * d + 16 * i + 4 * g, acc_o[i][f][0] * inv, acc_o[i][f][1] * inv,
-               acc_o[i][f][2] * inv, acc_o[i][f][3] * inv);
+      for (int i = 0; i < 8; ++i) {
+        const float o0 = acc_o[i][f][0] * inv, o1 = acc_o[i][f][1] * inv, o2 = acc_o[i][f][2] * inv,
+                    o3 = acc_o[i][f][3] * inv;
+        store4(Ob + (int64_t)q * d + 16 * i + 4 * g, o0, o1, o2, o3);
+        if (o_blk) store4(o_blk + blk_off((int64_t)b * S + q, h * kHD + 16 * i + 4 * g, d), o0, o1, o2, o3);
+      }
       if (g == 0) lse[(int64_t)bh * Sp + q] = mrow[f] + log2f(l);
     }
   }
@@ -331,8 +334,8 @@ constexpr int kDqQ = 64;
 
 __global__ __attribute__((amdgpu_flat_work_group_size(256, 256), amdgpu_waves_per_eu(2, 2))) void
 attn_dq_kernel(const uint16_t* __restrict__ qkv, const uint16_t* __restrict__ dout, const float* __restrict__ lse,
-               const float* __restrict__ delta, uint16_t* __restrict__ dqkv, int S, int Sp, int H, int nbh, float c2,
-               float scale) {
+               const float* __restrict__ delta, uint16_t* __restrict__ dqkv, uint16_t* __restrict__ dqkv_blk, int S,
+               int Sp, int H, int nbh, float c2, float scale) {
   __shared__ __attribute__((aligned(16))) uint16_t lds[2][2][kTileElems];  // [stage][K, V]
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
   const int g = lane >> 4, jq = lane & 15;
@@ -444,8 +447,11 @@ attn_dq_kernel(const uint16_t* __restrict__ qkv, const uint16_t* __restrict__ do
   if (q < S) {
     uint16_t* dQ = dqkv + ((int64_t)b * S + q) * ld + h * kHD;
 #pragma unroll
-    for (int i = 0; i < 8; ++i)
-      store4(dQ + 16 * i + 4 * g, acc[i][0] * scale, acc[i][1] * scale, acc[i][2] * scale, acc[i][3] * scale);
+    for (int i = 0; i < 8; ++i) {
+      const float v0 = acc[i][0] * scale, v1 = acc[i][1] * scale, v2 = acc[i][2] * scale, v3 = acc[i][3] * scale;
+      store4(dQ + 16 * i + 4 * g, v0, v1, v2, v3);
+      if (dqkv_blk) store4(dqkv_blk + blk_off((int64_t)b * S + q, h * kHD + 16 * i + 4 * g, ld), v0, v1, v2, v3);
+    }
   }
 }
 
@@ -459,7 +465,8 @@ constexpr int kKvK = 64;
 
 __global__ __attribute__((amdgpu_flat_work_group_size(256, 256), amdgpu_waves_per_eu(2, 2))) void
 attn_dkdv_kernel(const uint16_t* __restrict__ qkv, const uint16_t* __restrict__ dout, const float* __restrict__ lse,
-                 const float* __restrict__ delta, uint16_t* __restrict__ dqkv, int S, int Sp, int H, int nbh, float c2,
+                 const float* __restrict__ delta, uint16_t* __restrict__ dqkv, uint16_t* __restrict__ dqkv_blk, int S,
+                 int Sp, int H, int nbh, float c2,
                  float scale) {
   __shared__ __attribute__((aligned(16))) uint16_t lds[2][2][kTileElems];  // [stage][Q, dO]
   // [stage][lse (64), delta (64), zeros (128)]: one wave instruction fills a stage
@@ -614,25 +621,32 @@ attn_dkdv_kernel(const uint16_t* __restrict__ qkv, const uint16_t* __restrict__ 
     uint16_t* row = dqkv + ((int64_t)b * S + key) * ld + h * kHD;
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
-      store4(row + d + 16 * i + 4 * g, dk[i][0] * scale, dk[i][1] * scale, dk[i][2] * scale, dk[i][3] * scale);
+      const float k0v = dk[i][0] * scale, k1v = dk[i][1] * scale, k2v = dk[i][2] * scale, k3v = dk[i][3] * scale;
+      store4(row + d + 16 * i + 4 * g, k0v, k1v, k2v, k3v);
       store4(row + 2 * d + 16 * i + 4 * g, dv[i][0], dv[i][1], dv[i][2], dv[i][3]);
+      if (dqkv_blk) {
+        const int64_t t = (int64_t)b * S + key;
+        const int c = h * kHD + 16 * i + 4 * g;
+        store4(dqkv_blk + blk_off(t, d + c, ld), k0v, k1v, k2v, k3v);
+        store4(dqkv_blk + blk_off(t, 2 * d + c, ld), dv[i][0], dv[i][1], dv[i][2], dv[i][3]);
+      }
     }
   }
 }
 
 // ---------------------------------------------------------------- launchers
 // qkv/o/dout/dqkv point at the first token of `nseq` whole sequences.
-void launch_attn_fwd(const void* qkv, void* o, float* lse, int nseq, int S, int H, hipStream_t s) {
+void launch_attn_fwd(const void* qkv, void* o, float* lse, int nseq, int S, int H, hipStream_t s, void* o_blk) {
   if (nseq <= 0 || S <= 0) return;
   const int nbh = nseq * H;
   const int nqt = (S + kFwdQ - 1) / kFwdQ;
   const float c2 = kLog2e / sqrtf((float)kHD);
   hipLaunchKernelGGL(attn_fwd_kernel, dim3((unsigned)(nqt * nbh)), dim3(256), 0, s, (const uint16_t*)qkv,
-                     (uint16_t*)o, lse, S, attn_stat_stride(S), H, nbh, c2);
+                     (uint16_t*)o, (uint16_t*)o_blk, lse, S, attn_stat_stride(S), H, nbh, c2);
 }
 
 void launch_attn_bwd(const void* qkv, const void* o, const void* dout, const float* lse, float* delta, void* dqkv,
-                     int nseq, int S, int H, hipStream_t s) {
+                     int nseq, int S, int H, hipStream_t s, void* dqkv_blk) {
   if (nseq <= 0 || S <= 0) return;
   const int nbh = nseq * H;
   const int64_t T = (int64_t)nseq * S;
@@ -644,10 +658,10 @@ void launch_attn_bwd(const void* qkv, const void* o, const void* dout, const flo
   const float c2 = kLog2e * scale;
   const int nq = (S + kDqQ - 1) / kDqQ;
   hipLaunchKernelGGL(attn_dq_kernel, dim3((unsigned)(nq * nbh)), dim3(256), 0, s, (const uint16_t*)qkv,
-                     (const uint16_t*)dout, lse, delta, (uint16_t*)dqkv, S, Sp, H, nbh, c2, scale);
+                     (const uint16_t*)dout, lse, delta, (uint16_t*)dqkv, (uint16_t*)dqkv_blk, S, Sp, H, nbh, c2, scale);
   const int nk = (S + kKvK - 1) / kKvK;
   hipLaunchKernelGGL(attn_dkdv_kernel, dim3((unsigned)(nk * nbh)), dim3(256), 0, s, (const uint16_t*)qkv,
-                     (const uint16_t*)dout, lse, delta, (uint16_t*)dqkv, S, Sp, H, nbh, c2, scale);
+                     (const uint16_t*)dout, lse, delta, (uint16_t*)dqkv, (uint16_t*)dqkv_blk, S, Sp, H, nbh, c2, scale);
 }
 
 }  // namespace lmoe

@@ -191,11 +191,13 @@ hipError_t run_block(const moe_block_cfg& c, const moe_block_weights& W, const m
     std::vector<hipEvent_t> ev_disp(n);
     for (int i = 0; i < n; ++i) {  // pre-MoE stage, partitions in order
       const int64_t t0 = Tc * i;
-      launch_ln_fwd(bf(x, t0 * d), W.ln1_g, W.ln1_b, bfm(A.a, t0 * d), A.ln1_mean + t0, A.ln1_rstd + t0, Tc, d, Sc);
-      launch_pack_rows(bf(A.a, t0 * d), act_b, Tc, d, Sc);
+      // LN1 and attention write their outputs' blocked copies (act_b) for the
+      // projections that follow; each copy is used before the next is written.
+      launch_ln_fwd(bf(x, t0 * d), W.ln1_g, W.ln1_b, bfm(A.a, t0 * d), A.ln1_mean + t0, A.ln1_rstd + t0, Tc, d, Sc,
+                    act_b);
       launch_dense_wide(Tc, (int)d3, d, act_b, Wqkv_b, true, bfm(A.qkv, t0 * d3), d3, nullptr, Sc);
-      launch_attn_fwd(bf(A.qkv, t0 * d3), bfm(A.attn, t0 * d), A.lse + (int64_t)i * nseq * H * Sp, nseq, S, H, Sc);
-      launch_pack_rows(bf(A.attn, t0 * d), act_b, Tc, d, Sc);
+      launch_attn_fwd(bf(A.qkv, t0 * d3), bfm(A.attn, t0 * d), A.lse + (int64_t)i * nseq * H * Sp, nseq, S, H, Sc,
+                      act_b);
       launch_dense_wide(Tc, d, d, act_b, Wo_b, true, bfm(A.h, t0 * d), d, bf(x, t0 * d), Sc);
       launch_ln_fwd(bf(A.h, t0 * d), W.ln2_g, W.ln2_b, bfm(A.m, t0 * d), A.ln2_mean + t0, A.ln2_rstd + t0, Tc, d, Sc);
       launch_gate(pc, bf(A.m, t0 * d), W.Wg, nullptr, A.logits + t0 * E, A.idx + t0 * k, A.w + t0 * k, Sc);
@@ -229,8 +231,10 @@ hipError_t run_block(const moe_block_cfg& c, const moe_block_weights& W, const m
       return timed ? hipEventRecord(g_timing.ev[2 * op + which], s) : hipSuccess;
     };
     HIP_TRY(order(Sc, Sw));  // the weight stream starts after the caller's earlier work
-    launch_pack_rows(W.Wqkv, Wqkv_b, d3, d, Sc);
-    launch_pack_rows(W.Wo, Wo_b, d, d, Sc);
+    if (!(passes & MOE_BLOCK_FWD)) {   // a forward in the same call has packed them already
+      launch_pack_rows(W.Wqkv, Wqkv_b, d3, d, Sc);
+      launch_pack_rows(W.Wo, Wo_b, d, d, Sc);
+    }
     // The activation-gradient chain on Sc, recording after each operation
     // whose output a weight gradient reads the event that gradient waits for.
     hipEvent_t after[MOE_BOP_COUNT] = {};
@@ -252,21 +256,20 @@ hipError_t run_block(const moe_block_cfg& c, const moe_block_weights& W, const m
     HIP_TRY(mark(MOE_BOP_DISPATCH_BWD, 1, Sc));
     // LN2 backward with the residual: dh = dy + LN2'(dm)
     HIP_TRY(mark(MOE_BOP_LN2_BWD, 0, Sc));
-    launch_ln_bwd(A.dm, A.h, A.ln2_mean, A.ln2_rstd, W.ln2_g, dy, A.dh, (float*)(wsb + L.ln2), T, d, Sc);
+    launch_ln_bwd(A.dm, A.h, A.ln2_mean, A.ln2_rstd, W.ln2_g, dy, A.dh, (float*)(wsb + L.ln2), T, d, Sc,
+                  act_b);   // dh, and its blocked copy for d(attn out) = dh Wo
     HIP_TRY(mark(MOE_BOP_LN2_BWD, 1, Sc));
     HIP_TRY(produced(MOE_BOP_LN2_BWD));
     // attention backward
     HIP_TRY(mark(MOE_BOP_DATTN, 0, Sc));
-    launch_pack_rows(A.dh, act_b, T, d, Sc);
     launch_dense_wide(T, d, d, act_b, Wo_b, false, A.dattn, d, nullptr, Sc);  // do = dh Wo
     HIP_TRY(mark(MOE_BOP_DATTN, 1, Sc));
     HIP_TRY(mark(MOE_BOP_ATTN_BWD, 0, Sc));
-    launch_attn_bwd(A.qkv, A.attn, A.dattn, A.lse, A.delta, A.dqkv, c.B, S, H, Sc);
+    launch_attn_bwd(A.qkv, A.attn, A.dattn, A.lse, A.delta, A.dqkv, c.B, S, H, Sc, act_b);  // + blocked dqkv
     HIP_TRY(mark(MOE_BOP_ATTN_BWD, 1, Sc));
     HIP_TRY(produced(MOE_BOP_ATTN_BWD));
     // QKV projection and LN1 backward with the residual: dx = dh + LN1'(dqkv Wqkv)
     HIP_TRY(mark(MOE_BOP_DA, 0, Sc));
-    launch_pack_rows(A.dqkv, act_b, T, (int)d3, Sc);
     launch_dense_wide(T, d, (int)d3, act_b, Wqkv_b, false, A.da, d, nullptr, Sc);
     HIP_TRY(mark(MOE_BOP_DA, 1, Sc));
     HIP_TRY(mark(MOE_BOP_LN1_BWD, 0, Sc));

@@ -114,19 +114,25 @@ void launch_dense_wide(int64_t M, int N, int K, const void* A, const void* B, bo
 // the first token of nseq whole sequences of S tokens; lse and delta rows have
 // stride attn_stat_stride(S).
 inline int attn_stat_stride(int S) { return (S + 63) / 64 * 64; }
-void launch_attn_fwd(const void* qkv, void* o, float* lse, int nseq, int S, int H, hipStream_t s);
+// o_blk / dqkv_blk non-null: the output is also written in the 16 x 32 blocked
+// layout of the dense products ([pad16(nseq S)][d] / [..][3 d]; the padding
+// rows are not written).
+void launch_attn_fwd(const void* qkv, void* o, float* lse, int nseq, int S, int H, hipStream_t s,
+                     void* o_blk = nullptr);
 void launch_attn_bwd(const void* qkv, const void* o, const void* dout, const float* lse, float* delta, void* dqkv,
-                     int nseq, int S, int H, hipStream_t s);
+                     int nseq, int S, int H, hipStream_t s, void* dqkv_blk = nullptr);
 
 // norm.hip: LayerNorm (eps 1e-5) of bf16 rows of width d (multiple of 8, <= 4096).
 // The backward writes ln_bwd_blocks(T) x 2 x d float partials, reduced by
 // launch_ln_gain_reduce into the gain and bias gradients (the reduction
 // overwrites some partials: run it once per backward).
 int ln_bwd_blocks(int64_t T);
+// y_blk / dx_blk non-null (d a multiple of 32): the output is also written in
+// the 16 x 32 blocked layout of the dense products (padding rows not written).
 void launch_ln_fwd(const void* x, const void* g, const void* b, void* y, float* mean, float* rstd, int64_t T, int d,
-                   hipStream_t s);
+                   hipStream_t s, void* y_blk = nullptr);
 void launch_ln_bwd(const void* dyl, const void* x, const float* mean, const float* rstd, const void* g,
-                   const void* dres, void* dx, float* part, int64_t T, int d, hipStream_t s);
+                   const void* dres, void* dx, float* part, int64_t T, int d, hipStream_t s, void* dx_blk = nullptr);
 void launch_ln_gain_reduce(float* part, int64_t T, int d, float* dg, float* db, hipStream_t s);
 
 // block.cpp: the partitioned block (arguments validated by the C ABI layer).

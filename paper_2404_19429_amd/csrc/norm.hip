@@ -10,7 +10,10 @@
 // second kernel (deterministic).
 //
 // Rows are split into 16-byte chunks; lane l handles chunks l, l + 64, ...
-// (consecutive lanes read consecutive 16 bytes).
+// (consecutive lanes read consecutive 16 bytes).  Either kernel may also write
+// its output in the 16 x 32 blocked layout that the dense products read
+// (y_blk / dx_blk non-null; d a multiple of 32): each 16-byte chunk lies
+// within one block row, so it is one more 16-byte store.
 #include "internal.h"
 
 namespace lmoe {
@@ -39,8 +42,8 @@ __device__ __forceinline__ void unpack8(const u32x4& r, float* v) {
 template <int NC>
 __global__ __launch_bounds__(256) void ln_fwd_kernel(const uint16_t* __restrict__ x, const uint16_t* __restrict__ g,
                                                      const uint16_t* __restrict__ b, uint16_t* __restrict__ y,
-                                                     float* __restrict__ mean_out, float* __restrict__ rstd_out,
-                                                     int64_t T, int d, double eps) {
+                                                     uint16_t* __restrict__ y_blk, float* __restrict__ mean_out,
+                                                     float* __restrict__ rstd_out, int64_t T, int d, double eps) {
   const int lane = threadIdx.x & 63;
   const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   if (row >= T) return;
@@ -88,6 +91,7 @@ __global__ __launch_bounds__(256) void ln_fwd_kernel(const uint16_t* __restrict_
         r[i] = f64_to_bf16_bits(y0) | (f64_to_bf16_bits(y1) << 16);
       }
       *reinterpret_cast<u32x4*>(yr + 8 * ch) = r;
+      if (y_blk) *reinterpret_cast<u32x4*>(y_blk + blk_off(row, 8 * ch, d)) = r;
     }
   }
   if (lane == 0) {
@@ -101,8 +105,8 @@ template <int NC>
 __global__ __launch_bounds__(256) void ln_bwd_kernel(const uint16_t* __restrict__ dyl, const uint16_t* __restrict__ x,
                                                      const float* __restrict__ mean, const float* __restrict__ rstd,
                                                      const uint16_t* __restrict__ g, const uint16_t* __restrict__ dres,
-                                                     uint16_t* __restrict__ dx, float* __restrict__ part, int64_t T,
-                                                     int d) {
+                                                     uint16_t* __restrict__ dx, uint16_t* __restrict__ dx_blk,
+                                                     float* __restrict__ part, int64_t T, int d) {
   __shared__ __attribute__((aligned(16))) float red[4][64][16];
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
   const int nch = d / 8;
@@ -162,6 +166,7 @@ __global__ __launch_bounds__(256) void ln_bwd_kernel(const uint16_t* __restrict_
           o[i] = r[i] + rs * (dv[i] * gv[c][i] - s1 - xh * s2);
         }
         Vec<uint16_t>::store(dx + row * d + 8 * ch, o);
+        if (dx_blk) Vec<uint16_t>::store(dx_blk + blk_off(row, 8 * ch, d), o);
       }
     }
   }
@@ -222,25 +227,25 @@ static int ln_chunks(int d) {
 int ln_bwd_blocks(int64_t T) { return (int)((T + kLnBwdRows - 1) / kLnBwdRows); }
 
 void launch_ln_fwd(const void* x, const void* g, const void* b, void* y, float* mean, float* rstd, int64_t T, int d,
-                   hipStream_t s) {
+                   hipStream_t s, void* y_blk) {
   if (T <= 0) return;
   const dim3 grid((unsigned)((T + 3) / 4));
   const int nc = ln_chunks(d);
 #define LMOE_LN_FWD(NC)                                                                                     \
   hipLaunchKernelGGL(ln_fwd_kernel<NC>, grid, dim3(256), 0, s, (const uint16_t*)x, (const uint16_t*)g,      \
-                     (const uint16_t*)b, (uint16_t*)y, mean, rstd, T, d, 1e-5)
+                     (const uint16_t*)b, (uint16_t*)y, (uint16_t*)y_blk, mean, rstd, T, d, 1e-5)
   if (nc == 1) LMOE_LN_FWD(1); else if (nc == 2) LMOE_LN_FWD(2); else if (nc == 4) LMOE_LN_FWD(4); else LMOE_LN_FWD(8);
 #undef LMOE_LN_FWD
 }
 
 void launch_ln_bwd(const void* dyl, const void* x, const float* mean, const float* rstd, const void* g,
-                   const void* dres, void* dx, float* part, int64_t T, int d, hipStream_t s) {
+                   const void* dres, void* dx, float* part, int64_t T, int d, hipStream_t s, void* dx_blk) {
   if (T <= 0) return;
   const dim3 grid((unsigned)ln_bwd_blocks(T));
   const int nc = ln_chunks(d);
 #define LMOE_LN_BWD(NC)                                                                                     \
   hipLaunchKernelGGL(ln_bwd_kernel<NC>, grid, dim3(256), 0, s, (const uint16_t*)dyl, (const uint16_t*)x,    \
-                     mean, rstd, (const uint16_t*)g, (const uint16_t*)dres, (uint16_t*)dx, part, T, d)
+                     mean, rstd, (const uint16_t*)g, (const uint16_t*)dres, (uint16_t*)dx, (uint16_t*)dx_blk, part, T, d)
   if (nc == 1) LMOE_LN_BWD(1); else if (nc == 2) LMOE_LN_BWD(2); else if (nc == 4) LMOE_LN_BWD(4); else LMOE_LN_BWD(8);
 #undef LMOE_LN_BWD
 }
