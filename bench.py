@@ -23,12 +23,17 @@ eager step is timed too (eager_ms_per_step).  Per-call durations come from
 HIP events recorded around every C-ABI call on the stream the kernels run on,
 over the eager steps.  Those steps run over the same buffers (hot caches:
 the 256 MiB Infinity Cache may hold what the previous call wrote); the cold
-variant writes a 512 MiB scratch buffer before every step and before every
+variant reads a 512 MiB scratch buffer before every step and before every
 call, outside the timed events, so each call starts from HBM
 (cold_ms_per_step, cold_per_call_ms, cold_hbm_frac_per_call).  The roofline
-object reports the grouped expert GEMM call with the largest share of the
-step (its algorithmic 4 N d f flops over its event-timed duration, against
-the dense bf16 MFMA peak); roofline_calls lists all three.  The CPU
+object reports the expert-GEMM kernel with the largest time per step: its algorithmic
+2 N d f flops per launch over its average launch duration, timed by HIP events
+that the library records around each expert product on the kernels' own
+stream during the eager steps (moe_product_timing), against the dense bf16
+MFMA peak; traffic is the HBM-side bytes per launch from the committed PMC
+summary for the current GEMM sources.  roofline_kernels lists every product
+kernel, roofline_calls the three GEMM calls (4 N d f flops each over the
+call's event time, gathers included).  The CPU
 baseline is the float64 oracle on a bounded sample of the same workload.
 
 With --workload block: one step = forward + backward of the pre-LN MoE block
@@ -493,11 +498,14 @@ def main():
     torch.cuda.synchronize()
     evs = [[torch.cuda.Event(enable_timing=True) for _ in range(len(CALLS) + 1)] for _ in range(a.steps)]
     torch.cuda.synchronize()
+    L.moe_product_timing(True)   # each expert product's own duration, from events on the kernels' stream
     t0 = time.perf_counter()
     for i in range(a.steps):
         step(evs[i])
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
+    prod_ms, prod_n = L.moe_product_times()
+    L.moe_product_timing(False)
     per_call = {c: 0.0 for c in CALLS}
     for e in evs:
         for j, c in enumerate(CALLS):
@@ -611,6 +619,30 @@ def main():
                        "unit": "TFLOP/s", "frac": ach / MI355X_PEAK_BF16_TFLOPS,
                        "ms": per_call[c], "traffic": measured_traffic(spec.name, c)}
     dominant = max(gemm_calls, key=lambda c: per_call[c])
+    # Per kernel: each expert product is 2 N d f flops per launch.  The two dW
+    # products are launches of one kernel instantiation; the kernel with the
+    # largest time per step is the roofline's.
+    prod_flop = 2.0 * N * d * f
+    kernels = {
+        "fwd1": ("FWD1 H = X W1^T with the (H, act(H)) epilogue", ["fwd1"]),
+        "fwd2": ("FWD2 O = act(H) W2^T (+ K-split fix-up)", ["fwd2"]),
+        "dA": ("dA = dO W2 with the dH = dA act'(H) epilogue", ["dA"]),
+        "dXe": ("dXe = dH W1 (+ K-split fix-up)", ["dXe"]),
+        "dW": ("ragged-K dW2 = dO^T A and dW1 = dH^T X, two launches per step", ["dW2", "dW1"]),
+    }
+    pi = {p: i for i, p in enumerate(L.PRODUCTS)}
+    rl_kernels = {}
+    for kname, (what, prods) in kernels.items():
+        n_launch = int(sum(prod_n[pi[p]] for p in prods))
+        if n_launch == 0:
+            continue
+        avg_ms = float(sum(prod_ms[pi[p]] for p in prods)) / n_launch
+        ach = prod_flop / (avg_ms * 1e-3) / 1e12
+        rl_kernels[kname] = {"kernel": f"gemm_wide_kernel: {what}", "bound": "mfma", "achieved": ach,
+                             "peak": MI355X_PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": ach / MI355X_PEAK_BF16_TFLOPS,
+                             "launch_ms": avg_ms, "launches_per_step": n_launch / a.steps,
+                             "traffic": measured_traffic(spec.name, "kernel:" + kname)}
+    dom_kernel = max(rl_kernels, key=lambda k: rl_kernels[k]["launch_ms"] * rl_kernels[k]["launches_per_step"])
     eager_ms = wall / a.steps * 1e3
     working_set = sum(t.numel() * t.element_size() for t in vars(b).values() if isinstance(t, torch.Tensor))
     working_set += sum(t.numel() * t.element_size() for t in dev.values())
@@ -638,8 +670,9 @@ def main():
                    "C": C, "G": spec.G, "capacity_factor": f"{spec.cf_num}/{spec.cf_den}", "act": spec.act,
                    "routing": a.routing,
                    "kept_rows": N, "parallelism": "single GPU (one GPU's share; all-to-all not run)"},
-        "roofline": {k: v for k, v in rl_calls[dominant].items() if k != "ms"},
-        "roofline_call": dominant,
+        "roofline": {k: v for k, v in rl_kernels[dom_kernel].items() if k not in ("launch_ms", "launches_per_step")},
+        "roofline_kernel": dom_kernel,
+        "roofline_kernels": rl_kernels,
         "roofline_calls": rl_calls,
         "expert_gemm_mfma_frac": 3 * gemm_call_flop / (all_gemm_ms * 1e-3) / 1e12 / MI355X_PEAK_BF16_TFLOPS,
         "dispatch_GBps": dispatch_gbps,

@@ -257,6 +257,25 @@ moe_status moe_bwd_dw(const moe_cfg* cfg, const void* x, const float* dlogits,
                       const void* A, const void* dO, const void* dH, void* dW1, void* dW2, float* dWg,
                       void* ws, size_t ws_bytes, moe_stream_t stream);
 
+/* Per-product timing of the expert GEMMs, a measurement aid: the paper's
+ * planners work from measured per-operation times (Sec. 3 "Overview", its
+ * profiler and cost model), and a product's own duration is what its
+ * roofline needs.  moe_product_timing(1) makes every later expert-product
+ * launch of the calling thread, on the device current at this call, record
+ * a pair of HIP events around the product on that call's stream (a K-split
+ * fix-up launch falls inside its product's pair); moe_product_timing(0)
+ * stops.  Either clears the record.  Do not leave it on while a stream is
+ * being captured into a graph.  moe_product_times (host; waits for the
+ * events) writes, per product in the order FWD1 (H = X W1^T with act(H)),
+ * FWD2 (O = A W2^T), dA (with dH = dA act'(H)), dXe (dH W1), dW2, dW1, the
+ * summed milliseconds ms[6] and the launch counts counts[6] since the last
+ * clear, then clears.  The library owns the events (reused, kept until the
+ * process ends).  Errors: MOE_EDEVICE (no device), MOE_EINVAL (NULL
+ * arguments), MOE_ELAUNCH (an event could not be made or recorded, or a
+ * timed launch came on another device). */
+moe_status moe_product_timing(int32_t on);
+moe_status moe_product_times(double* ms, int32_t* counts);
+
 /* ------------------------------------------------------------------ block */
 
 /* The pre-LN transformer block whose FFN is the MoE layer, with its

@@ -205,6 +205,21 @@ moe_status moe_dispatch_bpr(const moe_cfg* cfg, const void* x, const float* logi
   return check_launch(fn);
 }
 
+moe_status moe_product_timing(int32_t on) {
+  const char* fn = "moe_product_timing";
+  const hipError_t e = lmoe::product_timing(on != 0);
+  if (e != hipSuccess) return fail(MOE_EDEVICE, "%s: %s", fn, hipGetErrorString(e));
+  return ok();
+}
+
+moe_status moe_product_times(double* ms, int32_t* counts) {
+  const char* fn = "moe_product_times";
+  if (ms == nullptr || counts == nullptr) return fail(MOE_EINVAL, "%s: ms and counts are required", fn);
+  const hipError_t e = lmoe::product_times(ms, counts);
+  if (e != hipSuccess) return fail(MOE_ELAUNCH, "%s: %s", fn, hipGetErrorString(e));
+  return ok();
+}
+
 moe_status moe_block_op_times(double* ms) {
   const char* fn = "moe_block_op_times";
   if (ms == nullptr) return fail(MOE_EINVAL, "%s: ms is NULL", fn);

@@ -21,6 +21,9 @@
 #include "internal.h"
 #include "lds_ops.h"
 
+#include <utility>
+#include <vector>
+
 namespace lmoe {
 
 // EPI_WGF32: the dense weight-gradient product C = A^T B of the block, both
@@ -1193,17 +1196,108 @@ static void run_expert(const moe_cfg& c, const GemmParams& p, int64_t rows, int 
 // Rows per expert block of an [E][C][*] buffer (C rounded up to 16 for bf16).
 static int64_t rows_alloc(const moe_cfg& c) { return c.dtype == MOE_BF16 ? pad16(c.C) : c.C; }
 
+// Per-product timing (moe_product_timing): while on, each expert product
+// launch of this thread is bracketed by a pair of events on its stream (the
+// K-split fix-up launch inside the pair); product_times sums them per product.
+namespace {
+struct ProductTimer {
+  bool on = false;
+  int dev = -1;
+  bool failed = false;
+  std::vector<hipEvent_t> pool;      // events of this device, reused after each readout
+  size_t next = 0;
+  std::vector<std::pair<int, size_t>> rec;   // (product, index of its first event)
+};
+thread_local ProductTimer g_ptimer;
+
+hipEvent_t ptimer_event() {
+  ProductTimer& t = g_ptimer;
+  if (t.next == t.pool.size()) {
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess) {
+      t.failed = true;
+      return nullptr;
+    }
+    t.pool.push_back(e);
+  }
+  return t.pool[t.next++];
+}
+// Records the opening event of product `prod` on s; returns false when timing is off.
+bool ptimer_begin(int prod, hipStream_t s) {
+  ProductTimer& t = g_ptimer;
+  if (!t.on) return false;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev != t.dev) {   // events belong to the device timing was started on
+    t.failed = true;
+    return false;
+  }
+  const size_t i = t.next;
+  hipEvent_t a = ptimer_event(), b = ptimer_event();
+  if (!a || !b || hipEventRecord(a, s) != hipSuccess) {
+    t.failed = true;
+    return false;
+  }
+  t.rec.push_back({prod, i});
+  return true;
+}
+void ptimer_end(bool begun, hipStream_t s) {
+  if (!begun) return;
+  ProductTimer& t = g_ptimer;
+  if (hipEventRecord(t.pool[t.rec.back().second + 1], s) != hipSuccess) t.failed = true;
+}
+}  // namespace
+
+hipError_t product_timing(bool on) {
+  ProductTimer& t = g_ptimer;
+  int dev = 0;
+  const hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev != t.dev) {   // a different device: the pool's events belong to the old one (left, not destroyed)
+    t.pool.clear();
+    t.dev = dev;
+  }
+  t.on = on;
+  t.failed = false;
+  t.next = 0;
+  t.rec.clear();
+  return hipSuccess;
+}
+
+hipError_t product_times(double* ms, int32_t* counts) {
+  ProductTimer& t = g_ptimer;
+  for (int q = 0; q < kProducts; ++q) {
+    ms[q] = 0.0;
+    counts[q] = 0;
+  }
+  if (t.failed) return hipErrorUnknown;
+  for (const auto& r : t.rec) {
+    hipError_t e = hipEventSynchronize(t.pool[r.second + 1]);
+    float v = 0.f;
+    if (e == hipSuccess) e = hipEventElapsedTime(&v, t.pool[r.second], t.pool[r.second + 1]);
+    if (e != hipSuccess) return e;
+    ms[r.first] += v;
+    counts[r.first] += 1;
+  }
+  t.next = 0;
+  t.rec.clear();
+  return hipSuccess;
+}
+
 void launch_expert_fwd(const moe_cfg& c, const void* X, const int32_t* rb, const int32_t* re, const void* W1,
                        const void* W2, void* H, void* A, void* O, void* ws, hipStream_t s) {
   const int64_t d = c.d_model, f = c.d_ff, C = c.C, Cp = rows_alloc(c);
   GemmParams p1{X, d, Cp * d, W1, d, f * d, H, f, Cp * f, A, nullptr, rb, re, 0, (int)f, (int)d, c.act, (int)C};
   p1.part = (float*)ws;
   p1.ksplit = c.ksplit;
+  bool tb = ptimer_begin(kProdFwd1, s);
   run_expert<true, false, EPI_FWD1, true>(c, p1, C, (int)f, s);
+  ptimer_end(tb, s);
   GemmParams p2{A, f, Cp * f, W2, f, d * f, O, d, Cp * d, nullptr, nullptr, rb, re, 0, (int)d, (int)f, c.act, (int)C};
   p2.part = (float*)ws;
   p2.ksplit = c.ksplit;
+  tb = ptimer_begin(kProdFwd2, s);
   run_expert<true, false, EPI_STORE, false>(c, p2, C, (int)d, s);   // expert_out row-major
+  ptimer_end(tb, s);
 }
 
 void launch_expert_bwd_dx(const moe_cfg& c, const void* dO, const int32_t* rb, const int32_t* re, const void* H,
@@ -1213,12 +1307,16 @@ void launch_expert_bwd_dx(const moe_cfg& c, const void* dO, const int32_t* rb, c
   GemmParams p1{dO, d, Cp * d, W2, f, d * f, dH, f, Cp * f, nullptr, H, rb, re, 0, (int)f, (int)d, c.act, (int)C};
   p1.part = (float*)ws;
   p1.ksplit = c.ksplit;
+  bool tb = ptimer_begin(kProdDA, s);
   run_expert<false, false, EPI_DACT, true>(c, p1, C, (int)f, s);
+  ptimer_end(tb, s);
   // dXe = dH W1_e  (B(k=i, n=j) = W1[e][i][j])
   GemmParams p2{dH, f, Cp * f, W1, d, f * d, dXe, d, Cp * d, nullptr, nullptr, rb, re, 0, (int)d, (int)f, c.act, (int)C};
   p2.part = (float*)ws;
   p2.ksplit = c.ksplit;
+  tb = ptimer_begin(kProdDXe, s);
   run_expert<false, false, EPI_STORE, false>(c, p2, C, (int)d, s);   // dXe row-major
+  ptimer_end(tb, s);
 }
 
 void launch_expert_bwd_dw(const moe_cfg& c, const void* X, const void* A, const void* dO, const void* dH,
@@ -1229,13 +1327,15 @@ void launch_expert_bwd_dw(const moe_cfg& c, const void* X, const void* A, const 
   GemmParams p2{dO, d, Cp * d, A, f, Cp * f, dW2, f, d * f, nullptr, nullptr, rb, re, (int)d, (int)f, 0, c.act, (int)C};
   // dW1_e [f][d] = dH_e^T X_e
   GemmParams p1{dH, f, Cp * f, X, d, Cp * d, dW1, d, f * d, nullptr, nullptr, rb, re, (int)f, (int)d, 0, c.act, (int)C};
-  if (c.wpacked && c.dtype == MOE_BF16) {
-    run_expert<false, true, EPI_STORE, true>(c, p2, d, (int)f, s);
-    run_expert<false, true, EPI_STORE, true>(c, p1, f, (int)d, s);
-  } else {
-    run_expert<false, true, EPI_STORE, false>(c, p2, d, (int)f, s);
-    run_expert<false, true, EPI_STORE, false>(c, p1, f, (int)d, s);
-  }
+  const bool blk = c.wpacked && c.dtype == MOE_BF16;
+  bool tb = ptimer_begin(kProdDW2, s);
+  if (blk) run_expert<false, true, EPI_STORE, true>(c, p2, d, (int)f, s);
+  else run_expert<false, true, EPI_STORE, false>(c, p2, d, (int)f, s);
+  ptimer_end(tb, s);
+  tb = ptimer_begin(kProdDW1, s);
+  if (blk) run_expert<false, true, EPI_STORE, true>(c, p1, f, (int)d, s);
+  else run_expert<false, true, EPI_STORE, false>(c, p1, f, (int)d, s);
+  ptimer_end(tb, s);
 }
 
 // Sum of the S float partials of a K-split weight gradient, in group order,

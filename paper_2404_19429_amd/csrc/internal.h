@@ -97,6 +97,14 @@ void launch_expert_bwd_dx(const moe_cfg& c, const void* dO, const int32_t* rb, c
                           const void* W1, const void* W2, void* dH, void* dXe, void* ws, hipStream_t s);
 void launch_expert_bwd_dw(const moe_cfg& c, const void* X, const void* A, const void* dO, const void* dH,
                           const int32_t* rb, const int32_t* re, void* dW1, void* dW2, hipStream_t s);
+// Per-product timing of the expert products on this thread (moe_product_timing):
+// product_timing(on) starts (or stops) and clears the record on the current
+// device; product_times sums the recorded durations (ms) and launch counts per
+// product and clears the record (hipErrorUnknown if an event could not be made
+// or recorded, or a launch came on another device).
+enum { kProdFwd1 = 0, kProdFwd2, kProdDA, kProdDXe, kProdDW2, kProdDW1, kProducts };
+hipError_t product_timing(bool on);
+hipError_t product_times(double* ms, int32_t* counts);
 
 // Dense bf16 products of the block (gemm.hip).
 // launch_dense_wgrad: C[M][N] = A^T B with A [K][M], B [K][N] row-major bf16

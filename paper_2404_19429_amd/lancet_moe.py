@@ -29,7 +29,10 @@ MOE_CALL_DISPATCH, MOE_CALL_BWD_DX, MOE_CALL_BWD_DW, MOE_CALL_FFN_FWD, MOE_CALL_
 EXPORTS = ["moe_capacity", "moe_workspace_bytes", "moe_last_error", "moe_gate_topk", "moe_dispatch",
            "moe_dispatch_noalloc", "moe_dispatch_bpr", "moe_pack_weights", "moe_expert_ffn_fwd", "moe_combine", "moe_bwd_dx", "moe_bwd_dw",
            "moe_block_workspace_bytes", "moe_block_chunked", "moe_block_op_times", "moe_block_dw_schedule",
-           "moe_dw_schedule", "moe_pipeline_plan", "moe_pipeline_range_cost"]
+           "moe_dw_schedule", "moe_pipeline_plan", "moe_pipeline_range_cost", "moe_product_timing",
+           "moe_product_times"]
+#: The expert products moe_product_times reports, in its order.
+PRODUCTS = ["fwd1", "fwd2", "dA", "dXe", "dW2", "dW1"]
 MOE_BLOCK_FWD, MOE_BLOCK_BWD, MOE_BLOCK_TIMED = 1, 2, 4
 #: The block backward's operations (moe_block_op): the chain 0..7, the weight-gradient groups 8..13.
 BLOCK_OPS = ["combine_bwd", "expert_dx", "dispatch_bwd", "ln2_bwd", "dattn", "attn_bwd", "da", "ln1_bwd",
@@ -95,6 +98,8 @@ def _load():
         "moe_bwd_dw": (I32, [CFG] + [P] * 12 + [SZ, P]),
         "moe_dw_schedule": (I32, [I32, P, P, I32, P, P, P, P, P]),
         "moe_block_op_times": (I32, [P]),
+        "moe_product_timing": (I32, [I32]),
+        "moe_product_times": (I32, [P, P]),
         "moe_block_dw_schedule": (I32, [P, ctypes.c_double, P, P, P]),
         "moe_pipeline_plan": (I32, [I32, I32, P, P, P, I32, P, P, P, P, P]),
         "moe_pipeline_range_cost": (I32, [I32, I32, P, P, P, I32, I32, I32, P]),
@@ -424,6 +429,20 @@ def make_block_cfg(B, S, heads, d_ff, E, k, C, G=1, act="gelu_tanh", renorm=1, d
     order = (ctypes.c_int32 * 6)(*([-1] * 6 if dw_order is None else [int(v) for v in dw_order]))
     return moe_block_cfg(int(B), int(S), int(heads),
                          make_cfg(B * S, d, d_ff, E, k, C, G, "bf16", act, renorm, wpacked=wpacked), order)
+
+
+def moe_product_timing(on):
+    """Start (True) or stop (False) recording per-product events on this thread; either clears the record."""
+    _check(_lib.moe_product_timing(1 if on else 0))
+
+
+def moe_product_times():
+    """(ms, counts) per expert product (PRODUCTS order) since the last clear; clears the record."""
+    import numpy as np
+    ms = np.zeros(len(PRODUCTS), np.float64)
+    counts = np.zeros(len(PRODUCTS), np.int32)
+    _check(_lib.moe_product_times(ms.ctypes.data, counts.ctypes.data))
+    return ms, counts
 
 
 def moe_block_op_times():

@@ -277,6 +277,16 @@ def test_block_cfg_layout_and_dw_order_validation():
     assert L.moe_block_workspace_bytes(L.make_block_cfg(2, 64, 2, 512, 8, 2, 40), 1) > 0
 
 
+def test_product_times_rejects_null_and_timing_needs_a_device():
+    ms = (ctypes.c_double * 6)()
+    counts = (ctypes.c_int32 * 6)()
+    assert L._lib.moe_product_times(None, counts) == L.MOE_EINVAL
+    assert L._lib.moe_product_times(ms, None) == L.MOE_EINVAL
+    # no device in this container: starting the record fails cleanly
+    assert L._lib.moe_product_timing(1) in (L.MOE_OK, L.MOE_EDEVICE)
+    L._lib.moe_product_timing(0)
+
+
 def test_block_op_times_without_a_timed_call():
     ms = (ctypes.c_double * 14)()
     assert L._lib.moe_block_op_times(ms) in (L.MOE_EINVAL, L.MOE_ELAUNCH)

@@ -98,6 +98,34 @@ def test_layer_is_deterministic_and_dw_stream_independent(L):
                                       kept_rows(ebuf(b2, name), fill), err_msg=name)
 
 
+def test_product_timing_counts_every_product_and_leaves_results_unchanged(L):
+    """moe_product_timing: one event pair per expert product of the step
+    (six products, positive durations), nothing recorded once it is off, and
+    every output bit for bit the same as without timing."""
+    spec = SMALL["bf16_zipf_T777_d128_f192_E16_drops"]
+    inp = layer_inputs(spec)
+    C = spec_C(spec)
+    b0, _ = run_layer(L, spec, inp, C)
+    L.moe_product_timing(True)
+    try:
+        b1, _ = run_layer(L, spec, inp, C)
+        ms, counts = L.moe_product_times()
+    finally:
+        L.moe_product_timing(False)
+    log(f"[timing] {dict(zip(L.PRODUCTS, np.round(ms, 4)))}")
+    assert counts.tolist() == [1] * len(L.PRODUCTS)
+    assert np.all(ms > 0)
+    run_layer(L, spec, inp, C)
+    ms2, counts2 = L.moe_product_times()
+    assert counts2.tolist() == [0] * len(L.PRODUCTS) and np.all(ms2 == 0)
+    fill = host(b0.fill)
+    for name in ("y", "dlogits", "dx", "dW1", "dW2", "dWg"):
+        np.testing.assert_array_equal(host(getattr(b0, name)), host(getattr(b1, name)), err_msg=name)
+    for name in ("H", "A", "O", "dO", "dH", "dXe"):
+        np.testing.assert_array_equal(kept_rows(ebuf(b0, name), fill), kept_rows(ebuf(b1, name), fill),
+                                      err_msg=name)
+
+
 def _unpack_weights(t, E, R, X):
     """[E][R][X] packed (16 x 32 blocks) bf16 matrices as row-major numpy."""
     return host(t).reshape(E, R // 16, X // 32, 16, 32).transpose(0, 1, 3, 2, 4).reshape(E, R, X)
