@@ -426,7 +426,7 @@ def main():
     a = _args()
     if a.gpus != 1:
         print(f"bench.py measures one GPU's share of the MoE layer step; --gpus {a.gpus} is not supported "
-              f"(the all-to-all between GPUs is not part of this build).", file=sys.stderr)
+              f"(the all-to-all between GPUs is not implemented by this library).", file=sys.stderr)
         sys.exit(2)
     if a.workload == "block":
         return main_block(a)

@@ -1,4 +1,4 @@
-"""Build-time check of the compiled MFMA kernels (gfx950 assembly of this build).
+"""Build-time check of the compiled MFMA kernels (the library's own gfx950 assembly).
 
 The GEMM and attention kernels read LDS fragments with inline-asm blocks that
 must end with ``s_waitcnt lgkmcnt(0)``.  This check scans the assembly of
