@@ -43,6 +43,8 @@ SMALL = {
     "bf16_G4_T640_d128_f128_E8": _s("f", T=640, d=128, f=128, E=8, G=4, seed=16),
     "f32_top1_E2_T129": _s("g", T=129, d=16, f=8, E=2, k=1, renorm=0, act="relu", dtype="f32", cf_num=1,
                            cf_den=1, seed=17),
+    # the largest top-k and expert count the library takes (k = 8 of 64 experts), with drops
+    "bf16_k8_E64_T300_d128_f64_drops": _s("h", T=300, d=128, f=64, E=64, k=8, cf_num=1, cf_den=2, seed=18),
 }
 
 
